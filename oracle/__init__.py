@@ -1,0 +1,117 @@
+"""CPU oracle for the error-feedback sparsification step (TEST INFRASTRUCTURE).
+
+Only the test suite, the smoke check and the benchmark's CPU-baseline leg may
+import this package.  It is a thin ctypes wrapper over ``oracle.c`` (plain,
+scalar C: the definitions of Algorithm 1's accumulate / compress / error
+update with the hard-threshold and Top-k sparsifiers, and the
+exchange-and-average step).  It shares no code with the HIP library.
+
+All functions take and return numpy arrays on the host.
+"""
+import ctypes
+import os
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_LIB_PATH = os.path.join(_HERE, "liboracle.so")
+_lib = None
+
+_f32p = ctypes.POINTER(ctypes.c_float)
+_i32p = ctypes.POINTER(ctypes.c_int32)
+_i64p = ctypes.POINTER(ctypes.c_int64)
+
+
+def _load():
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(_LIB_PATH):
+        from . import build as _b
+        _b.build()
+    lib = ctypes.CDLL(_LIB_PATH)
+    lib.orc_ht.argtypes = [_f32p, _f32p, ctypes.c_int64, ctypes.c_float, ctypes.c_float,
+                           _i32p, _f32p, ctypes.c_int64, _i64p]
+    lib.orc_ht.restype = None
+    lib.orc_topk.argtypes = [_f32p, _f32p, ctypes.c_int64, ctypes.c_float, ctypes.c_int64,
+                             _i32p, _f32p]
+    lib.orc_topk.restype = ctypes.c_int
+    lib.orc_accumulate.argtypes = [ctypes.POINTER(_i32p), ctypes.POINTER(_f32p), _i64p,
+                                   ctypes.c_int32, ctypes.c_int64, _f32p]
+    lib.orc_accumulate.restype = ctypes.c_int
+    _lib = lib
+    return lib
+
+
+def _f32(a):
+    return np.ascontiguousarray(a, dtype=np.float32)
+
+
+def _ptr(a, t):
+    return a.ctypes.data_as(t)
+
+
+def ht(g, e, lr, lam, cap=None):
+    """Hard-threshold EF step (Algorithm 1 with C_lambda, section 4.2).
+
+    Returns (idx int32[k], val float32[k], e_next float32[d], k) with the
+    payload in ascending index order.  ``e`` is not modified.
+    """
+    lib = _load()
+    g = _f32(g)
+    e_next = np.array(e, dtype=np.float32, copy=True)
+    d = g.size
+    assert e_next.size == d
+    if cap is None:
+        cap = d
+    idx = np.empty(max(cap, 1), dtype=np.int32)
+    val = np.empty(max(cap, 1), dtype=np.float32)
+    count = ctypes.c_int64(0)
+    lib.orc_ht(_ptr(g, _f32p), _ptr(e_next, _f32p), d, ctypes.c_float(lr),
+               ctypes.c_float(lam), _ptr(idx, _i32p), _ptr(val, _f32p), cap,
+               ctypes.byref(count))
+    k = count.value
+    n = min(k, cap)
+    return idx[:n].copy(), val[:n].copy(), e_next, k
+
+
+def topk(g, e, lr, k):
+    """Top-k EF step (Algorithm 1 with Top-k; Lemma 2).
+
+    Returns (idx int32[min(k,d)], val float32[...], e_next float32[d]) with
+    the payload in ascending index order.  ``e`` is not modified.
+    """
+    lib = _load()
+    g = _f32(g)
+    e_next = np.array(e, dtype=np.float32, copy=True)
+    d = g.size
+    assert e_next.size == d
+    kk = max(0, min(int(k), d))
+    idx = np.empty(max(kk, 1), dtype=np.int32)
+    val = np.empty(max(kk, 1), dtype=np.float32)
+    rc = lib.orc_topk(_ptr(g, _f32p), _ptr(e_next, _f32p), d, ctypes.c_float(lr), kk,
+                      _ptr(idx, _i32p), _ptr(val, _f32p))
+    if rc != 0:
+        raise MemoryError("oracle top-k scratch allocation failed")
+    return idx[:kk].copy(), val[:kk].copy(), e_next
+
+
+def accumulate(payloads, d):
+    """Exchange-and-average step: (sum_w decompress(payload_w)) / n.
+
+    ``payloads`` is a sequence of (idx, val) pairs, summed in that order.
+    """
+    lib = _load()
+    n = len(payloads)
+    idxs = [np.ascontiguousarray(p[0], dtype=np.int32) for p in payloads]
+    vals = [_f32(p[1]) for p in payloads]
+    for i, v in zip(idxs, vals):
+        assert i.size == v.size
+    idx_arr = (_i32p * max(n, 1))(*[_ptr(i, _i32p) for i in idxs])
+    val_arr = (_f32p * max(n, 1))(*[_ptr(v, _f32p) for v in vals])
+    counts = np.array([i.size for i in idxs] or [0], dtype=np.int64)
+    out = np.empty(d, dtype=np.float32)
+    rc = lib.orc_accumulate(idx_arr, val_arr, _ptr(counts, _i64p), n, d, _ptr(out, _f32p))
+    if rc != 0:
+        raise ValueError("payload index outside [0, d)")
+    return out

@@ -1,0 +1,164 @@
+/*
+ * Plain CPU oracle for the error-feedback sparsification step.
+ *
+ * TEST INFRASTRUCTURE ONLY.  Nothing in the product library links, loads or
+ * calls this file; only the test suite, the smoke check and the CPU baseline
+ * leg of the benchmark do.  It shares no code, header or constant with the
+ * HIP implementation.
+ *
+ * Paper: "Rethinking gradient sparsification as total error minimization"
+ * (arXiv 2108.00951).  Every function below is the plain definition written
+ * out, scalar, in ascending index order:
+ *
+ *   orc_ht          Algorithm 1 (the EF accumulate, compress and error-update
+ *                   steps) with the hard-threshold sparsifier C_lambda,
+ *                   S_lambda(x) = { i : |x[i]| >= lambda }  (section 4.2).
+ *   orc_topk        the same steps with the Top-k sparsifier (section 1,
+ *                   Lemma 2 in section 4.3); ties broken by lower index.
+ *   orc_accumulate  the exchange-and-average step of Algorithm 1,
+ *                   (1/n) * sum_i Delta_i, with the sum taken in worker order.
+ *
+ * Arithmetic: IEEE-754 binary32, round to nearest even.  The accumulate is an
+ * fp32 multiply followed by a separate fp32 add (never a fused multiply-add);
+ * build with -ffp-contract=off and without fast-math (x86-64 SSE arithmetic,
+ * so float expressions are evaluated in float).  No flush-to-zero.
+ *
+ * Readings taken where the paper is silent:
+ *   - lambda is in the units of p = e + lr*g (the value that is compressed);
+ *   - a kept coordinate leaves +0.0f in the error vector;
+ *   - the payload holds the kept entries of p (the sparsifier copies x[i]);
+ *   - Top-k emits exactly min(k, d) pairs, ranking by the bit pattern of |p|
+ *     (so -0 and +0 tie), larger first, then lower index first;
+ *   - the average divides the in-order fp32 sum by (float)n with one IEEE
+ *     division.
+ * Parity: pinned for all three functions (see the oracle tests).
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+/* p_i = e_i + lr * g_i, as two separately rounded fp32 operations
+ * (Algorithm 1, EF accumulate step). */
+static float ef_accumulate(float e, float lr, float g)
+{
+    float scaled = lr * g;
+    float p = e + scaled;
+    return p;
+}
+
+/* Hard-threshold EF step (Algorithm 1 with C = C_lambda, section 4.2).
+ *
+ * g[d]      gradient, read only.
+ * e[d]      error e_t on entry, e_{t+1} = p - Delta on return (in place).
+ * idx, val  payload, ascending index order; at most cap pairs written.
+ * *count    number of kept coordinates k_t (may exceed cap).
+ */
+void orc_ht(const float *g, float *e, int64_t d, float lr, float lambda,
+            int32_t *idx, float *val, int64_t cap, int64_t *count)
+{
+    int64_t k = 0;
+    for (int64_t i = 0; i < d; i++) {
+        float p = ef_accumulate(e[i], lr, g[i]);
+        if (fabsf(p) >= lambda) {           /* i in S_lambda(p) */
+            if (k < cap) {
+                idx[k] = (int32_t)i;
+                val[k] = p;
+            }
+            k++;
+            e[i] = 0.0f;                     /* p_i - p_i, written as +0 */
+        } else {
+            e[i] = p;                        /* p_i - 0 */
+        }
+    }
+    *count = k;
+}
+
+/* Ranking key of a coordinate for Top-k: the bit pattern of |p|. */
+typedef struct {
+    uint32_t key;
+    int32_t index;
+} orc_rank;
+
+static uint32_t magnitude_key(float p)
+{
+    uint32_t bits;
+    memcpy(&bits, &p, sizeof bits);
+    return bits & 0x7fffffffu;
+}
+
+/* Order: larger key first; equal keys by lower index first. */
+static int rank_cmp(const void *a, const void *b)
+{
+    const orc_rank *x = (const orc_rank *)a;
+    const orc_rank *y = (const orc_rank *)b;
+    if (x->key != y->key) return x->key > y->key ? -1 : 1;
+    if (x->index != y->index) return x->index < y->index ? -1 : 1;
+    return 0;
+}
+
+/* Top-k EF step (Algorithm 1 with C = Top-k; Lemma 2).
+ *
+ * Writes exactly min(k, d) pairs in ascending index order into idx/val and
+ * the new error into e (in place).  Returns 0, or -1 if scratch memory could
+ * not be allocated (nothing is then written).
+ */
+int orc_topk(const float *g, float *e, int64_t d, float lr, int64_t k,
+             int32_t *idx, float *val)
+{
+    if (k > d) k = d;
+    if (k < 0) k = 0;
+    orc_rank *rank = (orc_rank *)malloc((size_t)(d > 0 ? d : 1) * sizeof *rank);
+    unsigned char *kept = (unsigned char *)calloc((size_t)(d > 0 ? d : 1), 1);
+    if (!rank || !kept) {
+        free(rank);
+        free(kept);
+        return -1;
+    }
+    /* p = e + lr*g, held in e for now */
+    for (int64_t i = 0; i < d; i++) {
+        e[i] = ef_accumulate(e[i], lr, g[i]);
+        rank[i].key = magnitude_key(e[i]);
+        rank[i].index = (int32_t)i;
+    }
+    /* Sort all coordinates by the Top-k order and keep the first k. */
+    qsort(rank, (size_t)d, sizeof *rank, rank_cmp);
+    for (int64_t j = 0; j < k; j++) kept[rank[j].index] = 1;
+    /* Emit the kept pairs in ascending index order and form e_{t+1}. */
+    int64_t out = 0;
+    for (int64_t i = 0; i < d; i++) {
+        if (kept[i]) {
+            idx[out] = (int32_t)i;
+            val[out] = e[i];
+            out++;
+            e[i] = 0.0f;
+        }
+    }
+    free(rank);
+    free(kept);
+    return 0;
+}
+
+/* Exchange-and-average step of Algorithm 1, one device standing in for the
+ * n workers:  out = (sum over workers w = 0..n-1 of decompress(payload_w)) / n.
+ *
+ * Payload w holds counts[w] pairs (idx[w][j], val[w][j]); indices are
+ * distinct within one payload.  Sums are formed in worker order with fp32
+ * adds, then each coordinate is divided by (float)n.
+ * Returns 0, or -1 when an index is outside [0, d).
+ */
+int orc_accumulate(const int32_t *const *idx, const float *const *val,
+                   const int64_t *counts, int32_t n, int64_t d, float *out)
+{
+    for (int64_t i = 0; i < d; i++) out[i] = 0.0f;
+    for (int32_t w = 0; w < n; w++) {
+        for (int64_t j = 0; j < counts[w]; j++) {
+            int64_t i = idx[w][j];
+            if (i < 0 || i >= d) return -1;
+            out[i] = out[i] + val[w][j];
+        }
+    }
+    float fn = (float)n;
+    for (int64_t i = 0; i < d; i++) out[i] = out[i] / fn;
+    return 0;
+}

@@ -1,0 +1,211 @@
+"""Seeded synthetic gradient streams and parameter recipes.
+
+This module holds no part of the compression arithmetic: it only draws the
+inputs (gradients g_t, per worker and iteration) with numpy's counter-free
+PCG64 generator keyed by a SeedSequence, and picks the parameters (lambda, k)
+that the workloads are quoted at.  Both the HIP path and the CPU oracle are
+fed from here.
+
+The paper trains real models (Table 1 of Appendix C lists ResNet-18 with
+11,173,962 parameters, an LSTM with 28,949,319 and NCF with 31,832,577);
+those gradient streams are not available, so the workloads below stand in
+for them with synthetic vectors of that size class and a layer-wise
+(segment) structure, up to 1.5e9 elements.
+
+Draws are made per fixed block of BLOCK elements, each block with its own
+seed, so any element range of any gradient can be regenerated on its own
+(used to stream the 1.5e9-element case through the oracle chunk by chunk).
+"""
+from __future__ import annotations
+
+import dataclasses
+import math
+
+import numpy as np
+
+ROOT_ENTROPY = 2108_00951
+BLOCK = 1 << 22            # elements per independently seeded draw block
+LR = np.float32(0.1)       # step size gamma used by every workload
+
+
+@dataclasses.dataclass(frozen=True)
+class Workload:
+    """One synthetic gradient stream.
+
+    kind       "gauss" | "segments" | "student_t" | "outliers"
+    d          vector length
+    iters      EF iterations the workload runs
+    densities  hard-threshold target densities at the first iteration
+    topk_k     Top-k k values (one per density)
+    n_workers  simulated workers (>1 only for the aggregation workload)
+    nseg       number of contiguous segments (layer stand-ins)
+    """
+    ident: int
+    name: str
+    kind: str
+    d: int
+    iters: int
+    densities: tuple
+    topk_k: tuple
+    n_workers: int = 1
+    nseg: int = 0
+
+
+WORKLOADS = {
+    1: Workload(1, "gauss_1m", "gauss", 1_000_000, 10, (0.01,), (1_000,)),
+    2: Workload(2, "segments_25.6m", "segments", 25_557_032, 100, (0.001,), (25_557,),
+                nseg=161),
+    3: Workload(3, "student_t_110m", "student_t", 110_000_000, 50,
+                (0.01, 0.001, 0.0001), (1_100_000, 110_000, 11_000), nseg=200),
+    4: Workload(4, "segments_25.6m_x8", "segments", 25_557_032, 100, (0.001,), (25_557,),
+                n_workers=8, nseg=161),
+    5: Workload(5, "outliers_1.5b", "outliers", 1_500_000_000, 20, (0.001,), (1_500_000,)),
+}
+
+
+def _rng(*key):
+    ss = np.random.SeedSequence(entropy=ROOT_ENTROPY, spawn_key=tuple(int(k) for k in key))
+    return np.random.Generator(np.random.PCG64(ss))
+
+
+def segment_sizes(workload_id: int, nseg: int, d: int, lo: float = 64.0,
+                  hi: float = 2.4e6) -> np.ndarray:
+    """Contiguous segment sizes, log-uniform in [lo, hi], rescaled to sum d.
+
+    Sizes are floored after scaling; the remainder goes one element each to
+    the largest segments; every segment keeps at least one element.
+    """
+    rng = _rng(workload_id, 0, 0, 1)
+    raw = np.exp(rng.uniform(math.log(lo), math.log(hi), size=nseg))
+    scaled = raw * (d / raw.sum())
+    sizes = np.maximum(np.floor(scaled).astype(np.int64), 1)
+    rem = d - int(sizes.sum())
+    order = np.argsort(-scaled, kind="stable")
+    j = 0
+    while rem != 0:
+        s = order[j % nseg]
+        if rem > 0:
+            sizes[s] += 1
+            rem -= 1
+        elif sizes[s] > 1:
+            sizes[s] -= 1
+            rem += 1
+        j += 1
+    assert int(sizes.sum()) == d
+    return sizes
+
+
+def segment_scales(workload_id: int, nseg: int, lo: float, hi: float) -> np.ndarray:
+    """Per-segment scale, log-uniform in [lo, hi], drawn once per workload."""
+    rng = _rng(workload_id, 0, 0, 2)
+    return np.exp(rng.uniform(math.log(lo), math.log(hi), size=nseg)).astype(np.float32)
+
+
+class Stream:
+    """Gradient stream g_{w,t} of one workload (all workers share the layout)."""
+
+    def __init__(self, workload_id: int):
+        self.w = WORKLOADS[workload_id]
+        w = self.w
+        self.bounds = None
+        self.scales = None
+        if w.kind == "segments":
+            sizes = segment_sizes(w.ident if w.ident != 4 else 2, w.nseg, w.d)
+            self.bounds = np.concatenate([[0], np.cumsum(sizes)])
+            self.scales = segment_scales(w.ident if w.ident != 4 else 2, w.nseg, 1e-5, 1e-2)
+        elif w.kind == "student_t":
+            sizes = segment_sizes(w.ident, w.nseg, w.d)
+            self.bounds = np.concatenate([[0], np.cumsum(sizes)])
+            self.scales = (np.float32(1e-4) *
+                           segment_scales(w.ident, w.nseg, 0.1, 10.0)).astype(np.float32)
+
+    # -- per-element scale for a range --------------------------------------
+    def _segment_scale(self, start: int, stop: int) -> np.ndarray:
+        seg = np.searchsorted(self.bounds, np.arange(start, stop), side="right") - 1
+        return self.scales[seg]
+
+    def _block(self, worker: int, t: int, b: int) -> np.ndarray:
+        w = self.w
+        start = b * BLOCK
+        stop = min(w.d, start + BLOCK)
+        n = stop - start
+        rng = _rng(w.ident, worker, t, 100 + b)
+        if w.kind == "gauss":
+            return rng.standard_normal(n, dtype=np.float32) * np.float32(1e-3)
+        if w.kind == "segments":
+            z = rng.standard_normal(n, dtype=np.float32)
+            out = z * self._segment_scale(start, stop)
+            if w.n_workers > 1:
+                out += self._worker_shift(worker, b)
+            return out
+        if w.kind == "student_t":
+            z = rng.standard_t(3, size=n).astype(np.float32)
+            return z * self._segment_scale(start, stop)
+        if w.kind == "outliers":
+            z = rng.standard_normal(n, dtype=np.float32)
+            big = self._outlier_mask(b)
+            return z * np.where(big, np.float32(0.1), np.float32(1e-3))
+        raise ValueError(w.kind)
+
+    def _worker_shift(self, worker: int, b: int) -> np.ndarray:
+        """Fixed per-worker, per-coordinate offset mu_w ~ N(0, 1e-4^2)."""
+        start = b * BLOCK
+        n = min(self.w.d, start + BLOCK) - start
+        rng = _rng(self.w.ident, worker, 0, 1_000_000 + b)
+        return rng.standard_normal(n, dtype=np.float32) * np.float32(1e-4)
+
+    def _outlier_mask(self, b: int) -> np.ndarray:
+        """Fixed Bernoulli(0.05) set of large-gradient coordinates."""
+        start = b * BLOCK
+        n = min(self.w.d, start + BLOCK) - start
+        rng = _rng(self.w.ident, 0, 0, 2_000_000 + b)
+        return rng.random(n, dtype=np.float32) < np.float32(0.05)
+
+    def gradient(self, t: int, worker: int = 0, start: int = 0, stop: int | None = None,
+                 out: np.ndarray | None = None) -> np.ndarray:
+        """g_{worker,t}[start:stop] as float32."""
+        d = self.w.d
+        stop = d if stop is None else stop
+        assert 0 <= start <= stop <= d
+        if out is None:
+            out = np.empty(stop - start, dtype=np.float32)
+        b0 = start // BLOCK
+        b1 = (stop + BLOCK - 1) // BLOCK
+        for b in range(b0, b1):
+            bs = b * BLOCK
+            blk = self._block(worker, t, b)
+            lo = max(start, bs)
+            hi = min(stop, bs + blk.size)
+            out[lo - start:hi - start] = blk[lo - bs:hi - bs]
+        return out
+
+
+def small_gradient(seed: int, d: int, scale: float = 1e-3) -> np.ndarray:
+    """A small Gaussian vector for unit and parity tests."""
+    rng = _rng(9, seed, d, 3)
+    return (rng.standard_normal(d, dtype=np.float32) * np.float32(scale))
+
+
+def calibrate_lambda(g0: np.ndarray, density: float, lr=LR) -> np.float32:
+    """Threshold giving the requested density at the first iteration.
+
+    With e_0 = 0 the first compressed vector is a = fl(lr * g_0).  For
+    K = round(density * d) the threshold is the K-th largest |a|, the upper
+    end of the interval (A_(K+1), A_(K)] of Lemma 3, so the first iteration
+    keeps exactly K coordinates when that magnitude is not tied.
+    """
+    a = np.abs(np.float32(lr) * g0.astype(np.float32, copy=False))
+    d = a.size
+    K = int(round(density * d))
+    K = min(max(K, 1), d)
+    return np.float32(np.partition(a, d - K)[d - K])
+
+
+def lambda_from_k(k: int) -> float:
+    """Tuning rule lambda ~ 1/(2 sqrt(k)) of Appendix D (used for Table 5)."""
+    return 1.0 / (2.0 * math.sqrt(k))
+
+
+def lambda_in_update_units(lam_paper: float, lr=LR) -> np.float32:
+    """Algorithm 1 compresses p/gamma; its threshold in units of p is gamma*lambda."""
+    return np.float32(np.float32(lr) * np.float32(lam_paper))
