@@ -1,0 +1,131 @@
+/*
+ * efsparse — error-feedback gradient sparsification on MI355X (gfx950).
+ *
+ * C ABI of libefsparse.so.  Implements the per-worker compression step of
+ * "Rethinking gradient sparsification as total error minimization"
+ * (arXiv 2108.00951), Algorithm 1 (distributed EF SGD):
+ *
+ *     p      = e + lr * g                 EF accumulate
+ *     Delta  = C(p)                       compress (hard threshold or Top-k)
+ *     e'     = p - Delta                  error update
+ *     avg    = (1/n) sum_i Delta_i        exchange and average
+ *
+ * Conventions shared by every entry point
+ *   - Every array argument is a DEVICE pointer owned by the caller; the
+ *     library never allocates, frees or synchronises.  Work is enqueued on
+ *     `stream` (a hipStream_t; NULL means the legacy default stream) and is
+ *     complete only when that stream is.
+ *   - Arguments are validated on the host before anything is enqueued.  On a
+ *     non-OK status nothing was enqueued, except EFS_EHIP, which reports a
+ *     launch failure (kernels launched before it stay enqueued).
+ *     efs_last_error_message() then describes the failure (per thread).
+ *   - Arithmetic is IEEE binary32 with round to nearest even; the accumulate
+ *     is a multiply followed by a separately rounded add (never fused);
+ *     subnormals are kept.
+ *   - Indices are 0-based int32; d must not exceed INT32_MAX.
+ *   - Payload pair order is unspecified (consumers must not rely on it).
+ *     Payload values are the kept entries of p, unscaled.
+ */
+#ifndef EFSPARSE_H
+#define EFSPARSE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum efs_status {
+    EFS_OK = 0,
+    EFS_EINVAL = 1,   /* an argument failed validation; nothing enqueued      */
+    EFS_ESPACE = 2,   /* workspace smaller than the query said; nothing enqueued */
+    EFS_EHIP = 3      /* the HIP runtime rejected a launch                      */
+} efs_status;
+
+/* A counter object: EFS_COUNTER_WORDS uint32 words (16 bytes) of device
+ * memory, 8-byte aligned, zero-filled once by the caller before first use.
+ * Word 0 receives the payload count k_t of the last completed call; the
+ * other words are the library's and are back at zero whenever no call that
+ * uses the object is in flight.  One object must not be used by two calls
+ * that may run concurrently. */
+#define EFS_COUNTER_WORDS 4
+
+/* Hard-threshold sparsifier with error feedback (Algorithm 1 with the
+ * hard-threshold compressor C_lambda of section 4.2:
+ * S_lambda(p) = { i : |p_i| >= lambda }).
+ *
+ *   g        [d] fp32, read only: the stochastic gradient g_t.
+ *   e        [d] fp32, in place: e_t on entry, e_{t+1} on completion
+ *            (+0.0f at kept coordinates, p_i elsewhere).  Must not overlap g
+ *            or the payload.
+ *   d        vector length, 0 <= d <= INT32_MAX.
+ *   lr       step size gamma (finite).
+ *   lambda   threshold in the units of p (lambda >= 0, not NaN; +inf keeps
+ *            nothing).  Algorithm 1 writes the compressor as gamma*C(p/gamma);
+ *            for the threshold of C in those units pass gamma*lambda here.
+ *   idx,val  [cap] payload (int32 index, fp32 value p_i), unordered; only the
+ *            first min(k_t, cap) slots are written.  May be NULL when cap == 0.
+ *   cap      payload capacity, >= 0.
+ *   counter  counter object (see above); word 0 receives k_t, the TRUE
+ *            count even when it exceeds cap (then the payload is truncated
+ *            and must be treated as invalid; e' is complete regardless).
+ * Pointers g and e must be 4-byte aligned (16-byte alignment takes the
+ * vector path).  NaN entries of p are never kept. */
+efs_status ht_compress(const float *g, float *e, int64_t d, float lr, float lambda,
+                       int32_t *idx, float *val, int64_t cap, uint32_t *counter,
+                       void *stream);
+
+/* Bytes of device workspace topk_compress needs for (d, k). */
+size_t topk_workspace_bytes(int64_t d, int64_t k);
+
+/* Top-k sparsifier with error feedback (Algorithm 1 with Top-k, the
+ * per-iteration optimum of Lemma 2): keeps the k coordinates of largest |p|.
+ * Magnitudes are ranked by the bit pattern of |p| (so -0 and +0 tie, NaN
+ * ranks above +inf); equal magnitudes go to the lower index.
+ *
+ *   g, e, d, lr   as for ht_compress.
+ *   k             0 <= k <= d.
+ *   idx, val      [k] payload of exactly k pairs (unordered).
+ *   workspace     device memory of at least topk_workspace_bytes(d, k)
+ *                 bytes, 16-byte aligned; contents need no initialisation
+ *                 and are clobbered.  Not shareable between concurrent calls.
+ */
+efs_status topk_compress(const float *g, float *e, int64_t d, float lr, int64_t k,
+                         int32_t *idx, float *val, void *workspace,
+                         size_t workspace_bytes, void *stream);
+
+/* Exchange-and-average of n workers' payloads on one device (Algorithm 1):
+ *     out = (sum over w = 0..n-1, in that order, of decompress(payload_w)) / n
+ * with fp32 adds in worker order and one IEEE division by (float)n.
+ *
+ *   idx, val   HOST arrays of n_workers device pointers; payload w has
+ *              indices idx[w][0..c_w) (distinct within one payload) and
+ *              values val[w][0..c_w).
+ *   counts     HOST array of n_workers device pointers to the uint32 count of
+ *              each payload (word 0 of ht_compress's counter object), or NULL
+ *              entries / a NULL array meaning c_w = caps[w].
+ *   caps       HOST array of n_workers capacities; c_w = min(*counts[w], caps[w]).
+ *   d          length of out.
+ *   out        [d] fp32, 16-byte aligned, overwritten.
+ * Payload entries with an index outside [0, d) are ignored. */
+efs_status sparse_accumulate(const int32_t *const *idx, const float *const *val,
+                             const uint32_t *const *counts, const int64_t *caps,
+                             int32_t n_workers, int64_t d, float *out, void *stream);
+
+/* Streaming copy dst[0..n) = src[0..n) with the same 16-byte access pattern
+ * as the compression kernels: a bandwidth ceiling for measurements, not part
+ * of the method.  src and dst 16-byte aligned, n >= 0. */
+efs_status efs_copy_probe(const float *src, float *dst, int64_t n, void *stream);
+
+/* Static text for a status code. */
+const char *efs_status_string(efs_status status);
+
+/* Detail of the last non-OK status returned on the calling thread. */
+const char *efs_last_error_message(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* EFSPARSE_H */

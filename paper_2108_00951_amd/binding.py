@@ -1,0 +1,192 @@
+"""ctypes binding of libefsparse.so (argument marshalling only).
+
+Every function takes torch tensors that live on a ROCm device, passes their
+raw pointers and the current HIP stream to the C ABI declared in
+include/efsparse.h, and raises EfsError on a non-OK status.  No arithmetic
+of the method happens here; when the shared library is missing the import
+of a function fails loudly instead of falling back to anything else.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Sequence, Tuple
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libefsparse.so")
+
+EFS_OK, EFS_EINVAL, EFS_ESPACE, EFS_EHIP = 0, 1, 2, 3
+COUNTER_WORDS = 4
+
+_lib = None
+
+
+class EfsError(RuntimeError):
+    """A non-OK status from libefsparse."""
+
+    def __init__(self, status: int, message: str):
+        super().__init__("efsparse status %d: %s" % (status, message))
+        self.status = status
+
+
+def load_library(path: str = LIB_PATH):
+    """Load libefsparse.so once and declare the C signatures.
+
+    torch is imported first so that the library binds to the HIP runtime
+    torch already loaded (one runtime per process, shared streams).
+    """
+    global _lib
+    if _lib is not None:
+        return _lib
+    import torch  # noqa: F401  (binds the HIP runtime before the library loads)
+    if not os.path.exists(path):
+        raise ImportError("libefsparse.so not built at %s; run python -m paper_2108_00951_amd.build"
+                          % path)
+    lib = ctypes.CDLL(path)
+    declare(lib)
+    _lib = lib
+    return lib
+
+
+def declare(lib):
+    """Attach argtypes/restype of every exported function to a CDLL."""
+    vp, i64, f32, i32 = ctypes.c_void_p, ctypes.c_int64, ctypes.c_float, ctypes.c_int32
+    lib.ht_compress.argtypes = [vp, vp, i64, f32, f32, vp, vp, i64, vp, vp]
+    lib.ht_compress.restype = ctypes.c_int
+    lib.topk_workspace_bytes.argtypes = [i64, i64]
+    lib.topk_workspace_bytes.restype = ctypes.c_size_t
+    lib.topk_compress.argtypes = [vp, vp, i64, f32, i64, vp, vp, vp, ctypes.c_size_t, vp]
+    lib.topk_compress.restype = ctypes.c_int
+    lib.sparse_accumulate.argtypes = [ctypes.POINTER(vp), ctypes.POINTER(vp), ctypes.POINTER(vp),
+                                      ctypes.POINTER(i64), i32, i64, vp, vp]
+    lib.sparse_accumulate.restype = ctypes.c_int
+    lib.efs_copy_probe.argtypes = [vp, vp, i64, vp]
+    lib.efs_copy_probe.restype = ctypes.c_int
+    lib.efs_status_string.argtypes = [ctypes.c_int]
+    lib.efs_status_string.restype = ctypes.c_char_p
+    lib.efs_last_error_message.argtypes = []
+    lib.efs_last_error_message.restype = ctypes.c_char_p
+    return lib
+
+
+def _check(lib, rc: int):
+    if rc != EFS_OK:
+        raise EfsError(rc, lib.efs_last_error_message().decode())
+
+
+def _stream_handle(stream) -> int:
+    import torch
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return int(getattr(stream, "cuda_stream", stream))
+
+
+def _ptr(t) -> Optional[int]:
+    return t.data_ptr() if t is not None and t.numel() > 0 else None
+
+
+def _require(t, dtype, name):
+    import torch
+    if t.dtype != dtype:
+        raise TypeError("%s must be %s, got %s" % (name, dtype, t.dtype))
+    if t.device.type != "cuda":
+        raise TypeError("%s must be a device tensor" % name)
+    if not t.is_contiguous():
+        raise TypeError("%s must be contiguous" % name)
+    return torch
+
+
+def new_counter(device="cuda"):
+    """A zero-filled counter object (EFS_COUNTER_WORDS int32 words)."""
+    import torch
+    return torch.zeros(COUNTER_WORDS, dtype=torch.int32, device=device)
+
+
+def counter_value(counter) -> int:
+    """k_t from a counter object (synchronises with the device)."""
+    return int(counter[0].item()) & 0xFFFFFFFF
+
+
+def ht_compress(g, e, lr: float, lam: float, idx, val, counter, stream=None) -> None:
+    """Hard-threshold EF step; see ht_compress in include/efsparse.h."""
+    import torch
+    lib = load_library()
+    _require(g, torch.float32, "g")
+    _require(e, torch.float32, "e")
+    _require(idx, torch.int32, "idx")
+    _require(val, torch.float32, "val")
+    _require(counter, torch.int32, "counter")
+    if g.numel() != e.numel() or idx.numel() != val.numel() or counter.numel() < COUNTER_WORDS:
+        raise ValueError("size mismatch among g, e, idx, val, counter")
+    rc = lib.ht_compress(_ptr(g), _ptr(e), g.numel(), float(lr), float(lam), _ptr(idx), _ptr(val),
+                         idx.numel(), counter.data_ptr(), _stream_handle(stream))
+    _check(lib, rc)
+
+
+def topk_workspace_bytes(d: int, k: int) -> int:
+    return int(load_library().topk_workspace_bytes(int(d), int(k)))
+
+
+def new_topk_workspace(d: int, k: int, device="cuda"):
+    import torch
+    return torch.empty(max(topk_workspace_bytes(d, k), 1), dtype=torch.uint8, device=device)
+
+
+def topk_compress(g, e, lr: float, k: int, idx, val, workspace, stream=None) -> None:
+    """Top-k EF step; see topk_compress in include/efsparse.h."""
+    import torch
+    lib = load_library()
+    _require(g, torch.float32, "g")
+    _require(e, torch.float32, "e")
+    _require(idx, torch.int32, "idx")
+    _require(val, torch.float32, "val")
+    _require(workspace, torch.uint8, "workspace")
+    if g.numel() != e.numel() or idx.numel() < k or val.numel() < k:
+        raise ValueError("size mismatch among g, e, idx, val and k")
+    rc = lib.topk_compress(_ptr(g), _ptr(e), g.numel(), float(lr), int(k), _ptr(idx), _ptr(val),
+                           _ptr(workspace), workspace.numel(), _stream_handle(stream))
+    _check(lib, rc)
+
+
+def sparse_accumulate(payloads: Sequence[Tuple], d: int, out, stream=None) -> None:
+    """Average of n payloads into out; see sparse_accumulate in include/efsparse.h.
+
+    payloads: sequence of (idx, val, counter_or_None); without a counter the
+    whole idx/val tensor is the payload.
+    """
+    import torch
+    lib = load_library()
+    _require(out, torch.float32, "out")
+    if out.numel() != d:
+        raise ValueError("out must have d elements")
+    n = len(payloads)
+    vp = ctypes.c_void_p
+    idx_arr = (vp * max(n, 1))()
+    val_arr = (vp * max(n, 1))()
+    cnt_arr = (vp * max(n, 1))()
+    caps = (ctypes.c_int64 * max(n, 1))()
+    for w, p in enumerate(payloads):
+        idx, val = p[0], p[1]
+        cnt = p[2] if len(p) > 2 else None
+        _require(idx, torch.int32, "idx[%d]" % w)
+        _require(val, torch.float32, "val[%d]" % w)
+        if idx.numel() != val.numel():
+            raise ValueError("payload %d: idx and val differ in length" % w)
+        idx_arr[w] = _ptr(idx)
+        val_arr[w] = _ptr(val)
+        cnt_arr[w] = cnt.data_ptr() if cnt is not None else None
+        caps[w] = idx.numel()
+    rc = lib.sparse_accumulate(idx_arr, val_arr, cnt_arr, caps, n, int(d), _ptr(out),
+                               _stream_handle(stream))
+    _check(lib, rc)
+
+
+def copy_probe(src, dst, stream=None) -> None:
+    """Streaming copy used as the bandwidth ceiling in measurements."""
+    import torch
+    lib = load_library()
+    _require(src, torch.float32, "src")
+    _require(dst, torch.float32, "dst")
+    if src.numel() != dst.numel():
+        raise ValueError("src and dst differ in length")
+    _check(lib, lib.efs_copy_probe(_ptr(src), _ptr(dst), src.numel(), _stream_handle(stream)))

@@ -1,0 +1,152 @@
+// C ABI of libefsparse.so: host-side argument validation, status codes and
+// dispatch to the kernel launchers.  Nothing here touches the device until
+// every argument has been checked; nothing here allocates or synchronises.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdint>
+#include <cstdio>
+
+#include "../../include/efsparse.h"
+#include "launch.hpp"
+
+namespace {
+
+thread_local char g_message[256] = "";
+
+efs_status fail(efs_status s, const char *fmt, ...) {
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(g_message, sizeof g_message, fmt, ap);
+    va_end(ap);
+    return s;
+}
+
+efs_status check_launch(hipError_t err, const char *what) {
+    if (err != hipSuccess)
+        return fail(EFS_EHIP, "%s: kernel launch failed: %s", what, hipGetErrorString(err));
+    return EFS_OK;
+}
+
+bool aligned(const void *p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0; }
+
+constexpr int64_t kMaxLen = INT32_MAX;
+
+int g_cu_count[64];  // per device; 0 = not queried yet
+
+}  // namespace
+
+namespace efs {
+
+uint32_t persistent_grid(int64_t work_tiles) {
+    int dev = 0;
+    int cus = 256;
+    if (hipGetDevice(&dev) == hipSuccess && dev >= 0 && dev < 64) {
+        if (g_cu_count[dev] == 0) {
+            int v = 0;
+            if (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess &&
+                v > 0)
+                g_cu_count[dev] = v;
+            else
+                g_cu_count[dev] = 256;
+        }
+        cus = g_cu_count[dev];
+    }
+    const int64_t cap = int64_t(cus) * 8;
+    if (work_tiles < 1) work_tiles = 1;
+    return uint32_t(work_tiles < cap ? work_tiles : cap);
+}
+
+}  // namespace efs
+
+extern "C" {
+
+const char *efs_status_string(efs_status s) {
+    switch (s) {
+        case EFS_OK: return "ok";
+        case EFS_EINVAL: return "invalid argument";
+        case EFS_ESPACE: return "workspace too small";
+        case EFS_EHIP: return "HIP runtime error";
+    }
+    return "unknown status";
+}
+
+const char *efs_last_error_message(void) { return g_message; }
+
+efs_status ht_compress(const float *g, float *e, int64_t d, float lr, float lambda,
+                       int32_t *idx, float *val, int64_t cap, uint32_t *counter,
+                       void *stream) {
+    if (d < 0 || d > kMaxLen) return fail(EFS_EINVAL, "ht_compress: d=%lld outside [0, 2^31-1]", (long long)d);
+    if (d > 0 && (g == nullptr || e == nullptr)) return fail(EFS_EINVAL, "ht_compress: g or e is NULL");
+    if (!aligned(g, 4) || !aligned(e, 4)) return fail(EFS_EINVAL, "ht_compress: g and e must be 4-byte aligned");
+    if (!std::isfinite(lr)) return fail(EFS_EINVAL, "ht_compress: lr must be finite");
+    if (std::isnan(lambda) || lambda < 0.0f) return fail(EFS_EINVAL, "ht_compress: lambda must be >= 0 and not NaN");
+    if (cap < 0 || cap > kMaxLen) return fail(EFS_EINVAL, "ht_compress: cap=%lld outside [0, 2^31-1]", (long long)cap);
+    if (cap > 0 && (idx == nullptr || val == nullptr)) return fail(EFS_EINVAL, "ht_compress: idx or val is NULL");
+    if (!aligned(idx, 4) || !aligned(val, 4)) return fail(EFS_EINVAL, "ht_compress: idx and val must be 4-byte aligned");
+    if (counter == nullptr || !aligned(counter, 8)) return fail(EFS_EINVAL, "ht_compress: counter must be non-NULL and 8-byte aligned");
+    return check_launch(efs::launch_ht(g, e, d, lr, lambda, idx, val, cap, counter,
+                                       static_cast<hipStream_t>(stream)),
+                        "ht_compress");
+}
+
+size_t topk_workspace_bytes(int64_t d, int64_t k) {
+    (void)k;
+    if (d < 0 || d > kMaxLen) return 0;
+    return efs::topk_workspace_size(d);
+}
+
+efs_status topk_compress(const float *g, float *e, int64_t d, float lr, int64_t k,
+                         int32_t *idx, float *val, void *workspace, size_t workspace_bytes,
+                         void *stream) {
+    if (d < 0 || d > kMaxLen) return fail(EFS_EINVAL, "topk_compress: d=%lld outside [0, 2^31-1]", (long long)d);
+    if (k < 0 || k > d) return fail(EFS_EINVAL, "topk_compress: k=%lld outside [0, d]", (long long)k);
+    if (d > 0 && (g == nullptr || e == nullptr)) return fail(EFS_EINVAL, "topk_compress: g or e is NULL");
+    if (!aligned(g, 4) || !aligned(e, 4)) return fail(EFS_EINVAL, "topk_compress: g and e must be 4-byte aligned");
+    if (!std::isfinite(lr)) return fail(EFS_EINVAL, "topk_compress: lr must be finite");
+    if (k > 0 && (idx == nullptr || val == nullptr)) return fail(EFS_EINVAL, "topk_compress: idx or val is NULL");
+    if (!aligned(idx, 4) || !aligned(val, 4)) return fail(EFS_EINVAL, "topk_compress: idx and val must be 4-byte aligned");
+    if (d > 0 && (workspace == nullptr || !aligned(workspace, 16)))
+        return fail(EFS_EINVAL, "topk_compress: workspace must be non-NULL and 16-byte aligned");
+    if (d > 0 && workspace_bytes < efs::topk_workspace_size(d))
+        return fail(EFS_ESPACE, "topk_compress: workspace has %zu bytes, needs %zu", workspace_bytes,
+                    efs::topk_workspace_size(d));
+    return check_launch(efs::launch_topk(g, e, d, lr, k, idx, val, workspace,
+                                         static_cast<hipStream_t>(stream)),
+                        "topk_compress");
+}
+
+efs_status sparse_accumulate(const int32_t *const *idx, const float *const *val,
+                             const uint32_t *const *counts, const int64_t *caps,
+                             int32_t n_workers, int64_t d, float *out, void *stream) {
+    if (n_workers < 1) return fail(EFS_EINVAL, "sparse_accumulate: n_workers=%d < 1", n_workers);
+    if (d < 0 || d > kMaxLen) return fail(EFS_EINVAL, "sparse_accumulate: d=%lld outside [0, 2^31-1]", (long long)d);
+    if (idx == nullptr || val == nullptr || caps == nullptr)
+        return fail(EFS_EINVAL, "sparse_accumulate: idx, val and caps must be host arrays");
+    if (d > 0 && (out == nullptr || !aligned(out, 16)))
+        return fail(EFS_EINVAL, "sparse_accumulate: out must be non-NULL and 16-byte aligned");
+    for (int32_t w = 0; w < n_workers; ++w) {
+        if (caps[w] < 0 || caps[w] > kMaxLen)
+            return fail(EFS_EINVAL, "sparse_accumulate: caps[%d]=%lld outside [0, 2^31-1]", w, (long long)caps[w]);
+        if (caps[w] > 0 && (idx[w] == nullptr || val[w] == nullptr))
+            return fail(EFS_EINVAL, "sparse_accumulate: payload %d has a NULL pointer", w);
+        if (!aligned(idx[w], 4) || !aligned(val[w], 4))
+            return fail(EFS_EINVAL, "sparse_accumulate: payload %d is not 4-byte aligned", w);
+        if (counts != nullptr && counts[w] != nullptr && !aligned(counts[w], 4))
+            return fail(EFS_EINVAL, "sparse_accumulate: count %d is not 4-byte aligned", w);
+    }
+    return check_launch(efs::launch_accumulate(idx, val, counts, caps, n_workers, d, out,
+                                               static_cast<hipStream_t>(stream)),
+                        "sparse_accumulate");
+}
+
+efs_status efs_copy_probe(const float *src, float *dst, int64_t n, void *stream) {
+    if (n < 0) return fail(EFS_EINVAL, "efs_copy_probe: n < 0");
+    if (n > 0 && (src == nullptr || dst == nullptr || !aligned(src, 16) || !aligned(dst, 16)))
+        return fail(EFS_EINVAL, "efs_copy_probe: src and dst must be non-NULL and 16-byte aligned");
+    return check_launch(efs::launch_copy(src, dst, n, static_cast<hipStream_t>(stream)),
+                        "efs_copy_probe");
+}
+
+}  // extern "C"

@@ -1,0 +1,101 @@
+// Exchange-and-average of n workers' sparse payloads on one device
+// (Algorithm 1: the average (1/n) sum_i Delta_i of the compressed updates).
+//
+//   zero     out = +0 (16-byte stores)
+//   scatter  one launch per worker, in worker order: out[i] += v for every
+//            (i, v) of that payload.  Indices are distinct within a payload,
+//            so no two lanes of one launch touch the same coordinate and no
+//            atomics are needed; stream order between launches fixes the
+//            summation order, so the result is the same on every run.
+//   scale    out = out / n (IEEE division), skipped for n == 1.
+//
+// Also the streaming copy probe used to measure the bandwidth ceiling.
+#include "device_common.hpp"
+#include "launch.hpp"
+
+namespace efs {
+
+namespace {
+
+__global__ __launch_bounds__(kBlock) void fill_zero_kernel(float *__restrict__ out, int64_t d) {
+    const int64_t stride = int64_t(gridDim.x) * kBlock;
+    const int64_t nvec = d / 4;
+    f32x4 *o4 = reinterpret_cast<f32x4 *>(out);
+    const f32x4 z = {0.0f, 0.0f, 0.0f, 0.0f};
+    for (int64_t v = int64_t(blockIdx.x) * kBlock + threadIdx.x; v < nvec; v += stride) o4[v] = z;
+    const int64_t t = nvec * 4 + int64_t(blockIdx.x) * kBlock + threadIdx.x;
+    if (blockIdx.x == 0 && t < d) out[t] = 0.0f;
+}
+
+__global__ __launch_bounds__(kBlock) void scatter_add_kernel(const int32_t *__restrict__ idx,
+                                                             const float *__restrict__ val,
+                                                             const uint32_t *__restrict__ count,
+                                                             int64_t cap, int64_t d,
+                                                             float *__restrict__ out) {
+    int64_t n = cap;
+    if (count != nullptr) n = min(int64_t(*count), cap);
+    const int64_t stride = int64_t(gridDim.x) * kBlock;
+    for (int64_t j = int64_t(blockIdx.x) * kBlock + threadIdx.x; j < n; j += stride) {
+        const int32_t i = idx[j];
+        if (i >= 0 && int64_t(i) < d) out[i] = __fadd_rn(out[i], val[j]);
+    }
+}
+
+__global__ __launch_bounds__(kBlock) void scale_kernel(float *__restrict__ out, int64_t d,
+                                                       float n) {
+    const int64_t stride = int64_t(gridDim.x) * kBlock;
+    const int64_t nvec = d / 4;
+    f32x4 *o4 = reinterpret_cast<f32x4 *>(out);
+    for (int64_t v = int64_t(blockIdx.x) * kBlock + threadIdx.x; v < nvec; v += stride) {
+        f32x4 x = o4[v];
+#pragma unroll
+        for (int c = 0; c < 4; ++c) x[c] = __fdiv_rn(x[c], n);
+        o4[v] = x;
+    }
+    const int64_t t = nvec * 4 + int64_t(blockIdx.x) * kBlock + threadIdx.x;
+    if (blockIdx.x == 0 && t < d) out[t] = __fdiv_rn(out[t], n);
+}
+
+__global__ __launch_bounds__(kBlock) void copy_kernel(const f32x4 *__restrict__ src,
+                                                      f32x4 *__restrict__ dst, int64_t nvec,
+                                                      const float *__restrict__ src_s,
+                                                      float *__restrict__ dst_s, int64_t n) {
+    const int64_t stride = int64_t(gridDim.x) * kBlock;
+    for (int64_t v = int64_t(blockIdx.x) * kBlock + threadIdx.x; v < nvec; v += stride)
+        dst[v] = __builtin_nontemporal_load(src + v);
+    const int64_t t = nvec * 4 + int64_t(blockIdx.x) * kBlock + threadIdx.x;
+    if (blockIdx.x == 0 && t < n) dst_s[t] = src_s[t];
+}
+
+uint32_t stream_grid(int64_t nvec) {
+    return persistent_grid((nvec + int64_t(kBlock) * 4 - 1) / (int64_t(kBlock) * 4));
+}
+
+}  // namespace
+
+hipError_t launch_accumulate(const int32_t *const *idx, const float *const *val,
+                             const uint32_t *const *counts, const int64_t *caps,
+                             int32_t n, int64_t d, float *out, hipStream_t stream) {
+    // The dense passes use 16-byte accesses; `out` is required to be 16-byte
+    // aligned by the ABI layer.
+    const uint32_t dense_grid = stream_grid(d / 4 + 1);
+    fill_zero_kernel<<<dense_grid, kBlock, 0, stream>>>(out, d);
+    for (int32_t w = 0; w < n; ++w) {
+        const int64_t cap = caps[w];
+        if (cap <= 0) continue;
+        const uint32_t grid = persistent_grid((cap + kTile - 1) / kTile);
+        const uint32_t *cnt = counts != nullptr ? counts[w] : nullptr;
+        scatter_add_kernel<<<grid, kBlock, 0, stream>>>(idx[w], val[w], cnt, cap, d, out);
+    }
+    if (n > 1) scale_kernel<<<dense_grid, kBlock, 0, stream>>>(out, d, float(n));
+    return hipGetLastError();
+}
+
+hipError_t launch_copy(const float *src, float *dst, int64_t n, hipStream_t stream) {
+    const int64_t nvec = n / 4;
+    copy_kernel<<<stream_grid(nvec + 1), kBlock, 0, stream>>>(
+        reinterpret_cast<const f32x4 *>(src), reinterpret_cast<f32x4 *>(dst), nvec, src, dst, n);
+    return hipGetLastError();
+}
+
+}  // namespace efs

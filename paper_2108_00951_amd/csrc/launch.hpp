@@ -1,0 +1,29 @@
+// Host-side launchers of the efsparse kernels.  Arguments arrive here
+// already validated by the C ABI layer (abi.cpp).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace efs {
+
+hipError_t launch_ht(const float *g, float *e, int64_t d, float lr, float lambda,
+                     int32_t *idx, float *val, int64_t cap, uint32_t *counter,
+                     hipStream_t stream);
+
+size_t topk_workspace_size(int64_t d);
+hipError_t launch_topk(const float *g, float *e, int64_t d, float lr, int64_t k,
+                       int32_t *idx, float *val, void *workspace, hipStream_t stream);
+
+hipError_t launch_accumulate(const int32_t *const *idx, const float *const *val,
+                             const uint32_t *const *counts, const int64_t *caps,
+                             int32_t n, int64_t d, float *out, hipStream_t stream);
+
+hipError_t launch_copy(const float *src, float *dst, int64_t n, hipStream_t stream);
+
+// Workgroups for a grid-stride pass over `work_tiles` tiles: enough to fill
+// every compute unit several times over, never more than there is work.
+uint32_t persistent_grid(int64_t work_tiles);
+
+}  // namespace efs

@@ -1,0 +1,121 @@
+"""The C-ABI library on the host: it loads, exports every symbol that
+include/efsparse.h declares, and rejects invalid arguments before touching a
+device (no compute calls are made here)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2108_00951_amd import binding
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "efsparse.h")
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(binding.LIB_PATH):
+        pytest.fail("libefsparse.so is not built (run __graft_entry__.build())")
+    return binding.declare(ctypes.CDLL(binding.LIB_PATH))
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    names = re.findall(r"^\s*(?:const\s+)?[a-z_0-9]+\s*\*?\s*([a-z_0-9]+)\s*\(", text, flags=re.M)
+    return sorted(set(names))
+
+
+def test_header_declares_the_boundary():
+    names = declared_functions()
+    for want in ("ht_compress", "topk_compress", "topk_workspace_bytes", "sparse_accumulate"):
+        assert want in names
+
+
+def test_every_declared_symbol_is_exported(lib):
+    for name in declared_functions():
+        assert hasattr(lib, name), name
+
+
+def test_status_strings(lib):
+    assert lib.efs_status_string(0) == b"ok"
+    assert lib.efs_status_string(1) == b"invalid argument"
+    assert lib.efs_status_string(2) == b"workspace too small"
+
+
+NULL = None
+
+
+def test_ht_rejects_bad_arguments(lib):
+    fake = 0x10000  # never dereferenced: validation fails first
+    cases = [
+        dict(d=-1),
+        dict(d=2 ** 31),
+        dict(g=NULL),
+        dict(g=fake + 2),
+        dict(lr=float("nan")),
+        dict(lr=float("inf")),
+        dict(lam=float("nan")),
+        dict(lam=-1.0),
+        dict(cap=-1),
+        dict(idx=NULL),
+        dict(counter=NULL),
+        dict(counter=fake + 4),
+    ]
+    for over in cases:
+        a = dict(g=fake, e=fake, d=100, lr=0.1, lam=1e-3, idx=fake, val=fake, cap=10,
+                 counter=fake)
+        a.update(over)
+        rc = lib.ht_compress(a["g"], a["e"], a["d"], a["lr"], a["lam"], a["idx"], a["val"],
+                             a["cap"], a["counter"], None)
+        assert rc == binding.EFS_EINVAL, over
+        assert lib.efs_last_error_message()
+
+
+def test_topk_rejects_bad_arguments(lib):
+    fake = 0x10000
+    need = lib.topk_workspace_bytes(1000, 10)
+    assert need >= 256 + 16384
+    cases = [
+        (dict(k=-1), binding.EFS_EINVAL),
+        (dict(k=1001), binding.EFS_EINVAL),
+        (dict(d=-5), binding.EFS_EINVAL),
+        (dict(e=NULL), binding.EFS_EINVAL),
+        (dict(ws=NULL), binding.EFS_EINVAL),
+        (dict(ws=fake + 8), binding.EFS_EINVAL),
+        (dict(ws_bytes=need - 1), binding.EFS_ESPACE),
+        (dict(idx=NULL), binding.EFS_EINVAL),
+        (dict(lr=float("nan")), binding.EFS_EINVAL),
+    ]
+    for over, want in cases:
+        a = dict(g=fake, e=fake, d=1000, lr=0.1, k=10, idx=fake, val=fake, ws=fake,
+                 ws_bytes=need)
+        a.update(over)
+        rc = lib.topk_compress(a["g"], a["e"], a["d"], a["lr"], a["k"], a["idx"], a["val"],
+                               a["ws"], a["ws_bytes"], None)
+        assert rc == want, over
+
+
+def test_accumulate_rejects_bad_arguments(lib):
+    vp = ctypes.c_void_p
+    fake = 0x10000
+    idx = (vp * 2)(fake, fake)
+    val = (vp * 2)(fake, fake)
+    caps = (ctypes.c_int64 * 2)(5, 5)
+    assert lib.sparse_accumulate(idx, val, None, caps, 0, 10, fake, None) == binding.EFS_EINVAL
+    assert lib.sparse_accumulate(idx, val, None, caps, 2, -1, fake, None) == binding.EFS_EINVAL
+    assert lib.sparse_accumulate(idx, val, None, caps, 2, 10, fake + 4, None) == binding.EFS_EINVAL
+    bad = (ctypes.c_int64 * 2)(5, -1)
+    assert lib.sparse_accumulate(idx, val, None, bad, 2, 10, fake, None) == binding.EFS_EINVAL
+    nul = (vp * 2)(fake, None)
+    assert lib.sparse_accumulate(nul, val, None, caps, 2, 10, fake, None) == binding.EFS_EINVAL
+    assert lib.efs_copy_probe(fake + 4, fake, 8, None) == binding.EFS_EINVAL
+
+
+def test_workspace_size_grows_with_tiles(lib):
+    a = lib.topk_workspace_bytes(4096, 1)
+    b = lib.topk_workspace_bytes(4096 * 1000, 1)
+    assert b - a >= 4 * 999 - 255
+    assert lib.topk_workspace_bytes(-1, 1) == 0
+    assert lib.topk_workspace_bytes(1_500_000_000, 1_500_000) % 256 == 0

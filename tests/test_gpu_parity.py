@@ -1,0 +1,317 @@
+"""GPU parity: the HIP path through the C ABI against the CPU oracle, element
+by element, at sizes that span many 4096-element tiles and ragged tails,
+plus the edge cases of the method.  Bit-exact throughout: indices, counts,
+values and residuals are integer or copy results of one fp32 mul and add
+that both sides round the same way; the average is an in-order fp32 sum
+divided once, bit-exact as well (the 1e-6 relative bound is never needed).
+"""
+import numpy as np
+import pytest
+
+import oracle
+from paper_2108_00951_amd import synth
+from tests._checks import (assert_bits_equal, assert_payload_equal, bits, canonical,
+                           check_topk_properties)
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+from paper_2108_00951_amd import binding as efs  # noqa: E402
+
+LR = np.float32(0.1)
+DEV = "cuda"
+
+
+def say(*a):
+    print(*a, flush=True)
+
+
+def to_dev(a, unaligned=False):
+    """Copy a host array to the device; unaligned=True offsets it by one
+    element so the 16-byte vector path is not taken."""
+    a = np.ascontiguousarray(a)
+    if not unaligned:
+        return torch.from_numpy(a).to(DEV)
+    buf = torch.empty(a.size + 1, dtype=torch.from_numpy(a[:0]).dtype, device=DEV)
+    v = buf[1:]
+    v.copy_(torch.from_numpy(a))
+    return v
+
+
+class HT:
+    """One worker's hard-threshold EF state on the device."""
+
+    def __init__(self, d, cap=None, unaligned=False):
+        self.d = d
+        self.cap = d if cap is None else cap
+        self.e = to_dev(np.zeros(d, dtype=np.float32), unaligned)
+        self.idx = torch.empty(max(self.cap, 1), dtype=torch.int32, device=DEV)[:self.cap]
+        self.val = torch.empty(max(self.cap, 1), dtype=torch.float32, device=DEV)[:self.cap]
+        self.ctr = efs.new_counter(DEV)
+        self.unaligned = unaligned
+
+    def step(self, g_host, lam, lr=LR):
+        g = to_dev(g_host, self.unaligned)
+        efs.ht_compress(g, self.e, lr, lam, self.idx, self.val, self.ctr)
+        k = efs.counter_value(self.ctr)
+        n = min(k, self.cap)
+        return self.idx[:n].cpu().numpy(), self.val[:n].cpu().numpy(), self.e.cpu().numpy(), k
+
+
+def topk_gpu(g_host, e_host, k, lr=LR, unaligned=False):
+    d = g_host.size
+    g = to_dev(g_host, unaligned)
+    e = to_dev(e_host, unaligned)
+    idx = torch.empty(max(k, 1), dtype=torch.int32, device=DEV)[:k]
+    val = torch.empty(max(k, 1), dtype=torch.float32, device=DEV)[:k]
+    ws = efs.new_topk_workspace(d, k, DEV)
+    efs.topk_compress(g, e, lr, k, idx, val, ws)
+    return idx.cpu().numpy(), val.cpu().numpy(), e.cpu().numpy()
+
+
+SIZES = [1, 3, 63, 64, 65, 1023, 4095, 4096, 4097, 8191, 12_289, 100_003, 1_000_000]
+
+
+@pytest.mark.parametrize("unaligned", [False, True])
+@pytest.mark.parametrize("d", SIZES)
+def test_ht_ef_loop_matches_oracle(d, unaligned):
+    say("ht parity d=%d unaligned=%s" % (d, unaligned))
+    gs = [synth.small_gradient(10 + t, d) for t in range(3)]
+    lam = synth.calibrate_lambda(gs[0], 0.01)
+    st = HT(d, unaligned=unaligned)
+    e_ref = np.zeros(d, dtype=np.float32)
+    for t in range(3):
+        gi, gv, ge, gk = st.step(gs[t], lam)
+        ri, rv, e_ref, rk = oracle.ht(gs[t], e_ref, LR, lam)
+        assert gk == rk
+        assert_payload_equal(gi, gv, ri, rv, "t=%d" % t)
+        assert_bits_equal(ge, e_ref, "e' t=%d" % t)
+
+
+def test_ht_lambda_zero_and_infinity():
+    d = 70_001
+    g = synth.small_gradient(1, d)
+    g[17] = np.float32(-0.0)
+    st = HT(d)
+    gi, gv, ge, gk = st.step(g, 0.0)
+    ri, rv, re, rk = oracle.ht(g, np.zeros(d, np.float32), LR, 0.0)
+    assert gk == rk == d
+    assert_payload_equal(gi, gv, ri, rv)
+    assert np.all(bits(ge) == 0)
+    st = HT(d)
+    gi, gv, ge, gk = st.step(g, np.inf)
+    assert gk == 0
+    assert_bits_equal(ge, oracle.ht(g, np.zeros(d, np.float32), LR, np.inf)[2])
+
+
+def test_ht_special_values():
+    d = 4099
+    g = synth.small_gradient(2, d)
+    e = np.zeros(d, dtype=np.float32)
+    g[0], g[1], g[2], g[3] = np.nan, np.inf, -np.inf, np.float32(-0.0)
+    e[4] = np.frombuffer(np.uint32(7).tobytes(), dtype=np.float32)[0]   # subnormal
+    g[4] = 0.0
+    e[5] = np.frombuffer(np.uint32(0x807FFFFF).tobytes(), dtype=np.float32)[0]
+    g[5] = 0.0
+    lam = np.frombuffer(np.uint32(6).tobytes(), dtype=np.float32)[0]
+    for lam_ in (lam, np.float32(1e-4)):
+        st = HT(d)
+        st.e.copy_(torch.from_numpy(e))
+        gi, gv, ge, gk = st.step(g, lam_)
+        ri, rv, re, rk = oracle.ht(g, e, LR, lam_)
+        assert gk == rk
+        assert_payload_equal(gi, gv, ri, rv)
+        assert_bits_equal(ge, re)
+
+
+def test_ht_empty_vector():
+    st = HT(0, cap=0)
+    st.ctr.fill_(0)
+    st.ctr[0] = 12345
+    gi, gv, ge, gk = st.step(np.zeros(0, np.float32), 1e-3)
+    assert gk == 0 and gi.size == 0
+
+
+def test_ht_capacity_overflow():
+    d = 300_007
+    g = synth.small_gradient(3, d)
+    lam = synth.calibrate_lambda(g, 0.05)
+    cap = 1000
+    st = HT(d, cap=cap)
+    gi, gv, ge, gk = st.step(g, lam)
+    ri, rv, re, rk = oracle.ht(g, np.zeros(d, np.float32), LR, lam)
+    assert gk == rk > cap
+    assert gi.size == cap
+    # the cap written pairs are distinct members of the true payload
+    ci, cv = canonical(gi, gv)
+    assert np.all(np.diff(ci) > 0)
+    pos = np.searchsorted(ri, ci)
+    assert np.all(ri[pos] == ci)
+    assert_bits_equal(cv, rv[pos])
+    assert_bits_equal(ge, re)
+
+
+def test_ht_counter_returns_to_zero_between_calls():
+    st = HT(200_000)
+    for t, d in enumerate([200_000, 5, 4096 * 7 + 1, 0, 123_457]):
+        g = synth.small_gradient(40 + t, d)
+        e = torch.zeros(d, dtype=torch.float32, device=DEV)
+        efs.ht_compress(to_dev(g), e, LR, np.float32(1e-4), st.idx, st.val, st.ctr)
+        words = st.ctr.cpu().numpy()
+        assert words[2] == 0 and words[3] == 0
+        assert words[0] == oracle.ht(g, np.zeros(d, np.float32), LR, np.float32(1e-4))[3]
+
+
+def test_ht_repeat_is_deterministic():
+    d = 1_000_000
+    g = synth.small_gradient(5, d)
+    lam = synth.calibrate_lambda(g, 0.02)
+    outs = []
+    for _ in range(3):
+        st = HT(d)
+        gi, gv, ge, gk = st.step(g, lam)
+        outs.append((canonical(gi, gv), bits(ge).copy(), gk))
+    for o in outs[1:]:
+        assert o[2] == outs[0][2]
+        np.testing.assert_array_equal(o[0][0], outs[0][0][0])
+        np.testing.assert_array_equal(bits(o[0][1]), bits(outs[0][0][1]))
+        np.testing.assert_array_equal(o[1], outs[0][1])
+
+
+# ---------------------------------------------------------------------------
+# Top-k
+# ---------------------------------------------------------------------------
+
+TOPK_CASES = [(1, 1), (5, 3), (64, 64), (4097, 1), (4097, 4096), (12_289, 100),
+              (100_003, 1000), (100_003, 50_001), (1_000_000, 1000), (1_000_000, 10_000)]
+
+
+@pytest.mark.parametrize("unaligned", [False, True])
+@pytest.mark.parametrize("d,k", TOPK_CASES)
+def test_topk_matches_oracle(d, k, unaligned):
+    say("topk parity d=%d k=%d unaligned=%s" % (d, k, unaligned))
+    g = synth.small_gradient(60, d)
+    e = synth.small_gradient(61, d, scale=1e-4)
+    gi, gv, ge = topk_gpu(g, e, k, unaligned=unaligned)
+    ri, rv, re = oracle.topk(g, e, LR, k)
+    assert_payload_equal(gi, gv, ri, rv)
+    assert_bits_equal(ge, re)
+
+
+@pytest.mark.parametrize("d,k", [(10, 0), (100_000, 0), (100_000, 100_000), (4096, 4096)])
+def test_topk_keep_none_or_all(d, k):
+    g = synth.small_gradient(62, d)
+    e = np.zeros(d, dtype=np.float32)
+    gi, gv, ge = topk_gpu(g, e, k)
+    ri, rv, re = oracle.topk(g, e, LR, k)
+    assert_payload_equal(gi, gv, ri, rv)
+    assert_bits_equal(ge, re)
+
+
+@pytest.mark.parametrize("levels", [3, 41, 1001])
+@pytest.mark.parametrize("k", [1, 777, 5000, 33_333])
+def test_topk_ties_go_to_lower_index(levels, k):
+    # quantised gradients: thousands of exact ties at the k-th magnitude
+    d = 60_011
+    rng = np.random.default_rng(levels * 7 + k)
+    g = (rng.integers(-levels, levels + 1, size=d).astype(np.float32) * np.float32(1e-3))
+    e = np.zeros(d, dtype=np.float32)
+    gi, gv, ge = topk_gpu(g, e, k)
+    ri, rv, re = oracle.topk(g, e, LR, k)
+    assert_payload_equal(gi, gv, ri, rv, "levels=%d k=%d" % (levels, k))
+    assert_bits_equal(ge, re)
+
+
+def test_topk_all_equal_and_zero_vectors():
+    d = 50_000
+    for g in (np.full(d, 0.25, np.float32), np.zeros(d, np.float32),
+              np.where(np.arange(d) % 2 == 0, np.float32(-0.0), np.float32(0.0)).astype(np.float32)):
+        for k in (1, 12_345, d - 1):
+            gi, gv, ge = topk_gpu(g, np.zeros(d, np.float32), k)
+            ri, rv, re = oracle.topk(g, np.zeros(d, np.float32), LR, k)
+            assert_payload_equal(gi, gv, ri, rv)
+            assert_bits_equal(ge, re)
+
+
+def test_topk_special_values():
+    d = 9000
+    g = synth.small_gradient(63, d)
+    g[[5, 700, 4500]] = [np.nan, np.inf, -np.inf]
+    e = np.zeros(d, dtype=np.float32)
+    e[8] = np.frombuffer(np.uint32(3).tobytes(), dtype=np.float32)[0]
+    for k in (1, 2, 3, 4, 100, d):
+        gi, gv, ge = topk_gpu(g, e, k)
+        ri, rv, re = oracle.topk(g, e, LR, k)
+        assert_payload_equal(gi, gv, ri, rv, "k=%d" % k)
+        assert_bits_equal(ge, re)
+
+
+def test_topk_ef_loop_properties():
+    # five EF iterations with e carried on the device, checked each step
+    d, k = 2_000_003, 2000
+    g0 = synth.small_gradient(70, d)
+    e_dev = torch.zeros(d, dtype=torch.float32, device=DEV)
+    ws = efs.new_topk_workspace(d, k, DEV)
+    idx = torch.empty(k, dtype=torch.int32, device=DEV)
+    val = torch.empty(k, dtype=torch.float32, device=DEV)
+    e_host = np.zeros(d, dtype=np.float32)
+    for t in range(5):
+        g = synth.small_gradient(70 + t, d) if t else g0
+        acc = oracle.ht(g, e_host, LR, np.inf)[2]
+        efs.topk_compress(to_dev(g), e_dev, LR, k, idx, val, ws)
+        e_host = e_dev.cpu().numpy()
+        check_topk_properties(acc, k, idx.cpu().numpy(), val.cpu().numpy(), e_host)
+
+
+# ---------------------------------------------------------------------------
+# n-worker average
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("n", [1, 2, 3, 8])
+def test_accumulate_matches_oracle(n):
+    d = 400_009
+    lam = np.float32(2.2e-4)
+    payloads_dev, payloads_ref = [], []
+    for w in range(n):
+        g = synth.small_gradient(80 + w, d)
+        st = HT(d, cap=d // 10)
+        gi, gv, ge, gk = st.step(g, lam)
+        assert gk <= st.cap
+        payloads_dev.append((st.idx, st.val, st.ctr))
+        payloads_ref.append((gi, gv))
+    out = torch.empty(d, dtype=torch.float32, device=DEV)
+    efs.sparse_accumulate(payloads_dev, d, out)
+    ref = oracle.accumulate(payloads_ref, d)
+    assert_bits_equal(out.cpu().numpy(), ref)
+
+
+def test_accumulate_topk_payloads_and_tail():
+    d = 4096 * 3 + 3
+    ps_dev, ps_ref = [], []
+    for w in range(3):
+        g = synth.small_gradient(90 + w, d)
+        gi, gv, _ = topk_gpu(g, np.zeros(d, np.float32), 500)
+        ps_dev.append((to_dev(gi), to_dev(gv)))
+        ps_ref.append((gi, gv))
+    out = torch.empty(d, dtype=torch.float32, device=DEV)
+    efs.sparse_accumulate(ps_dev, d, out)
+    assert_bits_equal(out.cpu().numpy(), oracle.accumulate(ps_ref, d))
+
+
+def test_accumulate_ignores_out_of_range_indices():
+    d = 1000
+    idx = np.array([3, -1, 999, 1000, 7], dtype=np.int32)
+    val = np.array([1.0, 5.0, 2.0, 6.0, 3.0], dtype=np.float32)
+    out = torch.empty(d, dtype=torch.float32, device=DEV)
+    efs.sparse_accumulate([(to_dev(idx), to_dev(val)), (to_dev(idx[:1]), to_dev(val[:1]))], d, out)
+    keep = (idx >= 0) & (idx < d)
+    ref = oracle.accumulate([(idx[keep], val[keep]), (idx[:1], val[:1])], d)
+    assert_bits_equal(out.cpu().numpy(), ref)
+
+
+def test_copy_probe_copies():
+    for n in (0, 3, 4096 * 5 + 2):
+        src = torch.arange(n, dtype=torch.float32, device=DEV)
+        dst = torch.zeros(n, dtype=torch.float32, device=DEV)
+        efs.copy_probe(src, dst)
+        assert torch.equal(src, dst)
