@@ -8,12 +8,22 @@ log-uniform in [1e-5, 1e-2], lr = 0.1):
     average         sparse_accumulate of the hard-threshold payload (n = 1)
 Gradients rotate through a pool larger than the 256 MB Infinity Cache, so
 every step reads them from HBM; the error vectors are carried from step to
-step as in training.
+step as in training.  Inputs are resident on the device before timing.
 
-Prints one JSON line (rank 0).  value = gradient elements compressed per
-second over the whole step (2 d per step: d by each compressor).
+Prints one JSON line.  value = gradient elements compressed per second over
+the whole step (2 d per step: d by each compressor).
+
+The roofline entry is for the hard-threshold kernel: algorithmic bytes
+(12 per element + 8 per kept pair) over its launch duration, from HIP events
+around back-to-back launches (the per-step events also include the dispatch
+gaps between the step's kernels).  --traffic takes the counter-derived HBM
+bytes per launch written by --parse-pmc from two rocprofv3 --pmc runs of this
+script (FETCH_SIZE, then WRITE_SIZE), scaled by what the same counters read
+for the copy probe of known size.
 """
 import argparse
+import csv
+import glob
 import json
 import os
 import sys
@@ -24,6 +34,36 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBPS = 8000.0
+HT_KERNEL = "ht_fused_kernel"
+COPY_KERNEL = "copy_kernel"
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "ht_fused_kernel_segments_25.6m_pmc.txt")
+HT_SOURCES = ["ht.hip", "device_common.hpp", "launch.hpp"]
+
+
+def kernel_source_digest():
+    """sha256 over the sources that determine the hard-threshold kernel."""
+    import hashlib
+    h = hashlib.sha256()
+    for name in HT_SOURCES:
+        with open(os.path.join(ROOT, "paper_2108_00951_amd", "csrc", name), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
+def read_traffic(path):
+    """Counter-derived bytes per launch, or None when the file is absent or
+    was taken from a different version of the kernel sources."""
+    if not path or not os.path.exists(path):
+        return None
+    fields = {}
+    with open(path) as f:
+        for line in f:
+            parts = line.split()
+            if len(parts) == 2 and not line.startswith("#"):
+                fields[parts[0]] = parts[1]
+    if fields.get("kernel_source_sha256") != kernel_source_digest():
+        return None
+    return int(float(fields["ht_bytes_per_launch"]))
 
 
 def parse():
@@ -32,12 +72,63 @@ def parse():
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--pool", type=int, default=4, help="distinct gradients in the rotation")
+    ap.add_argument("--b2b", type=int, default=20,
+                    help="back-to-back launches timed for the kernel roofline")
     ap.add_argument("--cpu-steps", type=int, default=2,
                     help="steps of the CPU oracle for the baseline (0 to skip)")
-    ap.add_argument("--traffic", type=str, default=None,
-                    help="JSON file with counter-derived HBM bytes per launch of the "
-                         "hard-threshold kernel")
+    ap.add_argument("--traffic", type=str, default=TRAFFIC_FILE,
+                    help="summary written by --parse-pmc (HBM bytes per hard-threshold launch)")
+    ap.add_argument("--parse-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
+                    help="summarise two rocprofv3 --pmc output folders and exit")
     return ap.parse_args()
+
+
+def _pmc_rows(folder, counter):
+    """(kernel name, value) of every dispatch in a rocprofv3 counter CSV."""
+    rows = []
+    for path in glob.glob(os.path.join(folder, "**", "*counter_collection.csv"), recursive=True):
+        with open(path) as f:
+            for r in csv.DictReader(f):
+                if r.get("Counter_Name") == counter:
+                    rows.append((r["Kernel_Name"], float(r["Counter_Value"])))
+    return rows
+
+
+def parse_pmc(fetch_dir, write_dir, d):
+    """HBM bytes per launch of the hard-threshold kernel, scaled by the copy probe.
+
+    FETCH_SIZE and WRITE_SIZE are in KiB per dispatch.  The copy probe moves
+    exactly 4n bytes in and 4n bytes out (n = d); the ratio of those bytes to
+    what the counters report for it is the scale applied to the kernel."""
+    out = {}
+    for name, folder in (("FETCH_SIZE", fetch_dir), ("WRITE_SIZE", write_dir)):
+        rows = _pmc_rows(folder, name)
+        ht = [v for k, v in rows if HT_KERNEL in k]
+        cp = [v for k, v in rows if COPY_KERNEL in k]
+        if not ht or not cp:
+            raise SystemExit("no %s rows for %s / %s in %s" % (name, HT_KERNEL, COPY_KERNEL, folder))
+        ht_b = 1024.0 * sum(ht) / len(ht)
+        cp_b = 1024.0 * sum(cp) / len(cp)
+        scale = 4.0 * d / cp_b
+        out[name] = {"ht_kib_per_launch": ht_b / 1024, "copy_kib_per_launch": cp_b / 1024,
+                     "copy_expected_kib": 4.0 * d / 1024, "scale": scale,
+                     "ht_bytes_scaled": ht_b * scale, "launches": len(ht)}
+    out["ht_bytes_per_launch"] = out["FETCH_SIZE"]["ht_bytes_scaled"] + out["WRITE_SIZE"]["ht_bytes_scaled"]
+    return out
+
+
+def format_traffic(res):
+    lines = ["# HBM traffic of %s per launch from rocprofv3 counters" % HT_KERNEL,
+             "# (KiB per dispatch, averaged over the kernel's dispatches; each counter",
+             "# scaled by expected/measured for %s moving 4*d bytes each way)" % COPY_KERNEL]
+    for name in ("FETCH_SIZE", "WRITE_SIZE"):
+        r = res[name]
+        lines.append("# %s: kernel %.1f KiB, copy probe %.1f KiB (expected %.1f), scale %.5f, "
+                     "%d launches" % (name, r["ht_kib_per_launch"], r["copy_kib_per_launch"],
+                                      r["copy_expected_kib"], r["scale"], r["launches"]))
+    lines.append("ht_bytes_per_launch %d" % round(res["ht_bytes_per_launch"]))
+    lines.append("kernel_source_sha256 %s" % kernel_source_digest())
+    return "\n".join(lines) + "\n"
 
 
 def main():
@@ -48,17 +139,23 @@ def main():
         sys.exit(2)
 
     import numpy as np
+
+    from paper_2108_00951_amd import synth
+
+    wl = synth.WORKLOADS[2]
+    d, k, density = wl.d, wl.topk_k[0], wl.densities[0]
+    if args.parse_pmc:
+        sys.stdout.write(format_traffic(parse_pmc(args.parse_pmc[0], args.parse_pmc[1], d)))
+        return
+
     import torch
 
     from paper_2108_00951_amd import binding as efs
-    from paper_2108_00951_amd import synth
 
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     efs.load_library()
 
-    wl = synth.WORKLOADS[2]
-    d, k, density = wl.d, wl.topk_k[0], wl.densities[0]
     lr = synth.LR
     stream = synth.Stream(2)
     t0 = time.time()
@@ -70,7 +167,7 @@ def main():
 
     e_ht = torch.zeros(d, dtype=torch.float32, device=dev)
     e_tk = torch.zeros(d, dtype=torch.float32, device=dev)
-    cap = d // 50
+    cap = d   # k_t grows under error feedback with a fixed lambda; never truncate
     idx = torch.empty(cap, dtype=torch.int32, device=dev)
     val = torch.empty(cap, dtype=torch.float32, device=dev)
     ctr = efs.new_counter(dev)
@@ -80,46 +177,74 @@ def main():
     out = torch.empty(d, dtype=torch.float32, device=dev)
     cur = torch.cuda.current_stream()
 
-    def step(s, ev=None):
+    def ev():
+        return torch.cuda.Event(enable_timing=True)
+
+    def step(s, evs=None):
         g = pool[s % len(pool)]
-        if ev is not None:
-            ev[0].record(cur)
+        if evs is not None:
+            evs[0].record(cur)
         efs.ht_compress(g, e_ht, lr, lam, idx, val, ctr)
-        if ev is not None:
-            ev[1].record(cur)
+        if evs is not None:
+            evs[1].record(cur)
         efs.topk_compress(g, e_tk, lr, k, tidx, tval, ws)
-        if ev is not None:
-            ev[2].record(cur)
+        if evs is not None:
+            evs[2].record(cur)
         efs.sparse_accumulate([(idx, val, ctr)], d, out)
-        if ev is not None:
-            ev[3].record(cur)
+        if evs is not None:
+            evs[3].record(cur)
 
     for s in range(args.warmup):
         step(s)
     torch.cuda.synchronize()
-    kt_first = efs.counter_value(ctr)
-    if kt_first > cap:
-        raise RuntimeError("payload capacity exceeded: k_t=%d cap=%d" % (kt_first, cap))
+    e_ht_start = e_ht.clone()
 
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
-    begin = torch.cuda.Event(enable_timing=True)
-    end = torch.cuda.Event(enable_timing=True)
+    # ---- timed region: K whole steps -------------------------------------
+    evs = [[ev() for _ in range(4)] for _ in range(args.steps)]
+    begin, end = ev(), ev()
     torch.cuda.synchronize()
     begin.record(cur)
     for s in range(args.steps):
         step(args.warmup + s, evs[s])
     end.record(cur)
     torch.cuda.synchronize()
-    kt_last = efs.counter_value(ctr)
-    if kt_last > cap:
-        raise RuntimeError("payload capacity exceeded: k_t=%d cap=%d" % (kt_last, cap))
+    e_ht_end = e_ht.clone()
+
+    # k_t of every timed step, from a deterministic replay of the
+    # hard-threshold calls (same inputs, same starting e).
+    e_ht.copy_(e_ht_start)
+    kts = []
+    for s in range(args.steps):
+        efs.ht_compress(pool[(args.warmup + s) % len(pool)], e_ht, lr, lam, idx, val, ctr)
+        kts.append(efs.counter_value(ctr))
+
+    # ---- kernel durations: back-to-back launches -------------------------
+    # Hard threshold continuing the EF trajectory from the end of the timed
+    # region, then the copy probe on the same number of elements.
+    e_ht.copy_(e_ht_end)
+    a, b = ev(), ev()
+    torch.cuda.synchronize()
+    a.record(cur)
+    for s in range(args.b2b):
+        efs.ht_compress(pool[s % len(pool)], e_ht, lr, lam, idx, val, ctr)
+    b.record(cur)
+    torch.cuda.synchronize()
+    ht_b2b_us = a.elapsed_time(b) * 1e3 / args.b2b
+    kt_b2b = efs.counter_value(ctr)
+    a, b = ev(), ev()
+    a.record(cur)
+    for s in range(args.b2b):
+        efs.copy_probe(pool[s % len(pool)], out)
+    b.record(cur)
+    torch.cuda.synchronize()
+    copy_us = a.elapsed_time(b) * 1e3 / args.b2b
 
     total_ms = begin.elapsed_time(end)
     ms_step = total_ms / args.steps
-    ht_ms = [ev[0].elapsed_time(ev[1]) for ev in evs]
-    tk_ms = [ev[1].elapsed_time(ev[2]) for ev in evs]
-    ac_ms = [ev[2].elapsed_time(ev[3]) for ev in evs]
-    kt = 0.5 * (kt_first + kt_last)
+    ht_ms = [x[0].elapsed_time(x[1]) for x in evs]
+    tk_ms = [x[1].elapsed_time(x[2]) for x in evs]
+    ac_ms = [x[2].elapsed_time(x[3]) for x in evs]
+    kt = float(np.mean(kts))
 
     def stats(xs):
         a = np.sort(np.asarray(xs))
@@ -129,18 +254,16 @@ def main():
                 "p90_us": round(float(a[int(0.9 * (a.size - 1))]) * 1e3, 2)}
 
     ht_bytes = 12.0 * d + 8.0 * kt
+    ht_bytes_b2b = 12.0 * d + 8.0 * kt_b2b
     tk_bytes_ideal = 12.0 * d + 8.0 * k
     tk_bytes_twolook = 16.0 * d + 8.0 * k
     ac_bytes = 4.0 * d + 8.0 * kt
     ht_s = float(np.mean(ht_ms)) / 1e3
     tk_s = float(np.mean(tk_ms)) / 1e3
     ac_s = float(np.mean(ac_ms)) / 1e3
-    ht_gbps = ht_bytes / ht_s / 1e9
+    roof_gbps = ht_bytes_b2b / (ht_b2b_us * 1e-6) / 1e9
 
-    traffic = None
-    if args.traffic and os.path.exists(args.traffic):
-        with open(args.traffic) as f:
-            traffic = json.load(f).get("ht_bytes_per_launch")
+    traffic = read_traffic(args.traffic)
 
     line = {
         "metric": "G grad-elements/s compressed (hard-threshold, Top-k) + achieved HBM GB/s",
@@ -164,17 +287,23 @@ def main():
         },
         "hbm_gbps_step": round((ht_bytes + tk_bytes_twolook + ac_bytes) / (ms_step / 1e3) / 1e9, 1),
         "roofline": {
-            "kernel": "ht_fused_kernel",
+            "kernel": HT_KERNEL,
             "bound": "hbm",
-            "achieved": round(ht_gbps, 1),
+            "achieved": round(roof_gbps, 1),
             "peak": HBM_PEAK_GBPS,
             "unit": "GB/s",
-            "frac": round(ht_gbps / HBM_PEAK_GBPS, 4),
+            "frac": round(roof_gbps / HBM_PEAK_GBPS, 4),
             "traffic": traffic,
+            "launch_us": round(ht_b2b_us, 2),
+            "bytes_per_launch": ht_bytes_b2b,
+            "k_t": kt_b2b,
         },
+        "copy_probe": {"us": round(copy_us, 2), "gbps": round(8.0 * d / (copy_us * 1e-6) / 1e9, 1),
+                       "bytes": 8.0 * d},
         "ops": {
             "ht_compress": dict(stats(ht_ms), gelem_s=round(d / ht_s / 1e9, 2),
-                                gbps=round(ht_gbps, 1), bytes=ht_bytes, k_t=kt),
+                                gbps=round(ht_bytes / ht_s / 1e9, 1), k_t_mean=kt,
+                                k_t_first=kts[0], k_t_last=kts[-1]),
             "topk_compress": dict(stats(tk_ms), gelem_s=round(d / tk_s / 1e9, 2),
                                   gbps_ideal=round(tk_bytes_ideal / tk_s / 1e9, 1),
                                   gbps_twolook=round(tk_bytes_twolook / tk_s / 1e9, 1)),
@@ -191,6 +320,7 @@ def main():
 def cpu_baseline(pool_host, d, k, lam, lr, steps):
     """The CPU oracle (single-threaded C, as written) on the same step."""
     import numpy as np
+
     import oracle
 
     e_ht = np.zeros(d, dtype=np.float32)

@@ -39,7 +39,7 @@ int g_cu_count[64];  // per device; 0 = not queried yet
 
 namespace efs {
 
-uint32_t persistent_grid(int64_t work_tiles) {
+int device_cu_count() {
     int dev = 0;
     int cus = 256;
     if (hipGetDevice(&dev) == hipSuccess && dev >= 0 && dev < 64) {
@@ -53,7 +53,18 @@ uint32_t persistent_grid(int64_t work_tiles) {
         }
         cus = g_cu_count[dev];
     }
-    const int64_t cap = int64_t(cus) * 8;
+    return cus;
+}
+
+uint32_t balanced_grid(int64_t work_tiles, int workgroups_per_cu) {
+    if (work_tiles < 1) work_tiles = 1;
+    const int64_t resident = int64_t(device_cu_count()) * workgroups_per_cu;
+    const int64_t per_wg = (work_tiles + resident - 1) / resident;
+    return uint32_t((work_tiles + per_wg - 1) / per_wg);
+}
+
+uint32_t persistent_grid(int64_t work_tiles) {
+    const int64_t cap = int64_t(device_cu_count()) * 8;
     if (work_tiles < 1) work_tiles = 1;
     return uint32_t(work_tiles < cap ? work_tiles : cap);
 }

@@ -56,15 +56,26 @@ __global__ __launch_bounds__(kBlock) void scale_kernel(float *__restrict__ out, 
     if (blockIdx.x == 0 && t < d) out[t] = __fdiv_rn(out[t], n);
 }
 
-__global__ __launch_bounds__(kBlock) void copy_kernel(const f32x4 *__restrict__ src,
-                                                      f32x4 *__restrict__ dst, int64_t nvec,
-                                                      const float *__restrict__ src_s,
-                                                      float *__restrict__ dst_s, int64_t n) {
-    const int64_t stride = int64_t(gridDim.x) * kBlock;
-    for (int64_t v = int64_t(blockIdx.x) * kBlock + threadIdx.x; v < nvec; v += stride)
-        dst[v] = __builtin_nontemporal_load(src + v);
-    const int64_t t = nvec * 4 + int64_t(blockIdx.x) * kBlock + threadIdx.x;
-    if (blockIdx.x == 0 && t < n) dst_s[t] = src_s[t];
+// Same tile shape and grid sizing as the hard-threshold kernel: four 16-byte
+// loads per thread in flight, then four stores.
+__global__ __launch_bounds__(kBlock) void copy_kernel(const float *__restrict__ src,
+                                                      float *__restrict__ dst, int64_t n,
+                                                      uint32_t ntiles) {
+    const int tid = threadIdx.x;
+    for (uint32_t tile = blockIdx.x; tile < ntiles; tile += gridDim.x) {
+        const int64_t tile0 = int64_t(tile) * kTile;
+        if (tile0 + kTile <= n) {
+            const f32x4 *s4 = reinterpret_cast<const f32x4 *>(src + tile0);
+            f32x4 *d4 = reinterpret_cast<f32x4 *>(dst + tile0);
+            f32x4 v[kVecPerThread];
+#pragma unroll
+            for (int j = 0; j < kVecPerThread; ++j) v[j] = __builtin_nontemporal_load(s4 + j * kBlock + tid);
+#pragma unroll
+            for (int j = 0; j < kVecPerThread; ++j) d4[j * kBlock + tid] = v[j];
+        } else {
+            for (int64_t i = tile0 + tid; i < n; i += kBlock) dst[i] = src[i];
+        }
+    }
 }
 
 uint32_t stream_grid(int64_t nvec) {
@@ -92,9 +103,9 @@ hipError_t launch_accumulate(const int32_t *const *idx, const float *const *val,
 }
 
 hipError_t launch_copy(const float *src, float *dst, int64_t n, hipStream_t stream) {
-    const int64_t nvec = n / 4;
-    copy_kernel<<<stream_grid(nvec + 1), kBlock, 0, stream>>>(
-        reinterpret_cast<const f32x4 *>(src), reinterpret_cast<f32x4 *>(dst), nvec, src, dst, n);
+    const int64_t tiles = n > 0 ? (n + kTile - 1) / kTile : 1;
+    copy_kernel<<<balanced_grid(tiles, kHtWorkgroupsPerCU), kBlock, 0, stream>>>(src, dst, n,
+                                                                               uint32_t(tiles));
     return hipGetLastError();
 }
 

@@ -15,8 +15,8 @@ constexpr int kVecPerThread = 4;         // float4 per thread per tile
 constexpr int kTile = kBlock * kVecPerThread * 4;   // 4096 elements per tile
 
 // Counter word layout used for single-launch stream compaction: the low 40
-// bits accumulate the number of emitted pairs, the high 24 bits count tiles
-// that have reserved their slice (a ticket, so the last tile is known).
+// bits accumulate the number of emitted pairs, the high 24 bits count
+// workgroups that have finished (a ticket, so the last one is known).
 constexpr int kTicketShift = 40;
 constexpr uint64_t kCountMask = (uint64_t(1) << kTicketShift) - 1;
 constexpr uint64_t kTicketOne = uint64_t(1) << kTicketShift;
@@ -72,23 +72,47 @@ __device__ __forceinline__ uint32_t block_prefix_small(uint32_t c, uint32_t *s_w
     return pre + off;
 }
 
-__device__ __forceinline__ uint32_t atomic_load_u32(const uint32_t *p) {
-    return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
+// Workgroup-local staging of (index, value) pairs in LDS.  Kept pairs of
+// successive tiles are appended here and written to the global payload in
+// coalesced runs, one atomic per flush instead of one per tile.
+struct PairStage {
+    int32_t idx[kTile];
+    float val[kTile];
+    uint32_t wave[kWaves];
+    unsigned long long base;
+};
 
-// Last-workgroup election.  Every thread fences its own global writes
-// (release), the block synchronises, one thread takes a ticket; the block
-// holding the last ticket fences again (acquire) before reading what the
-// other blocks produced.  Returns true in all threads of the last block.
-__device__ __forceinline__ bool last_block_done(uint32_t *ticket, uint32_t nblocks,
-                                                uint32_t *s_flag) {
-    __threadfence();
+// Flushes the `fill` staged pairs to payload slots reserved by one atomic on
+// `word`.  With `last` the workgroup also takes its ticket; the workgroup
+// holding the final ticket (all others have added their pairs by then)
+// publishes the total to *count when count is non-null, and returns `word`
+// to zero for the next call.  Slots at or past `cap` are not written.
+// Called by every thread of the workgroup; contains barriers.
+__device__ __forceinline__ void stage_flush(PairStage &st, uint32_t fill, bool last,
+                                            unsigned long long *word, uint32_t *count,
+                                            uint64_t cap, int32_t *__restrict__ idx,
+                                            float *__restrict__ val) {
     __syncthreads();
-    if (threadIdx.x == 0) *s_flag = (atomicAdd(ticket, 1u) == nblocks - 1u) ? 1u : 0u;
+    if (threadIdx.x == 0) {
+        const uint64_t add = (last ? kTicketOne : 0ull) | fill;
+        const uint64_t old = add ? atomicAdd(word, (unsigned long long)add) : 0ull;
+        const uint64_t base = old & kCountMask;
+        if (last && (old >> kTicketShift) == uint64_t(gridDim.x - 1)) {
+            if (count != nullptr) *count = uint32_t(base + fill);
+            __hip_atomic_store(word, 0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
+        st.base = base;
+    }
     __syncthreads();
-    const bool last = *s_flag != 0u;
-    if (last) __threadfence();
-    return last;
+    const uint64_t base = st.base;
+    for (uint32_t j = threadIdx.x; j < fill; j += kBlock) {
+        const uint64_t o = base + j;
+        if (o < cap) {
+            idx[o] = st.idx[j];
+            val[o] = st.val[j];
+        }
+    }
+    __syncthreads();
 }
 
 }  // namespace efs

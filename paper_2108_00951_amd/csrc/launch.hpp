@@ -26,4 +26,17 @@ hipError_t launch_copy(const float *src, float *dst, int64_t n, hipStream_t stre
 // every compute unit several times over, never more than there is work.
 uint32_t persistent_grid(int64_t work_tiles);
 
+// Resident workgroups per compute unit assumed by the grid sizing below:
+// the hard-threshold pass (two 4-wave workgroups per CU measured fastest),
+// other kernels staging pairs in LDS (33 KiB each), histogram / scan passes.
+constexpr int kHtWorkgroupsPerCU = 2;
+constexpr int kStageWorkgroupsPerCU = 4;
+constexpr int kScanWorkgroupsPerCU = 8;
+
+// Grid for a grid-stride pass in which every workgroup stays resident: the
+// fewest tiles per workgroup that the resident workgroups allow, and just
+// enough workgroups to cover the tiles at that count (so no workgroup does
+// more than one tile beyond any other).
+uint32_t balanced_grid(int64_t work_tiles, int workgroups_per_cu);
+
 }  // namespace efs

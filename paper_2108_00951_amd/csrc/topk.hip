@@ -5,22 +5,26 @@
 // ranked larger first and, on equal keys, lower index first.  The k-th key T
 // is found by radix select over three digits (bits 30..20, 19..10, 9..0); the
 // paper notes radix select costs O(ceil(b/r) d) (section 1), here b = 31 and
-// r = 11/10/10.  Passes:
+// r = 11/10/10.  Launches, all on the caller's stream:
 //
 //   reset    zero the control block and histograms (one workgroup).
 //   pass1    p = e + lr*g, written into e (12 B/element); workgroup-local LDS
-//            histogram of the top digit, merged into global bins; the last
-//            workgroup picks the bin holding rank k.
-//   refine   (x2) read p (4 B/element); histogram the next digit of the keys
-//            that match the known prefix; the last workgroup narrows the
-//            prefix.  After the second refine T is exact, with G = #(key > T)
-//            and m = k - G of the `ties` keys equal to T to keep.
-//   ties     only when 0 < m < ties: per-tile counts of key == T and their
-//            exclusive scan, so every tied element knows its rank in index
-//            order (an early return otherwise).
+//            histogram of the top digit, merged into global bins.
+//   select   (one workgroup) the bin holding rank k, i.e. the next digit of T.
+//   refine   (x2, each followed by select) read p (4 B/element); histogram
+//            the next digit of the keys that match the known prefix.  After
+//            the third select T is exact, with G = #(key > T) and m = k - G
+//            of the `ties` keys equal to T to keep.
+//   ties     only when 0 < m < ties: per-tile counts of key == T, then their
+//            exclusive scan (one workgroup), so every tied element knows its
+//            rank in index order (both return at once otherwise).
 //   emit     read p (4 B/element); keep key > T and the tied elements whose
-//            rank is below m; compact the k pairs (ballot prefix sums, one
-//            atomic per tile) and zero e at the kept coordinates.
+//            rank is below m; compact the k pairs (ballot prefix sums into an
+//            LDS stage, one atomic per flush) and zero e at the kept
+//            coordinates.
+//
+// Workgroups exchange data only through global atomics and kernel
+// boundaries; no kernel waits on another workgroup.
 //
 // Workspace (all offsets 256-byte aligned):
 //   [0, 256)                  TopkCtl
@@ -44,9 +48,9 @@ struct TopkCtl {
     uint32_t m;          // tied elements (key == T) to keep
     uint32_t ties;       // elements with key == T
     uint32_t tie_mode;   // 1 when 0 < m < ties (rank ties by index)
-    uint32_t done[4];    // last-workgroup tickets: pass1, refine x2, ties
-    uint32_t pad[6];
-    unsigned long long emit;  // compaction word: tile tickets << 40 | pairs
+    uint32_t emitted;    // pairs emitted by the last call (equals k)
+    uint32_t pad[9];
+    unsigned long long emit;  // compaction word: workgroup tickets << 40 | pairs
 };
 static_assert(sizeof(TopkCtl) <= 256, "control block must fit its slot");
 
@@ -126,7 +130,7 @@ __device__ void select_bin(const uint32_t *hist, uint32_t need, uint32_t *s_scan
     uint32_t tot = 0;
 #pragma unroll
     for (int i = 0; i < kPer; ++i) {
-        c[i] = atomic_load_u32(hist + (kBins - 1 - (t * kPer + i)));
+        c[i] = hist[kBins - 1 - (t * kPer + i)];
         tot += c[i];
     }
     s_scan[t] = tot;
@@ -169,8 +173,6 @@ __global__ __launch_bounds__(kBlock) void topk_pass1_kernel(const float *__restr
                                                             float lr, uint32_t ntiles,
                                                             Workspace ws) {
     __shared__ uint32_t h[kBins1];
-    __shared__ uint32_t s_scan[kBlock];
-    __shared__ uint32_t s_sel[4];
     const int tid = threadIdx.x;
     for (int b = tid; b < kBins1; b += kBlock) h[b] = 0u;
     __syncthreads();
@@ -214,14 +216,6 @@ __global__ __launch_bounds__(kBlock) void topk_pass1_kernel(const float *__restr
     __syncthreads();
     for (int b = tid; b < kBins1; b += kBlock)
         if (h[b]) atomicAdd(ws.hist1 + b, h[b]);
-
-    if (!last_block_done(&ws.ctl->done[0], gridDim.x, &s_sel[3])) return;
-    const uint32_t need = ws.ctl->need;
-    select_bin<kBins1>(ws.hist1, need, s_scan, s_sel);
-    if (tid == 0) {
-        ws.ctl->prefix = s_sel[0];
-        ws.ctl->need = need - s_sel[1];
-    }
 }
 
 // Refinement pass: histogram of bits [kShift, kShift+10) over the keys whose
@@ -232,11 +226,8 @@ __global__ __launch_bounds__(kBlock) void topk_refine_kernel(const float *__rest
                                                              Workspace ws) {
     constexpr int kBins = 1024;
     __shared__ uint32_t h[kBins];
-    __shared__ uint32_t s_scan[kBlock];
-    __shared__ uint32_t s_sel[4];
     const int tid = threadIdx.x;
     uint32_t *hist = kShift == 10 ? ws.hist2 : ws.hist3;
-    uint32_t *ticket = &ws.ctl->done[kShift == 10 ? 1 : 2];
     for (int b = tid; b < kBins; b += kBlock) h[b] = 0u;
     const uint32_t prefix = ws.ctl->prefix;
     __syncthreads();
@@ -259,23 +250,32 @@ __global__ __launch_bounds__(kBlock) void topk_refine_kernel(const float *__rest
     __syncthreads();
     for (int b = tid; b < kBins; b += kBlock)
         if (h[b]) atomicAdd(hist + b, h[b]);
+}
 
-    if (!last_block_done(ticket, gridDim.x, &s_sel[3])) return;
+// One workgroup: picks the bin of the histogram of pass kPass (1, 2, 3) that
+// holds rank `need`, and narrows the threshold prefix.  After pass 3 the
+// threshold key T, the tie count and the number m of ties to keep are known.
+template <int kPass>
+__global__ __launch_bounds__(kBlock) void topk_select_kernel(Workspace ws) {
+    __shared__ uint32_t s_scan[kBlock];
+    __shared__ uint32_t s_sel[4];
     const uint32_t need = ws.ctl->need;
-    select_bin<kBins>(hist, need, s_scan, s_sel);
-    if (tid == 0) {
-        const uint32_t np = (prefix << 10) | s_sel[0];
-        if (kShift == 10) {
-            ws.ctl->prefix = np;
-            ws.ctl->need = need - s_sel[1];
-        } else {
-            const uint32_t m = need - s_sel[1];
-            ws.ctl->prefix = np;
-            ws.ctl->T = np;
-            ws.ctl->m = m;
-            ws.ctl->ties = s_sel[2];
-            ws.ctl->tie_mode = m < s_sel[2] ? 1u : 0u;
-        }
+    const uint32_t prefix = ws.ctl->prefix;
+    if (kPass == 1)
+        select_bin<kBins1>(ws.hist1, need, s_scan, s_sel);
+    else
+        select_bin<1024>(kPass == 2 ? ws.hist2 : ws.hist3, need, s_scan, s_sel);
+    if (threadIdx.x != 0) return;
+    const uint32_t np = kPass == 1 ? s_sel[0] : ((prefix << 10) | s_sel[0]);
+    ws.ctl->prefix = np;
+    if (kPass < 3) {
+        ws.ctl->need = need - s_sel[1];
+    } else {
+        const uint32_t m = need - s_sel[1];
+        ws.ctl->T = np;
+        ws.ctl->m = m;
+        ws.ctl->ties = s_sel[2];
+        ws.ctl->tie_mode = m < s_sel[2] ? 1u : 0u;
     }
 }
 
@@ -286,8 +286,6 @@ __global__ __launch_bounds__(kBlock) void topk_ties_kernel(const float *__restri
                                                            int64_t d, uint32_t ntiles,
                                                            Workspace ws) {
     __shared__ uint32_t s_wave[kWaves];
-    __shared__ uint32_t s_scan[kBlock];
-    __shared__ uint32_t s_flag;
     if (ws.ctl->tie_mode == 0u) return;
     const uint32_t T = ws.ctl->T;
     const int tid = threadIdx.x;
@@ -306,15 +304,19 @@ __global__ __launch_bounds__(kBlock) void topk_ties_kernel(const float *__restri
         block_prefix_small(cnt, s_wave, total);
         if (tid == 0) ws.tile_ties[tile] = total;
     }
-    if (!last_block_done(&ws.ctl->done[3], gridDim.x, &s_flag)) return;
+}
 
-    // Exclusive scan of tile_ties[0..ntiles) by one workgroup: each thread
-    // owns a contiguous chunk.
+// Exclusive scan of tile_ties[0..ntiles) in place by one workgroup; each
+// thread owns a contiguous chunk.
+__global__ __launch_bounds__(kBlock) void topk_ties_scan_kernel(uint32_t ntiles, Workspace ws) {
+    __shared__ uint32_t s_scan[kBlock];
+    if (ws.ctl->tie_mode == 0u) return;
+    const int tid = threadIdx.x;
     const uint32_t chunk = (ntiles + kBlock - 1) / kBlock;
     const uint32_t lo = min(ntiles, tid * chunk);
     const uint32_t hi = min(ntiles, lo + chunk);
     uint32_t sum = 0;
-    for (uint32_t i = lo; i < hi; ++i) sum += atomic_load_u32(ws.tile_ties + i);
+    for (uint32_t i = lo; i < hi; ++i) sum += ws.tile_ties[i];
     s_scan[tid] = sum;
     __syncthreads();
     for (int off = 1; off < kBlock; off <<= 1) {
@@ -335,80 +337,79 @@ template <bool kVector>
 __global__ __launch_bounds__(kBlock) void topk_emit_kernel(float *__restrict__ e, int64_t d,
                                                            int32_t *__restrict__ idx,
                                                            float *__restrict__ val,
-                                                           uint64_t cap, Workspace ws) {
-    __shared__ uint32_t s_wave[kWaves];
-    __shared__ uint64_t s_base;
+                                                           uint64_t cap, uint32_t ntiles,
+                                                           Workspace ws) {
+    __shared__ PairStage st;
     const int tid = threadIdx.x;
-    const uint32_t tile = blockIdx.x;
-    const int64_t tile0 = int64_t(tile) * kTile;
     const uint32_t T = ws.ctl->T;
     const bool tie_mode = ws.ctl->tie_mode != 0u;
+    const uint32_t m = ws.ctl->m;
+    uint32_t fill = 0;
 
-    float v[kVecPerThread][4];
-    uint32_t valid;
-    load_tile<kVector>(e, tile0, d, v, valid);
-    uint32_t keep = 0, tie = 0;
-#pragma unroll
-    for (int j = 0; j < kVecPerThread; ++j) {
-#pragma unroll
-        for (int c = 0; c < 4; ++c) {
-            const int b = 4 * j + c;
-            const uint32_t key = magnitude_key(v[j][c]);
-            const bool ok = (valid >> b) & 1u;
-            keep |= uint32_t(ok && key > T) << b;
-            tie |= uint32_t(ok && key == T) << b;
-        }
-    }
-    if (!tie_mode) {
-        keep |= tie;
-    } else {
-        // Rank of each tied element in index order: earlier tiles, then
-        // earlier vector slots j (all lower indices), then lower threads in
-        // slot j, then lower c within the thread.
-        const uint32_t m = ws.ctl->m;
-        uint32_t rank = ws.tile_ties[tile];
+    for (uint32_t tile = blockIdx.x; tile < ntiles; tile += gridDim.x) {
+        const int64_t tile0 = int64_t(tile) * kTile;
+        float v[kVecPerThread][4];
+        uint32_t valid;
+        load_tile<kVector>(e, tile0, d, v, valid);
+        uint32_t keep = 0, tie = 0;
 #pragma unroll
         for (int j = 0; j < kVecPerThread; ++j) {
-            const uint32_t tj = (tie >> (4 * j)) & 0xfu;
-            uint32_t slot_total;
-            uint32_t r = rank + block_prefix_small(__popc(tj), s_wave, slot_total);
 #pragma unroll
             for (int c = 0; c < 4; ++c) {
-                if ((tj >> c) & 1u) {
-                    keep |= uint32_t(r < m) << (4 * j + c);
-                    ++r;
-                }
+                const int b = 4 * j + c;
+                const uint32_t key = magnitude_key(v[j][c]);
+                const bool ok = (valid >> b) & 1u;
+                keep |= uint32_t(ok && key > T) << b;
+                tie |= uint32_t(ok && key == T) << b;
             }
-            rank += slot_total;
         }
-    }
+        if (!tie_mode) {
+            keep |= tie;
+        } else {
+            // Rank of each tied element in index order: earlier tiles, then
+            // earlier vector slots j (all lower indices), then lower threads
+            // in slot j, then lower c within the thread.
+            uint32_t rank = ws.tile_ties[tile];
+#pragma unroll
+            for (int j = 0; j < kVecPerThread; ++j) {
+                const uint32_t tj = (tie >> (4 * j)) & 0xfu;
+                uint32_t slot_total;
+                uint32_t r = rank + block_prefix_small(__popc(tj), st.wave, slot_total);
+#pragma unroll
+                for (int c = 0; c < 4; ++c) {
+                    if ((tj >> c) & 1u) {
+                        keep |= uint32_t(r < m) << (4 * j + c);
+                        ++r;
+                    }
+                }
+                rank += slot_total;
+            }
+        }
 
-    const uint32_t cnt = __popc(keep);
-    uint32_t total;
-    const uint32_t pos = block_prefix_small(cnt, s_wave, total);
-    if (tid == 0) {
-        const uint64_t old = atomicAdd(&ws.ctl->emit, (unsigned long long)(kTicketOne | total));
-        s_base = old & kCountMask;
-    }
-    __syncthreads();
-    if (cnt) {
-        uint64_t o = s_base + pos;
+        uint32_t total;
+        const uint32_t pos = block_prefix_small(__popc(keep), st.wave, total);
+        if (total == 0) continue;
+        if (fill + total > uint32_t(kTile)) {
+            stage_flush(st, fill, false, &ws.ctl->emit, nullptr, cap, idx, val);
+            fill = 0;
+        }
+        uint32_t o = fill + pos;
 #pragma unroll
         for (int j = 0; j < kVecPerThread; ++j) {
 #pragma unroll
             for (int c = 0; c < 4; ++c) {
                 if ((keep >> (4 * j + c)) & 1u) {
                     const int64_t i = elem_index(tile0, j, c);
-                    if (o < cap) {
-                        idx[o] = int32_t(i);
-                        val[o] = v[j][c];
-                    }
+                    st.idx[o] = int32_t(i);
+                    st.val[o] = v[j][c];
                     e[i] = 0.0f;
                     ++o;
                 }
             }
         }
+        fill += total;
     }
+    stage_flush(st, fill, true, &ws.ctl->emit, &ws.ctl->emitted, cap, idx, val);
 }
 
 }  // namespace
@@ -423,7 +424,8 @@ hipError_t launch_topk(const float *g, float *e, int64_t d, float lr, int64_t k,
                        int32_t *idx, float *val, void *workspace, hipStream_t stream) {
     if (d == 0) return hipSuccess;
     const uint32_t ntiles = uint32_t((d + kTile - 1) / kTile);
-    const uint32_t grid = persistent_grid(ntiles);
+    const uint32_t grid = balanced_grid(ntiles, kScanWorkgroupsPerCU);
+    const uint32_t egrid = balanced_grid(ntiles, kStageWorkgroupsPerCU);
     const Workspace ws = carve(workspace);
     const bool vec = ((reinterpret_cast<uintptr_t>(g) | reinterpret_cast<uintptr_t>(e)) & 15u) == 0;
 
@@ -433,16 +435,23 @@ hipError_t launch_topk(const float *g, float *e, int64_t d, float lr, int64_t k,
     else
         topk_pass1_kernel<false><<<grid, kBlock, 0, stream>>>(g, e, d, lr, ntiles, ws);
     if (k == 0) return hipGetLastError();
+    topk_select_kernel<1><<<1, kBlock, 0, stream>>>(ws);
     if (vec) {
         topk_refine_kernel<true, 10><<<grid, kBlock, 0, stream>>>(e, d, ntiles, ws);
+        topk_select_kernel<2><<<1, kBlock, 0, stream>>>(ws);
         topk_refine_kernel<true, 0><<<grid, kBlock, 0, stream>>>(e, d, ntiles, ws);
+        topk_select_kernel<3><<<1, kBlock, 0, stream>>>(ws);
         topk_ties_kernel<true><<<grid, kBlock, 0, stream>>>(e, d, ntiles, ws);
-        topk_emit_kernel<true><<<ntiles, kBlock, 0, stream>>>(e, d, idx, val, uint64_t(k), ws);
+        topk_ties_scan_kernel<<<1, kBlock, 0, stream>>>(ntiles, ws);
+        topk_emit_kernel<true><<<egrid, kBlock, 0, stream>>>(e, d, idx, val, uint64_t(k), ntiles, ws);
     } else {
         topk_refine_kernel<false, 10><<<grid, kBlock, 0, stream>>>(e, d, ntiles, ws);
+        topk_select_kernel<2><<<1, kBlock, 0, stream>>>(ws);
         topk_refine_kernel<false, 0><<<grid, kBlock, 0, stream>>>(e, d, ntiles, ws);
+        topk_select_kernel<3><<<1, kBlock, 0, stream>>>(ws);
         topk_ties_kernel<false><<<grid, kBlock, 0, stream>>>(e, d, ntiles, ws);
-        topk_emit_kernel<false><<<ntiles, kBlock, 0, stream>>>(e, d, idx, val, uint64_t(k), ws);
+        topk_ties_scan_kernel<<<1, kBlock, 0, stream>>>(ntiles, ws);
+        topk_emit_kernel<false><<<egrid, kBlock, 0, stream>>>(e, d, idx, val, uint64_t(k), ntiles, ws);
     }
     return hipGetLastError();
 }
