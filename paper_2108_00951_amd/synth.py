@@ -119,51 +119,49 @@ class Stream:
             self.scales = (np.float32(1e-4) *
                            segment_scales(w.ident, w.nseg, 0.1, 10.0)).astype(np.float32)
 
-    # -- per-element scale for a range --------------------------------------
-    def _segment_scale(self, start: int, stop: int) -> np.ndarray:
-        seg = np.searchsorted(self.bounds, np.arange(start, stop), side="right") - 1
-        return self.scales[seg]
-
-    def _block(self, worker: int, t: int, b: int) -> np.ndarray:
+    def _fill_block(self, worker: int, t: int, b: int, o: np.ndarray) -> None:
+        """Writes g_{worker,t}[b*BLOCK : b*BLOCK + o.size] into o (in place)."""
         w = self.w
         start = b * BLOCK
-        stop = min(w.d, start + BLOCK)
-        n = stop - start
+        n = o.size
         rng = _rng(w.ident, worker, t, 100 + b)
-        if w.kind == "gauss":
-            return rng.standard_normal(n, dtype=np.float32) * np.float32(1e-3)
-        if w.kind == "segments":
-            z = rng.standard_normal(n, dtype=np.float32)
-            out = z * self._segment_scale(start, stop)
-            if w.n_workers > 1:
-                out += self._worker_shift(worker, b)
-            return out
         if w.kind == "student_t":
-            z = rng.standard_t(3, size=n).astype(np.float32)
-            return z * self._segment_scale(start, stop)
-        if w.kind == "outliers":
-            z = rng.standard_normal(n, dtype=np.float32)
-            big = self._outlier_mask(b)
-            return z * np.where(big, np.float32(0.1), np.float32(1e-3))
-        raise ValueError(w.kind)
+            np.copyto(o, rng.standard_t(3, size=n), casting="same_kind")
+        else:
+            rng.standard_normal(out=o, dtype=np.float32)
+        if w.kind == "gauss":
+            o *= np.float32(1e-3)
+        elif w.kind in ("segments", "student_t"):
+            self._scale_segments(o, start)
+            if w.n_workers > 1:
+                shift = np.empty(n, dtype=np.float32)
+                _rng(w.ident, worker, 0, 1_000_000 + b).standard_normal(out=shift,
+                                                                        dtype=np.float32)
+                shift *= np.float32(1e-4)   # fixed per-worker offset mu_w ~ N(0, 1e-4^2)
+                o += shift
+        elif w.kind == "outliers":
+            # fixed Bernoulli(0.05) set of large-gradient coordinates
+            u = np.empty(n, dtype=np.float32)
+            _rng(w.ident, 0, 0, 2_000_000 + b).random(out=u, dtype=np.float32)
+            big = u < np.float32(0.05)
+            np.multiply(o, np.float32(0.1), out=o, where=big)
+            np.multiply(o, np.float32(1e-3), out=o, where=~big)
+        else:
+            raise ValueError(w.kind)
 
-    def _worker_shift(self, worker: int, b: int) -> np.ndarray:
-        """Fixed per-worker, per-coordinate offset mu_w ~ N(0, 1e-4^2)."""
-        start = b * BLOCK
-        n = min(self.w.d, start + BLOCK) - start
-        rng = _rng(self.w.ident, worker, 0, 1_000_000 + b)
-        return rng.standard_normal(n, dtype=np.float32) * np.float32(1e-4)
-
-    def _outlier_mask(self, b: int) -> np.ndarray:
-        """Fixed Bernoulli(0.05) set of large-gradient coordinates."""
-        start = b * BLOCK
-        n = min(self.w.d, start + BLOCK) - start
-        rng = _rng(self.w.ident, 0, 0, 2_000_000 + b)
-        return rng.random(n, dtype=np.float32) < np.float32(0.05)
+    def _scale_segments(self, o: np.ndarray, start: int) -> None:
+        stop = start + o.size
+        j0 = int(np.searchsorted(self.bounds, start, side="right")) - 1
+        j = j0
+        while j < self.scales.size and self.bounds[j] < stop:
+            lo = max(start, int(self.bounds[j]))
+            hi = min(stop, int(self.bounds[j + 1]))
+            o[lo - start:hi - start] *= self.scales[j]
+            j += 1
 
     def gradient(self, t: int, worker: int = 0, start: int = 0, stop: int | None = None,
-                 out: np.ndarray | None = None) -> np.ndarray:
-        """g_{worker,t}[start:stop] as float32."""
+                 out: np.ndarray | None = None, threads: int = 1) -> np.ndarray:
+        """g_{worker,t}[start:stop] as float32 (blocks drawn by `threads` threads)."""
         d = self.w.d
         stop = d if stop is None else stop
         assert 0 <= start <= stop <= d
@@ -171,12 +169,25 @@ class Stream:
             out = np.empty(stop - start, dtype=np.float32)
         b0 = start // BLOCK
         b1 = (stop + BLOCK - 1) // BLOCK
-        for b in range(b0, b1):
+
+        def one(b):
             bs = b * BLOCK
-            blk = self._block(worker, t, b)
-            lo = max(start, bs)
-            hi = min(stop, bs + blk.size)
-            out[lo - start:hi - start] = blk[lo - bs:hi - bs]
+            be = min(d, bs + BLOCK)
+            lo, hi = max(start, bs), min(stop, be)
+            if lo == bs and hi == be:
+                self._fill_block(worker, t, b, out[lo - start:hi - start])
+            else:
+                tmp = np.empty(be - bs, dtype=np.float32)
+                self._fill_block(worker, t, b, tmp)
+                out[lo - start:hi - start] = tmp[lo - bs:hi - bs]
+
+        if threads > 1 and b1 - b0 > 1:
+            from concurrent.futures import ThreadPoolExecutor
+            with ThreadPoolExecutor(threads) as ex:
+                list(ex.map(one, range(b0, b1)))
+        else:
+            for b in range(b0, b1):
+                one(b)
         return out
 
 
