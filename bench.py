@@ -80,6 +80,9 @@ def parse():
                     help="summary written by --parse-pmc (HBM bytes per hard-threshold launch)")
     ap.add_argument("--parse-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
                     help="summarise two rocprofv3 --pmc output folders and exit")
+    ap.add_argument("--sweep", action="store_true",
+                    help="also time the hard-threshold kernel on the 110e6 Student-t and "
+                         "1.5e9 outlier workloads (adds ~1 min of input generation)")
     return ap.parse_args()
 
 
@@ -159,7 +162,7 @@ def main():
     lr = synth.LR
     stream = synth.Stream(2)
     t0 = time.time()
-    pool_host = [stream.gradient(t) for t in range(args.pool)]
+    pool_host = [stream.gradient(t, threads=16) for t in range(args.pool)]
     lam = synth.calibrate_lambda(pool_host[0], density, lr)
     pool = [torch.from_numpy(g).to(dev) for g in pool_host]
     print("inputs ready: d=%d pool=%d lambda=%.6g k=%d (%.1fs)"
@@ -198,6 +201,7 @@ def main():
         step(s)
     torch.cuda.synchronize()
     e_ht_start = e_ht.clone()
+    e_tk_start = e_tk.clone()
 
     # ---- timed region: K whole steps -------------------------------------
     evs = [[ev() for _ in range(4)] for _ in range(args.steps)]
@@ -217,6 +221,13 @@ def main():
     for s in range(args.steps):
         efs.ht_compress(pool[(args.warmup + s) % len(pool)], e_ht, lr, lam, idx, val, ctr)
         kts.append(efs.counter_value(ctr))
+
+    # Which Top-k selection each timed step took (same replay idea).
+    e_tk.copy_(e_tk_start)
+    bracket_hits = 0
+    for s in range(args.steps):
+        efs.topk_compress(pool[(args.warmup + s) % len(pool)], e_tk, lr, k, tidx, tval, ws)
+        bracket_hits += efs.topk_took_bracket_path(ws)
 
     # ---- kernel durations: back-to-back launches -------------------------
     # Hard threshold continuing the EF trajectory from the end of the timed
@@ -305,6 +316,7 @@ def main():
                                 gbps=round(ht_bytes / ht_s / 1e9, 1), k_t_mean=kt,
                                 k_t_first=kts[0], k_t_last=kts[-1]),
             "topk_compress": dict(stats(tk_ms), gelem_s=round(d / tk_s / 1e9, 2),
+                                  bracket_path_steps=bracket_hits,
                                   gbps_ideal=round(tk_bytes_ideal / tk_s / 1e9, 1),
                                   gbps_twolook=round(tk_bytes_twolook / tk_s / 1e9, 1)),
             "sparse_accumulate": dict(stats(ac_ms),
@@ -312,9 +324,53 @@ def main():
         },
     }
 
+    if args.sweep:
+        del pool, e_tk, out, ws
+        line["ht_sweep"] = ht_sweep(efs, torch, synth, cur, args.b2b)
     if args.cpu_steps > 0:
         line["cpu_baseline"] = cpu_baseline(pool_host, d, k, lam, lr, args.cpu_steps)
     print(json.dumps(line), flush=True)
+
+
+def ht_sweep(efs, torch, synth, cur, reps):
+    """Back-to-back hard-threshold launches on the larger workloads (0.1 %
+    first-step density, e carried), two distinct gradients alternating."""
+    res = {}
+    for wid in (3, 5):
+        st = synth.Stream(wid)
+        d = st.w.d
+        gh = st.gradient(0, threads=16)
+        lam = synth.calibrate_lambda(gh, 0.001)
+        gs = [torch.from_numpy(gh).to("cuda")]
+        del gh
+        gs.append(torch.from_numpy(st.gradient(1, threads=16)).to("cuda"))
+        e = torch.zeros(d, dtype=torch.float32, device="cuda")
+        cap = d // 4
+        idx = torch.empty(cap, dtype=torch.int32, device="cuda")
+        val = torch.empty(cap, dtype=torch.float32, device="cuda")
+        ctr = efs.new_counter("cuda")
+        for s in range(2):
+            efs.ht_compress(gs[s % 2], e, synth.LR, lam, idx, val, ctr)
+        a = torch.cuda.Event(enable_timing=True)
+        b = torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        a.record(cur)
+        for s in range(reps):
+            efs.ht_compress(gs[s % 2], e, synth.LR, lam, idx, val, ctr)
+        b.record(cur)
+        torch.cuda.synchronize()
+        us = a.elapsed_time(b) * 1e3 / reps
+        kt = efs.counter_value(ctr)
+        if kt > cap:
+            raise RuntimeError("sweep payload capacity exceeded")
+        gbps = (12.0 * d + 8.0 * kt) / (us * 1e-6) / 1e9
+        res[st.w.name] = {"d": d, "launch_us": round(us, 2), "k_t": kt,
+                          "gbps": round(gbps, 1), "frac": round(gbps / HBM_PEAK_GBPS, 4),
+                          "gelem_s": round(d / (us * 1e-6) / 1e9, 1)}
+        print("sweep %s: %s" % (st.w.name, res[st.w.name]), file=sys.stderr, flush=True)
+        del gs, e, idx, val
+        torch.cuda.empty_cache()
+    return res
 
 
 def cpu_baseline(pool_host, d, k, lam, lr, steps):

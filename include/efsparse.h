@@ -88,12 +88,23 @@ size_t topk_workspace_bytes(int64_t d, int64_t k);
  *   k             0 <= k <= d.
  *   idx, val      [k] payload of exactly k pairs (unordered).
  *   workspace     device memory of at least topk_workspace_bytes(d, k)
- *                 bytes, 16-byte aligned; contents need no initialisation
- *                 and are clobbered.  Not shareable between concurrent calls.
+ *                 bytes, 16-byte aligned; contents need no initialisation.
+ *                 The library keeps the last threshold in it: a following
+ *                 call on the same workspace whose k-th magnitude lies within
+ *                 about 6 to 12 % of it (the error-feedback case) selects from a
+ *                 small candidate set instead of three more passes over p.
+ *                 Results never depend on what the workspace held.  Not
+ *                 shareable between concurrent calls.
  */
 efs_status topk_compress(const float *g, float *e, int64_t d, float lr, int64_t k,
                          int32_t *idx, float *val, void *workspace,
                          size_t workspace_bytes, void *stream);
+
+/* Byte offset, within a Top-k workspace, of a uint32 that is 1 after a call
+ * that selected from the candidate set around the previous threshold and 0
+ * after one that ran the full radix select (a diagnostic; read it after the
+ * call has completed). */
+size_t topk_path_flag_offset(void);
 
 /* Exchange-and-average of n workers' payloads on one device (Algorithm 1):
  *     out = (sum over w = 0..n-1, in that order, of decompress(payload_w)) / n

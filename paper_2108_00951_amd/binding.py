@@ -55,6 +55,8 @@ def declare(lib):
     lib.ht_compress.restype = ctypes.c_int
     lib.topk_workspace_bytes.argtypes = [i64, i64]
     lib.topk_workspace_bytes.restype = ctypes.c_size_t
+    lib.topk_path_flag_offset.argtypes = []
+    lib.topk_path_flag_offset.restype = ctypes.c_size_t
     lib.topk_compress.argtypes = [vp, vp, i64, f32, i64, vp, vp, vp, ctypes.c_size_t, vp]
     lib.topk_compress.restype = ctypes.c_int
     lib.sparse_accumulate.argtypes = [ctypes.POINTER(vp), ctypes.POINTER(vp), ctypes.POINTER(vp),
@@ -130,6 +132,13 @@ def topk_workspace_bytes(d: int, k: int) -> int:
 def new_topk_workspace(d: int, k: int, device="cuda"):
     import torch
     return torch.empty(max(topk_workspace_bytes(d, k), 1), dtype=torch.uint8, device=device)
+
+
+def topk_took_bracket_path(workspace) -> bool:
+    """True if the last completed topk_compress on this workspace selected
+    from the candidate set around the previous threshold (synchronises)."""
+    off = int(load_library().topk_path_flag_offset())
+    return bool(int(workspace[off:off + 4].cpu().numpy().view("<u4")[0]))
 
 
 def topk_compress(g, e, lr: float, k: int, idx, val, workspace, stream=None) -> None:

@@ -103,10 +103,11 @@ efs_status ht_compress(const float *g, float *e, int64_t d, float lr, float lamb
 }
 
 size_t topk_workspace_bytes(int64_t d, int64_t k) {
-    (void)k;
-    if (d < 0 || d > kMaxLen) return 0;
-    return efs::topk_workspace_size(d);
+    if (d < 0 || d > kMaxLen || k < 0 || k > d) return 0;
+    return efs::topk_workspace_size(d, k);
 }
+
+size_t topk_path_flag_offset(void) { return efs::topk_path_flag_offset(); }
 
 efs_status topk_compress(const float *g, float *e, int64_t d, float lr, int64_t k,
                          int32_t *idx, float *val, void *workspace, size_t workspace_bytes,
@@ -120,9 +121,9 @@ efs_status topk_compress(const float *g, float *e, int64_t d, float lr, int64_t 
     if (!aligned(idx, 4) || !aligned(val, 4)) return fail(EFS_EINVAL, "topk_compress: idx and val must be 4-byte aligned");
     if (d > 0 && (workspace == nullptr || !aligned(workspace, 16)))
         return fail(EFS_EINVAL, "topk_compress: workspace must be non-NULL and 16-byte aligned");
-    if (d > 0 && workspace_bytes < efs::topk_workspace_size(d))
+    if (d > 0 && workspace_bytes < efs::topk_workspace_size(d, k))
         return fail(EFS_ESPACE, "topk_compress: workspace has %zu bytes, needs %zu", workspace_bytes,
-                    efs::topk_workspace_size(d));
+                    efs::topk_workspace_size(d, k));
     return check_launch(efs::launch_topk(g, e, d, lr, k, idx, val, workspace,
                                          static_cast<hipStream_t>(stream)),
                         "topk_compress");

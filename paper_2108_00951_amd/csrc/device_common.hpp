@@ -72,15 +72,31 @@ __device__ __forceinline__ uint32_t block_prefix_small(uint32_t c, uint32_t *s_w
     return pre + off;
 }
 
+// Sum of a per-thread value over the workgroup (every thread gets it).
+// Uses kWaves words of LDS; contains two barriers.
+__device__ __forceinline__ uint32_t block_sum(uint32_t v, uint32_t *s_wave) {
+#pragma unroll
+    for (int off = kWave / 2; off > 0; off >>= 1) v += __shfl_xor(v, off);
+    if ((threadIdx.x & (kWave - 1)) == 0) s_wave[threadIdx.x / kWave] = v;
+    __syncthreads();
+    uint32_t tot = 0;
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) tot += s_wave[w];
+    __syncthreads();
+    return tot;
+}
+
 // Workgroup-local staging of (index, value) pairs in LDS.  Kept pairs of
 // successive tiles are appended here and written to the global payload in
 // coalesced runs, one atomic per flush instead of one per tile.
-struct PairStage {
-    int32_t idx[kTile];
-    float val[kTile];
+template <int N>
+struct PairStageN {
+    int32_t idx[N];
+    float val[N];
     uint32_t wave[kWaves];
     unsigned long long base;
 };
+using PairStage = PairStageN<kTile>;
 
 // Flushes the `fill` staged pairs to payload slots reserved by one atomic on
 // `word`.  With `last` the workgroup also takes its ticket; the workgroup
@@ -88,7 +104,8 @@ struct PairStage {
 // publishes the total to *count when count is non-null, and returns `word`
 // to zero for the next call.  Slots at or past `cap` are not written.
 // Called by every thread of the workgroup; contains barriers.
-__device__ __forceinline__ void stage_flush(PairStage &st, uint32_t fill, bool last,
+template <int N>
+__device__ __forceinline__ void stage_flush(PairStageN<N> &st, uint32_t fill, bool last,
                                             unsigned long long *word, uint32_t *count,
                                             uint64_t cap, int32_t *__restrict__ idx,
                                             float *__restrict__ val) {
@@ -113,6 +130,57 @@ __device__ __forceinline__ void stage_flush(PairStage &st, uint32_t fill, bool l
         }
     }
     __syncthreads();
+}
+
+// Appends the elements of one tile selected by `mask` (bit 4*j + c for
+// element (j, c) of this thread; index tile0 + (j*kBlock + tid)*4 + c, value
+// v[j][c]) to the stage, flushing first when they might not fit.  A tile
+// with more selected elements than the stage holds is written straight to
+// the payload behind its own atomic.  `fill` is identical in all threads.
+// Called by every thread of the workgroup; contains barriers.
+template <int N>
+__device__ __forceinline__ void stage_mask(PairStageN<N> &st, uint32_t &fill, uint32_t mask,
+                                           const float (&v)[kVecPerThread][4], int64_t tile0,
+                                           unsigned long long *word, uint64_t cap,
+                                           int32_t *__restrict__ idx, float *__restrict__ val) {
+    uint32_t total;
+    const uint32_t pos = block_prefix_small(__popc(mask), st.wave, total);
+    if (total == 0) return;
+    const bool direct = total > uint32_t(N);
+    if (direct || fill + total > uint32_t(N)) {
+        stage_flush(st, fill, false, word, nullptr, cap, idx, val);
+        fill = 0;
+    }
+    uint64_t o = fill + pos;
+    if (direct) {
+        // stage_flush ended with a barrier, so st.base is free to reuse
+        if (threadIdx.x == 0) st.base = atomicAdd(word, (unsigned long long)total) & kCountMask;
+        __syncthreads();
+        o += st.base;
+    }
+#pragma unroll
+    for (int j = 0; j < kVecPerThread; ++j) {
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+            if ((mask >> (4 * j + c)) & 1u) {
+                const int32_t i = int32_t(tile0 + int64_t(j * kBlock + int(threadIdx.x)) * 4 + c);
+                if (direct) {
+                    if (o < cap) {
+                        idx[o] = i;
+                        val[o] = v[j][c];
+                    }
+                } else {
+                    st.idx[o] = i;
+                    st.val[o] = v[j][c];
+                }
+                ++o;
+            }
+        }
+    }
+    if (direct)
+        __syncthreads();  // st.base is read above before any later flush rewrites it
+    else
+        fill += total;
 }
 
 }  // namespace efs

@@ -2,34 +2,48 @@
 // per-iteration optimum of Lemma 2).
 //
 // Keys are the 31-bit patterns of |p| (monotone in |p| for non-NaN values),
-// ranked larger first and, on equal keys, lower index first.  The k-th key T
-// is found by radix select over three digits (bits 30..20, 19..10, 9..0); the
-// paper notes radix select costs O(ceil(b/r) d) (section 1), here b = 31 and
-// r = 11/10/10.  Launches, all on the caller's stream:
+// ranked larger first and, on equal keys, lower index first.  Selection is a
+// radix select (the paper notes radix select costs O(ceil(b/r) d), section 1)
+// with a shortcut for error-feedback loops, where the k-th magnitude moves
+// little from one iteration to the next.  Six launches, always all enqueued
+// (work a call does not need returns at once):
 //
-//   reset    zero the control block and histograms (one workgroup).
-//   pass1    p = e + lr*g, written into e (12 B/element); workgroup-local LDS
-//            histogram of the top digit, merged into global bins.
-//   select   (one workgroup) the bin holding rank k, i.e. the next digit of T.
-//   refine   (x2, each followed by select) read p (4 B/element); histogram
-//            the next digit of the keys that match the known prefix.  After
-//            the third select T is exact, with G = #(key > T) and m = k - G
-//            of the `ties` keys equal to T to keep.
-//   ties     only when 0 < m < ties: per-tile counts of key == T, then their
-//            exclusive scan (one workgroup), so every tied element knows its
-//            rank in index order (both return at once otherwise).
-//   emit     read p (4 B/element); keep key > T and the tied elements whose
-//            rank is below m; compact the k pairs (ballot prefix sums into an
-//            LDS stage, one atomic per flush) and zero e at the kept
-//            coordinates.
+//   reset  zero the control block and histograms; form the key bracket
+//          [lo, hi] of 2^21 keys (about 6..12 % in magnitude either side)
+//          around the threshold of the previous call on this workspace.
+//   pass1  p = e + lr*g written into e (12 B/element); LDS histogram of key
+//          bits 30..20; with a bracket, keys above it go straight to the
+//          payload and keys inside it to a candidate buffer (staged
+//          compaction) and into coarse (1024) and fine (2^21) histograms of
+//          key - lo.
+//   step3  every workgroup first decides the path: the bracket path only
+//          when the counts prove the k-th key lies inside the bracket
+//          (#(key > hi) <= k <= #(key >= lo), every bracket key collected).
+//          Bracket path: select T from the coarse then fine histogram, append
+//          the candidates with key > T (all key == T too when no tie is
+//          dropped), zero e at every kept coordinate.  Radix path: select the
+//          top digit from the pass-1 histogram, histogram bits 19..10 of the
+//          keys under that prefix (a 4 B/element read of p).
+//   step4  radix path: select, histogram bits 9..0 (another read of p).
+//   step5  radix path: select the last digit, so T is exact.  Either path,
+//          when ties at T must be split (0 < m < #(key == T)): per-tile
+//          counts of key == T.
+//   emit   radix path: keep key > T and the ties of index rank < m (a read
+//          of p); bracket path: only the ties of rank < m, when some are
+//          dropped.  Tie ranks: exclusive sums of the per-tile counts (each
+//          workgroup sums the tiles before its own), then a block scan in
+//          index order inside the tile.
 //
-// Workgroups exchange data only through global atomics and kernel
-// boundaries; no kernel waits on another workgroup.
+// Selections made by every workgroup read the same histograms, so they agree;
+// workgroup 0 records them in the control block.  Workgroups exchange data
+// only through global atomics and kernel boundaries; none waits on another.
 //
-// Workspace (all offsets 256-byte aligned):
-//   [0, 256)                  TopkCtl
-//   [256, 256 + 16 KiB)       histograms: 2048 + 1024 + 1024 uint32
-//   [.., + 4*ntiles)          per-tile tie counts (exclusive prefix after scan)
+// Workspace (offsets 256-byte aligned):
+//   control block (256 B) | histograms: 2048 + 1024 + 1024 radix bins, 1024
+//   coarse + 2^21 fine bracket bins | per-tile tie counts | candidate buffer
+//   (int32 index, fp32 value) x ccap.
+#include <stddef.h>
+
 #include "device_common.hpp"
 #include "launch.hpp"
 
@@ -40,43 +54,89 @@ namespace {
 constexpr int kBins1 = 2048;  // bits 30..20
 constexpr int kBins2 = 1024;  // bits 19..10
 constexpr int kBins3 = 1024;  // bits 9..0
+constexpr int kCoarse = 1024;
+constexpr int kFineBits = 21;
+constexpr uint32_t kFine = 1u << kFineBits;        // bracket width in keys
+constexpr int kFinePerCoarse = int(kFine) / kCoarse;
+constexpr uint32_t kHintMagic = 0x48494e54u;
+constexpr int kStagePairs = 1024;
+constexpr uint32_t kNoKey = 0xffffffffu;            // larger than every 31-bit key
 
+// Fields are written by workgroup 0 of one launch and read by later
+// launches only, never by other workgroups of the launch that writes them.
 struct TopkCtl {
-    uint32_t prefix;     // known high bits of T (11, then 21, then all 31)
-    uint32_t need;       // elements still to take from the bucket `prefix`
-    uint32_t T;          // threshold key
-    uint32_t m;          // tied elements (key == T) to keep
-    uint32_t ties;       // elements with key == T
-    uint32_t tie_mode;   // 1 when 0 < m < ties (rank ties by index)
-    uint32_t emitted;    // pairs emitted by the last call (equals k)
-    uint32_t pad[9];
-    unsigned long long emit;  // compaction word: workgroup tickets << 40 | pairs
+    uint32_t p1, n1;      // radix path: top digit and the rank left under it (step 3)
+    uint32_t p2, n2;      // radix path: 21-bit prefix and the rank left under it (step 4)
+    uint32_t T;           // threshold key
+    uint32_t m;           // tied elements (key == T) to keep
+    uint32_t ties;        // elements with key == T
+    uint32_t tie_mode;    // 1 when 0 < m < ties
+    uint32_t fast;        // 1: bracket path
+    uint32_t lo, hi;      // bracket of keys
+    uint32_t bracket_on;  // pass 1 collected the bracket
+    uint32_t above;       // bracket path: pairs pass 1 sent (key > hi)
+    uint32_t ncand;       // bracket path: candidates collected
+    uint32_t pad[2];
+    unsigned long long emit;   // pass 1: pairs above the bracket (count in the low bits)
+    unsigned long long cand;   // pass 1: bracket candidates
+    unsigned long long emit2;  // pairs appended after pass 1 (steps 3 and emit)
+    // Kept across calls (not cleared by reset): threshold of the last call.
+    uint32_t hint_key;
+    uint32_t hint_magic;
 };
 static_assert(sizeof(TopkCtl) <= 256, "control block must fit its slot");
+constexpr int kCtlClearWords = offsetof(TopkCtl, hint_key) / 4;
+static_assert(kCtlClearWords <= kBlock, "reset clears the control block with one workgroup");
 
 constexpr size_t kCtlBytes = 256;
-constexpr size_t kHistBytes = sizeof(uint32_t) * (kBins1 + kBins2 + kBins3);
+constexpr size_t kHistWords = kBins1 + kBins2 + kBins3 + kCoarse + size_t(kFine);
+constexpr size_t kHistBytes = sizeof(uint32_t) * kHistWords;
+static_assert(kHistWords % 4 == 0, "histograms are cleared with 16-byte stores");
+
+size_t round256(size_t b) { return (b + 255) & ~size_t(255); }
 
 struct Workspace {
     TopkCtl *ctl;
-    uint32_t *hist1, *hist2, *hist3, *tile_ties;
+    uint32_t *hist1, *hist2, *hist3, *coarse, *fine, *tile_ties;
+    int32_t *cand_idx;
+    float *cand_val;
+    uint32_t ccap;
 };
 
-Workspace carve(void *ws) {
+// Candidate buffer size: the bracket around the k-th magnitude of an
+// error-feedback vector holds several times k keys (about 8k measured on the
+// segmented 25.6e6-element workload), so room for 16k.
+int64_t candidate_capacity(int64_t d, int64_t k) {
+    int64_t c = 16 * k;
+    if (c < 262144) c = 262144;
+    if (c > d) c = d;
+    if (c < 1) c = 1;
+    return c;
+}
+
+Workspace carve(void *ws, int64_t d, int64_t k) {
     char *b = static_cast<char *>(ws);
+    const int64_t tiles = d > 0 ? (d + kTile - 1) / kTile : 1;
     Workspace w;
     w.ctl = reinterpret_cast<TopkCtl *>(b);
     w.hist1 = reinterpret_cast<uint32_t *>(b + kCtlBytes);
     w.hist2 = w.hist1 + kBins1;
     w.hist3 = w.hist2 + kBins2;
-    w.tile_ties = reinterpret_cast<uint32_t *>(b + kCtlBytes + kHistBytes);
+    w.coarse = w.hist3 + kBins3;
+    w.fine = w.coarse + kCoarse;
+    size_t off = kCtlBytes + round256(kHistBytes);
+    w.tile_ties = reinterpret_cast<uint32_t *>(b + off);
+    off += round256(sizeof(uint32_t) * size_t(tiles));
+    w.ccap = uint32_t(candidate_capacity(d, k));
+    w.cand_idx = reinterpret_cast<int32_t *>(b + off);
+    off += round256(sizeof(int32_t) * size_t(w.ccap));
+    w.cand_val = reinterpret_cast<float *>(b + off);
     return w;
 }
 
-// Loads the 16 values element (j, c) of a tile for this thread into v, with
-// the same element map as the hard-threshold kernel:
-//   index = tile0 + (j * kBlock + tid) * 4 + c.
-// Elements past d read as NaN-free zeros and are flagged invalid in `valid`.
+// Loads the 16 values of a tile for this thread (index = tile0 + (j * kBlock
+// + tid) * 4 + c, the hard-threshold kernel's map).  Elements past d read as
+// zero and are cleared in `valid`.
 template <bool kVector>
 __device__ __forceinline__ void load_tile(const float *__restrict__ src, int64_t tile0,
                                           int64_t d, float (&v)[kVecPerThread][4],
@@ -114,8 +174,8 @@ __device__ __forceinline__ int64_t elem_index(int64_t tile0, int j, int c) {
 
 // Called by every thread of one workgroup.  Bins are ranked from the top
 // (highest bin first); finds the bin where the running count first reaches
-// `need` (1 <= need <= sum of bins).  Thread 0 of the owning chunk writes
-// {bin, count above the bin, count in the bin} to s_out.
+// `need` (1 <= need <= sum of bins) and writes {bin, count above the bin,
+// count in the bin} to s_out ({0, 0, 0} if no bin qualifies).
 template <int kBins>
 __device__ void select_bin(const uint32_t *hist, uint32_t need, uint32_t *s_scan,
                            uint32_t *s_out) {
@@ -159,26 +219,59 @@ __device__ void select_bin(const uint32_t *hist, uint32_t need, uint32_t *s_scan
     __syncthreads();
 }
 
-__global__ __launch_bounds__(kBlock) void topk_reset_kernel(TopkCtl *ctl, uint32_t *hist,
-                                                            uint32_t k) {
-    uint32_t *w = reinterpret_cast<uint32_t *>(ctl);
-    for (int i = threadIdx.x; i < int(kCtlBytes / 4); i += kBlock) w[i] = 0u;
-    for (int i = threadIdx.x; i < kBins1 + kBins2 + kBins3; i += kBlock) hist[i] = 0u;
-    if (threadIdx.x == 0) ctl->need = k;
+// Zeroes the control block (except the hint) and every histogram, and forms
+// the bracket from the hint.  Grid-stride over the histogram words.
+__global__ __launch_bounds__(kBlock) void topk_reset_kernel(Workspace ws) {
+    if (blockIdx.x == 0) {
+        uint32_t *w = reinterpret_cast<uint32_t *>(ws.ctl);
+        if (int(threadIdx.x) < kCtlClearWords) w[threadIdx.x] = 0u;
+        __syncthreads();
+        if (threadIdx.x == 0) {
+            TopkCtl *c = ws.ctl;
+            if (c->hint_magic == kHintMagic) {
+                const uint32_t h = c->hint_key & 0x7fffffffu;
+                const uint32_t lo = h > kFine / 2 ? h - kFine / 2 : 0u;
+                c->lo = lo;
+                c->hi = lo + (kFine - 1);
+                c->bracket_on = 1u;
+            }
+        }
+    }
+    f32x4 *h4 = reinterpret_cast<f32x4 *>(ws.hist1);
+    const f32x4 z = {0.0f, 0.0f, 0.0f, 0.0f};
+    const size_t n4 = kHistWords / 4;
+    for (size_t i = size_t(blockIdx.x) * kBlock + threadIdx.x; i < n4;
+         i += size_t(gridDim.x) * kBlock)
+        h4[i] = z;
 }
+
+struct Pass1Shared {
+    uint32_t h[kBins1];
+    uint32_t coarse[kCoarse];
+    PairStageN<kStagePairs> above;   // keys above the bracket -> payload
+    PairStageN<kStagePairs> inside;  // keys in the bracket -> candidates
+};
 
 template <bool kVector>
 __global__ __launch_bounds__(kBlock) void topk_pass1_kernel(const float *__restrict__ g,
                                                             float *__restrict__ e, int64_t d,
-                                                            float lr, uint32_t ntiles,
+                                                            float lr, uint32_t ntiles, uint32_t k,
+                                                            int32_t *__restrict__ idx,
+                                                            float *__restrict__ val,
                                                             Workspace ws) {
-    __shared__ uint32_t h[kBins1];
+    __shared__ Pass1Shared sh;
     const int tid = threadIdx.x;
-    for (int b = tid; b < kBins1; b += kBlock) h[b] = 0u;
+    const bool bracket = ws.ctl->bracket_on != 0u;
+    const uint32_t lo = ws.ctl->lo, hi = ws.ctl->hi;
+    for (int b = tid; b < kBins1; b += kBlock) sh.h[b] = 0u;
+    for (int b = tid; b < kCoarse; b += kBlock) sh.coarse[b] = 0u;
     __syncthreads();
+    uint32_t fill_above = 0, fill_inside = 0;
 
     for (uint32_t tile = blockIdx.x; tile < ntiles; tile += gridDim.x) {
         const int64_t tile0 = int64_t(tile) * kTile;
+        float p[kVecPerThread][4];
+        uint32_t valid;
         if (kVector && tile0 + kTile <= d) {
             const f32x4 *g4 = reinterpret_cast<const f32x4 *>(g + tile0);
             f32x4 *e4 = reinterpret_cast<f32x4 *>(e + tile0);
@@ -190,48 +283,80 @@ __global__ __launch_bounds__(kBlock) void topk_pass1_kernel(const float *__restr
             }
 #pragma unroll
             for (int j = 0; j < kVecPerThread; ++j) {
-                f32x4 p;
+                f32x4 o;
 #pragma unroll
                 for (int c = 0; c < 4; ++c) {
-                    p[c] = ef_accumulate(ev[j][c], lr, gv[j][c]);
-                    atomicAdd(&h[magnitude_key(p[c]) >> 20], 1u);
+                    o[c] = ef_accumulate(ev[j][c], lr, gv[j][c]);
+                    p[j][c] = o[c];
                 }
-                e4[j * kBlock + tid] = p;
+                e4[j * kBlock + tid] = o;
             }
+            valid = 0xffffu;
         } else {
+            valid = 0;
 #pragma unroll
             for (int j = 0; j < kVecPerThread; ++j) {
 #pragma unroll
                 for (int c = 0; c < 4; ++c) {
                     const int64_t i = elem_index(tile0, j, c);
+                    p[j][c] = 0.0f;
                     if (i < d) {
-                        const float p = ef_accumulate(e[i], lr, g[i]);
-                        e[i] = p;
-                        atomicAdd(&h[magnitude_key(p) >> 20], 1u);
+                        p[j][c] = ef_accumulate(e[i], lr, g[i]);
+                        e[i] = p[j][c];
+                        valid |= 1u << (4 * j + c);
                     }
                 }
             }
         }
+        uint32_t m_above = 0, m_inside = 0;
+#pragma unroll
+        for (int j = 0; j < kVecPerThread; ++j) {
+#pragma unroll
+            for (int c = 0; c < 4; ++c) {
+                const int b = 4 * j + c;
+                if ((valid >> b) & 1u) {
+                    const uint32_t key = magnitude_key(p[j][c]);
+                    atomicAdd(&sh.h[key >> 20], 1u);
+                    if (bracket) {
+                        const bool in = key >= lo && key <= hi;
+                        m_above |= uint32_t(key > hi) << b;
+                        m_inside |= uint32_t(in) << b;
+                        if (in) {
+                            atomicAdd(&sh.coarse[(key - lo) / kFinePerCoarse], 1u);
+                            atomicAdd(ws.fine + (key - lo), 1u);
+                        }
+                    }
+                }
+            }
+        }
+        if (bracket) {
+            stage_mask(sh.above, fill_above, m_above, p, tile0, &ws.ctl->emit, k, idx, val);
+            stage_mask(sh.inside, fill_inside, m_inside, p, tile0, &ws.ctl->cand, ws.ccap,
+                       ws.cand_idx, ws.cand_val);
+        }
+    }
+    if (bracket) {
+        stage_flush(sh.above, fill_above, false, &ws.ctl->emit, nullptr, k, idx, val);
+        stage_flush(sh.inside, fill_inside, false, &ws.ctl->cand, nullptr, ws.ccap, ws.cand_idx,
+                    ws.cand_val);
     }
     __syncthreads();
     for (int b = tid; b < kBins1; b += kBlock)
-        if (h[b]) atomicAdd(ws.hist1 + b, h[b]);
+        if (sh.h[b]) atomicAdd(ws.hist1 + b, sh.h[b]);
+    if (bracket)
+        for (int b = tid; b < kCoarse; b += kBlock)
+            if (sh.coarse[b]) atomicAdd(ws.coarse + b, sh.coarse[b]);
 }
 
-// Refinement pass: histogram of bits [kShift, kShift+10) over the keys whose
-// bits above kShift+10 equal the prefix found so far.
+// Radix path: histogram of bits [kShift, kShift+10) over the keys whose
+// higher bits equal `prefix`.
 template <bool kVector, int kShift>
-__global__ __launch_bounds__(kBlock) void topk_refine_kernel(const float *__restrict__ e,
-                                                             int64_t d, uint32_t ntiles,
-                                                             Workspace ws) {
+__device__ void radix_refine(const float *__restrict__ e, int64_t d, uint32_t ntiles,
+                             uint32_t prefix, uint32_t *hist, uint32_t *h) {
     constexpr int kBins = 1024;
-    __shared__ uint32_t h[kBins];
     const int tid = threadIdx.x;
-    uint32_t *hist = kShift == 10 ? ws.hist2 : ws.hist3;
     for (int b = tid; b < kBins; b += kBlock) h[b] = 0u;
-    const uint32_t prefix = ws.ctl->prefix;
     __syncthreads();
-
     for (uint32_t tile = blockIdx.x; tile < ntiles; tile += gridDim.x) {
         const int64_t tile0 = int64_t(tile) * kTile;
         float v[kVecPerThread][4];
@@ -252,43 +377,156 @@ __global__ __launch_bounds__(kBlock) void topk_refine_kernel(const float *__rest
         if (h[b]) atomicAdd(hist + b, h[b]);
 }
 
-// One workgroup: picks the bin of the histogram of pass kPass (1, 2, 3) that
-// holds rank `need`, and narrows the threshold prefix.  After pass 3 the
-// threshold key T, the tie count and the number m of ties to keep are known.
-template <int kPass>
-__global__ __launch_bounds__(kBlock) void topk_select_kernel(Workspace ws) {
-    __shared__ uint32_t s_scan[kBlock];
-    __shared__ uint32_t s_sel[4];
-    const uint32_t need = ws.ctl->need;
-    const uint32_t prefix = ws.ctl->prefix;
-    if (kPass == 1)
-        select_bin<kBins1>(ws.hist1, need, s_scan, s_sel);
-    else
-        select_bin<1024>(kPass == 2 ? ws.hist2 : ws.hist3, need, s_scan, s_sel);
-    if (threadIdx.x != 0) return;
-    const uint32_t np = kPass == 1 ? s_sel[0] : ((prefix << 10) | s_sel[0]);
-    ws.ctl->prefix = np;
-    if (kPass < 3) {
-        ws.ctl->need = need - s_sel[1];
-    } else {
-        const uint32_t m = need - s_sel[1];
-        ws.ctl->T = np;
-        ws.ctl->m = m;
-        ws.ctl->ties = s_sel[2];
-        ws.ctl->tie_mode = m < s_sel[2] ? 1u : 0u;
+// Threshold and tie bookkeeping, written by workgroup 0 once T is exact; T
+// is also kept as the next call's bracket hint.
+__device__ __forceinline__ void set_threshold(TopkCtl *c, uint32_t T, uint32_t m, uint32_t ties) {
+    c->T = T;
+    c->m = m;
+    c->ties = ties;
+    c->tie_mode = m < ties ? 1u : 0u;
+    c->hint_key = T;
+    c->hint_magic = kHintMagic;
+}
+
+struct SelectShared {
+    uint32_t scan[kBlock];
+    uint32_t sel[4];
+};
+
+// Step 3: path decision, then the bracket path's selection and emission or
+// the radix path's second digit histogram.
+template <bool kVector>
+__global__ __launch_bounds__(kBlock) void topk_step3_kernel(float *__restrict__ e, int64_t d,
+                                                            uint32_t ntiles, uint32_t k,
+                                                            int32_t *__restrict__ idx,
+                                                            float *__restrict__ val,
+                                                            Workspace ws) {
+    __shared__ SelectShared ss;
+    __shared__ uint32_t h[1024];
+    __shared__ uint32_t s_wave[kWaves];
+    __shared__ unsigned long long s_base;
+    TopkCtl *c = ws.ctl;
+    const int tid = threadIdx.x;
+    const bool lead = blockIdx.x == 0 && tid == 0;
+    const uint64_t above = c->emit & kCountMask;
+    const uint64_t inside = c->cand & kCountMask;
+    const bool fast = c->bracket_on != 0u && above <= k && above + inside >= k &&
+                      inside <= ws.ccap;
+    if (!fast) {
+        // the pairs pass 1 sent are ignored: the radix path writes the whole
+        // payload from slot 0 in the emit launch
+        select_bin<kBins1>(ws.hist1, k, ss.scan, ss.sel);
+        const uint32_t prefix = ss.sel[0];
+        if (lead) {
+            c->fast = 0u;
+            c->p1 = prefix;
+            c->n1 = k - ss.sel[1];
+        }
+        radix_refine<kVector, 10>(e, d, ntiles, prefix, ws.hist2, h);
+        return;
+    }
+
+    // Bracket path: rank `need` among the candidates, coarse then fine.
+    const uint32_t need = k - uint32_t(above);
+    uint32_t T = kNoKey, m = 0u, ties = 0u;
+    if (need > 0u) {
+        select_bin<kCoarse>(ws.coarse, need, ss.scan, ss.sel);
+        const uint32_t cb = ss.sel[0], above_c = ss.sel[1];
+        __syncthreads();
+        select_bin<kFinePerCoarse>(ws.fine + size_t(cb) * kFinePerCoarse, need - above_c, ss.scan,
+                                   ss.sel);
+        T = c->lo + cb * uint32_t(kFinePerCoarse) + ss.sel[0];
+        m = need - above_c - ss.sel[1];
+        ties = ss.sel[2];
+    }
+    const bool all_ties = m >= ties;
+    if (lead) {
+        c->fast = 1u;
+        c->above = uint32_t(above);
+        c->ncand = uint32_t(inside);
+        if (need > 0u) {
+            set_threshold(c, T, m, ties);
+        } else {  // pass 1 already sent exactly k pairs
+            c->T = kNoKey;
+            c->m = 0u;
+            c->ties = 0u;
+            c->tie_mode = 0u;
+        }
+    }
+    // pairs pass 1 sent: zero their residuals (above <= k, so all were written)
+    for (uint32_t j = blockIdx.x * kBlock + tid; j < uint32_t(above); j += gridDim.x * kBlock)
+        e[idx[j]] = 0.0f;
+    // candidates: one block-wide prefix and one atomic per round
+    const uint32_t n = uint32_t(inside);
+    const uint32_t stride = gridDim.x * kBlock;
+    const uint32_t rounds = (n + stride - 1) / stride;
+    for (uint32_t r = 0; r < rounds; ++r) {
+        const uint32_t j = r * stride + blockIdx.x * kBlock + tid;
+        bool keep = false;
+        int32_t i = 0;
+        float v = 0.0f;
+        if (j < n) {
+            i = ws.cand_idx[j];
+            v = ws.cand_val[j];
+            const uint32_t key = magnitude_key(v);
+            keep = key > T || (all_ties && key == T);
+        }
+        uint32_t total;
+        const uint32_t pos = block_prefix_small(keep ? 1u : 0u, s_wave, total);
+        if (total == 0) continue;
+        if (tid == 0) s_base = atomicAdd(&c->emit2, (unsigned long long)total) & kCountMask;
+        __syncthreads();
+        if (keep) {
+            const uint64_t o = above + s_base + pos;
+            if (o < k) {
+                idx[o] = i;
+                val[o] = v;
+            }
+            e[i] = 0.0f;
+        }
+        __syncthreads();
     }
 }
 
-// Tie ranks (only when some but not all elements tied at T are kept): count
-// key == T per tile, then an exclusive scan over tiles in index order.
+// Step 4 (radix path): select the second digit, histogram bits 9..0.
 template <bool kVector>
-__global__ __launch_bounds__(kBlock) void topk_ties_kernel(const float *__restrict__ e,
-                                                           int64_t d, uint32_t ntiles,
-                                                           Workspace ws) {
+__global__ __launch_bounds__(kBlock) void topk_step4_kernel(const float *__restrict__ e, int64_t d,
+                                                            uint32_t ntiles, Workspace ws) {
+    __shared__ SelectShared ss;
+    __shared__ uint32_t h[1024];
+    TopkCtl *c = ws.ctl;
+    if (c->fast != 0u) return;
+    const uint32_t need = c->n1;
+    select_bin<kBins2>(ws.hist2, need, ss.scan, ss.sel);
+    const uint32_t prefix = (c->p1 << 10) | ss.sel[0];
+    if (blockIdx.x == 0 && threadIdx.x == 0) {
+        c->p2 = prefix;
+        c->n2 = need - ss.sel[1];
+    }
+    radix_refine<kVector, 0>(e, d, ntiles, prefix, ws.hist3, h);
+}
+
+// Step 5: radix path, the last digit (T exact); then, on either path, the
+// per-tile tie counts when ties at T must be split.
+template <bool kVector>
+__global__ __launch_bounds__(kBlock) void topk_step5_kernel(const float *__restrict__ e, int64_t d,
+                                                            uint32_t ntiles, Workspace ws) {
+    __shared__ SelectShared ss;
     __shared__ uint32_t s_wave[kWaves];
-    if (ws.ctl->tie_mode == 0u) return;
-    const uint32_t T = ws.ctl->T;
-    const int tid = threadIdx.x;
+    TopkCtl *c = ws.ctl;
+    uint32_t T, tie_mode;
+    if (c->fast == 0u) {
+        const uint32_t need = c->n2;
+        select_bin<kBins3>(ws.hist3, need, ss.scan, ss.sel);
+        T = (c->p2 << 10) | ss.sel[0];
+        const uint32_t m = need - ss.sel[1];
+        tie_mode = m < ss.sel[2] ? 1u : 0u;
+        if (blockIdx.x == 0 && threadIdx.x == 0) set_threshold(c, T, m, ss.sel[2]);
+    } else {
+        T = c->T;
+        tie_mode = c->tie_mode;
+    }
+    if (tie_mode == 0u) return;
     for (uint32_t tile = blockIdx.x; tile < ntiles; tile += gridDim.x) {
         const int64_t tile0 = int64_t(tile) * kTile;
         float v[kVecPerThread][4];
@@ -298,41 +536,26 @@ __global__ __launch_bounds__(kBlock) void topk_ties_kernel(const float *__restri
 #pragma unroll
         for (int j = 0; j < kVecPerThread; ++j)
 #pragma unroll
-            for (int c = 0; c < 4; ++c)
-                cnt += (((valid >> (4 * j + c)) & 1u) && magnitude_key(v[j][c]) == T) ? 1u : 0u;
+            for (int cc = 0; cc < 4; ++cc)
+                cnt += (((valid >> (4 * j + cc)) & 1u) && magnitude_key(v[j][cc]) == T) ? 1u : 0u;
         uint32_t total;
         block_prefix_small(cnt, s_wave, total);
-        if (tid == 0) ws.tile_ties[tile] = total;
+        if (threadIdx.x == 0) ws.tile_ties[tile] = total;
     }
 }
 
-// Exclusive scan of tile_ties[0..ntiles) in place by one workgroup; each
-// thread owns a contiguous chunk.
-__global__ __launch_bounds__(kBlock) void topk_ties_scan_kernel(uint32_t ntiles, Workspace ws) {
-    __shared__ uint32_t s_scan[kBlock];
-    if (ws.ctl->tie_mode == 0u) return;
-    const int tid = threadIdx.x;
-    const uint32_t chunk = (ntiles + kBlock - 1) / kBlock;
-    const uint32_t lo = min(ntiles, tid * chunk);
-    const uint32_t hi = min(ntiles, lo + chunk);
-    uint32_t sum = 0;
-    for (uint32_t i = lo; i < hi; ++i) sum += ws.tile_ties[i];
-    s_scan[tid] = sum;
-    __syncthreads();
-    for (int off = 1; off < kBlock; off <<= 1) {
-        const uint32_t add = tid >= off ? s_scan[tid - off] : 0u;
-        __syncthreads();
-        s_scan[tid] += add;
-        __syncthreads();
-    }
-    uint32_t run = s_scan[tid] - sum;
-    for (uint32_t i = lo; i < hi; ++i) {
-        const uint32_t c = ws.tile_ties[i];
-        ws.tile_ties[i] = run;
-        run += c;
-    }
+// Sum of tile_ties[lo, hi) over the workgroup.
+__device__ __forceinline__ uint32_t tie_count_range(const uint32_t *tile_ties, uint32_t lo,
+                                                    uint32_t hi, uint32_t *s_wave) {
+    uint32_t v = 0;
+    for (uint32_t i = lo + threadIdx.x; i < hi; i += kBlock) v += tile_ties[i];
+    return block_sum(v, s_wave);
 }
 
+// Final emission over the whole vector.  Radix path: every key > T plus the
+// ties of rank < m (all ties when none is dropped).  Bracket path: only the
+// ties of rank < m when some are dropped (everything else is already sent);
+// returns at once otherwise.
 template <bool kVector>
 __global__ __launch_bounds__(kBlock) void topk_emit_kernel(float *__restrict__ e, int64_t d,
                                                            int32_t *__restrict__ idx,
@@ -340,11 +563,20 @@ __global__ __launch_bounds__(kBlock) void topk_emit_kernel(float *__restrict__ e
                                                            uint64_t cap, uint32_t ntiles,
                                                            Workspace ws) {
     __shared__ PairStage st;
-    const int tid = threadIdx.x;
-    const uint32_t T = ws.ctl->T;
+    const bool fast = ws.ctl->fast != 0u;
     const bool tie_mode = ws.ctl->tie_mode != 0u;
+    if (fast && !tie_mode) return;
+    const uint32_t T = ws.ctl->T;
     const uint32_t m = ws.ctl->m;
+    // Radix path: the whole payload from slot 0.  Bracket path: after the
+    // pairs of pass 1 (above) and step 3 (counted in emit2).
+    const uint64_t base = fast ? ws.ctl->above : 0u;
+    idx += base;
+    val += base;
+    cap -= base;
     uint32_t fill = 0;
+    // ties in the tiles before this workgroup's current tile
+    uint32_t ties_before = 0, counted_to = 0;
 
     for (uint32_t tile = blockIdx.x; tile < ntiles; tile += gridDim.x) {
         const int64_t tile0 = int64_t(tile) * kTile;
@@ -359,7 +591,7 @@ __global__ __launch_bounds__(kBlock) void topk_emit_kernel(float *__restrict__ e
                 const int b = 4 * j + c;
                 const uint32_t key = magnitude_key(v[j][c]);
                 const bool ok = (valid >> b) & 1u;
-                keep |= uint32_t(ok && key > T) << b;
+                keep |= uint32_t(ok && !fast && key > T) << b;
                 tie |= uint32_t(ok && key == T) << b;
             }
         }
@@ -369,7 +601,9 @@ __global__ __launch_bounds__(kBlock) void topk_emit_kernel(float *__restrict__ e
             // Rank of each tied element in index order: earlier tiles, then
             // earlier vector slots j (all lower indices), then lower threads
             // in slot j, then lower c within the thread.
-            uint32_t rank = ws.tile_ties[tile];
+            ties_before += tie_count_range(ws.tile_ties, counted_to, tile, st.wave);
+            counted_to = tile;
+            uint32_t rank = ties_before;
 #pragma unroll
             for (int j = 0; j < kVecPerThread; ++j) {
                 const uint32_t tj = (tie >> (4 * j)) & 0xfu;
@@ -385,39 +619,25 @@ __global__ __launch_bounds__(kBlock) void topk_emit_kernel(float *__restrict__ e
                 rank += slot_total;
             }
         }
-
-        uint32_t total;
-        const uint32_t pos = block_prefix_small(__popc(keep), st.wave, total);
-        if (total == 0) continue;
-        if (fill + total > uint32_t(kTile)) {
-            stage_flush(st, fill, false, &ws.ctl->emit, nullptr, cap, idx, val);
-            fill = 0;
-        }
-        uint32_t o = fill + pos;
+        stage_mask(st, fill, keep, v, tile0, &ws.ctl->emit2, cap, idx, val);
 #pragma unroll
-        for (int j = 0; j < kVecPerThread; ++j) {
+        for (int j = 0; j < kVecPerThread; ++j)
 #pragma unroll
-            for (int c = 0; c < 4; ++c) {
-                if ((keep >> (4 * j + c)) & 1u) {
-                    const int64_t i = elem_index(tile0, j, c);
-                    st.idx[o] = int32_t(i);
-                    st.val[o] = v[j][c];
-                    e[i] = 0.0f;
-                    ++o;
-                }
-            }
-        }
-        fill += total;
+            for (int c = 0; c < 4; ++c)
+                if ((keep >> (4 * j + c)) & 1u) e[elem_index(tile0, j, c)] = 0.0f;
     }
-    stage_flush(st, fill, true, &ws.ctl->emit, &ws.ctl->emitted, cap, idx, val);
+    stage_flush(st, fill, false, &ws.ctl->emit2, nullptr, cap, idx, val);
 }
 
 }  // namespace
 
-size_t topk_workspace_size(int64_t d) {
+size_t topk_path_flag_offset() { return offsetof(TopkCtl, fast); }
+
+size_t topk_workspace_size(int64_t d, int64_t k) {
     const int64_t tiles = d > 0 ? (d + kTile - 1) / kTile : 1;
-    const size_t bytes = kCtlBytes + kHistBytes + sizeof(uint32_t) * size_t(tiles);
-    return (bytes + 255) & ~size_t(255);
+    const int64_t ccap = candidate_capacity(d, k);
+    return kCtlBytes + round256(kHistBytes) + round256(sizeof(uint32_t) * size_t(tiles)) +
+           round256(sizeof(int32_t) * size_t(ccap)) + round256(sizeof(float) * size_t(ccap));
 }
 
 hipError_t launch_topk(const float *g, float *e, int64_t d, float lr, int64_t k,
@@ -425,33 +645,27 @@ hipError_t launch_topk(const float *g, float *e, int64_t d, float lr, int64_t k,
     if (d == 0) return hipSuccess;
     const uint32_t ntiles = uint32_t((d + kTile - 1) / kTile);
     const uint32_t grid = balanced_grid(ntiles, kScanWorkgroupsPerCU);
-    const uint32_t egrid = balanced_grid(ntiles, kStageWorkgroupsPerCU);
-    const Workspace ws = carve(workspace);
+    const uint32_t sgrid = balanced_grid(ntiles, kStageWorkgroupsPerCU);
+    const Workspace ws = carve(workspace, d, k);
+    const uint32_t kk = uint32_t(k);
     const bool vec = ((reinterpret_cast<uintptr_t>(g) | reinterpret_cast<uintptr_t>(e)) & 15u) == 0;
 
-    topk_reset_kernel<<<1, kBlock, 0, stream>>>(ws.ctl, ws.hist1, uint32_t(k));
+    topk_reset_kernel<<<persistent_grid(64), kBlock, 0, stream>>>(ws);
     if (vec)
-        topk_pass1_kernel<true><<<grid, kBlock, 0, stream>>>(g, e, d, lr, ntiles, ws);
+        topk_pass1_kernel<true><<<sgrid, kBlock, 0, stream>>>(g, e, d, lr, ntiles, kk, idx, val, ws);
     else
-        topk_pass1_kernel<false><<<grid, kBlock, 0, stream>>>(g, e, d, lr, ntiles, ws);
+        topk_pass1_kernel<false><<<sgrid, kBlock, 0, stream>>>(g, e, d, lr, ntiles, kk, idx, val, ws);
     if (k == 0) return hipGetLastError();
-    topk_select_kernel<1><<<1, kBlock, 0, stream>>>(ws);
     if (vec) {
-        topk_refine_kernel<true, 10><<<grid, kBlock, 0, stream>>>(e, d, ntiles, ws);
-        topk_select_kernel<2><<<1, kBlock, 0, stream>>>(ws);
-        topk_refine_kernel<true, 0><<<grid, kBlock, 0, stream>>>(e, d, ntiles, ws);
-        topk_select_kernel<3><<<1, kBlock, 0, stream>>>(ws);
-        topk_ties_kernel<true><<<grid, kBlock, 0, stream>>>(e, d, ntiles, ws);
-        topk_ties_scan_kernel<<<1, kBlock, 0, stream>>>(ntiles, ws);
-        topk_emit_kernel<true><<<egrid, kBlock, 0, stream>>>(e, d, idx, val, uint64_t(k), ntiles, ws);
+        topk_step3_kernel<true><<<grid, kBlock, 0, stream>>>(e, d, ntiles, kk, idx, val, ws);
+        topk_step4_kernel<true><<<grid, kBlock, 0, stream>>>(e, d, ntiles, ws);
+        topk_step5_kernel<true><<<grid, kBlock, 0, stream>>>(e, d, ntiles, ws);
+        topk_emit_kernel<true><<<sgrid, kBlock, 0, stream>>>(e, d, idx, val, uint64_t(k), ntiles, ws);
     } else {
-        topk_refine_kernel<false, 10><<<grid, kBlock, 0, stream>>>(e, d, ntiles, ws);
-        topk_select_kernel<2><<<1, kBlock, 0, stream>>>(ws);
-        topk_refine_kernel<false, 0><<<grid, kBlock, 0, stream>>>(e, d, ntiles, ws);
-        topk_select_kernel<3><<<1, kBlock, 0, stream>>>(ws);
-        topk_ties_kernel<false><<<grid, kBlock, 0, stream>>>(e, d, ntiles, ws);
-        topk_ties_scan_kernel<<<1, kBlock, 0, stream>>>(ntiles, ws);
-        topk_emit_kernel<false><<<egrid, kBlock, 0, stream>>>(e, d, idx, val, uint64_t(k), ntiles, ws);
+        topk_step3_kernel<false><<<grid, kBlock, 0, stream>>>(e, d, ntiles, kk, idx, val, ws);
+        topk_step4_kernel<false><<<grid, kBlock, 0, stream>>>(e, d, ntiles, ws);
+        topk_step5_kernel<false><<<grid, kBlock, 0, stream>>>(e, d, ntiles, ws);
+        topk_emit_kernel<false><<<sgrid, kBlock, 0, stream>>>(e, d, idx, val, uint64_t(k), ntiles, ws);
     }
     return hipGetLastError();
 }

@@ -263,6 +263,108 @@ def test_topk_ef_loop_properties():
         check_topk_properties(acc, k, idx.cpu().numpy(), val.cpu().numpy(), e_host)
 
 
+class TopkState:
+    """One Top-k EF trajectory on the device, with one workspace kept across
+    calls (so later calls may take the bracket path)."""
+
+    def __init__(self, d, kmax):
+        self.d = d
+        self.e = torch.zeros(d, dtype=torch.float32, device=DEV)
+        self.ws = efs.new_topk_workspace(d, kmax, DEV)
+        self.idx = torch.empty(kmax, dtype=torch.int32, device=DEV)
+        self.val = torch.empty(kmax, dtype=torch.float32, device=DEV)
+
+    def step(self, g_host, k, e_host):
+        """One call from e_host; returns the device result."""
+        self.e.copy_(torch.from_numpy(e_host))
+        efs.topk_compress(to_dev(g_host), self.e, LR, k, self.idx[:k], self.val[:k], self.ws)
+        return self.idx[:k].cpu().numpy(), self.val[:k].cpu().numpy(), self.e.cpu().numpy()
+
+    def bracket(self):
+        return efs.topk_took_bracket_path(self.ws)
+
+
+def test_topk_workspace_reuse_matches_oracle():
+    # A sequence of calls on one workspace: repeats of a distribution (the
+    # bracket around the previous threshold holds), jumps in scale (it does
+    # not), changes of k, ties split by index, and a call whose payload is
+    # exactly the keys above the bracket.
+    d = 300_007
+    st = TopkState(d, 20_000)
+    rng = np.random.default_rng(123)
+    e = np.zeros(d, np.float32)
+    calls = []   # (name, g, k, path expected: True bracket / False radix / None either)
+    for t in range(4):
+        calls.append(("gauss", (rng.standard_normal(d) * 1e-3).astype(np.float32), 3000,
+                      False if t == 0 else True))
+    calls.append(("scaled x50", (rng.standard_normal(d) * 5e-2).astype(np.float32), 3000, False))
+    calls.append(("scaled back", (rng.standard_normal(d) * 1e-3).astype(np.float32), 3000, False))
+    calls.append(("k up", (rng.standard_normal(d) * 1e-3).astype(np.float32), 20_000, None))
+    calls.append(("k down", (rng.standard_normal(d) * 1e-3).astype(np.float32), 100, None))
+    q = (rng.integers(-40, 41, size=d).astype(np.float32) * np.float32(1e-4))
+    calls.append(("ties a", q, 7777, None))
+    calls.append(("ties b", q[::-1].copy(), 7777, True))
+    for name, g, k, path in calls:
+        if name in ("gauss", "ties a", "ties b"):
+            # fresh error: the same magnitude distribution (and exact ties for
+            # the quantised vectors) in every call of the group
+            e = np.zeros(d, np.float32)
+        gi, gv, ge = st.step(g, k, e)
+        ri, rv, re = oracle.topk(g, e, LR, k)
+        assert_payload_equal(gi, gv, ri, rv, name)
+        assert_bits_equal(ge, re, name)
+        if path is not None:
+            assert st.bracket() == path, name
+        e = re
+    # exactly k keys far above the previous threshold, the rest far below
+    e = np.zeros(d, np.float32)
+    g = np.full(d, 1e-6, np.float32)
+    k = 500
+    st.step(synth.small_gradient(5, d), k, e)        # sets a threshold near 3e-4
+    g[rng.choice(d, k, replace=False)] = np.float32(1.0)
+    gi, gv, ge = st.step(g, k, e)
+    ri, rv, re = oracle.topk(g, e, LR, k)
+    assert_payload_equal(gi, gv, ri, rv, "exactly k above")
+    assert_bits_equal(ge, re, "exactly k above")
+    assert st.bracket()
+
+
+def test_topk_workspace_contents_do_not_matter():
+    d, k = 200_003, 1500
+    g = synth.small_gradient(77, d)
+    ri, rv, re = oracle.topk(g, np.zeros(d, np.float32), LR, k)
+    for fill in (0x00, 0xFF, 0x54, None):
+        ws = efs.new_topk_workspace(d, k, DEV)
+        if fill is None:
+            ws.copy_(torch.from_numpy(np.random.default_rng(9).integers(0, 256, ws.numel(),
+                                                                          dtype=np.uint8)))
+        else:
+            ws.fill_(fill)
+        e = torch.zeros(d, dtype=torch.float32, device=DEV)
+        idx = torch.empty(k, dtype=torch.int32, device=DEV)
+        val = torch.empty(k, dtype=torch.float32, device=DEV)
+        efs.topk_compress(to_dev(g), e, LR, k, idx, val, ws)
+        assert_payload_equal(idx.cpu().numpy(), val.cpu().numpy(), ri, rv, "fill %r" % fill)
+        assert_bits_equal(e.cpu().numpy(), re, "fill %r" % fill)
+
+
+def test_topk_ef_loop_matches_oracle_each_step():
+    # the training-like case: e carried, one workspace, 12 iterations
+    d, k = 500_009, 2500
+    st = TopkState(d, k)
+    e = np.zeros(d, np.float32)
+    hits = 0
+    for t in range(12):
+        g = synth.small_gradient(300 + t, d)
+        gi, gv, ge = st.step(g, k, e)
+        ri, rv, e = oracle.topk(g, e, LR, k)
+        assert_payload_equal(gi, gv, ri, rv, "t=%d" % t)
+        assert_bits_equal(ge, e, "t=%d" % t)
+        hits += st.bracket()
+    say("bracket path taken in %d of 12 iterations" % hits)
+    assert hits >= 1
+
+
 # ---------------------------------------------------------------------------
 # n-worker average
 # ---------------------------------------------------------------------------
