@@ -89,10 +89,11 @@ size_t topk_workspace_bytes(int64_t d, int64_t k);
  *   idx, val      [k] payload of exactly k pairs (unordered).
  *   workspace     device memory of at least topk_workspace_bytes(d, k)
  *                 bytes, 16-byte aligned; contents need no initialisation.
- *                 The library keeps the last threshold in it: a following
- *                 call on the same workspace whose k-th magnitude lies within
- *                 about 6 to 12 % of it (the error-feedback case) selects from a
- *                 small candidate set instead of three more passes over p.
+ *                 The library keeps the last two thresholds in it: a
+ *                 following call on the same workspace whose k-th magnitude
+ *                 lies within about 3 to 6 % of their linear extrapolation
+ *                 (the error-feedback case) selects from a small candidate
+ *                 set instead of three more passes over p.
  *                 Results never depend on what the workspace held.  Not
  *                 shareable between concurrent calls.
  */

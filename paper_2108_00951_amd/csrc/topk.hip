@@ -9,8 +9,9 @@
 // (work a call does not need returns at once):
 //
 //   reset  zero the control block and histograms; form the key bracket
-//          [lo, hi] of 2^21 keys (about 6..12 % in magnitude either side)
-//          around the threshold of the previous call on this workspace.
+//          [lo, hi] of 2^20 keys (about 3..6 % in magnitude either side)
+//          around the threshold predicted from the previous two calls on
+//          this workspace (linear extrapolation of the key).
 //   pass1  p = e + lr*g written into e (12 B/element); LDS histogram of key
 //          bits 30..20; with a bracket, keys above it go straight to the
 //          payload and keys inside it to a candidate buffer (staged
@@ -40,7 +41,7 @@
 //
 // Workspace (offsets 256-byte aligned):
 //   control block (256 B) | histograms: 2048 + 1024 + 1024 radix bins, 1024
-//   coarse + 2^21 fine bracket bins | per-tile tie counts | candidate buffer
+//   coarse + 2^20 fine bracket bins | per-tile tie counts | candidate buffer
 //   (int32 index, fp32 value) x ccap.
 #include <stddef.h>
 
@@ -55,7 +56,7 @@ constexpr int kBins1 = 2048;  // bits 30..20
 constexpr int kBins2 = 1024;  // bits 19..10
 constexpr int kBins3 = 1024;  // bits 9..0
 constexpr int kCoarse = 1024;
-constexpr int kFineBits = 21;
+constexpr int kFineBits = 20;
 constexpr uint32_t kFine = 1u << kFineBits;        // bracket width in keys
 constexpr int kFinePerCoarse = int(kFine) / kCoarse;
 constexpr uint32_t kHintMagic = 0x48494e54u;
@@ -80,12 +81,16 @@ struct TopkCtl {
     unsigned long long emit;   // pass 1: pairs above the bracket (count in the low bits)
     unsigned long long cand;   // pass 1: bracket candidates
     unsigned long long emit2;  // pairs appended after pass 1 (steps 3 and emit)
-    // Kept across calls (not cleared by reset): threshold of the last call.
-    uint32_t hint_key;
-    uint32_t hint_magic;
+    uint32_t last;             // threshold of the previous call (kNoKey if none)
+    uint32_t pad2;
+    // Kept across calls (not cleared by reset): the thresholds of the last
+    // two calls, each valid when its magic word is set.
+    uint32_t hint_key, hint_magic;
+    uint32_t prev_key, prev_magic;
 };
 static_assert(sizeof(TopkCtl) <= 256, "control block must fit its slot");
 constexpr int kCtlClearWords = offsetof(TopkCtl, hint_key) / 4;
+static_assert(offsetof(TopkCtl, hint_key) % 4 == 0, "control words are 32-bit");
 static_assert(kCtlClearWords <= kBlock, "reset clears the control block with one workgroup");
 
 constexpr size_t kCtlBytes = 256;
@@ -219,8 +224,11 @@ __device__ void select_bin(const uint32_t *hist, uint32_t need, uint32_t *s_scan
     __syncthreads();
 }
 
-// Zeroes the control block (except the hint) and every histogram, and forms
-// the bracket from the hint.  Grid-stride over the histogram words.
+// Zeroes the control block (except the hints) and every histogram, and
+// forms the bracket: 2^20 keys centred on the threshold predicted from the
+// last two calls (the last threshold plus the last step in key space, the
+// step capped at 2^18 keys; the last threshold alone when only one is
+// known).  Grid-stride over the histogram words.
 __global__ __launch_bounds__(kBlock) void topk_reset_kernel(Workspace ws) {
     if (blockIdx.x == 0) {
         uint32_t *w = reinterpret_cast<uint32_t *>(ws.ctl);
@@ -228,9 +236,23 @@ __global__ __launch_bounds__(kBlock) void topk_reset_kernel(Workspace ws) {
         __syncthreads();
         if (threadIdx.x == 0) {
             TopkCtl *c = ws.ctl;
+            c->last = kNoKey;
             if (c->hint_magic == kHintMagic) {
-                const uint32_t h = c->hint_key & 0x7fffffffu;
-                const uint32_t lo = h > kFine / 2 ? h - kFine / 2 : 0u;
+                // the step since the previous call, capped at a quarter of
+                // the bracket so the last threshold always stays inside it
+                const int64_t h1 = int64_t(c->hint_key & 0x7fffffffu);
+                int64_t pred = h1;
+                if (c->prev_magic == kHintMagic) {
+                    int64_t step = h1 - int64_t(c->prev_key & 0x7fffffffu);
+                    const int64_t cap = int64_t(kFine / 4);
+                    step = step > cap ? cap : (step < -cap ? -cap : step);
+                    pred = h1 + step;
+                    if (pred < 0) pred = 0;
+                    if (pred > 0x7fffffff) pred = 0x7fffffff;
+                }
+                const uint32_t p = uint32_t(pred);
+                const uint32_t lo = p > kFine / 2 ? p - kFine / 2 : 0u;
+                c->last = uint32_t(h1);
                 c->lo = lo;
                 c->hi = lo + (kFine - 1);
                 c->bracket_on = 1u;
@@ -378,12 +400,14 @@ __device__ void radix_refine(const float *__restrict__ e, int64_t d, uint32_t nt
 }
 
 // Threshold and tie bookkeeping, written by workgroup 0 once T is exact; T
-// is also kept as the next call's bracket hint.
+// and the previous call's threshold are kept for the next call's bracket.
 __device__ __forceinline__ void set_threshold(TopkCtl *c, uint32_t T, uint32_t m, uint32_t ties) {
     c->T = T;
     c->m = m;
     c->ties = ties;
     c->tie_mode = m < ties ? 1u : 0u;
+    c->prev_key = c->last;
+    c->prev_magic = c->last != kNoKey ? kHintMagic : 0u;
     c->hint_key = T;
     c->hint_magic = kHintMagic;
 }
