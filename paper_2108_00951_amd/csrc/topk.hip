@@ -5,17 +5,17 @@
 // ranked larger first and, on equal keys, lower index first.  Selection is a
 // radix select (the paper notes radix select costs O(ceil(b/r) d), section 1)
 // with a shortcut for error-feedback loops, where the k-th magnitude moves
-// little from one iteration to the next.  Six launches, always all enqueued
+// little from one iteration to the next.  Five launches, always all enqueued
 // (work a call does not need returns at once):
 //
 //   reset  zero the control block and histograms; form the key bracket
 //          [lo, hi] of 2^20 keys (about 3..6 % in magnitude either side)
 //          around the threshold predicted from the previous two calls on
-//          this workspace (linear extrapolation of the key).
+//          this workspace.
 //   pass1  p = e + lr*g written into e (12 B/element); LDS histogram of key
 //          bits 30..20; with a bracket, keys above it go straight to the
 //          payload and keys inside it to a candidate buffer (staged
-//          compaction) and into coarse (1024) and fine (2^21) histograms of
+//          compaction) and into coarse (1024) and fine (2^20) histograms of
 //          key - lo.
 //   step3  every workgroup first decides the path: the bracket path only
 //          when the counts prove the k-th key lies inside the bracket
@@ -23,11 +23,11 @@
 //          Bracket path: select T from the coarse then fine histogram, append
 //          the candidates with key > T (all key == T too when no tie is
 //          dropped), zero e at every kept coordinate.  Radix path: select the
-//          top digit from the pass-1 histogram, histogram bits 19..10 of the
-//          keys under that prefix (a 4 B/element read of p).
-//   step4  radix path: select, histogram bits 9..0 (another read of p).
-//   step5  radix path: select the last digit, so T is exact.  Either path,
-//          when ties at T must be split (0 < m < #(key == T)): per-tile
+//          top digit from the pass-1 histogram, then histogram bits 19..0 of
+//          the keys under it (a 4 B/element read of p) into 1024 coarse and
+//          2^20 fine bins.
+//   step4  radix path: coarse then fine selection, so T is exact.  Either
+//          path, when ties at T must be split (0 < m < #(key == T)): per-tile
 //          counts of key == T.
 //   emit   radix path: keep key > T and the ties of index rank < m (a read
 //          of p); bracket path: only the ties of rank < m, when some are
@@ -40,8 +40,8 @@
 // only through global atomics and kernel boundaries; none waits on another.
 //
 // Workspace (offsets 256-byte aligned):
-//   control block (256 B) | histograms: 2048 + 1024 + 1024 radix bins, 1024
-//   coarse + 2^20 fine bracket bins | per-tile tie counts | candidate buffer
+//   control block (256 B) | histograms: 2048 top-digit bins, 1024 + 2^20
+//   radix bins, 1024 + 2^20 bracket bins | per-tile tie counts | candidates
 //   (int32 index, fp32 value) x ccap.
 #include <stddef.h>
 
@@ -53,9 +53,7 @@ namespace efs {
 namespace {
 
 constexpr int kBins1 = 2048;  // bits 30..20
-constexpr int kBins2 = 1024;  // bits 19..10
-constexpr int kBins3 = 1024;  // bits 9..0
-constexpr int kCoarse = 1024;
+constexpr int kCoarse = 1024; // coarse bins of a 20-bit range (1024 keys each)
 constexpr int kFineBits = 20;
 constexpr uint32_t kFine = 1u << kFineBits;        // bracket width in keys
 constexpr int kFinePerCoarse = int(kFine) / kCoarse;
@@ -67,7 +65,7 @@ constexpr uint32_t kNoKey = 0xffffffffu;            // larger than every 31-bit 
 // launches only, never by other workgroups of the launch that writes them.
 struct TopkCtl {
     uint32_t p1, n1;      // radix path: top digit and the rank left under it (step 3)
-    uint32_t p2, n2;      // radix path: 21-bit prefix and the rank left under it (step 4)
+    uint32_t pad0[2];
     uint32_t T;           // threshold key
     uint32_t m;           // tied elements (key == T) to keep
     uint32_t ties;        // elements with key == T
@@ -94,7 +92,9 @@ static_assert(offsetof(TopkCtl, hint_key) % 4 == 0, "control words are 32-bit");
 static_assert(kCtlClearWords <= kBlock, "reset clears the control block with one workgroup");
 
 constexpr size_t kCtlBytes = 256;
-constexpr size_t kHistWords = kBins1 + kBins2 + kBins3 + kCoarse + size_t(kFine);
+// radix path: 1024 coarse + 2^20 fine bins for bits 19..0; bracket path:
+// 1024 coarse + 2^20 fine bins for key - lo
+constexpr size_t kHistWords = kBins1 + 2 * (kCoarse + size_t(kFine));
 constexpr size_t kHistBytes = sizeof(uint32_t) * kHistWords;
 static_assert(kHistWords % 4 == 0, "histograms are cleared with 16-byte stores");
 
@@ -102,7 +102,7 @@ size_t round256(size_t b) { return (b + 255) & ~size_t(255); }
 
 struct Workspace {
     TopkCtl *ctl;
-    uint32_t *hist1, *hist2, *hist3, *coarse, *fine, *tile_ties;
+    uint32_t *hist1, *rcoarse, *rfine, *coarse, *fine, *tile_ties;
     int32_t *cand_idx;
     float *cand_val;
     uint32_t ccap;
@@ -125,9 +125,9 @@ Workspace carve(void *ws, int64_t d, int64_t k) {
     Workspace w;
     w.ctl = reinterpret_cast<TopkCtl *>(b);
     w.hist1 = reinterpret_cast<uint32_t *>(b + kCtlBytes);
-    w.hist2 = w.hist1 + kBins1;
-    w.hist3 = w.hist2 + kBins2;
-    w.coarse = w.hist3 + kBins3;
+    w.rcoarse = w.hist1 + kBins1;
+    w.rfine = w.rcoarse + kCoarse;
+    w.coarse = w.rfine + kFine;
     w.fine = w.coarse + kCoarse;
     size_t off = kCtlBytes + round256(kHistBytes);
     w.tile_ties = reinterpret_cast<uint32_t *>(b + off);
@@ -370,14 +370,31 @@ __global__ __launch_bounds__(kBlock) void topk_pass1_kernel(const float *__restr
             if (sh.coarse[b]) atomicAdd(ws.coarse + b, sh.coarse[b]);
 }
 
-// Radix path: histogram of bits [kShift, kShift+10) over the keys whose
-// higher bits equal `prefix`.
-template <bool kVector, int kShift>
-__device__ void radix_refine(const float *__restrict__ e, int64_t d, uint32_t ntiles,
-                             uint32_t prefix, uint32_t *hist, uint32_t *h) {
-    constexpr int kBins = 1024;
+// Adds 1 to hist[bin] for every active lane of the wave; the lanes that share
+// the first active lane's bin add together with one atomic (a vector of equal
+// magnitudes costs one atomic per wave, not 64).  Called by all lanes.
+__device__ __forceinline__ void wave_aggregated_add(uint32_t *hist, uint32_t bin, bool active) {
+    const uint64_t act = __ballot(active);
+    if (act == 0) return;
+    const int leader = __ffsll(static_cast<unsigned long long>(act)) - 1;
+    const uint32_t lbin = __shfl(bin, leader);
+    const bool same = active && bin == lbin;
+    const uint64_t mates = __ballot(same);
+    if (same) {
+        if (int(threadIdx.x & (kWave - 1)) == leader) atomicAdd(hist + lbin, uint32_t(__popcll(mates)));
+    } else if (active) {
+        atomicAdd(hist + bin, 1u);
+    }
+}
+
+// Radix path: histograms of bits 19..0 of the keys whose bits 30..20 equal
+// `prefix`: bits 19..10 in 1024 coarse bins (LDS, then merged), all twenty
+// bits in 2^20 fine bins (global).
+template <bool kVector>
+__device__ void radix_refine20(const float *__restrict__ e, int64_t d, uint32_t ntiles,
+                               uint32_t prefix, uint32_t *coarse, uint32_t *fine, uint32_t *h) {
     const int tid = threadIdx.x;
-    for (int b = tid; b < kBins; b += kBlock) h[b] = 0u;
+    for (int b = tid; b < kCoarse; b += kBlock) h[b] = 0u;
     __syncthreads();
     for (uint32_t tile = blockIdx.x; tile < ntiles; tile += gridDim.x) {
         const int64_t tile0 = int64_t(tile) * kTile;
@@ -389,14 +406,15 @@ __device__ void radix_refine(const float *__restrict__ e, int64_t d, uint32_t nt
 #pragma unroll
             for (int c = 0; c < 4; ++c) {
                 const uint32_t key = magnitude_key(v[j][c]);
-                if (((valid >> (4 * j + c)) & 1u) && (key >> (kShift + 10)) == prefix)
-                    atomicAdd(&h[(key >> kShift) & (kBins - 1)], 1u);
+                const bool in = ((valid >> (4 * j + c)) & 1u) && (key >> 20) == prefix;
+                if (in) atomicAdd(&h[(key >> 10) & (kCoarse - 1)], 1u);
+                wave_aggregated_add(fine, key & (kFine - 1), in);
             }
         }
     }
     __syncthreads();
-    for (int b = tid; b < kBins; b += kBlock)
-        if (h[b]) atomicAdd(hist + b, h[b]);
+    for (int b = tid; b < kCoarse; b += kBlock)
+        if (h[b]) atomicAdd(coarse + b, h[b]);
 }
 
 // Threshold and tie bookkeeping, written by workgroup 0 once T is exact; T
@@ -446,7 +464,7 @@ __global__ __launch_bounds__(kBlock) void topk_step3_kernel(float *__restrict__ 
             c->p1 = prefix;
             c->n1 = k - ss.sel[1];
         }
-        radix_refine<kVector, 10>(e, d, ntiles, prefix, ws.hist2, h);
+        radix_refine20<kVector>(e, d, ntiles, prefix, ws.rcoarse, ws.rfine, h);
         return;
     }
 
@@ -512,38 +530,24 @@ __global__ __launch_bounds__(kBlock) void topk_step3_kernel(float *__restrict__ 
     }
 }
 
-// Step 4 (radix path): select the second digit, histogram bits 9..0.
+// Step 4: radix path, coarse then fine selection of bits 19..0 (T exact);
+// then, on either path, the per-tile tie counts when ties at T must be split.
 template <bool kVector>
 __global__ __launch_bounds__(kBlock) void topk_step4_kernel(const float *__restrict__ e, int64_t d,
-                                                            uint32_t ntiles, Workspace ws) {
-    __shared__ SelectShared ss;
-    __shared__ uint32_t h[1024];
-    TopkCtl *c = ws.ctl;
-    if (c->fast != 0u) return;
-    const uint32_t need = c->n1;
-    select_bin<kBins2>(ws.hist2, need, ss.scan, ss.sel);
-    const uint32_t prefix = (c->p1 << 10) | ss.sel[0];
-    if (blockIdx.x == 0 && threadIdx.x == 0) {
-        c->p2 = prefix;
-        c->n2 = need - ss.sel[1];
-    }
-    radix_refine<kVector, 0>(e, d, ntiles, prefix, ws.hist3, h);
-}
-
-// Step 5: radix path, the last digit (T exact); then, on either path, the
-// per-tile tie counts when ties at T must be split.
-template <bool kVector>
-__global__ __launch_bounds__(kBlock) void topk_step5_kernel(const float *__restrict__ e, int64_t d,
                                                             uint32_t ntiles, Workspace ws) {
     __shared__ SelectShared ss;
     __shared__ uint32_t s_wave[kWaves];
     TopkCtl *c = ws.ctl;
     uint32_t T, tie_mode;
     if (c->fast == 0u) {
-        const uint32_t need = c->n2;
-        select_bin<kBins3>(ws.hist3, need, ss.scan, ss.sel);
-        T = (c->p2 << 10) | ss.sel[0];
-        const uint32_t m = need - ss.sel[1];
+        const uint32_t need = c->n1;
+        select_bin<kCoarse>(ws.rcoarse, need, ss.scan, ss.sel);
+        const uint32_t cb = ss.sel[0], above_c = ss.sel[1];
+        __syncthreads();
+        select_bin<kFinePerCoarse>(ws.rfine + size_t(cb) * kFinePerCoarse, need - above_c,
+                                   ss.scan, ss.sel);
+        T = (c->p1 << 20) | (cb << 10) | ss.sel[0];
+        const uint32_t m = need - above_c - ss.sel[1];
         tie_mode = m < ss.sel[2] ? 1u : 0u;
         if (blockIdx.x == 0 && threadIdx.x == 0) set_threshold(c, T, m, ss.sel[2]);
     } else {
@@ -683,12 +687,10 @@ hipError_t launch_topk(const float *g, float *e, int64_t d, float lr, int64_t k,
     if (vec) {
         topk_step3_kernel<true><<<grid, kBlock, 0, stream>>>(e, d, ntiles, kk, idx, val, ws);
         topk_step4_kernel<true><<<grid, kBlock, 0, stream>>>(e, d, ntiles, ws);
-        topk_step5_kernel<true><<<grid, kBlock, 0, stream>>>(e, d, ntiles, ws);
         topk_emit_kernel<true><<<sgrid, kBlock, 0, stream>>>(e, d, idx, val, uint64_t(k), ntiles, ws);
     } else {
         topk_step3_kernel<false><<<grid, kBlock, 0, stream>>>(e, d, ntiles, kk, idx, val, ws);
         topk_step4_kernel<false><<<grid, kBlock, 0, stream>>>(e, d, ntiles, ws);
-        topk_step5_kernel<false><<<grid, kBlock, 0, stream>>>(e, d, ntiles, ws);
         topk_emit_kernel<false><<<sgrid, kBlock, 0, stream>>>(e, d, idx, val, uint64_t(k), ntiles, ws);
     }
     return hipGetLastError();
