@@ -38,7 +38,7 @@ HBM_PEAK_GBPS = 8000.0
 HT_KERNEL = "ht_fused_kernel"
 COPY_KERNEL = "copy_kernel"
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "ht_fused_kernel_segments_25.6m_pmc.txt")
-HT_SOURCES = ["ht.hip", "device_common.hpp", "launch.hpp"]
+HT_SOURCES = ["ht.hip", "device_common.hpp"]
 
 
 def kernel_source_digest():
@@ -380,6 +380,20 @@ def ht_sweep(efs, torch, synth, cur, reps):
         res[st.w.name] = {"d": d, "launch_us": round(us, 2), "k_t": kt,
                           "gbps": round(gbps, 1), "frac": round(gbps / HBM_PEAK_GBPS, 4),
                           "gelem_s": round(d / (us * 1e-6) / 1e9, 1)}
+        # streaming ceilings on the same buffers (whole tiles): copy, read,
+        # write, and two reads + one write (the hard threshold's pattern)
+        nt = (d // 4096) * 4096
+        ceil = {}
+        for mode, name, nbytes in ((0, "copy", 8.0), (1, "read", 4.0), (2, "write", 4.0),
+                                   (3, "2r1w", 12.0)):
+            a.record(cur)
+            for s in range(reps):
+                efs.stream_probe(gs[0][:nt], gs[1][:nt], mode)
+            b.record(cur)
+            torch.cuda.synchronize()
+            pus = a.elapsed_time(b) * 1e3 / reps
+            ceil[name] = round(nbytes * nt / (pus * 1e-6) / 1e9, 1)
+        res[st.w.name]["ceiling_gbps"] = ceil
         print("sweep %s: %s" % (st.w.name, res[st.w.name]), file=sys.stderr, flush=True)
         del gs, e, idx, val
         torch.cuda.empty_cache()

@@ -130,6 +130,17 @@ efs_status sparse_accumulate(const int32_t *const *idx, const float *const *val,
  * of the method.  src and dst 16-byte aligned, n >= 0. */
 efs_status efs_copy_probe(const float *src, float *dst, int64_t n, void *stream);
 
+/* Streaming bandwidth probes over n floats with the same tile shape and grid
+ * as the compression kernels (measurement aids, not part of the method):
+ *   mode 0  copy       y = x                (4n bytes read, 4n written)
+ *   mode 1  read       sum of x, discarded  (4n read; y[0..255] reserved)
+ *   mode 2  write      y = constant         (4n written)
+ *   mode 3  2R1W       y = y + 0.5 x        (8n read, 4n written; the
+ *                                            access pattern of ht_compress)
+ * Modes 1-3 cover whole 4096-element tiles only.  x and y 16-byte aligned,
+ * n >= 0; for mode 1, y must hold at least 256 floats. */
+efs_status efs_stream_probe(const float *x, float *y, int64_t n, int mode, void *stream);
+
 /* Static text for a status code. */
 const char *efs_status_string(efs_status status);
 

@@ -64,6 +64,8 @@ def declare(lib):
     lib.sparse_accumulate.restype = ctypes.c_int
     lib.efs_copy_probe.argtypes = [vp, vp, i64, vp]
     lib.efs_copy_probe.restype = ctypes.c_int
+    lib.efs_stream_probe.argtypes = [vp, vp, i64, ctypes.c_int, vp]
+    lib.efs_stream_probe.restype = ctypes.c_int
     lib.efs_status_string.argtypes = [ctypes.c_int]
     lib.efs_status_string.restype = ctypes.c_char_p
     lib.efs_last_error_message.argtypes = []
@@ -199,3 +201,14 @@ def copy_probe(src, dst, stream=None) -> None:
     if src.numel() != dst.numel():
         raise ValueError("src and dst differ in length")
     _check(lib, lib.efs_copy_probe(_ptr(src), _ptr(dst), src.numel(), _stream_handle(stream)))
+
+
+def stream_probe(x, y, mode: int, stream=None) -> None:
+    """Bandwidth probe: 0 copy, 1 read, 2 write, 3 two reads + one write."""
+    import torch
+    lib = load_library()
+    _require(x, torch.float32, "x")
+    _require(y, torch.float32, "y")
+    if mode != 1 and x.numel() != y.numel():
+        raise ValueError("x and y differ in length")
+    _check(lib, lib.efs_stream_probe(_ptr(x), _ptr(y), x.numel(), int(mode), _stream_handle(stream)))

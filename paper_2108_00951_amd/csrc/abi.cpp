@@ -161,4 +161,16 @@ efs_status efs_copy_probe(const float *src, float *dst, int64_t n, void *stream)
                         "efs_copy_probe");
 }
 
+efs_status efs_stream_probe(const float *x, float *y, int64_t n, int mode, void *stream) {
+    if (n < 0) return fail(EFS_EINVAL, "efs_stream_probe: n < 0");
+    if (mode < 0 || mode > 3) return fail(EFS_EINVAL, "efs_stream_probe: mode %d outside 0..3", mode);
+    if (n > 0 && (x == nullptr || y == nullptr || !aligned(x, 16) || !aligned(y, 16)))
+        return fail(EFS_EINVAL, "efs_stream_probe: x and y must be non-NULL and 16-byte aligned");
+    if (mode == 0)
+        return check_launch(efs::launch_copy(x, y, n, static_cast<hipStream_t>(stream)),
+                            "efs_stream_probe");
+    return check_launch(efs::launch_stream_probe(x, y, n, mode, static_cast<hipStream_t>(stream)),
+                        "efs_stream_probe");
+}
+
 }  // extern "C"

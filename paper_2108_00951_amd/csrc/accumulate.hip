@@ -78,6 +78,42 @@ __global__ __launch_bounds__(kBlock) void copy_kernel(const float *__restrict__ 
     }
 }
 
+// Streaming ceilings with the same tile shape and grid: read only (a sum
+// whose result is written only if it equals an impossible value), write only
+// (a constant fill), and two reads plus one write in place (y = y + 0.5 x,
+// the access pattern of the error-feedback passes).
+template <int kMode>
+__global__ __launch_bounds__(kBlock) void stream_probe_kernel(const float *__restrict__ x,
+                                                              float *__restrict__ y, int64_t n,
+                                                              uint32_t ntiles) {
+    const int tid = threadIdx.x;
+    f32x4 acc = {0.0f, 0.0f, 0.0f, 0.0f};
+    for (uint32_t tile = blockIdx.x; tile < ntiles; tile += gridDim.x) {
+        const int64_t tile0 = int64_t(tile) * kTile;
+        if (tile0 + kTile > n) continue;  // the probe covers whole tiles only
+        const f32x4 *x4 = reinterpret_cast<const f32x4 *>(x + tile0);
+        f32x4 *y4 = reinterpret_cast<f32x4 *>(y + tile0);
+        if (kMode == 1) {
+#pragma unroll
+            for (int j = 0; j < kVecPerThread; ++j) acc += __builtin_nontemporal_load(x4 + j * kBlock + tid);
+        } else if (kMode == 2) {
+            const f32x4 c = {1.0f, 2.0f, 3.0f, 4.0f};
+#pragma unroll
+            for (int j = 0; j < kVecPerThread; ++j) y4[j * kBlock + tid] = c;
+        } else {
+            f32x4 a[kVecPerThread], b[kVecPerThread];
+#pragma unroll
+            for (int j = 0; j < kVecPerThread; ++j) {
+                a[j] = __builtin_nontemporal_load(x4 + j * kBlock + tid);
+                b[j] = y4[j * kBlock + tid];
+            }
+#pragma unroll
+            for (int j = 0; j < kVecPerThread; ++j) y4[j * kBlock + tid] = b[j] + 0.5f * a[j];
+        }
+    }
+    if (kMode == 1 && acc.x == -1234.5f) y[tid] = acc.y;
+}
+
 uint32_t stream_grid(int64_t nvec) {
     return persistent_grid((nvec + int64_t(kBlock) * 4 - 1) / (int64_t(kBlock) * 4));
 }
@@ -99,6 +135,19 @@ hipError_t launch_accumulate(const int32_t *const *idx, const float *const *val,
         scatter_add_kernel<<<grid, kBlock, 0, stream>>>(idx[w], val[w], cnt, cap, d, out);
     }
     if (n > 1) scale_kernel<<<dense_grid, kBlock, 0, stream>>>(out, d, float(n));
+    return hipGetLastError();
+}
+
+hipError_t launch_stream_probe(const float *x, float *y, int64_t n, int mode,
+                               hipStream_t stream) {
+    const int64_t tiles = n > 0 ? (n + kTile - 1) / kTile : 1;
+    const uint32_t grid = balanced_grid(tiles, kHtWorkgroupsPerCU);
+    if (mode == 1)
+        stream_probe_kernel<1><<<grid, kBlock, 0, stream>>>(x, y, n, uint32_t(tiles));
+    else if (mode == 2)
+        stream_probe_kernel<2><<<grid, kBlock, 0, stream>>>(x, y, n, uint32_t(tiles));
+    else
+        stream_probe_kernel<3><<<grid, kBlock, 0, stream>>>(x, y, n, uint32_t(tiles));
     return hipGetLastError();
 }
 

@@ -14,6 +14,14 @@ constexpr int kWaves = kBlock / kWave;
 constexpr int kVecPerThread = 4;         // float4 per thread per tile
 constexpr int kTile = kBlock * kVecPerThread * 4;   // 4096 elements per tile
 
+// Resident workgroups per compute unit assumed by the grid sizing
+// (balanced_grid): the hard-threshold pass (two 4-wave workgroups per CU
+// measured fastest), kernels staging pairs in LDS (up to 33 KiB each), and
+// histogram / scan passes.
+constexpr int kHtWorkgroupsPerCU = 2;
+constexpr int kStageWorkgroupsPerCU = 4;
+constexpr int kScanWorkgroupsPerCU = 8;
+
 // Counter word layout used for single-launch stream compaction: the low 40
 // bits accumulate the number of emitted pairs, the high 24 bits count
 // workgroups that have finished (a ticket, so the last one is known).

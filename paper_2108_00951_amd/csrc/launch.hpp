@@ -22,17 +22,11 @@ hipError_t launch_accumulate(const int32_t *const *idx, const float *const *val,
                              int32_t n, int64_t d, float *out, hipStream_t stream);
 
 hipError_t launch_copy(const float *src, float *dst, int64_t n, hipStream_t stream);
+hipError_t launch_stream_probe(const float *x, float *y, int64_t n, int mode, hipStream_t stream);
 
 // Workgroups for a grid-stride pass over `work_tiles` tiles: enough to fill
 // every compute unit several times over, never more than there is work.
 uint32_t persistent_grid(int64_t work_tiles);
-
-// Resident workgroups per compute unit assumed by the grid sizing below:
-// the hard-threshold pass (two 4-wave workgroups per CU measured fastest),
-// other kernels staging pairs in LDS (33 KiB each), histogram / scan passes.
-constexpr int kHtWorkgroupsPerCU = 2;
-constexpr int kStageWorkgroupsPerCU = 4;
-constexpr int kScanWorkgroupsPerCU = 8;
 
 // Grid for a grid-stride pass in which every workgroup stays resident: the
 // fewest tiles per workgroup that the resident workgroups allow, and just

@@ -417,3 +417,19 @@ def test_copy_probe_copies():
         dst = torch.zeros(n, dtype=torch.float32, device=DEV)
         efs.copy_probe(src, dst)
         assert torch.equal(src, dst)
+
+
+def test_stream_probes():
+    n = 4096 * 7 + 5
+    x = torch.arange(n, dtype=torch.float32, device=DEV)
+    y = torch.full((n,), 2.0, dtype=torch.float32, device=DEV)
+    efs.stream_probe(x, y, 0)
+    assert torch.equal(x, y)
+    y.fill_(2.0)
+    efs.stream_probe(x, y, 3)
+    whole = 4096 * 7
+    assert torch.equal(y[:whole], 2.0 + 0.5 * x[:whole])
+    assert torch.all(y[whole:] == 2.0)
+    efs.stream_probe(x, y, 2)
+    assert torch.equal(y[:8], torch.tensor([1, 2, 3, 4, 1, 2, 3, 4], dtype=torch.float32, device=DEV))
+    efs.stream_probe(x, y, 1)
