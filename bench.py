@@ -255,6 +255,16 @@ def main():
     torch.cuda.synchronize()
     ht_b2b_us = a.elapsed_time(b) * 1e3 / args.b2b
     kt_b2b = efs.counter_value(ctr)
+    # the same with the fused telemetry (total error, pairs sent, max |e'|)
+    tel = efs.new_telemetry(dev)
+    a, b = ev(), ev()
+    torch.cuda.synchronize()
+    a.record(cur)
+    for s in range(args.b2b):
+        efs.ht_compress_telemetry(pool[s % len(pool)], e_ht, lr, lam, idx, val, ctr, tel)
+    b.record(cur)
+    torch.cuda.synchronize()
+    ht_tel_us = a.elapsed_time(b) * 1e3 / args.b2b
     a, b = ev(), ev()
     a.record(cur)
     for s in range(args.b2b):
@@ -325,6 +335,7 @@ def main():
         "copy_probe": {"us": round(copy_us, 2), "gbps": round(8.0 * d / (copy_us * 1e-6) / 1e9, 1),
                        "bytes": 8.0 * d},
         "ops": {
+            "ht_compress_telemetry": {"launch_us": round(ht_tel_us, 2)},
             "ht_compress": dict(stats(ht_ms), gelem_s=round(d / ht_s / 1e9, 2),
                                 gbps=round(ht_bytes / ht_s / 1e9, 1), k_t_mean=kt,
                                 k_t_first=kts[0], k_t_last=kts[-1]),

@@ -76,6 +76,30 @@ efs_status ht_compress(const float *g, float *e, int64_t d, float lr, float lamb
                        int32_t *idx, float *val, int64_t cap, uint32_t *counter,
                        void *stream);
 
+/* A telemetry object: EFS_TELEMETRY_BYTES of device memory, 8-byte aligned,
+ * zero-filled by the caller before the first call; every call adds to it:
+ *   double   err2_total    sum over calls of ||e_{t+1}||^2, the total error
+ *                          of Remark 4 (section 3) when the calls are the
+ *                          iterations t = 0..T-1;
+ *   double   sent_total    sum over calls of k_t (average density =
+ *                          sent_total / (calls * d), the measure of data
+ *                          volume used in section 6);
+ *   uint32_t max_abs_bits  running max of |e_{t+1}| as the bit pattern of a
+ *                          non-negative float (the hard threshold keeps it
+ *                          below lambda: the absolute-compressor bound of
+ *                          section 5);
+ *   uint32_t calls         number of calls accumulated;
+ *   8 bytes reserved.
+ * The norm is summed in binary64 by one atomic per workgroup, so its last
+ * bits can vary with the order of the additions. */
+#define EFS_TELEMETRY_BYTES 32
+
+/* ht_compress, and in the same pass the telemetry above added to
+ * `telemetry` (device pointer, see EFS_TELEMETRY_BYTES). */
+efs_status ht_compress_telemetry(const float *g, float *e, int64_t d, float lr, float lambda,
+                                 int32_t *idx, float *val, int64_t cap, uint32_t *counter,
+                                 void *telemetry, void *stream);
+
 /* Bytes of device workspace topk_compress needs for (d, k). */
 size_t topk_workspace_bytes(int64_t d, int64_t k);
 

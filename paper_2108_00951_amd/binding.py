@@ -53,6 +53,8 @@ def declare(lib):
     vp, i64, f32, i32 = ctypes.c_void_p, ctypes.c_int64, ctypes.c_float, ctypes.c_int32
     lib.ht_compress.argtypes = [vp, vp, i64, f32, f32, vp, vp, i64, vp, vp]
     lib.ht_compress.restype = ctypes.c_int
+    lib.ht_compress_telemetry.argtypes = [vp, vp, i64, f32, f32, vp, vp, i64, vp, vp, vp]
+    lib.ht_compress_telemetry.restype = ctypes.c_int
     lib.topk_workspace_bytes.argtypes = [i64, i64]
     lib.topk_workspace_bytes.restype = ctypes.c_size_t
     lib.topk_path_flag_offset.argtypes = []
@@ -124,6 +126,46 @@ def ht_compress(g, e, lr: float, lam: float, idx, val, counter, stream=None) -> 
         raise ValueError("size mismatch among g, e, idx, val, counter")
     rc = lib.ht_compress(_ptr(g), _ptr(e), g.numel(), float(lr), float(lam), _ptr(idx), _ptr(val),
                          idx.numel(), counter.data_ptr(), _stream_handle(stream))
+    _check(lib, rc)
+
+
+TELEMETRY_BYTES = 32
+
+
+def new_telemetry(device="cuda"):
+    """A zero-filled telemetry object (see EFS_TELEMETRY_BYTES)."""
+    import torch
+    return torch.zeros(TELEMETRY_BYTES, dtype=torch.uint8, device=device)
+
+
+def read_telemetry(tel) -> dict:
+    """Decode a telemetry object (synchronises with the device)."""
+    import numpy as np
+    raw = tel.cpu().numpy().tobytes()
+    err2, sent = np.frombuffer(raw[:16], dtype="<f8")
+    max_bits, calls = np.frombuffer(raw[16:24], dtype="<u4")
+    return {"err2_total": float(err2), "sent_total": float(sent),
+            "max_abs": float(np.array([max_bits], dtype=np.uint32).view(np.float32)[0]),
+            "max_abs_bits": int(max_bits), "calls": int(calls)}
+
+
+def ht_compress_telemetry(g, e, lr: float, lam: float, idx, val, counter, telemetry,
+                          stream=None) -> None:
+    """ht_compress plus telemetry; see ht_compress_telemetry in include/efsparse.h."""
+    import torch
+    lib = load_library()
+    _require(g, torch.float32, "g")
+    _require(e, torch.float32, "e")
+    _require(idx, torch.int32, "idx")
+    _require(val, torch.float32, "val")
+    _require(counter, torch.int32, "counter")
+    _require(telemetry, torch.uint8, "telemetry")
+    if g.numel() != e.numel() or idx.numel() != val.numel() or counter.numel() < COUNTER_WORDS \
+            or telemetry.numel() < TELEMETRY_BYTES:
+        raise ValueError("size mismatch among g, e, idx, val, counter, telemetry")
+    rc = lib.ht_compress_telemetry(_ptr(g), _ptr(e), g.numel(), float(lr), float(lam), _ptr(idx),
+                                   _ptr(val), idx.numel(), counter.data_ptr(), telemetry.data_ptr(),
+                                   _stream_handle(stream))
     _check(lib, rc)
 
 

@@ -85,21 +85,36 @@ const char *efs_status_string(efs_status s) {
 
 const char *efs_last_error_message(void) { return g_message; }
 
+static efs_status ht_common(const char *name, const float *g, float *e, int64_t d, float lr,
+                            float lambda, int32_t *idx, float *val, int64_t cap, uint32_t *counter,
+                            void *telemetry, void *stream) {
+    if (d < 0 || d > kMaxLen) return fail(EFS_EINVAL, "%s: d=%lld outside [0, 2^31-1]", name, (long long)d);
+    if (d > 0 && (g == nullptr || e == nullptr)) return fail(EFS_EINVAL, "%s: g or e is NULL", name);
+    if (!aligned(g, 4) || !aligned(e, 4)) return fail(EFS_EINVAL, "%s: g and e must be 4-byte aligned", name);
+    if (!std::isfinite(lr)) return fail(EFS_EINVAL, "%s: lr must be finite", name);
+    if (std::isnan(lambda) || lambda < 0.0f) return fail(EFS_EINVAL, "%s: lambda must be >= 0 and not NaN", name);
+    if (cap < 0 || cap > kMaxLen) return fail(EFS_EINVAL, "%s: cap=%lld outside [0, 2^31-1]", name, (long long)cap);
+    if (cap > 0 && (idx == nullptr || val == nullptr)) return fail(EFS_EINVAL, "%s: idx or val is NULL", name);
+    if (!aligned(idx, 4) || !aligned(val, 4)) return fail(EFS_EINVAL, "%s: idx and val must be 4-byte aligned", name);
+    if (counter == nullptr || !aligned(counter, 8)) return fail(EFS_EINVAL, "%s: counter must be non-NULL and 8-byte aligned", name);
+    return check_launch(efs::launch_ht(g, e, d, lr, lambda, idx, val, cap, counter, telemetry,
+                                       static_cast<hipStream_t>(stream)),
+                        name);
+}
+
 efs_status ht_compress(const float *g, float *e, int64_t d, float lr, float lambda,
                        int32_t *idx, float *val, int64_t cap, uint32_t *counter,
                        void *stream) {
-    if (d < 0 || d > kMaxLen) return fail(EFS_EINVAL, "ht_compress: d=%lld outside [0, 2^31-1]", (long long)d);
-    if (d > 0 && (g == nullptr || e == nullptr)) return fail(EFS_EINVAL, "ht_compress: g or e is NULL");
-    if (!aligned(g, 4) || !aligned(e, 4)) return fail(EFS_EINVAL, "ht_compress: g and e must be 4-byte aligned");
-    if (!std::isfinite(lr)) return fail(EFS_EINVAL, "ht_compress: lr must be finite");
-    if (std::isnan(lambda) || lambda < 0.0f) return fail(EFS_EINVAL, "ht_compress: lambda must be >= 0 and not NaN");
-    if (cap < 0 || cap > kMaxLen) return fail(EFS_EINVAL, "ht_compress: cap=%lld outside [0, 2^31-1]", (long long)cap);
-    if (cap > 0 && (idx == nullptr || val == nullptr)) return fail(EFS_EINVAL, "ht_compress: idx or val is NULL");
-    if (!aligned(idx, 4) || !aligned(val, 4)) return fail(EFS_EINVAL, "ht_compress: idx and val must be 4-byte aligned");
-    if (counter == nullptr || !aligned(counter, 8)) return fail(EFS_EINVAL, "ht_compress: counter must be non-NULL and 8-byte aligned");
-    return check_launch(efs::launch_ht(g, e, d, lr, lambda, idx, val, cap, counter,
-                                       static_cast<hipStream_t>(stream)),
-                        "ht_compress");
+    return ht_common("ht_compress", g, e, d, lr, lambda, idx, val, cap, counter, nullptr, stream);
+}
+
+efs_status ht_compress_telemetry(const float *g, float *e, int64_t d, float lr, float lambda,
+                                 int32_t *idx, float *val, int64_t cap, uint32_t *counter,
+                                 void *telemetry, void *stream) {
+    if (telemetry == nullptr || !aligned(telemetry, 8))
+        return fail(EFS_EINVAL, "ht_compress_telemetry: telemetry must be non-NULL and 8-byte aligned");
+    return ht_common("ht_compress_telemetry", g, e, d, lr, lambda, idx, val, cap, counter,
+                     telemetry, stream);
 }
 
 size_t topk_workspace_bytes(int64_t d, int64_t k) {

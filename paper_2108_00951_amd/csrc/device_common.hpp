@@ -94,6 +94,33 @@ __device__ __forceinline__ uint32_t block_sum(uint32_t v, uint32_t *s_wave) {
     return tot;
 }
 
+// Sum of a per-thread double over the workgroup (thread 0's result is the
+// total).  Uses kWaves doubles of LDS; contains two barriers.
+__device__ __forceinline__ double block_sum_f64(double v, double *s_wave) {
+#pragma unroll
+    for (int off = kWave / 2; off > 0; off >>= 1) v += __shfl_xor(v, off);
+    if ((threadIdx.x & (kWave - 1)) == 0) s_wave[threadIdx.x / kWave] = v;
+    __syncthreads();
+    double tot = 0.0;
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) tot += s_wave[w];
+    __syncthreads();
+    return tot;
+}
+
+// Maximum of a per-thread value over the workgroup (every thread gets it).
+__device__ __forceinline__ uint32_t block_max(uint32_t v, uint32_t *s_wave) {
+#pragma unroll
+    for (int off = kWave / 2; off > 0; off >>= 1) v = max(v, uint32_t(__shfl_xor(int(v), off)));
+    if ((threadIdx.x & (kWave - 1)) == 0) s_wave[threadIdx.x / kWave] = v;
+    __syncthreads();
+    uint32_t m = 0;
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) m = max(m, s_wave[w]);
+    __syncthreads();
+    return m;
+}
+
 // Workgroup-local staging of (index, value) pairs in LDS.  Kept pairs of
 // successive tiles are appended here and written to the global payload in
 // coalesced runs, one atomic per flush instead of one per tile.
@@ -112,11 +139,24 @@ using PairStage = PairStageN<kTile>;
 // publishes the total to *count when count is non-null, and returns `word`
 // to zero for the next call.  Slots at or past `cap` are not written.
 // Called by every thread of the workgroup; contains barriers.
+// Error-feedback telemetry accumulated across calls (layout of the C ABI's
+// telemetry object): total error sum_t ||e_{t+1}||^2, total pairs sent
+// sum_t k_t, running max of |e_{t+1}| as a bit pattern, number of calls.
+struct Telemetry {
+    double err2_total;
+    double sent_total;
+    uint32_t max_abs_bits;
+    uint32_t calls;
+    uint64_t reserved;
+};
+static_assert(sizeof(Telemetry) == 32, "telemetry object is 32 bytes");
+
 template <int N>
 __device__ __forceinline__ void stage_flush(PairStageN<N> &st, uint32_t fill, bool last,
                                             unsigned long long *word, uint32_t *count,
                                             uint64_t cap, int32_t *__restrict__ idx,
-                                            float *__restrict__ val) {
+                                            float *__restrict__ val,
+                                            Telemetry *tel = nullptr) {
     __syncthreads();
     if (threadIdx.x == 0) {
         const uint64_t add = (last ? kTicketOne : 0ull) | fill;
@@ -124,6 +164,10 @@ __device__ __forceinline__ void stage_flush(PairStageN<N> &st, uint32_t fill, bo
         const uint64_t base = old & kCountMask;
         if (last && (old >> kTicketShift) == uint64_t(gridDim.x - 1)) {
             if (count != nullptr) *count = uint32_t(base + fill);
+            if (tel != nullptr) {
+                atomicAdd(&tel->sent_total, double(base + fill));
+                atomicAdd(&tel->calls, 1u);
+            }
             __hip_atomic_store(word, 0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         }
         st.base = base;

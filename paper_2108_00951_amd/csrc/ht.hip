@@ -21,15 +21,21 @@
 
 namespace efs {
 
-template <bool kVector>
+// With kStats, every workgroup also sums ||e'||^2 (binary64) and the max of
+// |e'| over its elements and adds them to the telemetry object with one
+// atomic each; the last workgroup adds k_t and counts the call.
+template <bool kVector, bool kStats>
 __global__ __launch_bounds__(kBlock) void ht_fused_kernel(
     const float *__restrict__ g, float *__restrict__ e, int64_t d, float lr, float lambda,
     int32_t *__restrict__ idx, float *__restrict__ val, int64_t cap,
-    uint32_t *__restrict__ counter, uint32_t ntiles) {
+    uint32_t *__restrict__ counter, Telemetry *__restrict__ tel, uint32_t ntiles) {
     __shared__ PairStage st;
+    __shared__ double s_f64[kWaves];
     unsigned long long *word = reinterpret_cast<unsigned long long *>(counter + 2);
     const int tid = threadIdx.x;
     uint32_t fill = 0;  // pairs staged; identical in every thread
+    double err2 = 0.0;  // kStats: sum of e'^2 over this thread's elements
+    uint32_t max_bits = 0u;
 
     for (uint32_t tile = blockIdx.x; tile < ntiles; tile += gridDim.x) {
         const int64_t tile0 = int64_t(tile) * kTile;
@@ -55,6 +61,10 @@ __global__ __launch_bounds__(kBlock) void ht_fused_kernel(
                     p[j][c] = a;
                     keep |= uint32_t(k) << (4 * j + c);
                     out[c] = k ? 0.0f : a;
+                    if (kStats) {
+                        err2 += double(out[c]) * double(out[c]);
+                        max_bits = max(max_bits, magnitude_key(out[c]));
+                    }
                 }
                 e4[j * kBlock + tid] = out;
             }
@@ -72,7 +82,12 @@ __global__ __launch_bounds__(kBlock) void ht_fused_kernel(
                         const bool k = fabsf(a) >= lambda;
                         p[j][c] = a;
                         keep |= uint32_t(k) << (4 * j + c);
-                        e[i] = k ? 0.0f : a;
+                        const float r = k ? 0.0f : a;
+                        e[i] = r;
+                        if (kStats) {
+                            err2 += double(r) * double(r);
+                            max_bits = max(max_bits, magnitude_key(r));
+                        }
                     }
                 }
             }
@@ -99,22 +114,40 @@ __global__ __launch_bounds__(kBlock) void ht_fused_kernel(
         }
         fill += total;
     }
-    stage_flush(st, fill, true, word, counter, uint64_t(cap), idx, val);
+    if (kStats) {
+        const double wg_err2 = block_sum_f64(err2, s_f64);
+        const uint32_t wg_max = block_max(max_bits, st.wave);
+        if (tid == 0) {
+            atomicAdd(&tel->err2_total, wg_err2);
+            atomicMax(&tel->max_abs_bits, wg_max);
+        }
+    }
+    stage_flush(st, fill, true, word, counter, uint64_t(cap), idx, val, kStats ? tel : nullptr);
 }
 
 hipError_t launch_ht(const float *g, float *e, int64_t d, float lr, float lambda,
                      int32_t *idx, float *val, int64_t cap, uint32_t *counter,
-                     hipStream_t stream) {
+                     void *telemetry, hipStream_t stream) {
     const int64_t tiles = d > 0 ? (d + kTile - 1) / kTile : 1;
     const uint32_t ntiles = uint32_t(tiles);
     const uint32_t grid = balanced_grid(tiles, kHtWorkgroupsPerCU);
     const bool vec = ((reinterpret_cast<uintptr_t>(g) | reinterpret_cast<uintptr_t>(e)) & 15u) == 0;
-    if (vec)
-        ht_fused_kernel<true><<<grid, kBlock, 0, stream>>>(g, e, d, lr, lambda, idx, val, cap,
-                                                          counter, ntiles);
-    else
-        ht_fused_kernel<false><<<grid, kBlock, 0, stream>>>(g, e, d, lr, lambda, idx, val, cap,
-                                                           counter, ntiles);
+    Telemetry *tel = static_cast<Telemetry *>(telemetry);
+    if (tel != nullptr) {
+        if (vec)
+            ht_fused_kernel<true, true><<<grid, kBlock, 0, stream>>>(g, e, d, lr, lambda, idx, val,
+                                                                    cap, counter, tel, ntiles);
+        else
+            ht_fused_kernel<false, true><<<grid, kBlock, 0, stream>>>(g, e, d, lr, lambda, idx, val,
+                                                                     cap, counter, tel, ntiles);
+    } else {
+        if (vec)
+            ht_fused_kernel<true, false><<<grid, kBlock, 0, stream>>>(g, e, d, lr, lambda, idx, val,
+                                                                     cap, counter, tel, ntiles);
+        else
+            ht_fused_kernel<false, false><<<grid, kBlock, 0, stream>>>(g, e, d, lr, lambda, idx,
+                                                                      val, cap, counter, tel, ntiles);
+    }
     return hipGetLastError();
 }
 

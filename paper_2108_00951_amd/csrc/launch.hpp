@@ -10,7 +10,7 @@ namespace efs {
 
 hipError_t launch_ht(const float *g, float *e, int64_t d, float lr, float lambda,
                      int32_t *idx, float *val, int64_t cap, uint32_t *counter,
-                     hipStream_t stream);
+                     void *telemetry, hipStream_t stream);
 
 size_t topk_workspace_size(int64_t d, int64_t k);
 size_t topk_path_flag_offset();

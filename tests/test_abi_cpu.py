@@ -73,6 +73,15 @@ def test_ht_rejects_bad_arguments(lib):
         assert lib.efs_last_error_message()
 
 
+def test_ht_telemetry_rejects_bad_arguments(lib):
+    fake = 0x10000
+    for tel in (None, fake + 4):
+        rc = lib.ht_compress_telemetry(fake, fake, 100, 0.1, 1e-3, fake, fake, 10, fake, tel, None)
+        assert rc == binding.EFS_EINVAL
+    rc = lib.ht_compress_telemetry(fake, fake, -1, 0.1, 1e-3, fake, fake, 10, fake, fake, None)
+    assert rc == binding.EFS_EINVAL
+
+
 def test_topk_rejects_bad_arguments(lib):
     fake = 0x10000
     need = lib.topk_workspace_bytes(1000, 10)

@@ -178,6 +178,44 @@ def test_ht_repeat_is_deterministic():
         np.testing.assert_array_equal(o[1], outs[0][1])
 
 
+@pytest.mark.parametrize("unaligned", [False, True])
+def test_ht_telemetry_totals(unaligned):
+    # total error sum_t ||e_{t+1}||^2, total pairs sent and the running max of
+    # |e'|, accumulated over an EF loop, against the oracle's residuals
+    d, T = 1_000_003, 6
+    gs = [synth.small_gradient(500 + t, d) for t in range(T)]
+    lam = synth.calibrate_lambda(gs[0], 0.005)
+    st = HT(d, unaligned=unaligned)
+    tel = efs.new_telemetry(DEV)
+    e_ref = np.zeros(d, dtype=np.float32)
+    err2, sent, maxbits = 0.0, 0, 0
+    for t in range(T):
+        efs.ht_compress_telemetry(to_dev(gs[t], unaligned), st.e, LR, lam, st.idx, st.val, st.ctr,
+                                  tel)
+        ri, rv, e_ref, rk = oracle.ht(gs[t], e_ref, LR, lam)
+        assert efs.counter_value(st.ctr) == rk
+        assert_bits_equal(st.e.cpu().numpy(), e_ref, "e' t=%d" % t)
+        err2 += float(np.sum(e_ref.astype(np.float64) ** 2))
+        sent += rk
+        maxbits = max(maxbits, int(np.max(bits(e_ref) & np.uint32(0x7FFFFFFF))))
+    got = efs.read_telemetry(tel)
+    assert got["calls"] == T
+    assert got["sent_total"] == sent
+    assert got["max_abs_bits"] == maxbits
+    assert got["max_abs"] < lam          # absolute compressor: every residual below lambda
+    assert abs(got["err2_total"] - err2) <= 1e-9 * err2
+
+
+def test_ht_telemetry_empty_and_all_sent():
+    st = HT(4096 * 3 + 1)
+    tel = efs.new_telemetry(DEV)
+    g = synth.small_gradient(9, st.d)
+    efs.ht_compress_telemetry(to_dev(g), st.e, LR, 0.0, st.idx, st.val, st.ctr, tel)
+    got = efs.read_telemetry(tel)
+    assert got == {"err2_total": 0.0, "sent_total": float(st.d), "max_abs": 0.0,
+                   "max_abs_bits": 0, "calls": 1}
+
+
 # ---------------------------------------------------------------------------
 # Top-k
 # ---------------------------------------------------------------------------
