@@ -39,6 +39,10 @@ def _load():
     lib.orc_accumulate.argtypes = [ctypes.POINTER(_i32p), ctypes.POINTER(_f32p), _i64p,
                                    ctypes.c_int32, ctypes.c_int64, _f32p]
     lib.orc_accumulate.restype = ctypes.c_int
+    lib.orc_update.argtypes = [ctypes.POINTER(_i32p), ctypes.POINTER(_f32p), _i64p,
+                               ctypes.c_int32, ctypes.c_int64, ctypes.c_int, _f32p, _f32p,
+                               ctypes.c_float, ctypes.c_float]
+    lib.orc_update.restype = ctypes.c_int
     _lib = lib
     return lib
 
@@ -115,3 +119,26 @@ def accumulate(payloads, d):
     if rc != 0:
         raise ValueError("payload index outside [0, d)")
     return out
+
+
+def update(payloads, x, mode, m=None, beta=0.0, gamma=0.0):
+    """Model update after averaging the payloads: mode 1 x - avg (Algorithm 1),
+    mode 2 the momentum form of Algorithm 2.  Returns (x_new, m_new); the
+    inputs are not modified."""
+    lib = _load()
+    n = len(payloads)
+    idxs = [np.ascontiguousarray(p[0], dtype=np.int32) for p in payloads]
+    vals = [_f32(p[1]) for p in payloads]
+    idx_arr = (_i32p * max(n, 1))(*[_ptr(i, _i32p) for i in idxs])
+    val_arr = (_f32p * max(n, 1))(*[_ptr(v, _f32p) for v in vals])
+    counts = np.array([i.size for i in idxs] or [0], dtype=np.int64)
+    x_new = np.array(x, dtype=np.float32, copy=True)
+    d = x_new.size
+    m_new = (np.zeros(d, dtype=np.float32) if m is None
+             else np.array(m, dtype=np.float32, copy=True))
+    rc = lib.orc_update(idx_arr, val_arr, _ptr(counts, _i64p), n, d, int(mode),
+                        _ptr(x_new, _f32p), _ptr(m_new, _f32p), ctypes.c_float(beta),
+                        ctypes.c_float(gamma))
+    if rc != 0:
+        raise ValueError("bad payload index or mode")
+    return x_new, m_new

@@ -17,6 +17,9 @@
  *                   Lemma 2 in section 4.3); ties broken by lower index.
  *   orc_accumulate  the exchange-and-average step of Algorithm 1,
  *                   (1/n) * sum_i Delta_i, with the sum taken in worker order.
+ *   orc_update      the model update that follows it: x <- x - avg
+ *                   (Algorithm 1) or the momentum form of Algorithm 2
+ *                   (Appendix C.6.2).
  *
  * Arithmetic: IEEE-754 binary32, round to nearest even.  The accumulate is an
  * fp32 multiply followed by a separate fp32 add (never a fused multiply-add);
@@ -30,8 +33,10 @@
  *   - Top-k emits exactly min(k, d) pairs, ranking by the bit pattern of |p|
  *     (so -0 and +0 tie), larger first, then lower index first;
  *   - the average divides the in-order fp32 sum by (float)n with one IEEE
- *     division.
- * Parity: pinned for all three functions (see the oracle tests).
+ *     division;
+ *   - AGGREGATE then DECOMPRESS in Algorithm 2 is that same average, and its
+ *     step size gamma multiplies (avg + m) with m already updated.
+ * Parity: pinned for all four functions (see the oracle tests).
  */
 #include <math.h>
 #include <stdint.h>
@@ -160,5 +165,41 @@ int orc_accumulate(const int32_t *const *idx, const float *const *val,
     }
     float fn = (float)n;
     for (int64_t i = 0; i < d; i++) out[i] = out[i] / fn;
+    return 0;
+}
+
+/* Model update after the exchange-and-average step, applied to every
+ * coordinate with the average avg of orc_accumulate:
+ *   mode 1 (Algorithm 1):  x <- x - avg
+ *   mode 2 (Appendix C.6.2, Algorithm 2: EF SGD with momentum and gradient
+ *           compression; the paper's momentum factor is `beta` here, its
+ *           learning rate `gamma`; the update uses the new m):
+ *           m <- beta*m + avg ;  x <- x - gamma*(avg + m)   (new m)
+ * Each operation is one separately rounded fp32 operation, in the order
+ * written.  Returns 0, or -1 on an index outside [0, d) or an unknown mode.
+ */
+int orc_update(const int32_t *const *idx, const float *const *val,
+               const int64_t *counts, int32_t n, int64_t d, int mode,
+               float *x, float *m, float beta, float gamma)
+{
+    if (mode != 1 && mode != 2) return -1;
+    float *avg = (float *)malloc((size_t)(d > 0 ? d : 1) * sizeof *avg);
+    if (!avg) return -1;
+    if (orc_accumulate(idx, val, counts, n, d, avg) != 0) {
+        free(avg);
+        return -1;
+    }
+    for (int64_t i = 0; i < d; i++) {
+        if (mode == 1) {
+            x[i] = x[i] - avg[i];
+        } else {
+            float decayed = beta * m[i];
+            m[i] = decayed + avg[i];
+            float step = avg[i] + m[i];
+            float scaled = gamma * step;
+            x[i] = x[i] - scaled;
+        }
+    }
+    free(avg);
     return 0;
 }

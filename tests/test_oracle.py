@@ -344,6 +344,110 @@ def test_accumulate_rejects_out_of_range():
 
 
 # --------------------------------------------------------------------------
+# Model update after the average (Algorithm 1; Appendix C.6.2, Algorithm 2)
+# --------------------------------------------------------------------------
+
+def _update_example():
+    ex = G.load("update_example.txt")
+    payloads = [(G.i32(ex["w0_idx"]), G.f32(ex["w0_val"])),
+                (G.i32(ex["w1_idx"]), G.f32(ex["w1_val"]))]
+    return ex, payloads
+
+
+def test_update_hand_example_sgd():
+    ex, payloads = _update_example()
+    x = G.f32(ex["x"])
+    x_new, _ = oracle.update(payloads, x, 1)
+    np.testing.assert_array_equal(bits(x_new), bits(G.f32(ex["sgd_x"])))
+    np.testing.assert_array_equal(bits(x), bits(G.f32(ex["x"])))  # input untouched
+
+
+def test_update_hand_example_momentum():
+    ex, payloads = _update_example()
+    beta, gamma = float(ex["beta"][0]), float(ex["gamma"][0])
+    x_new, m_new = oracle.update(payloads, G.f32(ex["x"]), 2, m=G.f32(ex["m"]),
+                                 beta=beta, gamma=gamma)
+    np.testing.assert_array_equal(bits(m_new), bits(G.f32(ex["mom_m"])))
+    np.testing.assert_array_equal(bits(x_new), bits(G.f32(ex["mom_x"])))
+
+
+def test_update_momentum_without_decay_is_sgd():
+    # beta = 0, gamma = 1/2, one worker: m' = v and x' = x - (v + v)/2 = x - v,
+    # every step exact (doubling and halving a binary32 value are exact)
+    rng = np.random.default_rng(21)
+    d = 4000
+    idx = np.sort(rng.choice(d, 700, replace=False)).astype(np.int32)
+    val = (rng.standard_normal(700) * 1e-2).astype(F32)
+    x = rng.standard_normal(d).astype(F32)
+    x1, _ = oracle.update([(idx, val)], x, 1)
+    x2, m2 = oracle.update([(idx, val)], x, 2, m=rng.standard_normal(d).astype(F32),
+                           beta=0.0, gamma=0.5)
+    np.testing.assert_array_equal(bits(x2), bits(x1))
+    want_m = np.zeros(d, dtype=F32)
+    want_m[idx] = val
+    np.testing.assert_array_equal(bits(m2), bits(want_m))
+
+
+def test_update_untouched_coordinates_keep_x():
+    # x - (+0) = x for every non-NaN binary32 x, -0 and subnormals included
+    x = np.array([-0.0, 0.0, 1e-45, -3e-39, 7.0, -np.inf, np.inf, 2.5], dtype=F32)
+    x_new, _ = oracle.update([(np.array([7], dtype=np.int32), np.array([0.5], dtype=F32))],
+                             x, 1)
+    np.testing.assert_array_equal(bits(x_new[:7]), bits(x[:7]))
+    assert x_new[7] == F32(2.0)
+
+
+def test_update_sgd_uses_in_order_average():
+    # the average of (1, 2^-24, 2^-24) in worker order is fl(1/3) = 0x3EAAAAAB;
+    # x' is x minus that, rounded once (binary64 difference rounded to binary32)
+    ps = [(np.array([0], dtype=np.int32), np.array([v], dtype=F32))
+          for v in (1.0, 2.0 ** -24, 2.0 ** -24)]
+    x = np.array([1.0], dtype=F32)
+    x_new, _ = oracle.update(ps, x, 1)
+    avg = np.float64(f32_from_bits(0x3EAAAAAB))
+    assert bits(x_new)[0] == bits(np.array([1.0 - avg]).astype(F32))[0]
+
+
+def test_update_momentum_closed_form():
+    # constant average a, m_0 = 0: m_t = a (1 - beta^t) / (1 - beta) and
+    # x_T = x_0 - gamma * sum_t (a + m_t)
+    #     = x_0 - gamma * (T a + a/(1-beta) * (T - beta (1 - beta^T)/(1 - beta)))
+    # checked against T fp32 steps within a running rounding-error bound
+    rng = np.random.default_rng(22)
+    d, T, beta, gamma = 64, 40, F32(0.9), F32(0.05)
+    idx = np.arange(d, dtype=np.int32)
+    a = (rng.standard_normal(d) * 1e-2).astype(F32)
+    x = rng.standard_normal(d).astype(F32)
+    x0 = x.astype(np.float64)
+    m = np.zeros(d, dtype=F32)
+    for _ in range(T):
+        x, m = oracle.update([(idx, a)], x, 2, m=m, beta=float(beta), gamma=float(gamma))
+    b, g, a64 = np.float64(beta), np.float64(gamma), a.astype(np.float64)
+    m_exact = a64 * (1 - b ** T) / (1 - b)
+    x_exact = x0 - g * (T * a64 + a64 / (1 - b) * (T - b * (1 - b ** T) / (1 - b)))
+    u = 2.0 ** -24
+    # each m step: two roundings of size <= u*|m_t|, damped by beta afterwards
+    m_bound = 2 * u * np.abs(m_exact) / (1 - b) * 1.01 + 1e-30
+    np.testing.assert_array_less(np.abs(m.astype(np.float64) - m_exact), m_bound)
+    # each x step: roundings of (a+m), gamma*(.), x - (.), plus gamma times m's error
+    x_bound = T * (u * (np.abs(x0) + np.abs(x_exact)) * 1.01 +
+                   6 * u * g * (np.abs(a64) + np.abs(m_exact)) +
+                   g * m_bound) + 1e-30
+    np.testing.assert_array_less(np.abs(x.astype(np.float64) - x_exact), x_bound)
+    # and the recurrence really moved x by the closed-form amount
+    assert np.all(np.abs(x_exact - x0) > 100 * x_bound)
+
+
+def test_update_rejects_bad_mode_and_index():
+    p = [(np.array([3], dtype=np.int32), np.array([1.0], dtype=F32))]
+    with pytest.raises(ValueError):
+        oracle.update(p, np.zeros(3, dtype=F32), 1)
+    with pytest.raises(ValueError):
+        oracle.update([(np.array([0], dtype=np.int32), np.array([1.0], dtype=F32))],
+                      np.zeros(3, dtype=F32), 3)
+
+
+# --------------------------------------------------------------------------
 # The EF loop: virtual-iterate telescoping (Appendix B.2, n = 1)
 # --------------------------------------------------------------------------
 
