@@ -81,6 +81,8 @@ def parse():
                     help="summary written by --parse-pmc (HBM bytes per hard-threshold launch)")
     ap.add_argument("--parse-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
                     help="summarise two rocprofv3 --pmc output folders and exit")
+    ap.add_argument("--no-apply", action="store_true",
+                    help="skip the fused update timings (sparse_apply, 1 and 8 workers)")
     ap.add_argument("--sweep", action="store_true",
                     help="also time the hard-threshold kernel on the 110e6 Student-t and "
                          "1.5e9 outlier workloads (adds ~1 min of input generation)")
@@ -348,6 +350,9 @@ def main():
         },
     }
 
+    if not args.no_apply:
+        line["sparse_apply"] = apply_bench(efs, torch, synth, cur, args.b2b, (idx, val, ctr), d,
+                                           out)
     if args.sweep:
         del pool, e_tk, out, ws
         line["ht_sweep"] = ht_sweep(efs, torch, synth, cur, args.b2b)
@@ -408,6 +413,71 @@ def ht_sweep(efs, torch, synth, cur, reps):
         print("sweep %s: %s" % (st.w.name, res[st.w.name]), file=sys.stderr, flush=True)
         del gs, e, idx, val
         torch.cuda.empty_cache()
+    return res
+
+
+def apply_bench(efs, torch, synth, cur, reps, ht_payload, d, out):
+    """Back-to-back sparse_apply launches in each mode: on the step's own
+    hard-threshold payload (1 worker), and on 8 workers' payloads of the
+    8-worker workload (same d and segment layout, 0.1 % first-step density),
+    next to sparse_accumulate on the same payloads.  Algorithmic bytes:
+    average 8 per pair + 4 d; sgd 8 per pair + 8 per touched coordinate;
+    momentum 8 per pair + 16 d."""
+    import numpy as np
+
+    def timed(fn):
+        a = torch.cuda.Event(enable_timing=True)
+        b = torch.cuda.Event(enable_timing=True)
+        fn()
+        torch.cuda.synchronize()
+        a.record(cur)
+        for _ in range(reps):
+            fn()
+        b.record(cur)
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) * 1e3 / reps
+
+    def measure(payloads):
+        pairs = sum(efs.counter_value(p[2]) for p in payloads)
+        touched = int(torch.unique(torch.cat(
+            [p[0][:efs.counter_value(p[2])] for p in payloads])).numel())
+        ws = efs.new_apply_workspace(payloads, d, "cuda")
+        x = torch.zeros(d, dtype=torch.float32, device="cuda")
+        m = torch.zeros(d, dtype=torch.float32, device="cuda")
+        res = {"pairs": pairs, "touched": touched, "workspace_mb": round(ws.numel() / 2 ** 20, 1)}
+        for mode, name, nbytes in (
+                (efs.APPLY_AVERAGE, "average", 8.0 * pairs + 4.0 * d),
+                (efs.APPLY_SGD, "sgd", 8.0 * pairs + 8.0 * touched),
+                (efs.APPLY_MOMENTUM, "momentum", 8.0 * pairs + 16.0 * d)):
+            us = timed(efs.prepare_sparse_apply(payloads, d, mode, x, ws, m=m, beta=0.9,
+                                                gamma=0.05))
+            res[name] = {"us": round(us, 2), "gbps": round(nbytes / (us * 1e-6) / 1e9, 1)}
+        us = timed(efs.prepare_sparse_accumulate(payloads, d, out))
+        res["sparse_accumulate_us"] = round(us, 2)
+        del ws, x, m
+        return res
+
+    res = {"workers_1": measure([ht_payload])}
+    st = synth.Stream(4)
+    w = st.w
+    assert w.d == d
+    lam = synth.calibrate_lambda(st.gradient(0, worker=0, threads=16), w.densities[0])
+    payloads = []
+    for wk in range(w.n_workers):
+        g = torch.from_numpy(st.gradient(0, worker=wk, threads=16)).to("cuda")
+        e = torch.zeros(d, dtype=torch.float32, device="cuda")
+        cap = d // 100
+        idx = torch.empty(cap, dtype=torch.int32, device="cuda")
+        val = torch.empty(cap, dtype=torch.float32, device="cuda")
+        ctr = efs.new_counter("cuda")
+        efs.ht_compress(g, e, synth.LR, lam, idx, val, ctr)
+        if efs.counter_value(ctr) > cap:
+            raise RuntimeError("apply bench payload capacity exceeded")
+        payloads.append((idx, val, ctr))
+        del g, e
+    res["workers_8"] = measure(payloads)
+    print("sparse_apply: %s" % res, file=sys.stderr, flush=True)
+    torch.cuda.empty_cache()
     return res
 
 

@@ -149,6 +149,53 @@ efs_status sparse_accumulate(const int32_t *const *idx, const float *const *val,
                              const uint32_t *const *counts, const int64_t *caps,
                              int32_t n_workers, int64_t d, float *out, void *stream);
 
+/* Exchange-and-average fused with the model update that follows it.
+ *
+ *   avg = (sum over w = 0..n-1, in that order, of decompress(payload_w)) / n
+ * exactly as sparse_accumulate computes it (fp32 adds in worker order, one
+ * IEEE division by (float)n), then, by mode:
+ *   EFS_APPLY_AVERAGE   x = avg at every coordinate (x is the output).
+ *   EFS_APPLY_SGD       x = x - avg (Algorithm 1, model update).  Only
+ *                       coordinates that some payload touches are written;
+ *                       the others keep x, which equals x - (+0) for every
+ *                       value except a signalling NaN.
+ *   EFS_APPLY_MOMENTUM  m = beta*m + avg, then x = x - gamma*(avg + m) with the
+ *                       new m, at every coordinate (Appendix C.6.2,
+ *                       Algorithm 2: EF SGD with momentum and gradient
+ *                       compression; the paper writes the momentum factor
+ *                       as lambda and the learning rate as gamma).
+ * Every operation is one separately rounded fp32 operation, in the order
+ * written (no fused multiply-add).
+ *
+ *   idx, val, counts, caps, n_workers   as for sparse_accumulate, with
+ *              1 <= n_workers <= EFS_APPLY_MAX_WORKERS and
+ *              sum of caps <= 2^32 - 1.  Entries with an index outside
+ *              [0, d) are ignored.
+ *   x          [d] fp32, 16-byte aligned, read and written in place (mode
+ *              EFS_APPLY_AVERAGE only writes it).  Must not overlap a payload.
+ *   m          [d] fp32 momentum, 16-byte aligned, read and written in place;
+ *              used by EFS_APPLY_MOMENTUM only (may be NULL otherwise).
+ *   beta, gamma  momentum factor and learning rate (finite); used by
+ *              EFS_APPLY_MOMENTUM only.
+ *   workspace  device memory of at least
+ *              sparse_apply_workspace_bytes(n_workers, d, sum of caps) bytes,
+ *              16-byte aligned: one counter per range of 8192
+ *              coordinates, and 8 bytes per payload slot for the pairs
+ *              grouped by range.  Results never depend on its prior
+ *              contents.  Not shareable between concurrent calls.
+ * Returns EFS_ESPACE if the workspace is too small, EFS_EINVAL on any other
+ * invalid argument; nothing is launched then.  d == 0 is a no-op. */
+#define EFS_APPLY_MAX_WORKERS 32
+enum { EFS_APPLY_AVERAGE = 0, EFS_APPLY_SGD = 1, EFS_APPLY_MOMENTUM = 2 };
+
+/* Workspace bytes for sparse_apply; 0 if the arguments are out of range. */
+size_t sparse_apply_workspace_bytes(int32_t n_workers, int64_t d, int64_t total_cap);
+
+efs_status sparse_apply(const int32_t *const *idx, const float *const *val,
+                        const uint32_t *const *counts, const int64_t *caps, int32_t n_workers,
+                        int64_t d, int mode, float *x, float *m, float beta, float gamma,
+                        void *workspace, size_t workspace_bytes, void *stream);
+
 /* Streaming copy dst[0..n) = src[0..n) with the same 16-byte access pattern
  * as the compression kernels: a bandwidth ceiling for measurements, not part
  * of the method.  src and dst 16-byte aligned, n >= 0. */

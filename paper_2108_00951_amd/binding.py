@@ -64,6 +64,12 @@ def declare(lib):
     lib.sparse_accumulate.argtypes = [ctypes.POINTER(vp), ctypes.POINTER(vp), ctypes.POINTER(vp),
                                       ctypes.POINTER(i64), i32, i64, vp, vp]
     lib.sparse_accumulate.restype = ctypes.c_int
+    lib.sparse_apply_workspace_bytes.argtypes = [i32, i64, i64]
+    lib.sparse_apply_workspace_bytes.restype = ctypes.c_size_t
+    lib.sparse_apply.argtypes = [ctypes.POINTER(vp), ctypes.POINTER(vp), ctypes.POINTER(vp),
+                                 ctypes.POINTER(i64), i32, i64, ctypes.c_int, vp, vp, f32, f32, vp,
+                                 ctypes.c_size_t, vp]
+    lib.sparse_apply.restype = ctypes.c_int
     lib.efs_copy_probe.argtypes = [vp, vp, i64, vp]
     lib.efs_copy_probe.restype = ctypes.c_int
     lib.efs_stream_probe.argtypes = [vp, vp, i64, ctypes.c_int, vp]
@@ -201,17 +207,11 @@ def topk_compress(g, e, lr: float, k: int, idx, val, workspace, stream=None) -> 
     _check(lib, rc)
 
 
-def sparse_accumulate(payloads: Sequence[Tuple], d: int, out, stream=None) -> None:
-    """Average of n payloads into out; see sparse_accumulate in include/efsparse.h.
-
-    payloads: sequence of (idx, val, counter_or_None); without a counter the
-    whole idx/val tensor is the payload.
-    """
+def _payload_arrays(payloads: Sequence[Tuple]):
+    """Host arrays of device pointers and capacities for n payloads, each
+    (idx, val, counter_or_None); without a counter the whole idx/val tensor
+    is the payload."""
     import torch
-    lib = load_library()
-    _require(out, torch.float32, "out")
-    if out.numel() != d:
-        raise ValueError("out must have d elements")
     n = len(payloads)
     vp = ctypes.c_void_p
     idx_arr = (vp * max(n, 1))()
@@ -225,13 +225,86 @@ def sparse_accumulate(payloads: Sequence[Tuple], d: int, out, stream=None) -> No
         _require(val, torch.float32, "val[%d]" % w)
         if idx.numel() != val.numel():
             raise ValueError("payload %d: idx and val differ in length" % w)
+        if cnt is not None:
+            _require(cnt, torch.int32, "counter[%d]" % w)
         idx_arr[w] = _ptr(idx)
         val_arr[w] = _ptr(val)
         cnt_arr[w] = cnt.data_ptr() if cnt is not None else None
         caps[w] = idx.numel()
-    rc = lib.sparse_accumulate(idx_arr, val_arr, cnt_arr, caps, n, int(d), _ptr(out),
-                               _stream_handle(stream))
-    _check(lib, rc)
+    return idx_arr, val_arr, cnt_arr, caps
+
+
+def sparse_accumulate(payloads: Sequence[Tuple], d: int, out, stream=None) -> None:
+    """Average of n payloads into out; see sparse_accumulate in include/efsparse.h.
+
+    payloads: sequence of (idx, val, counter_or_None).
+    """
+    prepare_sparse_accumulate(payloads, d, out, stream)()
+
+
+APPLY_AVERAGE, APPLY_SGD, APPLY_MOMENTUM = 0, 1, 2
+
+
+def sparse_apply_workspace_bytes(n_workers: int, d: int, total_cap: int) -> int:
+    return int(load_library().sparse_apply_workspace_bytes(int(n_workers), int(d), int(total_cap)))
+
+
+def new_apply_workspace(payloads: Sequence[Tuple], d: int, device="cuda"):
+    """A workspace for sparse_apply over payloads of these capacities."""
+    import torch
+    total = sum(int(p[0].numel()) for p in payloads)
+    nbytes = sparse_apply_workspace_bytes(len(payloads), d, total)
+    return torch.empty(max(nbytes, 16), dtype=torch.uint8, device=device)
+
+
+def prepare_sparse_apply(payloads: Sequence[Tuple], d: int, mode: int, x, workspace, m=None,
+                         beta: float = 0.0, gamma: float = 0.0, stream=None):
+    """Marshal the arguments of sparse_apply once and return a callable that
+    issues the call with them (for loops that repeat the same call on the
+    same buffers: the per-call cost is then one C call)."""
+    import torch
+    lib = load_library()
+    _require(x, torch.float32, "x")
+    _require(workspace, torch.uint8, "workspace")
+    if x.numel() != d:
+        raise ValueError("x must have d elements")
+    if m is not None:
+        _require(m, torch.float32, "m")
+        if m.numel() != d:
+            raise ValueError("m must have d elements")
+    idx_arr, val_arr, cnt_arr, caps = _payload_arrays(payloads)
+    args = (idx_arr, val_arr, cnt_arr, caps, len(payloads), int(d), int(mode), _ptr(x), _ptr(m),
+            float(beta), float(gamma), _ptr(workspace), workspace.numel(), _stream_handle(stream))
+    fn = lib.sparse_apply
+
+    def call():
+        _check(lib, fn(*args))
+    return call
+
+
+def sparse_apply(payloads: Sequence[Tuple], d: int, mode: int, x, workspace, m=None,
+                 beta: float = 0.0, gamma: float = 0.0, stream=None) -> None:
+    """Average of n payloads fused with the model update; see sparse_apply in
+    include/efsparse.h.  payloads as for sparse_accumulate."""
+    prepare_sparse_apply(payloads, d, mode, x, workspace, m, beta, gamma, stream)()
+
+
+def prepare_sparse_accumulate(payloads: Sequence[Tuple], d: int, out, stream=None):
+    """sparse_accumulate with its arguments marshalled once (see
+    prepare_sparse_apply)."""
+    import torch
+    lib = load_library()
+    _require(out, torch.float32, "out")
+    if out.numel() != d:
+        raise ValueError("out must have d elements")
+    idx_arr, val_arr, cnt_arr, caps = _payload_arrays(payloads)
+    args = (idx_arr, val_arr, cnt_arr, caps, len(payloads), int(d), _ptr(out),
+            _stream_handle(stream))
+    fn = lib.sparse_accumulate
+
+    def call():
+        _check(lib, fn(*args))
+    return call
 
 
 def copy_probe(src, dst, stream=None) -> None:

@@ -11,6 +11,8 @@
 #include "../../include/efsparse.h"
 #include "launch.hpp"
 
+static_assert(efs::kMaxApplyWorkers == EFS_APPLY_MAX_WORKERS, "worker limit differs from the header");
+
 namespace {
 
 thread_local char g_message[256] = "";
@@ -166,6 +168,59 @@ efs_status sparse_accumulate(const int32_t *const *idx, const float *const *val,
     return check_launch(efs::launch_accumulate(idx, val, counts, caps, n_workers, d, out,
                                                static_cast<hipStream_t>(stream)),
                         "sparse_accumulate");
+}
+
+size_t sparse_apply_workspace_bytes(int32_t n_workers, int64_t d, int64_t total_cap) {
+    if (n_workers < 1 || n_workers > efs::kMaxApplyWorkers || d < 0 || d > kMaxLen ||
+        total_cap < 0 || total_cap > int64_t(UINT32_MAX))
+        return 0;
+    return efs::apply_workspace_size(n_workers, d, total_cap);
+}
+
+efs_status sparse_apply(const int32_t *const *idx, const float *const *val,
+                        const uint32_t *const *counts, const int64_t *caps, int32_t n_workers,
+                        int64_t d, int mode, float *x, float *m, float beta, float gamma,
+                        void *workspace, size_t workspace_bytes, void *stream) {
+    if (n_workers < 1 || n_workers > efs::kMaxApplyWorkers)
+        return fail(EFS_EINVAL, "sparse_apply: n_workers=%d outside [1, %d]", n_workers,
+                    efs::kMaxApplyWorkers);
+    if (d < 0 || d > kMaxLen) return fail(EFS_EINVAL, "sparse_apply: d=%lld outside [0, 2^31-1]", (long long)d);
+    if (mode < EFS_APPLY_AVERAGE || mode > EFS_APPLY_MOMENTUM)
+        return fail(EFS_EINVAL, "sparse_apply: mode %d is not one of EFS_APPLY_*", mode);
+    if (idx == nullptr || val == nullptr || caps == nullptr)
+        return fail(EFS_EINVAL, "sparse_apply: idx, val and caps must be host arrays");
+    if (d > 0 && (x == nullptr || !aligned(x, 16)))
+        return fail(EFS_EINVAL, "sparse_apply: x must be non-NULL and 16-byte aligned");
+    if (mode == EFS_APPLY_MOMENTUM) {
+        if (d > 0 && (m == nullptr || !aligned(m, 16)))
+            return fail(EFS_EINVAL, "sparse_apply: m must be non-NULL and 16-byte aligned");
+        if (d > 0 && m == x) return fail(EFS_EINVAL, "sparse_apply: m and x must not alias");
+        if (!std::isfinite(beta) || !std::isfinite(gamma))
+            return fail(EFS_EINVAL, "sparse_apply: beta and gamma must be finite");
+    }
+    int64_t total = 0;
+    for (int32_t w = 0; w < n_workers; ++w) {
+        if (caps[w] < 0 || caps[w] > kMaxLen)
+            return fail(EFS_EINVAL, "sparse_apply: caps[%d]=%lld outside [0, 2^31-1]", w, (long long)caps[w]);
+        if (caps[w] > 0 && (idx[w] == nullptr || val[w] == nullptr))
+            return fail(EFS_EINVAL, "sparse_apply: payload %d has a NULL pointer", w);
+        if (!aligned(idx[w], 4) || !aligned(val[w], 4))
+            return fail(EFS_EINVAL, "sparse_apply: payload %d is not 4-byte aligned", w);
+        if (counts != nullptr && counts[w] != nullptr && !aligned(counts[w], 4))
+            return fail(EFS_EINVAL, "sparse_apply: count %d is not 4-byte aligned", w);
+        total += caps[w];
+    }
+    if (total > int64_t(UINT32_MAX))
+        return fail(EFS_EINVAL, "sparse_apply: total capacity %lld exceeds 2^32-1 pairs", (long long)total);
+    if (d == 0) return EFS_OK;
+    if (workspace == nullptr || !aligned(workspace, 16))
+        return fail(EFS_EINVAL, "sparse_apply: workspace must be non-NULL and 16-byte aligned");
+    const size_t need = efs::apply_workspace_size(n_workers, d, total);
+    if (workspace_bytes < need)
+        return fail(EFS_ESPACE, "sparse_apply: workspace has %zu bytes, needs %zu", workspace_bytes, need);
+    return check_launch(efs::launch_apply(idx, val, counts, caps, n_workers, d, mode, x, m, beta,
+                                          gamma, workspace, static_cast<hipStream_t>(stream)),
+                        "sparse_apply");
 }
 
 efs_status efs_copy_probe(const float *src, float *dst, int64_t n, void *stream) {

@@ -21,12 +21,23 @@ hipError_t launch_accumulate(const int32_t *const *idx, const float *const *val,
                              const uint32_t *const *counts, const int64_t *caps,
                              int32_t n, int64_t d, float *out, hipStream_t stream);
 
+// Exchange-and-average fused with the model update (apply.hip).
+constexpr int kMaxApplyWorkers = 32;
+size_t apply_workspace_size(int32_t n, int64_t d, int64_t total_cap);
+hipError_t launch_apply(const int32_t *const *idx, const float *const *val,
+                        const uint32_t *const *counts, const int64_t *caps, int32_t n,
+                        int64_t d, int mode, float *x, float *m, float beta, float gamma,
+                        void *workspace, hipStream_t stream);
+
 hipError_t launch_copy(const float *src, float *dst, int64_t n, hipStream_t stream);
 hipError_t launch_stream_probe(const float *x, float *y, int64_t n, int mode, hipStream_t stream);
 
 // Workgroups for a grid-stride pass over `work_tiles` tiles: enough to fill
 // every compute unit several times over, never more than there is work.
 uint32_t persistent_grid(int64_t work_tiles);
+
+// Compute units of the current device (queried once per device).
+int device_cu_count();
 
 // Grid for a grid-stride pass in which every workgroup stays resident: the
 // fewest tiles per workgroup that the resident workgroups allow, and just

@@ -128,3 +128,60 @@ def test_workspace_size_grows_with_tiles(lib):
     assert b - a >= 4 * 999 - 255
     assert lib.topk_workspace_bytes(-1, 1) == 0
     assert lib.topk_workspace_bytes(1_500_000_000, 1_500_000) % 256 == 0
+
+
+def test_apply_rejects_bad_arguments(lib):
+    vp = ctypes.c_void_p
+    fake = 0x10000
+    idx = (vp * 2)(fake, fake)
+    val = (vp * 2)(fake, fake)
+    caps = (ctypes.c_int64 * 2)(5, 5)
+    need = lib.sparse_apply_workspace_bytes(2, 100, 10)
+    assert need >= 10 * 8
+
+    def call(**over):
+        a = dict(idx=idx, val=val, caps=caps, n=2, d=100, mode=binding.APPLY_MOMENTUM, x=fake,
+                 m=fake + 4096, beta=0.9, gamma=0.1, ws=fake, ws_bytes=need)
+        a.update(over)
+        return lib.sparse_apply(a["idx"], a["val"], None, a["caps"], a["n"], a["d"], a["mode"],
+                                a["x"], a["m"], a["beta"], a["gamma"], a["ws"], a["ws_bytes"],
+                                None)
+
+    cases = [
+        (dict(n=0), binding.EFS_EINVAL),
+        (dict(n=33), binding.EFS_EINVAL),
+        (dict(d=-1), binding.EFS_EINVAL),
+        (dict(mode=3), binding.EFS_EINVAL),
+        (dict(mode=-1), binding.EFS_EINVAL),
+        (dict(x=NULL), binding.EFS_EINVAL),
+        (dict(x=fake + 4), binding.EFS_EINVAL),
+        (dict(m=NULL), binding.EFS_EINVAL),
+        (dict(m=fake + 8), binding.EFS_EINVAL),
+        (dict(m=fake), binding.EFS_EINVAL),              # aliases x
+        (dict(beta=float("nan")), binding.EFS_EINVAL),
+        (dict(gamma=float("inf")), binding.EFS_EINVAL),
+        (dict(caps=(ctypes.c_int64 * 2)(5, -1)), binding.EFS_EINVAL),
+        (dict(idx=(vp * 2)(fake, None)), binding.EFS_EINVAL),
+        (dict(val=(vp * 2)(fake + 2, fake)), binding.EFS_EINVAL),
+        (dict(ws=NULL), binding.EFS_EINVAL),
+        (dict(ws=fake + 8), binding.EFS_EINVAL),
+        (dict(ws_bytes=need - 1), binding.EFS_ESPACE),
+    ]
+    for over, want in cases:
+        assert call(**over) == want, over
+        assert lib.efs_last_error_message()
+    # m, beta and gamma are not used by the other modes; d = 0 is a no-op
+    assert call(mode=binding.APPLY_SGD, m=NULL, beta=float("nan"), ws_bytes=need - 1) == \
+        binding.EFS_ESPACE
+    assert call(d=0, ws=NULL) == binding.EFS_OK
+
+
+def test_apply_workspace_size(lib):
+    assert lib.sparse_apply_workspace_bytes(0, 100, 10) == 0
+    assert lib.sparse_apply_workspace_bytes(33, 100, 10) == 0
+    assert lib.sparse_apply_workspace_bytes(2, -1, 10) == 0
+    assert lib.sparse_apply_workspace_bytes(2, 100, 2 ** 32) == 0
+    a = lib.sparse_apply_workspace_bytes(8, 25_600_000, 0)
+    b = lib.sparse_apply_workspace_bytes(8, 25_600_000, 1000)
+    assert b - a == 8000                     # 8 bytes per pair slot
+    assert a >= (25_600_000 // 8192) * 4       # one counter per 8192-coordinate range

@@ -145,6 +145,14 @@ def test_workload4_eight_workers_average():
     workers = [Worker(w.d, w.d // 4) for _ in range(w.n_workers)]
     e_ref = [np.zeros(w.d, np.float32) for _ in range(w.n_workers)]
     out = torch.empty(w.d, dtype=torch.float32, device=DEV)
+    # model state for the fused update (Algorithm 2's momentum form and
+    # Algorithm 1's x - avg on a copy)
+    rng = np.random.default_rng(4)
+    x_ref = rng.standard_normal(w.d).astype(np.float32)
+    m_ref = np.zeros(w.d, np.float32)
+    x, m = torch.from_numpy(x_ref).to(DEV), torch.from_numpy(m_ref).to(DEV)
+    p_dev = [(o.idx, o.val, o.ctr) for o in workers]
+    ws = efs.new_apply_workspace(p_dev, w.d, DEV)
     for t in range(2):
         payloads = []
         for wk in range(w.n_workers):
@@ -156,11 +164,21 @@ def test_workload4_eight_workers_average():
             assert_payload_equal(gi, gv, ri, rv, "worker %d t=%d" % (wk, t))
             # the device payload, in its own (unspecified) order, is what is averaged
             payloads.append((gi, gv))
-        efs.sparse_accumulate([(x.idx, x.val, x.ctr) for x in workers], w.d, out)
+        efs.sparse_accumulate(p_dev, w.d, out)
         ref = oracle.accumulate(payloads, w.d)
         assert_bits_equal(out.cpu().numpy(), ref, "average t=%d" % t)
         say("workload 4 t=%d: 8 workers averaged, k_t=%s" % (
-            t, [efs.counter_value(x.ctr) for x in workers]))
+            t, [efs.counter_value(o.ctr) for o in workers]))
+        x_sgd = x.clone()
+        efs.sparse_apply(p_dev, w.d, efs.APPLY_SGD, x_sgd, ws)
+        want_sgd, _ = oracle.update(payloads, x_ref, 1)
+        assert_bits_equal(x_sgd.cpu().numpy(), want_sgd, "sgd update t=%d" % t)
+        del x_sgd, want_sgd
+        efs.sparse_apply(p_dev, w.d, efs.APPLY_MOMENTUM, x, ws, m=m, beta=0.9, gamma=0.05)
+        x_ref, m_ref = oracle.update(payloads, x_ref, 2, m=m_ref, beta=0.9, gamma=0.05)
+        assert_bits_equal(m.cpu().numpy(), m_ref, "momentum m t=%d" % t)
+        assert_bits_equal(x.cpu().numpy(), x_ref, "momentum x t=%d" % t)
+        say("workload 4 t=%d: fused sgd and momentum updates ok" % t)
 
 
 @pytest.mark.timeout(900)
