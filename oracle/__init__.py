@@ -43,6 +43,9 @@ def _load():
                                ctypes.c_int32, ctypes.c_int64, ctypes.c_int, _f32p, _f32p,
                                ctypes.c_float, ctypes.c_float]
     lib.orc_update.restype = ctypes.c_int
+    lib.orc_topk_segmented.argtypes = [_f32p, _f32p, ctypes.c_int64, ctypes.c_float,
+                                       ctypes.c_int32, _i64p, _i64p, _i32p, _f32p]
+    lib.orc_topk_segmented.restype = ctypes.c_int64
     _lib = lib
     return lib
 
@@ -142,3 +145,26 @@ def update(payloads, x, mode, m=None, beta=0.0, gamma=0.0):
     if rc != 0:
         raise ValueError("bad payload index or mode")
     return x_new, m_new
+
+
+def topk_segmented(g, e, lr, offsets, ks):
+    """Layer-wise Top-k (Appendix C.5): Top-k with k = ks[s] on each segment
+    [offsets[s], offsets[s+1]).  Returns (idx, val, e_next): segment by
+    segment, ascending index order within each, global indices."""
+    lib = _load()
+    g = _f32(g)
+    e_next = np.array(e, dtype=np.float32, copy=True)
+    d = g.size
+    off = np.ascontiguousarray(offsets, dtype=np.int64)
+    k = np.ascontiguousarray(ks, dtype=np.int64)
+    nseg = k.size
+    assert off.size == nseg + 1
+    total = int(np.minimum(np.maximum(k, 0), np.diff(off)).sum()) if nseg else 0
+    idx = np.empty(max(total, 1), dtype=np.int32)
+    val = np.empty(max(total, 1), dtype=np.float32)
+    n = lib.orc_topk_segmented(_ptr(g, _f32p), _ptr(e_next, _f32p), d, ctypes.c_float(lr), nseg,
+                               _ptr(off, _i64p), _ptr(k, _i64p), _ptr(idx, _i32p),
+                               _ptr(val, _f32p))
+    if n < 0:
+        raise ValueError("bad segment layout")
+    return idx[:n].copy(), val[:n].copy(), e_next

@@ -15,6 +15,8 @@
  *                   S_lambda(x) = { i : |x[i]| >= lambda }  (section 4.2).
  *   orc_topk        the same steps with the Top-k sparsifier (section 1,
  *                   Lemma 2 in section 4.3); ties broken by lower index.
+ *   orc_topk_segmented  layer-wise Top-k (Appendix C.5): orc_topk on each
+ *                   segment of the vector with its own k.
  *   orc_accumulate  the exchange-and-average step of Algorithm 1,
  *                   (1/n) * sum_i Delta_i, with the sum taken in worker order.
  *   orc_update      the model update that follows it: x <- x - avg
@@ -36,7 +38,7 @@
  *     division;
  *   - AGGREGATE then DECOMPRESS in Algorithm 2 is that same average, and its
  *     step size gamma multiplies (avg + m) with m already updated.
- * Parity: pinned for all four functions (see the oracle tests).
+ * Parity: pinned for all five functions (see the oracle tests).
  */
 #include <math.h>
 #include <stdint.h>
@@ -142,6 +144,32 @@ int orc_topk(const float *g, float *e, int64_t d, float lr, int64_t k,
     free(rank);
     free(kept);
     return 0;
+}
+
+/* Layer-wise Top-k (Appendix C.5): the Top-k sparsifier applied to each
+ * layer separately.  Segment s is coordinates [off[s], off[s+1]) and keeps
+ * min(k[s], its size) of them, chosen exactly as orc_topk chooses them within
+ * the segment.  The payload lists segment 0's pairs, then segment 1's, and so
+ * on, each segment's in ascending index order; indices are global.  e is
+ * updated in place as by orc_topk.  Returns the number of pairs written, or
+ * -1 on a bad layout (off[0] != 0, off[nseg] != d, a decreasing offset, a
+ * negative k) or a failed scratch allocation.
+ */
+int64_t orc_topk_segmented(const float *g, float *e, int64_t d, float lr, int32_t nseg,
+                           const int64_t *off, const int64_t *k, int32_t *idx, float *val)
+{
+    if (nseg < 1 || off[0] != 0 || off[nseg] != d) return -1;
+    for (int32_t s = 0; s < nseg; s++)
+        if (off[s + 1] < off[s] || k[s] < 0) return -1;
+    int64_t out = 0;
+    for (int32_t s = 0; s < nseg; s++) {
+        const int64_t size = off[s + 1] - off[s];
+        const int64_t ks = k[s] < size ? k[s] : size;
+        if (orc_topk(g + off[s], e + off[s], size, lr, ks, idx + out, val + out) != 0) return -1;
+        for (int64_t j = 0; j < ks; j++) idx[out + j] += (int32_t)off[s];
+        out += ks;
+    }
+    return out;
 }
 
 /* Exchange-and-average step of Algorithm 1, one device standing in for the

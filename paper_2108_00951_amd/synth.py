@@ -220,3 +220,12 @@ def lambda_from_k(k: int) -> float:
 def lambda_in_update_units(lam_paper: float, lr=LR) -> np.float32:
     """Algorithm 1 compresses p/gamma; its threshold in units of p is gamma*lambda."""
     return np.float32(np.float32(lr) * np.float32(lam_paper))
+
+
+def layerwise_k(bounds, density: float) -> np.ndarray:
+    """Per-layer budgets for layer-wise Top-k at a density: k_s = ceil(rho d_s)
+    for each segment [bounds[s], bounds[s+1]) (at least one coordinate of a
+    non-empty segment, never more than the segment holds)."""
+    sizes = np.diff(np.asarray(bounds, dtype=np.int64))
+    k = np.ceil(sizes * float(density)).astype(np.int64)
+    return np.minimum(np.maximum(k, (sizes > 0).astype(np.int64)), sizes)

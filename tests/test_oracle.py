@@ -246,6 +246,120 @@ def test_topk_unfused_multiply_add():
 
 
 # --------------------------------------------------------------------------
+# Layer-wise Top-k (Appendix C.5)
+# --------------------------------------------------------------------------
+
+def test_topk_layerwise_hand_example():
+    gd = G.load("topk_layerwise_example.txt")
+    g, e, lr = G.f32(gd["g"]), G.f32(gd["e"]), float(gd["lr"][0])
+    off = [int(v) for v in gd["offsets"]]
+    ks = [int(v) for v in gd["k"]]
+    idx, val, e_next = oracle.topk_segmented(g, e, lr, off, ks)
+    np.testing.assert_array_equal(idx, G.i32(gd["idx"]))
+    np.testing.assert_array_equal(bits(val), bits(G.f32(gd["val"])))
+    np.testing.assert_array_equal(bits(e_next), bits(G.f32(gd["e_next"])))
+    # the entire-model Top-4 of the same vector differs (Appendix C.5)
+    idx4, _, _ = oracle.topk(g, e, lr, 4)
+    np.testing.assert_array_equal(idx4, G.i32(gd["entire4_idx"]))
+    assert list(idx4) != list(idx)
+
+
+@pytest.mark.parametrize("seed", range(8))
+def test_topk_layerwise_brute_force_tiny(seed):
+    # every segment against the Lemma 1 brute force on its own coordinates
+    rng = np.random.default_rng(300 + seed)
+    d = int(rng.integers(1, 13))
+    cuts = np.sort(rng.integers(0, d + 1, size=int(rng.integers(0, 4))))
+    off = np.concatenate([[0], cuts, [d]]).astype(np.int64)
+    g = (rng.integers(-4, 5, size=d) * 0.25).astype(F32)
+    e = (rng.integers(-2, 3, size=d) * 0.125).astype(F32)
+    acc = fl_acc_via_double(g, e, 0.5)
+    ks = rng.integers(0, 6, size=off.size - 1)
+    idx, val, e_next = oracle.topk_segmented(g, e, 0.5, off, ks)
+    want = []
+    for s in range(off.size - 1):
+        lo, hi = int(off[s]), int(off[s + 1])
+        kk = min(int(ks[s]), hi - lo)
+        want += [lo + i for i in _brute_topk(acc[lo:hi], kk)]
+    assert list(idx) == want
+    np.testing.assert_array_equal(bits(val), bits(acc[want]))
+    rest = np.ones(d, dtype=bool)
+    rest[want] = False
+    np.testing.assert_array_equal(bits(e_next[rest]), bits(acc[rest]))
+    assert np.all(bits(e_next[~rest]) == 0)
+
+
+def test_topk_layerwise_one_segment_is_entire_model():
+    rng = np.random.default_rng(31)
+    d = 20_000
+    g = (rng.standard_normal(d) * 1e-3).astype(F32)
+    e = (rng.standard_normal(d) * 1e-4).astype(F32)
+    for k in (0, 1, 333, d, d + 5):
+        a = oracle.topk_segmented(g, e, 0.1, [0, d], [k])
+        b = oracle.topk(g, e, 0.1, k)
+        for x, y in zip(a, b):
+            np.testing.assert_array_equal(bits(x) if x.dtype == F32 else x,
+                                          bits(y) if y.dtype == F32 else y)
+
+
+def test_topk_layerwise_invariants_per_segment():
+    rng = np.random.default_rng(32)
+    sizes = [0, 1, 64, 4096, 4097, 700, 0, 12_345]
+    off = np.concatenate([[0], np.cumsum(sizes)]).astype(np.int64)
+    d = int(off[-1])
+    g = (rng.standard_normal(d) * 1e-3).astype(F32)
+    e = (rng.standard_normal(d) * 1e-4).astype(F32)
+    ks = np.array([3, 5, 1, 40, 4097, 700, 0, 13], dtype=np.int64)
+    acc = fl_acc_via_double(g, e, 0.1)
+    idx, val, e_next = oracle.topk_segmented(g, e, 0.1, off, ks)
+    pos = 0
+    for s, size in enumerate(sizes):
+        lo, hi = int(off[s]), int(off[s + 1])
+        kk = min(int(ks[s]), size)
+        seg = idx[pos:pos + kk]
+        pos += kk
+        assert np.all((seg >= lo) & (seg < hi)) and np.all(np.diff(seg) > 0)
+        kept = np.zeros(size, dtype=bool)
+        kept[seg - lo] = True
+        a = np.abs(acc[lo:hi])
+        if 0 < kk < size:
+            assert a[kept].min() >= a[~kept].max()
+        # delta-contraction of each segment with delta = k_s / d_s (section 4.5)
+        en = float(np.sum(e_next[lo:hi].astype(np.float64) ** 2))
+        an = float(np.sum(acc[lo:hi].astype(np.float64) ** 2))
+        if size:
+            assert en <= (1.0 - kk / size) * an * (1 + 1e-12)
+    assert pos == idx.size
+
+
+def test_ht_layerwise_equals_entire_model():
+    # the hard threshold is element-wise, so applying it per segment and
+    # concatenating with index offsets is the entire-model result (App. C.5)
+    rng = np.random.default_rng(33)
+    sizes = [5, 4096, 1, 3000, 77]
+    off = np.concatenate([[0], np.cumsum(sizes)])
+    d = int(off[-1])
+    g = (rng.standard_normal(d) * 1e-3).astype(F32)
+    e = (rng.standard_normal(d) * 1e-4).astype(F32)
+    lam = F32(1.5e-4)
+    idx, val, e_next, k = oracle.ht(g, e, 0.1, lam)
+    parts = [oracle.ht(g[off[s]:off[s + 1]], e[off[s]:off[s + 1]], 0.1, lam)
+             for s in range(len(sizes))]
+    np.testing.assert_array_equal(idx, np.concatenate([p[0] + off[s] for s, p in enumerate(parts)]))
+    np.testing.assert_array_equal(bits(val), bits(np.concatenate([p[1] for p in parts])))
+    np.testing.assert_array_equal(bits(e_next), bits(np.concatenate([p[2] for p in parts])))
+    assert k == sum(p[3] for p in parts)
+
+
+def test_topk_layerwise_rejects_bad_layout():
+    g = np.zeros(10, dtype=F32)
+    for off, ks in (([0, 5, 9], [1, 1]), ([1, 5, 10], [1, 1]), ([0, 6, 5, 10], [1, 1, 1]),
+                    ([0, 5, 10], [1, -1])):
+        with pytest.raises(ValueError):
+            oracle.topk_segmented(g, g, 0.1, off, ks)
+
+
+# --------------------------------------------------------------------------
 # Lemma 3: hard threshold at the K-th magnitude equals Top-K up to ties
 # --------------------------------------------------------------------------
 
