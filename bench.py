@@ -274,6 +274,28 @@ def main():
     b.record(cur)
     torch.cuda.synchronize()
     copy_us = a.elapsed_time(b) * 1e3 / args.b2b
+    # layer-wise Top-k over the workload's 161 segments, k_s = ceil(0.1 % d_s)
+    seg_ks = synth.layerwise_k(stream.bounds, density)
+    seg_ktot = int(seg_ks.sum())
+    seg_off_d = torch.from_numpy(stream.bounds.astype(np.int64)).to(dev)
+    seg_k_d = torch.from_numpy(seg_ks).to(dev)
+    seg_idx = torch.empty(seg_ktot, dtype=torch.int32, device=dev)
+    seg_val = torch.empty(seg_ktot, dtype=torch.float32, device=dev)
+    seg_ws = efs.new_topk_segmented_workspace(seg_ks.size, seg_ktot, dev)
+    e_seg = torch.zeros(d, dtype=torch.float32, device=dev)
+    for s in range(2):
+        efs.topk_segmented_compress(pool[s % len(pool)], e_seg, lr, seg_off_d, seg_k_d, seg_idx,
+                                    seg_val, seg_ws)
+    a, b = ev(), ev()
+    torch.cuda.synchronize()
+    a.record(cur)
+    for s in range(args.b2b):
+        efs.topk_segmented_compress(pool[s % len(pool)], e_seg, lr, seg_off_d, seg_k_d, seg_idx,
+                                    seg_val, seg_ws)
+    b.record(cur)
+    torch.cuda.synchronize()
+    seg_us = a.elapsed_time(b) * 1e3 / args.b2b
+    del e_seg, seg_ws
 
     total_ms = begin.elapsed_time(end)
     ms_step = total_ms / args.steps
@@ -338,6 +360,11 @@ def main():
                        "bytes": 8.0 * d},
         "ops": {
             "ht_compress_telemetry": {"launch_us": round(ht_tel_us, 2)},
+            "topk_segmented_compress": {
+                "launch_us": round(seg_us, 2), "segments": int(seg_ks.size), "k_total": seg_ktot,
+                "gelem_s": round(d / (seg_us * 1e-6) / 1e9, 2),
+                "gbps_ideal": round((12.0 * d + 8.0 * seg_ktot) / (seg_us * 1e-6) / 1e9, 1),
+                "gbps_two_pass": round((16.0 * d + 8.0 * seg_ktot) / (seg_us * 1e-6) / 1e9, 1)},
             "ht_compress": dict(stats(ht_ms), gelem_s=round(d / ht_s / 1e9, 2),
                                 gbps=round(ht_bytes / ht_s / 1e9, 1), k_t_mean=kt,
                                 k_t_first=kts[0], k_t_last=kts[-1]),

@@ -131,6 +131,48 @@ efs_status topk_compress(const float *g, float *e, int64_t d, float lr, int64_t 
  * call has completed). */
 size_t topk_path_flag_offset(void);
 
+/* Layer-wise Top-k EF step (Appendix C.5: the sparsifier applied to each
+ * layer's tensor on its own; Algorithm 1 for the error):
+ *     p = e + lr*g ;  in every segment s = [offsets[s], offsets[s+1]) keep the
+ *     min(k[s], size_s) entries of largest |p| (equal magnitudes: lower index
+ *     first, as topk_compress ranks them) ;  e' = p with +0 at every kept entry.
+ *
+ *   g, e        as for topk_compress (e in/out, in place).
+ *   nseg        number of segments, 1 <= nseg <= EFS_SEG_MAX.
+ *   offsets     DEVICE int64[nseg + 1], 8-byte aligned: offsets[0] = 0,
+ *               non-decreasing, offsets[nseg] = d (empty segments allowed).
+ *   k           DEVICE int64[nseg], 8-byte aligned: k[s] >= 0; values above
+ *               a segment's size keep the whole segment.
+ *   k_total     capacity of idx/val; must be >= sum of min(k[s], size_s).
+ *   idx, val    payload: segment s's pairs occupy
+ *               [kout_s, kout_s + min(k[s], size_s)), kout the exclusive
+ *               prefix of those counts; order within a segment unspecified.
+ *   workspace   >= topk_segmented_workspace_bytes(nseg, k_total) bytes,
+ *               16-byte aligned: per-segment tables and histograms (36 KiB per
+ *               segment) and a candidate region of 16*k_total + 4096*nseg
+ *               (key, index) pairs.  Results never depend on its contents.
+ *               Not shareable between concurrent calls.
+ * Host-visible arguments are checked before anything is launched (EFS_EINVAL,
+ * EFS_ESPACE).  offsets and k live on the device and are checked there: a
+ * layout that breaks the rules above, or a k_total below the sum, makes the
+ * call change nothing (no payload written, e untouched) and leaves the uint32
+ * at topk_segmented_status_offset() in the workspace at 1 (0 after an
+ * accepted call).  d == 0 is a no-op. */
+#define EFS_SEG_MAX 65536
+size_t topk_segmented_workspace_bytes(int32_t nseg, int64_t k_total);
+size_t topk_segmented_status_offset(void);
+
+/* Byte offset, within a layer-wise Top-k workspace, of a uint32 counting the
+ * segments of the last completed call that selected among the keys in a
+ * bracket around the threshold predicted from that segment's earlier calls
+ * (instead of the full radix select; a diagnostic, read after the call has
+ * completed). */
+size_t topk_segmented_bracket_offset(void);
+efs_status topk_segmented_compress(const float *g, float *e, int64_t d, float lr, int32_t nseg,
+                                   const int64_t *offsets, const int64_t *k, int64_t k_total,
+                                   int32_t *idx, float *val, void *workspace,
+                                   size_t workspace_bytes, void *stream);
+
 /* Exchange-and-average of n workers' payloads on one device (Algorithm 1):
  *     out = (sum over w = 0..n-1, in that order, of decompress(payload_w)) / n
  * with fp32 adds in worker order and one IEEE division by (float)n.

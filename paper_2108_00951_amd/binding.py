@@ -64,6 +64,15 @@ def declare(lib):
     lib.sparse_accumulate.argtypes = [ctypes.POINTER(vp), ctypes.POINTER(vp), ctypes.POINTER(vp),
                                       ctypes.POINTER(i64), i32, i64, vp, vp]
     lib.sparse_accumulate.restype = ctypes.c_int
+    lib.topk_segmented_workspace_bytes.argtypes = [i32, i64]
+    lib.topk_segmented_workspace_bytes.restype = ctypes.c_size_t
+    lib.topk_segmented_status_offset.argtypes = []
+    lib.topk_segmented_status_offset.restype = ctypes.c_size_t
+    lib.topk_segmented_bracket_offset.argtypes = []
+    lib.topk_segmented_bracket_offset.restype = ctypes.c_size_t
+    lib.topk_segmented_compress.argtypes = [vp, vp, i64, f32, i32, vp, vp, i64, vp, vp, vp,
+                                            ctypes.c_size_t, vp]
+    lib.topk_segmented_compress.restype = ctypes.c_int
     lib.sparse_apply_workspace_bytes.argtypes = [i32, i64, i64]
     lib.sparse_apply_workspace_bytes.restype = ctypes.c_size_t
     lib.sparse_apply.argtypes = [ctypes.POINTER(vp), ctypes.POINTER(vp), ctypes.POINTER(vp),
@@ -204,6 +213,53 @@ def topk_compress(g, e, lr: float, k: int, idx, val, workspace, stream=None) -> 
         raise ValueError("size mismatch among g, e, idx, val and k")
     rc = lib.topk_compress(_ptr(g), _ptr(e), g.numel(), float(lr), int(k), _ptr(idx), _ptr(val),
                            _ptr(workspace), workspace.numel(), _stream_handle(stream))
+    _check(lib, rc)
+
+
+def topk_segmented_workspace_bytes(nseg: int, k_total: int) -> int:
+    return int(load_library().topk_segmented_workspace_bytes(int(nseg), int(k_total)))
+
+
+def new_topk_segmented_workspace(nseg: int, k_total: int, device="cuda"):
+    import torch
+    return torch.empty(max(topk_segmented_workspace_bytes(nseg, k_total), 16), dtype=torch.uint8,
+                       device=device)
+
+
+def topk_segmented_status(workspace) -> int:
+    """0 if the last completed topk_segmented_compress on this workspace
+    accepted the layout, 1 if it rejected it (synchronises)."""
+    off = int(load_library().topk_segmented_status_offset())
+    return int(workspace[off:off + 4].cpu().numpy().view("<u4")[0])
+
+
+def topk_segmented_bracket_segments(workspace) -> int:
+    """Segments of the last completed topk_segmented_compress on this
+    workspace that selected from the bracket around the previous threshold
+    (synchronises)."""
+    off = int(load_library().topk_segmented_bracket_offset())
+    return int(workspace[off:off + 4].cpu().numpy().view("<u4")[0])
+
+
+def topk_segmented_compress(g, e, lr: float, offsets, k, idx, val, workspace, stream=None) -> None:
+    """Layer-wise Top-k EF step; see topk_segmented_compress in include/efsparse.h.
+    offsets: int64 device tensor [nseg + 1]; k: int64 device tensor [nseg];
+    the payload capacity k_total is idx.numel()."""
+    import torch
+    lib = load_library()
+    _require(g, torch.float32, "g")
+    _require(e, torch.float32, "e")
+    _require(offsets, torch.int64, "offsets")
+    _require(k, torch.int64, "k")
+    _require(idx, torch.int32, "idx")
+    _require(val, torch.float32, "val")
+    _require(workspace, torch.uint8, "workspace")
+    if g.numel() != e.numel() or idx.numel() != val.numel() or offsets.numel() != k.numel() + 1:
+        raise ValueError("size mismatch among g, e, idx, val, offsets and k")
+    rc = lib.topk_segmented_compress(_ptr(g), _ptr(e), g.numel(), float(lr), k.numel(),
+                                     offsets.data_ptr(), k.data_ptr(), idx.numel(), _ptr(idx),
+                                     _ptr(val), _ptr(workspace), workspace.numel(),
+                                     _stream_handle(stream))
     _check(lib, rc)
 
 

@@ -12,6 +12,7 @@
 #include "launch.hpp"
 
 static_assert(efs::kMaxApplyWorkers == EFS_APPLY_MAX_WORKERS, "worker limit differs from the header");
+static_assert(efs::kMaxSegments == EFS_SEG_MAX, "segment limit differs from the header");
 
 namespace {
 
@@ -168,6 +169,42 @@ efs_status sparse_accumulate(const int32_t *const *idx, const float *const *val,
     return check_launch(efs::launch_accumulate(idx, val, counts, caps, n_workers, d, out,
                                                static_cast<hipStream_t>(stream)),
                         "sparse_accumulate");
+}
+
+size_t topk_segmented_workspace_bytes(int32_t nseg, int64_t k_total) {
+    if (nseg < 1 || nseg > efs::kMaxSegments || k_total < 0 || k_total > kMaxLen) return 0;
+    return efs::topk_segmented_workspace_size(nseg, k_total);
+}
+
+size_t topk_segmented_status_offset(void) { return efs::topk_segmented_status_offset(); }
+
+size_t topk_segmented_bracket_offset(void) { return efs::topk_segmented_bracket_offset(); }
+
+efs_status topk_segmented_compress(const float *g, float *e, int64_t d, float lr, int32_t nseg,
+                                   const int64_t *offsets, const int64_t *k, int64_t k_total,
+                                   int32_t *idx, float *val, void *workspace,
+                                   size_t workspace_bytes, void *stream) {
+    const char *name = "topk_segmented_compress";
+    if (d < 0 || d > kMaxLen) return fail(EFS_EINVAL, "%s: d=%lld outside [0, 2^31-1]", name, (long long)d);
+    if (nseg < 1 || nseg > efs::kMaxSegments)
+        return fail(EFS_EINVAL, "%s: nseg=%d outside [1, %d]", name, nseg, efs::kMaxSegments);
+    if (k_total < 0 || k_total > d) return fail(EFS_EINVAL, "%s: k_total=%lld outside [0, d]", name, (long long)k_total);
+    if (d > 0 && (g == nullptr || e == nullptr)) return fail(EFS_EINVAL, "%s: g or e is NULL", name);
+    if (!aligned(g, 4) || !aligned(e, 4)) return fail(EFS_EINVAL, "%s: g and e must be 4-byte aligned", name);
+    if (!std::isfinite(lr)) return fail(EFS_EINVAL, "%s: lr must be finite", name);
+    if (offsets == nullptr || k == nullptr || !aligned(offsets, 8) || !aligned(k, 8))
+        return fail(EFS_EINVAL, "%s: offsets and k must be non-NULL and 8-byte aligned", name);
+    if (k_total > 0 && (idx == nullptr || val == nullptr)) return fail(EFS_EINVAL, "%s: idx or val is NULL", name);
+    if (!aligned(idx, 4) || !aligned(val, 4)) return fail(EFS_EINVAL, "%s: idx and val must be 4-byte aligned", name);
+    if (d == 0) return EFS_OK;
+    if (workspace == nullptr || !aligned(workspace, 16))
+        return fail(EFS_EINVAL, "%s: workspace must be non-NULL and 16-byte aligned", name);
+    const size_t need = efs::topk_segmented_workspace_size(nseg, k_total);
+    if (workspace_bytes < need)
+        return fail(EFS_ESPACE, "%s: workspace has %zu bytes, needs %zu", name, workspace_bytes, need);
+    return check_launch(efs::launch_topk_segmented(g, e, d, lr, nseg, offsets, k, k_total, idx, val,
+                                                   workspace, static_cast<hipStream_t>(stream)),
+                        name);
 }
 
 size_t sparse_apply_workspace_bytes(int32_t n_workers, int64_t d, int64_t total_cap) {

@@ -21,6 +21,15 @@ hipError_t launch_accumulate(const int32_t *const *idx, const float *const *val,
                              const uint32_t *const *counts, const int64_t *caps,
                              int32_t n, int64_t d, float *out, hipStream_t stream);
 
+// Layer-wise Top-k (topk_seg.hip).
+constexpr int32_t kMaxSegments = 1 << 16;
+size_t topk_segmented_workspace_size(int32_t nseg, int64_t k_total);
+size_t topk_segmented_status_offset();
+size_t topk_segmented_bracket_offset();
+hipError_t launch_topk_segmented(const float *g, float *e, int64_t d, float lr, int32_t nseg,
+                                 const int64_t *offsets, const int64_t *k, int64_t k_total,
+                                 int32_t *idx, float *val, void *workspace, hipStream_t stream);
+
 // Exchange-and-average fused with the model update (apply.hip).
 constexpr int kMaxApplyWorkers = 32;
 size_t apply_workspace_size(int32_t n, int64_t d, int64_t total_cap);

@@ -1,0 +1,917 @@
+// Layer-wise Top-k with error feedback (Appendix C.5: the Top-k sparsifier
+// applied to each layer's tensor on its own; Algorithm 1 for the error).
+// Segment s is coordinates [off[s], off[s+1]) and keeps min(k[s], size)
+// of them: the largest keys (31-bit patterns of |p|), equal keys to the
+// lower index, exactly as the flat Top-k ranks them.
+//
+// Work is cut into tiles: the 4096-element blocks of the vector, clipped to
+// each segment, so every tile belongs to one segment and every whole tile is
+// 16-byte aligned.  Five launches:
+//
+//   reset    one workgroup checks the layout and forms the per-segment
+//            tables (tile ranges, payload offsets, candidate regions); the
+//            others zero the per-segment histograms.
+//   pass1    p = e + lr*g written into e (12 B/element); LDS histogram of key
+//            bits 30..18 (8192 bins) per segment, flushed (non-zero bins) to
+//            the segment's global histogram.  With a bracket [lo, hi] around
+//            the segment's threshold predicted from its last two calls on this
+//            workspace (error feedback moves it little; the bracket's width,
+//            2^13..2^20 keys, adapts per segment to how many keys it caught
+//            and whether it missed), keys above hi go straight to the payload
+//            and keys inside it to the candidates.
+//   select1  one workgroup per segment: when pass1 had a bracket and its
+//            counts prove the k-th key inside it, the segment selects from
+//            the bracket (below).  Otherwise the digit D1 holding the k-th
+//            key and the mode: none (k = 0), all (k = size), candidates (the
+//            keys in D1 fit the segment's candidate region) or scan (they do
+//            not: a large set of equal or nearly equal magnitudes).
+//   pass2    radix path only, a read of p (4 B/element): keys above D1 go to
+//            the payload and
+//            their e to +0 (mode all: every key); keys in D1 are appended to
+//            the candidate region and histogrammed by bits 17..8.
+//   final    one workgroup per segment selects among its candidates: bits
+//            17..8, then 7..0 (the exact threshold T; from the bracket: bits
+//            19..10 then 9..0 of key - lo), then, when only some keys equal to
+//            T are kept, the lowest indices among them by a radix select on
+//            the index; emits, clears e, and keeps T as the next hint.  Scan
+//            mode does the same over the segment's elements.  Results never
+//            depend on the hint.
+//
+// Payload: segment s's pairs at [kout[s], kout[s] + min(k[s], size)), kout the
+// exclusive prefix of those counts; order within a segment unspecified.
+#include <stddef.h>
+
+#include "device_common.hpp"
+#include "launch.hpp"
+
+namespace efs {
+
+namespace {
+
+constexpr int kShift1 = 18;     // digit 1: key bits 30..18
+constexpr int kShift2 = 8;      // digit 2: key bits 17..8; digit 3: bits 7..0
+constexpr int kDigit1 = 1 << (31 - kShift1);
+constexpr int kDigit2 = 1 << (kShift1 - kShift2);
+constexpr int kDigit3 = 1 << kShift2;
+constexpr int kIdxBins = 2048;  // index radix for ties: 11 + 10 + 10 bits
+constexpr int kCandLds = 18432;  // candidates the final pass holds in LDS (144 KiB)
+constexpr int64_t kCandPerK = 16;
+constexpr int64_t kCandExtra = 4096;
+
+enum : uint32_t { kModeNone = 0, kModeAll = 1, kModeCand = 2, kModeScan = 3, kModeFast = 4 };
+
+// bracket = prediction -/+ 2^w keys, w adapted per segment between these
+// (2^19 keys is about 4.6 % in |p|, 2^12 about 0.05 %)
+constexpr uint32_t kWidthMax = 19, kWidthMin = 12, kWidthStart = 17;
+constexpr int64_t kMaxStep = 1 << 18;          // cap on the extrapolated step, in keys
+constexpr uint32_t kHintMagic = 0x53454748u;
+
+struct SegCtl {
+    uint32_t status;   // 0: layout accepted; 1: rejected (the call changed nothing)
+    uint32_t tiles;    // tiles of all segments
+    uint32_t bracket;  // segments that selected from the bracket (a diagnostic)
+    uint32_t pass2;    // segments that need pass2
+    uint32_t pad[60];
+};
+static_assert(sizeof(SegCtl) == 256, "control block is 256 bytes");
+
+struct SegInfo {
+    int64_t off, size, kout, k, coff, ccap;
+    uint32_t tile0, ntiles;
+    uint32_t pad[2];
+};
+static_assert(sizeof(SegInfo) == 64, "segment info is 64 bytes");
+
+struct SegState {
+    uint32_t mode, d1, need1, c1;
+    uint32_t emit;     // pairs written to the payload (pass1 with a bracket, or pass2)
+    uint32_t ccur;     // candidates appended (pass1 with a bracket, or pass2)
+    uint32_t bracket;  // 1: pass1 collects keys in [lo, hi], emits keys above hi
+    uint32_t lo, hi;
+    uint32_t pad[7];
+};
+static_assert(sizeof(SegState) == 64, "segment state is 64 bytes");
+
+// Threshold of the last call on this workspace, kept across calls (the
+// reset does not touch it); it only decides the bracket, never a result.
+struct SegHint {
+    uint32_t key, prev, magic, width;  // last threshold, the one before, validity, log2 half-width
+};
+
+struct SegWs {
+    SegCtl *ctl;
+    SegHint *hint;          // [nseg]
+    SegInfo *info;
+    uint32_t *tile_prefix;  // [nseg + 1]
+    SegState *st;
+    uint32_t *hist1;        // [nseg][kDigit1]
+    uint32_t *hist2;        // [nseg][kDigit2]
+    uint2 *cand;            // (bits of p, index)
+    int64_t ccap_total;
+};
+
+struct SegLayout {
+    size_t info, tile_prefix, st, hint, hist1, hist2, cand, bytes;
+    int64_t ccap_total;
+};
+
+size_t round256(size_t b) { return (b + 255) & ~size_t(255); }
+
+SegLayout seg_layout(int32_t nseg, int64_t k_total) {
+    SegLayout L;
+    L.ccap_total = kCandPerK * k_total + kCandExtra * nseg;
+    size_t o = sizeof(SegCtl);
+    L.info = o;
+    o += round256(sizeof(SegInfo) * size_t(nseg));
+    L.tile_prefix = o;
+    o += round256(4 * (size_t(nseg) + 1));
+    L.st = o;
+    o += round256(sizeof(SegState) * size_t(nseg));
+    L.hint = o;
+    o += round256(sizeof(SegHint) * size_t(nseg));
+    L.hist1 = o;
+    o += round256(4 * size_t(kDigit1) * size_t(nseg));
+    L.hist2 = o;
+    o += round256(4 * size_t(kDigit2) * size_t(nseg));
+    L.cand = o;
+    o += round256(8 * size_t(L.ccap_total));
+    L.bytes = o;
+    return L;
+}
+
+// ---------------------------------------------------------------------------
+// Block-wide helpers (every thread of the workgroup calls them)
+// ---------------------------------------------------------------------------
+
+__device__ __forceinline__ uint32_t wave_incl_u32(uint32_t v) {
+    const int lane = threadIdx.x & (kWave - 1);
+#pragma unroll
+    for (int off = 1; off < kWave; off <<= 1) {
+        const uint32_t o = __shfl_up(v, off);
+        if (lane >= off) v += o;
+    }
+    return v;
+}
+
+__device__ __forceinline__ int64_t wave_incl_i64(int64_t v) {
+    const int lane = threadIdx.x & (kWave - 1);
+#pragma unroll
+    for (int off = 1; off < kWave; off <<= 1) {
+        const int64_t o = __shfl_up(v, off);
+        if (lane >= off) v += o;
+    }
+    return v;
+}
+
+// Exclusive prefix of v over the workgroup's threads in order; `total` gets
+// the sum.  Uses kWaves int64 of LDS; two barriers.
+__device__ __forceinline__ int64_t block_excl_i64(int64_t v, int64_t *s_wave, int64_t &total) {
+    const int lane = threadIdx.x & (kWave - 1);
+    const int wave = threadIdx.x / kWave;
+    const int64_t incl = wave_incl_i64(v);
+    if (lane == kWave - 1) s_wave[wave] = incl;
+    __syncthreads();
+    int64_t off = 0, tot = 0;
+#pragma unroll
+    for (int q = 0; q < kWaves; ++q) {
+        off += q < wave ? s_wave[q] : 0;
+        tot += s_wave[q];
+    }
+    __syncthreads();
+    total = tot;
+    return off + incl - v;
+}
+
+// In a histogram of kBins bins (LDS), ranked from the top (kFromTop) or from
+// the bottom, the bin where the running count first reaches `need`
+// (1 <= need <= sum).  s_out gets {bin, count before the bin, count in the
+// bin}; {0, 0, 0} when no bin qualifies.  Three barriers.
+template <int kBins, bool kFromTop>
+__device__ void pick_bin(const uint32_t *hist, uint32_t need, uint32_t *s_wave, uint32_t *s_out) {
+    constexpr int kPer = kBins / kBlock;
+    const int t = threadIdx.x;
+    const int lane = t & (kWave - 1);
+    const int wave = t / kWave;
+    if (t == 0) {
+        s_out[0] = 0u;
+        s_out[1] = 0u;
+        s_out[2] = 0u;
+    }
+    uint32_t c[kPer];
+    uint32_t tot = 0;
+#pragma unroll
+    for (int i = 0; i < kPer; ++i) {
+        const int r = t * kPer + i;  // rank position
+        c[i] = hist[kFromTop ? kBins - 1 - r : r];
+        tot += c[i];
+    }
+    const uint32_t incl_w = wave_incl_u32(tot);
+    if (lane == kWave - 1) s_wave[wave] = incl_w;
+    __syncthreads();
+    uint32_t off = 0;
+#pragma unroll
+    for (int q = 0; q < kWaves; ++q) off += q < wave ? s_wave[q] : 0u;
+    const uint32_t incl = off + incl_w;
+    const uint32_t excl = incl - tot;
+    if (excl < need && incl >= need) {
+        uint32_t run = excl;
+#pragma unroll
+        for (int i = 0; i < kPer; ++i) {
+            if (run + c[i] >= need) {
+                const int r = t * kPer + i;
+                s_out[0] = uint32_t(kFromTop ? kBins - 1 - r : r);
+                s_out[1] = run;
+                s_out[2] = c[i];
+                break;
+            }
+            run += c[i];
+        }
+    }
+    __syncthreads();
+}
+
+// Segment holding tile t: the largest s with tile_prefix[s] <= t, which
+// then has t < tile_prefix[s+1] (empty segments own no tiles and are never
+// returned).  A 64-way search: each round every lane of the wave probes one
+// position, so nseg <= 4096 takes two rounds of loads instead of twelve
+// dependent ones.  Every wave computes the same result.
+__device__ __forceinline__ int32_t segment_of_tile(const uint32_t *tp, int32_t nseg, uint32_t t) {
+    const int lane = threadIdx.x & (kWave - 1);
+    int32_t lo = 0, hi = nseg;  // tp[lo] <= t, and the answer is below hi
+    while (hi - lo > 1) {
+        const int32_t step = (hi - lo + kWave - 1) / kWave;
+        const int32_t probe = lo + lane * step;
+        const bool ok = probe < hi && tp[probe] <= t;
+        const uint64_t m = __ballot(ok);  // lanes 0..L, lane 0 always set
+        const int32_t L = 63 - __clzll(m);
+        lo += L * step;
+        hi = min(hi, lo + step);
+    }
+    return lo;
+}
+
+// Element (j, c) of this thread in the 4096-element block starting at
+// `block0` (index block0 + (j * kBlock + tid) * 4 + c, the hard threshold's
+// map).
+__device__ __forceinline__ int64_t tile_elem(int64_t block0, int j, int c) {
+    return block0 + int64_t(j * kBlock + int(threadIdx.x)) * 4 + c;
+}
+
+// Tiles of a segment: the 4096-element blocks it overlaps.
+__host__ __device__ __forceinline__ int64_t segment_tiles(int64_t off, int64_t size) {
+    return size == 0 ? 0 : ((off + size - 1) / kTile) - (off / kTile) + 1;
+}
+
+// Tile t of segment `inf`: the block start and the element range [lo, hi).
+struct TileRange {
+    int64_t block0, lo, hi;
+};
+
+__device__ __forceinline__ TileRange tile_range(const SegInfo &inf, uint32_t t) {
+    TileRange r;
+    r.block0 = (inf.off / kTile + int64_t(t - inf.tile0)) * kTile;
+    r.lo = max(inf.off, r.block0);
+    r.hi = min(inf.off + inf.size, r.block0 + kTile);
+    return r;
+}
+
+// ---------------------------------------------------------------------------
+// reset
+// ---------------------------------------------------------------------------
+
+__global__ __launch_bounds__(kBlock) void seg_reset_kernel(SegWs ws, const int64_t *__restrict__ off,
+                                                           const int64_t *__restrict__ kin,
+                                                           int32_t nseg, int64_t d, int64_t k_total) {
+    if (blockIdx.x > 0) {
+        // zero both histogram arrays (contiguous) with the other workgroups
+        const int64_t words = int64_t(nseg) * (kDigit1 + kDigit2);
+        uint32_t *h = ws.hist1;
+        const int64_t stride = int64_t(gridDim.x - 1) * kBlock;
+        for (int64_t i = int64_t(blockIdx.x - 1) * kBlock + threadIdx.x; i < words; i += stride) {
+            if (i < int64_t(nseg) * kDigit1) h[i] = 0u;
+            else ws.hist2[i - int64_t(nseg) * kDigit1] = 0u;
+        }
+        return;
+    }
+    __shared__ int64_t s_wave[kWaves];
+    __shared__ uint32_t s_bad;
+    const int t = threadIdx.x;
+    if (t == 0) s_bad = 0u;
+    __syncthreads();
+    const int32_t per = (nseg + kBlock - 1) / kBlock;
+    const int32_t s0 = min(nseg, t * per), s1 = min(nseg, s0 + per);
+    int64_t sum_k = 0, sum_c = 0, sum_t = 0;
+    bool bad = false;
+    for (int32_t s = s0; s < s1; ++s) {
+        const int64_t lo = off[s], hi = off[s + 1], kk = kin[s];
+        const int64_t size = hi - lo;
+        if (size < 0 || kk < 0 || lo < 0 || hi > d) {
+            bad = true;
+            continue;
+        }
+        const int64_t keff = kk < size ? kk : size;
+        sum_k += keff;
+        sum_c += (keff > 0 && keff < size) ? kCandPerK * keff + kCandExtra : 0;
+        sum_t += segment_tiles(lo, size);
+    }
+    if (t == 0 && off[0] != 0) bad = true;
+    if (t == 0 && off[nseg] != d) bad = true;
+    if (bad) atomicOr(&s_bad, 1u);
+    int64_t tot_k, tot_c, tot_t;
+    int64_t base_k = block_excl_i64(sum_k, s_wave, tot_k);
+    int64_t base_c = block_excl_i64(sum_c, s_wave, tot_c);
+    int64_t base_t = block_excl_i64(sum_t, s_wave, tot_t);
+    // the barriers above also publish s_bad
+    const bool reject = s_bad != 0u || tot_k > k_total || tot_c > ws.ccap_total ||
+                        tot_t > int64_t(UINT32_MAX);
+    if (!reject) {
+        for (int32_t s = s0; s < s1; ++s) {
+            const int64_t lo = off[s], size = off[s + 1] - lo, kk = kin[s];
+            const int64_t keff = kk < size ? kk : size;
+            const int64_t ccap = (keff > 0 && keff < size) ? kCandPerK * keff + kCandExtra : 0;
+            const uint32_t nt = uint32_t(segment_tiles(lo, size));
+            SegInfo inf;
+            inf.off = lo;
+            inf.size = size;
+            inf.kout = base_k;
+            inf.k = keff;
+            inf.coff = base_c;
+            inf.ccap = ccap;
+            inf.tile0 = uint32_t(base_t);
+            inf.ntiles = nt;
+            inf.pad[0] = inf.pad[1] = 0u;
+            ws.info[s] = inf;
+            ws.tile_prefix[s] = uint32_t(base_t);
+            SegState z = {};
+            const SegHint h = ws.hint[s];
+            if (keff > 0 && keff < size && h.magic == kHintMagic && h.key <= 0x7fffffffu &&
+                h.prev <= 0x7fffffffu && h.width >= kWidthMin && h.width <= kWidthMax) {
+                const int64_t half = int64_t(1) << h.width;
+                // last threshold plus the last step (capped): error feedback
+                // makes thresholds drift smoothly from call to call
+                const int64_t step = max(-kMaxStep, min(kMaxStep, int64_t(h.key) - int64_t(h.prev)));
+                const int64_t pred = max(int64_t(0), min(int64_t(0x7fffffff), int64_t(h.key) + step));
+                z.bracket = 1u;
+                z.lo = uint32_t(max(int64_t(0), pred - half));
+                z.hi = uint32_t(min(int64_t(z.lo) + 2 * half - 1, int64_t(0x7fffffff)));
+            }
+            ws.st[s] = z;
+            base_k += keff;
+            base_c += ccap;
+            base_t += nt;
+        }
+    }
+    if (t == 0) {
+        ws.ctl->bracket = 0u;
+        ws.ctl->pass2 = 0u;
+        ws.ctl->status = reject ? 1u : 0u;
+        ws.ctl->tiles = reject ? 0u : uint32_t(tot_t);
+        if (!reject) ws.tile_prefix[nseg] = uint32_t(tot_t);
+    }
+}
+
+// ---------------------------------------------------------------------------
+// pass1: p = e + lr*g into e, histogram of key bits 30..18 per segment
+// ---------------------------------------------------------------------------
+
+__device__ __forceinline__ void flush_hist(uint32_t *lds, int bins, uint32_t *global) {
+    __syncthreads();
+    for (int b = threadIdx.x; b < bins; b += kBlock) {
+        const uint32_t v = lds[b];
+        if (v != 0u) {
+            atomicAdd(&global[b], v);
+            lds[b] = 0u;
+        }
+    }
+    __syncthreads();
+}
+
+// Wave-aggregated reservation: every lane asks for `c` (< 32) slots of the
+// counter; returns the lane's first slot.
+__device__ __forceinline__ uint32_t reserve(uint32_t *counter, uint32_t c) {
+    uint32_t wtot;
+    const uint32_t pre = wave_prefix_small(c, wtot);
+    uint32_t base = 0;
+    const int lane = threadIdx.x & (kWave - 1);
+    if (lane == 0 && wtot != 0u) base = atomicAdd(counter, wtot);
+    base = __shfl(base, 0);
+    return base + pre;
+}
+
+// Appends this thread's elements selected by `emit_mask` to the segment's
+// payload and those in `cand_mask` to its candidate region (slots past the
+// region ends are counted but not written).  zero_e also clears e at the
+// emitted elements.
+__device__ __forceinline__ void append_pairs(const float (&p)[kVecPerThread][4], int64_t block0,
+                                             uint32_t emit_mask, uint32_t cand_mask,
+                                             const SegInfo &inf, SegState *st, const SegWs &ws,
+                                             int32_t *idx, float *val, float *e, bool zero_e) {
+    uint32_t slot = reserve(&st->emit, uint32_t(__popc(emit_mask)));
+    uint32_t cslot = reserve(&st->ccur, uint32_t(__popc(cand_mask)));
+    if ((emit_mask | cand_mask) == 0u) return;
+#pragma unroll
+    for (int j = 0; j < kVecPerThread; ++j) {
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+            const uint32_t bit = 1u << (4 * j + c);
+            const int64_t i = tile_elem(block0, j, c);
+            if (emit_mask & bit) {
+                if (int64_t(slot) < inf.k) {
+                    idx[inf.kout + slot] = int32_t(i);
+                    val[inf.kout + slot] = p[j][c];
+                    if (zero_e) e[i] = 0.0f;
+                }
+                ++slot;
+            }
+            if (cand_mask & bit) {
+                if (int64_t(cslot) < inf.ccap)
+                    ws.cand[inf.coff + cslot] = make_uint2(__float_as_uint(p[j][c]), uint32_t(i));
+                ++cslot;
+            }
+        }
+    }
+}
+
+template <bool kAligned>
+__global__ __launch_bounds__(kBlock) void seg_pass1_kernel(const float *__restrict__ g,
+                                                           float *__restrict__ e, float lr,
+                                                           int32_t *__restrict__ idx,
+                                                           float *__restrict__ val, int32_t nseg,
+                                                           SegWs ws, uint32_t tiles_per_wg) {
+    __shared__ uint32_t hist[kDigit1];
+    if (ws.ctl->status != 0u) return;
+    const uint32_t T = ws.ctl->tiles;
+    const uint32_t t0 = blockIdx.x * tiles_per_wg;
+    if (t0 >= T) return;
+    const uint32_t t1 = min(T, t0 + tiles_per_wg);
+    for (int b = threadIdx.x; b < kDigit1; b += kBlock) hist[b] = 0u;
+    int32_t s = segment_of_tile(ws.tile_prefix, nseg, t0);
+    uint32_t next = ws.tile_prefix[s + 1];
+    SegInfo inf = ws.info[s];
+    SegState *st = ws.st + s;
+    uint32_t bracket = st->bracket, lo = st->lo, hi = st->hi;
+    __syncthreads();
+    for (uint32_t t = t0; t < t1; ++t) {
+        if (t >= next) {
+            flush_hist(hist, kDigit1, ws.hist1 + int64_t(s) * kDigit1);
+            s = segment_of_tile(ws.tile_prefix, nseg, t);
+            next = ws.tile_prefix[s + 1];
+            inf = ws.info[s];
+            st = ws.st + s;
+            bracket = st->bracket;
+            lo = st->lo;
+            hi = st->hi;
+        }
+        const TileRange r = tile_range(inf, t);
+        float p[kVecPerThread][4];
+        uint32_t valid = 0;
+        if (kAligned && r.lo == r.block0 && r.hi == r.block0 + kTile) {
+            const f32x4 *g4 = reinterpret_cast<const f32x4 *>(g + r.block0);
+            f32x4 *e4 = reinterpret_cast<f32x4 *>(e + r.block0);
+            f32x4 gv[kVecPerThread], ev[kVecPerThread];
+#pragma unroll
+            for (int j = 0; j < kVecPerThread; ++j) {
+                gv[j] = __builtin_nontemporal_load(g4 + j * kBlock + threadIdx.x);
+                ev[j] = e4[j * kBlock + threadIdx.x];
+            }
+#pragma unroll
+            for (int j = 0; j < kVecPerThread; ++j) {
+                f32x4 pv;
+#pragma unroll
+                for (int c = 0; c < 4; ++c) {
+                    pv[c] = ef_accumulate(ev[j][c], lr, gv[j][c]);
+                    p[j][c] = pv[c];
+                }
+                e4[j * kBlock + threadIdx.x] = pv;
+            }
+            valid = 0xffffu;
+        } else {
+            // a segment's first or last block: only its own elements are
+            // read and written (the rest of the block belongs to neighbours)
+#pragma unroll
+            for (int j = 0; j < kVecPerThread; ++j) {
+#pragma unroll
+                for (int c = 0; c < 4; ++c) {
+                    const int64_t i = tile_elem(r.block0, j, c);
+                    p[j][c] = 0.0f;
+                    if (i >= r.lo && i < r.hi) {
+                        p[j][c] = ef_accumulate(e[i], lr, g[i]);
+                        e[i] = p[j][c];
+                        valid |= 1u << (4 * j + c);
+                    }
+                }
+            }
+        }
+        uint32_t emit_mask = 0, cand_mask = 0;
+#pragma unroll
+        for (int j = 0; j < kVecPerThread; ++j) {
+#pragma unroll
+            for (int c = 0; c < 4; ++c) {
+                const uint32_t bit = 1u << (4 * j + c);
+                if (!(valid & bit)) continue;
+                const uint32_t key = magnitude_key(p[j][c]);
+                atomicAdd(&hist[key >> kShift1], 1u);
+                if (key > hi) emit_mask |= bit;
+                else if (key >= lo) cand_mask |= bit;
+            }
+        }
+        // keys above the bracket go to the payload (e is cleared only once
+        // the bracket is confirmed), keys inside it to the candidates
+        if (bracket)
+            append_pairs(p, r.block0, emit_mask, cand_mask, inf, st, ws, idx, val, e, false);
+    }
+    flush_hist(hist, kDigit1, ws.hist1 + int64_t(s) * kDigit1);
+}
+
+// ---------------------------------------------------------------------------
+// select1: per segment, the digit of the k-th key and the mode
+// ---------------------------------------------------------------------------
+
+__global__ __launch_bounds__(kBlock) void seg_select1_kernel(SegWs ws) {
+    __shared__ uint32_t s_wave[kWaves];
+    __shared__ uint32_t s_out[3];
+    if (ws.ctl->status != 0u) return;
+    const int32_t s = blockIdx.x;
+    const SegInfo inf = ws.info[s];
+    SegState *st = ws.st + s;
+    if (inf.k == 0 || inf.k == inf.size) {
+        if (threadIdx.x == 0) {
+            st->mode = inf.k == 0 ? kModeNone : kModeAll;
+            if (inf.k != 0) atomicAdd(&ws.ctl->pass2, 1u);
+        }
+        return;
+    }
+    // bracket confirmed when #(key > hi) <= k <= #(key >= lo) and every key in
+    // the bracket was collected: the selection continues among candidates
+    const SegState cur = *st;
+    if (cur.bracket && int64_t(cur.emit) <= inf.k && int64_t(cur.emit) + cur.ccur >= inf.k &&
+        int64_t(cur.ccur) <= inf.ccap) {
+        if (threadIdx.x == 0) {
+            st->mode = kModeFast;
+            st->need1 = uint32_t(inf.k) - cur.emit;
+            atomicAdd(&ws.ctl->bracket, 1u);
+        }
+        return;
+    }
+    pick_bin<kDigit1, true>(ws.hist1 + int64_t(s) * kDigit1, uint32_t(inf.k), s_wave, s_out);
+    if (threadIdx.x == 0) {
+        // the radix path emits and collects from scratch in pass2
+        st->emit = 0u;
+        st->ccur = 0u;
+        const uint32_t c1 = s_out[2];
+        st->d1 = s_out[0];
+        st->need1 = uint32_t(inf.k) - s_out[1];
+        st->c1 = c1;
+        st->mode = c1 == 0u ? kModeNone : (int64_t(c1) <= inf.ccap ? kModeCand : kModeScan);
+        if (c1 != 0u) atomicAdd(&ws.ctl->pass2, 1u);
+    }
+}
+
+// ---------------------------------------------------------------------------
+// pass2: keys above D1 to the payload, keys in D1 to the candidates
+// ---------------------------------------------------------------------------
+
+template <bool kAligned>
+__global__ __launch_bounds__(kBlock) void seg_pass2_kernel(float *__restrict__ e,
+                                                           int32_t *__restrict__ idx,
+                                                           float *__restrict__ val, int32_t nseg,
+                                                           SegWs ws, uint32_t tiles_per_wg) {
+    __shared__ uint32_t hist[kDigit2];
+    if (ws.ctl->status != 0u || ws.ctl->pass2 == 0u) return;
+    const uint32_t T = ws.ctl->tiles;
+    const uint32_t t0 = blockIdx.x * tiles_per_wg;
+    if (t0 >= T) return;
+    const uint32_t t1 = min(T, t0 + tiles_per_wg);
+    for (int b = threadIdx.x; b < kDigit2; b += kBlock) hist[b] = 0u;
+    int32_t s = segment_of_tile(ws.tile_prefix, nseg, t0);
+    uint32_t next = ws.tile_prefix[s + 1];
+    SegInfo inf = ws.info[s];
+    SegState *st = ws.st + s;
+    uint32_t mode = st->mode, D1 = st->d1;
+    bool dirty = false;
+    __syncthreads();
+    for (uint32_t t = t0; t < t1; ++t) {
+        if (t >= next) {
+            if (dirty) flush_hist(hist, kDigit2, ws.hist2 + int64_t(s) * kDigit2);
+            dirty = false;
+            s = segment_of_tile(ws.tile_prefix, nseg, t);
+            next = ws.tile_prefix[s + 1];
+            inf = ws.info[s];
+            st = ws.st + s;
+            mode = st->mode;
+            D1 = st->d1;
+        }
+        if (mode == kModeNone || mode == kModeFast) {
+            t = next - 1;  // nothing to do in this segment: skip its tiles
+            continue;
+        }
+        const TileRange r = tile_range(inf, t);
+        float p[kVecPerThread][4];
+        uint32_t valid = 0;
+        if (kAligned && r.lo == r.block0 && r.hi == r.block0 + kTile) {
+            const f32x4 *e4 = reinterpret_cast<const f32x4 *>(e + r.block0);
+#pragma unroll
+            for (int j = 0; j < kVecPerThread; ++j) {
+                const f32x4 v = e4[j * kBlock + threadIdx.x];
+#pragma unroll
+                for (int c = 0; c < 4; ++c) p[j][c] = v[c];
+            }
+            valid = 0xffffu;
+        } else {
+#pragma unroll
+            for (int j = 0; j < kVecPerThread; ++j) {
+#pragma unroll
+                for (int c = 0; c < 4; ++c) {
+                    const int64_t i = tile_elem(r.block0, j, c);
+                    p[j][c] = 0.0f;
+                    if (i >= r.lo && i < r.hi) {
+                        p[j][c] = e[i];
+                        valid |= 1u << (4 * j + c);
+                    }
+                }
+            }
+        }
+        uint32_t emit_mask = 0, cand_mask = 0;
+#pragma unroll
+        for (int j = 0; j < kVecPerThread; ++j) {
+#pragma unroll
+            for (int c = 0; c < 4; ++c) {
+                const uint32_t bit = 1u << (4 * j + c);
+                if (!(valid & bit)) continue;
+                const uint32_t key = magnitude_key(p[j][c]);
+                const uint32_t dg = key >> kShift1;
+                if (mode == kModeAll || (mode == kModeCand && dg > D1)) emit_mask |= bit;
+                if (dg == D1 && mode != kModeAll) {
+                    atomicAdd(&hist[(key >> kShift2) & (kDigit2 - 1)], 1u);
+                    if (mode == kModeCand) cand_mask |= bit;
+                }
+            }
+        }
+        dirty = dirty || mode != kModeAll;
+        if (mode != kModeScan)
+            append_pairs(p, r.block0, emit_mask, cand_mask, inf, st, ws, idx, val, e, true);
+    }
+    if (dirty) flush_hist(hist, kDigit2, ws.hist2 + int64_t(s) * kDigit2);
+}
+
+// ---------------------------------------------------------------------------
+// final: exact selection inside D1 for each segment
+// ---------------------------------------------------------------------------
+
+struct FinalShared {
+    uint32_t hist[kIdxBins];
+    uint2 cand[kCandLds];
+    uint32_t wave[kWaves];
+    uint32_t out[3];
+    uint32_t cursor;
+};
+
+constexpr uint32_t kNone = 0xffffffffu;  // no item (larger than every index)
+constexpr int kUnroll = 8;               // items loaded per thread at a time
+
+// Calls f(key, index, bits of p) for every item of the segment's selection
+// set: the candidate list (LDS or global), or, in scan mode, every element
+// of the segment.  kUnroll loads per thread are in flight together.
+template <int kMode, bool kLds, typename F>
+__device__ __forceinline__ void for_items(const FinalShared &sh, const uint2 *cand,
+                                          const float *e, const SegInfo &inf, int64_t n, F f) {
+    for (int64_t base = 0; base < n; base += int64_t(kUnroll) * kBlock) {
+        uint2 it[kUnroll];
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u) {
+            const int64_t q = base + u * kBlock + threadIdx.x;
+            it[u] = make_uint2(0u, kNone);
+            if (q < n) {
+                if (kMode == kModeCand) {
+                    it[u] = kLds ? sh.cand[q] : cand[q];
+                } else {
+                    const int64_t i = inf.off + q;
+                    it[u] = make_uint2(__float_as_uint(e[i]), uint32_t(i));
+                }
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u)
+            if (it[u].y != kNone) f(it[u].x & 0x7fffffffu, it[u].y, it[u].x);
+    }
+}
+
+// With the threshold key T known and `need3` of the `ties` keys equal to T
+// to keep: choose the ties (the lowest indices, by a radix select on the
+// index: bits 30..20, 19..10, 9..0, unless all are kept), emit every item
+// above T and the chosen ties from payload slot `cursor0` on, clear their e,
+// and record T as the next call's hint.
+template <int kMode, bool kLds>
+__device__ void finish(FinalShared &sh, const SegInfo &inf, const uint2 *cand, int64_t n,
+                       float *e, int32_t *idx, float *val, uint32_t T, uint32_t need3,
+                       uint32_t ties, uint32_t cursor0, SegHint *hint, uint32_t width) {
+    const int tid = threadIdx.x;
+    uint32_t imax = 0xffffffffu;
+    if (need3 < ties) {
+        uint32_t prefix = 0, rem = need3;
+#pragma unroll 1
+        for (int level = 0; level < 3; ++level) {
+            const int shift = 20 - 10 * level;
+            for (int b = tid; b < kIdxBins; b += kBlock) sh.hist[b] = 0u;
+            __syncthreads();
+            for_items<kMode, kLds>(sh, cand, e, inf, n, [&](uint32_t key, uint32_t i, uint32_t) {
+                if (key != T) return;
+                if (level > 0 && (i >> (shift + 10)) != prefix) return;
+                atomicAdd(&sh.hist[(i >> shift) & (level == 0 ? kIdxBins - 1 : 1023)], 1u);
+            });
+            __syncthreads();
+            if (level == 0) pick_bin<kIdxBins, false>(sh.hist, rem, sh.wave, sh.out);
+            else pick_bin<1024, false>(sh.hist, rem, sh.wave, sh.out);
+            prefix = (prefix << (level == 0 ? 11 : 10)) | sh.out[0];
+            rem -= sh.out[1];
+            __syncthreads();
+        }
+        imax = prefix;
+    }
+    if (tid == 0) sh.cursor = cursor0;
+    __syncthreads();
+    const int64_t kend = inf.k;
+    for_items<kMode, kLds>(sh, cand, e, inf, n, [&](uint32_t key, uint32_t i, uint32_t bits) {
+        if (!(key > T || (key == T && i <= imax))) return;
+        const uint32_t slot = atomicAdd(&sh.cursor, 1u);
+        if (int64_t(slot) < kend) {
+            idx[inf.kout + slot] = int32_t(i);
+            val[inf.kout + slot] = __uint_as_float(bits);
+            e[i] = 0.0f;
+        }
+    });
+    if (tid == 0) {
+        const SegHint old = *hint;
+        *hint = SegHint{T, old.magic == kHintMagic ? old.key : T, kHintMagic, width};
+    }
+}
+
+// Radix path: D1 from pass1, digit 2 from pass2's histogram of the keys in
+// D1, digit 3 from a pass over the items.  Scan mode also emits every key
+// above D1 (pass2 left them in place).
+template <int kMode, bool kLds>
+__device__ void final_select(FinalShared &sh, const SegInfo &inf, const SegState &st,
+                             const uint2 *cand, int64_t n, float *e, int32_t *idx, float *val,
+                             const uint32_t *hist2, SegHint *hint, uint32_t width) {
+    const int tid = threadIdx.x;
+    const uint32_t D1 = st.d1;
+    for (int b = tid; b < kDigit2; b += kBlock) sh.hist[b] = hist2[b];
+    __syncthreads();
+    pick_bin<kDigit2, true>(sh.hist, st.need1, sh.wave, sh.out);
+    const uint32_t D2 = sh.out[0];
+    const uint32_t need2 = st.need1 - sh.out[1];
+    const uint32_t P2 = (D1 << (kShift1 - kShift2)) | D2;  // key >> kShift2 of (D1, D2)
+    __syncthreads();
+    for (int b = tid; b < kDigit3; b += kBlock) sh.hist[b] = 0u;
+    __syncthreads();
+    for_items<kMode, kLds>(sh, cand, e, inf, n, [&](uint32_t key, uint32_t, uint32_t) {
+        if ((key >> kShift2) == P2) atomicAdd(&sh.hist[key & (kDigit3 - 1)], 1u);
+    });
+    __syncthreads();
+    pick_bin<kDigit3, true>(sh.hist, need2, sh.wave, sh.out);
+    const uint32_t T = (P2 << kShift2) | sh.out[0];
+    const uint32_t need3 = need2 - sh.out[1];
+    const uint32_t ties = sh.out[2];
+    __syncthreads();
+    finish<kMode, kLds>(sh, inf, cand, n, e, idx, val, T, need3, ties,
+                        kMode == kModeCand ? st.emit : 0u, hint, width);
+}
+
+// Bracket path: pass1 put the keys above hi in the payload (e not yet
+// cleared) and the keys in [lo, hi] (at most 2^20 keys) in the candidates;
+// select the remaining need1 among them by (key - lo) bits 19..10, then 9..0.
+template <bool kLds>
+__device__ void final_bracket(FinalShared &sh, const SegInfo &inf, const SegState &st,
+                              const uint2 *cand, int64_t n, float *e, int32_t *idx, float *val,
+                              SegHint *hint, uint32_t width) {
+    const int tid = threadIdx.x;
+    const uint32_t above = min(st.emit, uint32_t(inf.k));
+    for (uint32_t j = tid; j < above; j += kBlock) e[idx[inf.kout + j]] = 0.0f;
+    const uint32_t need = st.need1;
+    if (need == 0u) return;
+    const uint32_t lo = st.lo;
+    for (int b = tid; b < 1024; b += kBlock) sh.hist[b] = 0u;
+    __syncthreads();
+    for_items<kModeCand, kLds>(sh, cand, e, inf, n, [&](uint32_t key, uint32_t, uint32_t) {
+        atomicAdd(&sh.hist[((key - lo) >> 10) & 1023u], 1u);
+    });
+    __syncthreads();
+    pick_bin<1024, true>(sh.hist, need, sh.wave, sh.out);
+    const uint32_t DA = sh.out[0];
+    const uint32_t needA = need - sh.out[1];
+    __syncthreads();
+    for (int b = tid; b < 1024; b += kBlock) sh.hist[b] = 0u;
+    __syncthreads();
+    for_items<kModeCand, kLds>(sh, cand, e, inf, n, [&](uint32_t key, uint32_t, uint32_t) {
+        if (((key - lo) >> 10) == DA) atomicAdd(&sh.hist[(key - lo) & 1023u], 1u);
+    });
+    __syncthreads();
+    pick_bin<1024, true>(sh.hist, needA, sh.wave, sh.out);
+    const uint32_t T = lo + ((DA << 10) | sh.out[0]);
+    const uint32_t need3 = needA - sh.out[1];
+    const uint32_t ties = sh.out[2];
+    __syncthreads();
+    finish<kModeCand, kLds>(sh, inf, cand, n, e, idx, val, T, need3, ties, above, hint, width);
+}
+
+__global__ __launch_bounds__(kBlock) void seg_final_kernel(float *__restrict__ e,
+                                                           int32_t *__restrict__ idx,
+                                                           float *__restrict__ val, SegWs ws) {
+    __shared__ FinalShared sh;
+    if (ws.ctl->status != 0u) return;
+    const int32_t s = blockIdx.x;
+    const SegState st = ws.st[s];
+    if (st.mode != kModeCand && st.mode != kModeScan && st.mode != kModeFast) return;
+    const SegInfo inf = ws.info[s];
+    SegHint *hint = ws.hint + s;
+    // next bracket width: narrower after a bracket that held many more keys
+    // than needed, wider after one that missed the k-th key
+    const SegHint oh = *hint;
+    uint32_t width = (oh.magic == kHintMagic && oh.width >= kWidthMin && oh.width <= kWidthMax)
+                         ? oh.width : kWidthStart;
+    if (st.mode == kModeFast) {
+        if (int64_t(st.ccur) > 4 * inf.k + 1024 && width > kWidthMin) --width;
+    } else if (st.bracket && width < kWidthMax) {
+        ++width;
+    }
+    const uint32_t *h2 = ws.hist2 + int64_t(s) * kDigit2;
+    if (st.mode == kModeScan) {
+        final_select<kModeScan, false>(sh, inf, st, nullptr, inf.size, e, idx, val, h2, hint, width);
+        return;
+    }
+    const int64_t n = min(int64_t(st.ccur), inf.ccap);
+    const uint2 *cand = ws.cand + inf.coff;
+    const bool lds = n <= kCandLds;
+    if (lds) {
+        for (int64_t base = 0; base < n; base += int64_t(kUnroll) * kBlock) {
+            uint2 v[kUnroll];
+#pragma unroll
+            for (int u = 0; u < kUnroll; ++u) {
+                const int64_t q = base + u * kBlock + threadIdx.x;
+                if (q < n) v[u] = cand[q];
+            }
+#pragma unroll
+            for (int u = 0; u < kUnroll; ++u) {
+                const int64_t q = base + u * kBlock + threadIdx.x;
+                if (q < n) sh.cand[q] = v[u];
+            }
+        }
+        __syncthreads();
+    }
+    if (st.mode == kModeFast) {
+        if (lds) final_bracket<true>(sh, inf, st, cand, n, e, idx, val, hint, width);
+        else final_bracket<false>(sh, inf, st, cand, n, e, idx, val, hint, width);
+    } else {
+        if (lds) final_select<kModeCand, true>(sh, inf, st, cand, n, e, idx, val, h2, hint, width);
+        else final_select<kModeCand, false>(sh, inf, st, cand, n, e, idx, val, h2, hint, width);
+    }
+}
+
+}  // namespace
+
+size_t topk_segmented_workspace_size(int32_t nseg, int64_t k_total) {
+    return seg_layout(nseg, k_total).bytes;
+}
+
+size_t topk_segmented_status_offset() { return offsetof(SegCtl, status); }
+size_t topk_segmented_bracket_offset() { return offsetof(SegCtl, bracket); }
+
+hipError_t launch_topk_segmented(const float *g, float *e, int64_t d, float lr, int32_t nseg,
+                                 const int64_t *offsets, const int64_t *k, int64_t k_total,
+                                 int32_t *idx, float *val, void *workspace, hipStream_t stream) {
+    const SegLayout L = seg_layout(nseg, k_total);
+    char *base = static_cast<char *>(workspace);
+    SegWs ws;
+    ws.ctl = reinterpret_cast<SegCtl *>(base);
+    ws.info = reinterpret_cast<SegInfo *>(base + L.info);
+    ws.tile_prefix = reinterpret_cast<uint32_t *>(base + L.tile_prefix);
+    ws.st = reinterpret_cast<SegState *>(base + L.st);
+    ws.hint = reinterpret_cast<SegHint *>(base + L.hint);
+    ws.hist1 = reinterpret_cast<uint32_t *>(base + L.hist1);
+    ws.hist2 = reinterpret_cast<uint32_t *>(base + L.hist2);
+    ws.cand = reinterpret_cast<uint2 *>(base + L.cand);
+    ws.ccap_total = L.ccap_total;
+
+    const int64_t hist_words = int64_t(nseg) * (kDigit1 + kDigit2);
+    const uint32_t zero_grid = persistent_grid((hist_words + int64_t(kBlock) * 4 - 1) /
+                                               (int64_t(kBlock) * 4));
+    seg_reset_kernel<<<1 + zero_grid, kBlock, 0, stream>>>(ws, offsets, k, nseg, d, k_total);
+
+    const int64_t max_tiles = (d + kTile - 1) / kTile + nseg;
+    const uint32_t grid = balanced_grid(max_tiles, kStageWorkgroupsPerCU);
+    const uint32_t per_wg = uint32_t((max_tiles + grid - 1) / grid);
+    const bool aligned = ((reinterpret_cast<uintptr_t>(g) | reinterpret_cast<uintptr_t>(e)) & 15) == 0;
+    if (aligned)
+        seg_pass1_kernel<true><<<grid, kBlock, 0, stream>>>(g, e, lr, idx, val, nseg, ws, per_wg);
+    else
+        seg_pass1_kernel<false><<<grid, kBlock, 0, stream>>>(g, e, lr, idx, val, nseg, ws, per_wg);
+    seg_select1_kernel<<<uint32_t(nseg), kBlock, 0, stream>>>(ws);
+    if (aligned)
+        seg_pass2_kernel<true><<<grid, kBlock, 0, stream>>>(e, idx, val, nseg, ws, per_wg);
+    else
+        seg_pass2_kernel<false><<<grid, kBlock, 0, stream>>>(e, idx, val, nseg, ws, per_wg);
+    seg_final_kernel<<<uint32_t(nseg), kBlock, 0, stream>>>(e, idx, val, ws);
+    return hipGetLastError();
+}
+
+}  // namespace efs

@@ -185,3 +185,38 @@ def test_apply_workspace_size(lib):
     b = lib.sparse_apply_workspace_bytes(8, 25_600_000, 1000)
     assert b - a == 8000                     # 8 bytes per pair slot
     assert a >= (25_600_000 // 8192) * 4       # one counter per 8192-coordinate range
+
+
+def test_topk_segmented_rejects_bad_arguments(lib):
+    fake = 0x10000
+    need = lib.topk_segmented_workspace_bytes(3, 10)
+    assert need >= 256 + 3 * (8192 + 1024) * 4 + (16 * 10 + 3 * 4096) * 8
+    cases = [
+        (dict(d=-1), binding.EFS_EINVAL),
+        (dict(nseg=0), binding.EFS_EINVAL),
+        (dict(nseg=65537), binding.EFS_EINVAL),
+        (dict(k_total=-1), binding.EFS_EINVAL),
+        (dict(k_total=1001), binding.EFS_EINVAL),
+        (dict(g=NULL), binding.EFS_EINVAL),
+        (dict(e=fake + 2), binding.EFS_EINVAL),
+        (dict(lr=float("inf")), binding.EFS_EINVAL),
+        (dict(off=NULL), binding.EFS_EINVAL),
+        (dict(k=fake + 4), binding.EFS_EINVAL),
+        (dict(idx=NULL), binding.EFS_EINVAL),
+        (dict(ws=NULL), binding.EFS_EINVAL),
+        (dict(ws=fake + 8), binding.EFS_EINVAL),
+        (dict(ws_bytes=need - 1), binding.EFS_ESPACE),
+    ]
+    for over, want in cases:
+        a = dict(g=fake, e=fake, d=1000, lr=0.1, nseg=3, off=fake, k=fake, k_total=10, idx=fake,
+                 val=fake, ws=fake, ws_bytes=need)
+        a.update(over)
+        rc = lib.topk_segmented_compress(a["g"], a["e"], a["d"], a["lr"], a["nseg"], a["off"],
+                                         a["k"], a["k_total"], a["idx"], a["val"], a["ws"],
+                                         a["ws_bytes"], None)
+        assert rc == want, over
+    # d == 0 is a no-op that launches nothing
+    assert lib.topk_segmented_compress(None, None, 0, 0.1, 1, fake, fake, 0, None, None, None, 0,
+                                       None) == binding.EFS_OK
+    assert lib.topk_segmented_workspace_bytes(0, 1) == 0
+    assert lib.topk_segmented_workspace_bytes(1, -1) == 0

@@ -1,0 +1,287 @@
+"""GPU parity of the layer-wise Top-k (topk_segmented_compress; Appendix
+C.5: Top-k on each layer's tensor on its own) against the CPU oracle.
+
+Within a segment the payload order is unspecified, so each segment's pairs
+are compared after sorting by index; indices, values and the whole error
+vector are compared bit for bit.  Layouts mix empty, tiny, 4096-aligned and
+unaligned segments; budgets cover k = 0, k = size, k > size; values cover
+ties at the threshold (quantised values, all-zero segments), special values,
+and candidate sets larger than the final pass holds in LDS.
+"""
+import numpy as np
+import pytest
+
+import oracle
+from paper_2108_00951_amd import synth
+from tests._checks import assert_bits_equal, bits
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+from paper_2108_00951_amd import binding as efs  # noqa: E402
+
+LR = np.float32(0.1)
+DEV = "cuda"
+
+
+def say(*a):
+    print(*a, flush=True)
+
+
+def dev(a, unaligned=False):
+    a = np.ascontiguousarray(a)
+    if not unaligned:
+        return torch.from_numpy(a).to(DEV)
+    buf = torch.empty(a.size + 1, dtype=torch.from_numpy(a[:0]).dtype, device=DEV)
+    v = buf[1:]
+    v.copy_(torch.from_numpy(a))
+    return v
+
+
+def run_gpu(g, e, offsets, ks, lr=LR, unaligned=False, k_total=None, ws=None):
+    """One call; returns (idx, val, e_next, workspace) on the host."""
+    offsets = np.asarray(offsets, dtype=np.int64)
+    ks = np.asarray(ks, dtype=np.int64)
+    sizes = np.diff(offsets)
+    total = int(np.minimum(np.maximum(ks, 0), np.maximum(sizes, 0)).sum())
+    if k_total is None:
+        k_total = total
+    gd, ed = dev(g, unaligned), dev(e, unaligned)
+    idx = torch.full((max(k_total, 1),), -7, dtype=torch.int32, device=DEV)[:k_total]
+    val = torch.full((max(k_total, 1),), -7.0, dtype=torch.float32, device=DEV)[:k_total]
+    if ws is None:
+        ws = efs.new_topk_segmented_workspace(ks.size, k_total, DEV)
+    efs.topk_segmented_compress(gd, ed, lr, dev(offsets), dev(ks), idx, val, ws)
+    return idx.cpu().numpy(), val.cpu().numpy(), ed.cpu().numpy(), ws
+
+
+def check(g, e, offsets, ks, lr=LR, unaligned=False, what=""):
+    gi, gv, ge, ws = run_gpu(g, e, offsets, ks, lr, unaligned)
+    assert efs.topk_segmented_status(ws) == 0
+    ri, rv, re = oracle.topk_segmented(g, e, lr, offsets, ks)
+    assert gi.size == ri.size, what
+    # per segment: same region, same pairs after sorting by index
+    offsets = np.asarray(offsets)
+    pos = 0
+    for s in range(len(ks)):
+        n = int(min(max(int(ks[s]), 0), int(offsets[s + 1] - offsets[s])))
+        seg_i, seg_v = gi[pos:pos + n], gv[pos:pos + n]
+        order = np.argsort(seg_i, kind="stable")
+        np.testing.assert_array_equal(seg_i[order], ri[pos:pos + n], "%s segment %d" % (what, s))
+        assert_bits_equal(seg_v[order], rv[pos:pos + n], "%s segment %d values" % (what, s))
+        pos += n
+    assert_bits_equal(ge, re, "%s e'" % what)
+    return gi, gv, ge
+
+
+def random_layout(rng, d, nseg):
+    cuts = np.sort(rng.integers(0, d + 1, size=nseg - 1))
+    return np.concatenate([[0], cuts, [d]]).astype(np.int64)
+
+
+@pytest.mark.parametrize("unaligned", [False, True])
+def test_segmented_mixed_layout(unaligned):
+    sizes = [0, 1, 64, 4096, 4097, 8192 * 3, 0, 70_001, 5, 4095, 250_000, 1]
+    off = np.concatenate([[0], np.cumsum(sizes)]).astype(np.int64)
+    d = int(off[-1])
+    ks = np.array([0, 1, 3, 40, 4097, 100, 2, 70, 9, 0, 2500, 1], dtype=np.int64)
+    g = synth.small_gradient(401, d)
+    e = (synth.small_gradient(402, d) * np.float32(0.1)).astype(np.float32)
+    say("segmented mixed layout unaligned=%s d=%d" % (unaligned, d))
+    check(g, e, off, ks, unaligned=unaligned, what="mixed")
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_segmented_random_layouts(seed):
+    rng = np.random.default_rng(410 + seed)
+    d = int(rng.integers(10_000, 400_000))
+    nseg = int(rng.integers(1, 60))
+    off = random_layout(rng, d, nseg)
+    sizes = np.diff(off)
+    ks = np.ceil(sizes * 10.0 ** rng.uniform(-3.5, -0.5, size=nseg)).astype(np.int64)
+    ks[rng.random(nseg) < 0.1] = 0
+    g = synth.small_gradient(420 + seed, d)
+    e = np.zeros(d, np.float32)
+    say("segmented random layout seed=%d d=%d nseg=%d" % (seed, d, nseg))
+    check(g, e, off, ks, what="random %d" % seed)
+
+
+@pytest.mark.parametrize("levels", [3, 17])
+def test_segmented_ties_at_threshold(levels):
+    # few distinct magnitudes: the k-th key is shared by many coordinates
+    # and only the lowest indices among them are kept
+    rng = np.random.default_rng(430 + levels)
+    d = 300_000
+    off = random_layout(rng, d, 9)
+    sizes = np.diff(off)
+    g = (rng.integers(-levels, levels + 1, size=d) * np.float32(0.125)).astype(np.float32)
+    e = np.zeros(d, np.float32)
+    ks = np.maximum(sizes // 7 + 3, 1)
+    say("segmented ties levels=%d" % levels)
+    check(g, e, off, ks, lr=np.float32(1.0), what="ties")
+
+
+def test_segmented_zero_segments_take_lowest_indices():
+    # all-zero segments with a partial budget: every key is 0, so the kept
+    # set is the k lowest indices (and the candidate region cannot hold the
+    # tie bin: the scan path)
+    sizes = [100_000, 9, 50_000, 4096]
+    off = np.concatenate([[0], np.cumsum(sizes)]).astype(np.int64)
+    d = int(off[-1])
+    g = np.zeros(d, np.float32)
+    g[100_000:100_009] = 1.0           # segment 1 is not all zero
+    g[-1] = -0.0                       # -0 ties with +0
+    e = np.zeros(d, np.float32)
+    ks = np.array([10, 4, 1234, 4000], dtype=np.int64)
+    say("segmented zero segments")
+    gi, _, _ = check(g, e, off, ks, what="zeros")
+    np.testing.assert_array_equal(np.sort(gi[:10]), np.arange(10))
+
+
+def test_segmented_large_candidate_sets():
+    # a budget of several thousand in a large segment: more candidates than
+    # the final pass holds in LDS
+    d = 2_000_000
+    off = np.array([0, 37, 1_500_000, d], dtype=np.int64)
+    ks = np.array([5, 6000, 3000], dtype=np.int64)
+    g = synth.small_gradient(440, d)
+    e = np.zeros(d, np.float32)
+    say("segmented large candidate sets")
+    check(g, e, off, ks, what="large")
+
+
+def test_segmented_special_values():
+    d = 5000
+    off = np.array([0, 1000, 2500, d], dtype=np.int64)
+    rng = np.random.default_rng(450)
+    g = (rng.standard_normal(d) * 1e-3).astype(np.float32)
+    g[[3, 1500, 4000]] = np.nan
+    g[[7, 2600]] = np.inf
+    g[[8, 2601]] = -np.inf
+    g[[9, 10, 1501]] = np.float32(1e-41)
+    g[11] = -0.0
+    e = np.zeros(d, np.float32)
+    ks = np.array([4, 2, 3], dtype=np.int64)
+    say("segmented special values")
+    check(g, e, off, ks, what="special")
+
+
+def test_segmented_one_segment_matches_flat_topk():
+    d = 1_000_003
+    g = synth.small_gradient(460, d)
+    e = np.zeros(d, np.float32)
+    k = 1234
+    gi, gv, ge, _ = run_gpu(g, e, [0, d], [k])
+    ws = efs.new_topk_workspace(d, k)
+    ed = dev(e)
+    idx = torch.empty(k, dtype=torch.int32, device=DEV)
+    val = torch.empty(k, dtype=torch.float32, device=DEV)
+    efs.topk_compress(dev(g), ed, LR, k, idx, val, ws)
+    fi = idx.cpu().numpy()
+    np.testing.assert_array_equal(np.sort(gi), np.sort(fi))
+    assert_bits_equal(ge, ed.cpu().numpy())
+
+
+def test_segmented_ef_loop():
+    # five EF steps with e carried, layer-wise budgets at 0.5 %
+    rng = np.random.default_rng(470)
+    d = 600_000
+    off = random_layout(rng, d, 25)
+    ks = synth.layerwise_k(off, 0.005)
+    e_ref = np.zeros(d, np.float32)
+    ed = torch.zeros(d, dtype=torch.float32, device=DEV)
+    k_total = int(ks.sum())
+    idx = torch.empty(k_total, dtype=torch.int32, device=DEV)
+    val = torch.empty(k_total, dtype=torch.float32, device=DEV)
+    ws = efs.new_topk_segmented_workspace(ks.size, k_total, DEV)
+    ws.zero_()
+    offd, kd = dev(off), dev(ks)
+    hits = []
+    for t in range(5):
+        g = synth.small_gradient(480 + t, d)
+        efs.topk_segmented_compress(dev(g), ed, LR, offd, kd, idx, val, ws)
+        ri, rv, e_ref = oracle.topk_segmented(g, e_ref, LR, off, ks)
+        gi = idx.cpu().numpy()
+        pos = 0
+        for s in range(ks.size):
+            n = int(ks[s])
+            np.testing.assert_array_equal(np.sort(gi[pos:pos + n]), ri[pos:pos + n])
+            pos += n
+        assert_bits_equal(ed.cpu().numpy(), e_ref, "e' t=%d" % t)
+        hits.append(efs.topk_segmented_bracket_segments(ws))
+        say("  segmented EF step %d ok (bracket in %d of %d segments)" % (t, hits[-1], ks.size))
+    assert hits[0] == 0          # no hint on the first call
+    assert sum(hits[1:]) > 0     # error feedback keeps thresholds close
+
+
+@pytest.mark.parametrize("case", ["first_offset", "decreasing", "last_offset", "negative_k",
+                                  "budget"])
+def test_segmented_bad_layout_changes_nothing(case):
+    d = 10_000
+    off = np.array([0, 3000, 7000, d], dtype=np.int64)
+    ks = np.array([10, 20, 30], dtype=np.int64)
+    k_total = 60
+    if case == "first_offset":
+        off[0] = 5
+    elif case == "decreasing":
+        off[1] = 7500
+    elif case == "last_offset":
+        off[3] = d - 1
+    elif case == "negative_k":
+        ks[1] = -1
+    else:
+        k_total = 59
+    g = synth.small_gradient(490, d)
+    e = synth.small_gradient(491, d)
+    gi, gv, ge, ws = run_gpu(g, e, off, ks, k_total=k_total)
+    assert efs.topk_segmented_status(ws) == 1
+    assert_bits_equal(ge, e)
+    assert np.all(gi == -7)
+    # the same workspace then serves a good call
+    good_off, good_ks = np.array([0, 3000, 7000, d]), np.array([10, 20, 30])
+    gi, gv, ge, _ = run_gpu(g, e, good_off, good_ks, k_total=k_total if case != "budget" else 60,
+                            ws=ws if case != "budget" else None)
+    assert efs.topk_segmented_status(ws) == (0 if case != "budget" else 1)
+    ri, rv, re = oracle.topk_segmented(g, e, LR, good_off, good_ks)
+    np.testing.assert_array_equal(np.sort(gi[:60]), np.sort(ri))
+    assert_bits_equal(ge, re)
+
+
+def test_segmented_workspace_contents_do_not_matter():
+    rng = np.random.default_rng(495)
+    d = 200_000
+    off = random_layout(rng, d, 12)
+    ks = synth.layerwise_k(off, 0.01)
+    g = synth.small_gradient(496, d)
+    e = np.zeros(d, np.float32)
+    ri, rv, re = oracle.topk_segmented(g, e, LR, off, ks)
+    ws = efs.new_topk_segmented_workspace(ks.size, int(ks.sum()), DEV)
+    for fill in (0, 255, 0x3C):
+        ws.fill_(fill)
+        gi, gv, ge, _ = run_gpu(g, e, off, ks, ws=ws)
+        np.testing.assert_array_equal(np.sort(gi), np.sort(ri))
+        assert_bits_equal(ge, re)
+
+
+def test_segmented_bracket_from_another_scale_falls_back():
+    # hints learned on one scale make a bracket that misses the next call's
+    # thresholds (50x larger): the radix path takes over, results exact; the
+    # call after that, on the same scale, selects from the bracket
+    rng = np.random.default_rng(497)
+    d = 300_000
+    off = random_layout(rng, d, 10)
+    ks = synth.layerwise_k(off, 0.01)
+    ws = efs.new_topk_segmented_workspace(ks.size, int(ks.sum()), DEV)
+    ws.zero_()   # no hints yet (a reused allocation could hold some)
+    g1 = synth.small_gradient(498, d)
+    g2 = (synth.small_gradient(499, d) * np.float32(50.0)).astype(np.float32)
+    e = np.zeros(d, np.float32)
+    hits = []
+    for g in (g1, g2, g2):
+        gi, gv, ge, _ = run_gpu(g, e, off, ks, ws=ws)
+        ri, rv, re = oracle.topk_segmented(g, e, LR, off, ks)
+        np.testing.assert_array_equal(np.sort(gi), np.sort(ri))
+        assert_bits_equal(ge, re)
+        hits.append(efs.topk_segmented_bracket_segments(ws))
+    assert hits[0] == 0 and hits[1] == 0
+    assert hits[2] == ks.size

@@ -113,6 +113,74 @@ def test_workload2_segments_25m():
         say("workload 2 t=%d: ht k_t=%d, topk ok" % (t, n))
 
 
+def _segmented(d, bounds, ks):
+    """Device buffers for layer-wise Top-k over the given layout."""
+    k_total = int(ks.sum())
+    return dict(off=torch.from_numpy(np.asarray(bounds, np.int64)).to(DEV),
+                k=torch.from_numpy(np.asarray(ks, np.int64)).to(DEV),
+                idx=torch.empty(k_total, dtype=torch.int32, device=DEV),
+                val=torch.empty(k_total, dtype=torch.float32, device=DEV),
+                ws=efs.new_topk_segmented_workspace(len(ks), k_total, DEV),
+                e=torch.zeros(d, dtype=torch.float32, device=DEV))
+
+
+def _check_segments(acc, bounds, ks, gi, gv, e_next):
+    pos = 0
+    for s in range(len(ks)):
+        lo, hi, n = int(bounds[s]), int(bounds[s + 1]), int(ks[s])
+        check_topk_properties(acc[lo:hi], n, gi[pos:pos + n] - lo, gv[pos:pos + n], e_next[lo:hi])
+        pos += n
+
+
+def test_workload2_layerwise_topk():
+    # layer-wise Top-k over the 161 segments, k_s = ceil(0.1 % of d_s), e
+    # carried for three steps: the oracle at t = 0 and 1, properties after
+    st = synth.Stream(2)
+    w = st.w
+    ks = synth.layerwise_k(st.bounds, w.densities[0])
+    b = _segmented(w.d, st.bounds, ks)
+    e_ref = np.zeros(w.d, np.float32)
+    for t in range(3):
+        g = st.gradient(t, threads=THREADS)
+        acc = oracle.ht(g, e_ref, LR, np.inf)[2]
+        efs.topk_segmented_compress(torch.from_numpy(g).to(DEV), b["e"], LR, b["off"], b["k"],
+                                    b["idx"], b["val"], b["ws"])
+        assert efs.topk_segmented_status(b["ws"]) == 0
+        gi, gv, ge = b["idx"].cpu().numpy(), b["val"].cpu().numpy(), b["e"].cpu().numpy()
+        if t < 2:
+            ri, rv, re = oracle.topk_segmented(g, e_ref, LR, st.bounds, ks)
+            pos = 0
+            for s in range(ks.size):
+                n = int(ks[s])
+                assert_payload_equal(gi[pos:pos + n], gv[pos:pos + n], ri[pos:pos + n],
+                                     rv[pos:pos + n], "segment %d t=%d" % (s, t))
+                pos += n
+            assert_bits_equal(ge, re, "layer-wise e' t=%d" % t)
+        _check_segments(acc, st.bounds, ks, gi, gv, ge)
+        e_ref = ge
+        say("workload 2 layer-wise t=%d: %d pairs in %d segments ok" % (t, ks.sum(), ks.size))
+
+
+def test_workload3_layerwise_topk():
+    # 110e6 elements in 200 segments at 1 % and 0.01 % per segment
+    st = synth.Stream(3)
+    w = st.w
+    g = st.gradient(0, threads=THREADS)
+    acc = oracle.ht(g, np.zeros(w.d, np.float32), LR, np.inf)[2]   # p with e = 0
+    g_dev = torch.from_numpy(g).to(DEV)
+    for rho in (0.01, 0.0001):
+        ks = synth.layerwise_k(st.bounds, rho)
+        b = _segmented(w.d, st.bounds, ks)
+        efs.topk_segmented_compress(g_dev, b["e"], LR, b["off"], b["k"], b["idx"], b["val"],
+                                    b["ws"])
+        assert efs.topk_segmented_status(b["ws"]) == 0
+        _check_segments(acc, st.bounds, ks, b["idx"].cpu().numpy(), b["val"].cpu().numpy(),
+                        b["e"].cpu().numpy())
+        say("workload 3 layer-wise rho=%g: %d pairs ok" % (rho, ks.sum()))
+        del b
+        torch.cuda.empty_cache()
+
+
 def test_workload3_student_t_110m():
     st = synth.Stream(3)
     w = st.w
