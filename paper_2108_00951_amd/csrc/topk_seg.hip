@@ -386,29 +386,95 @@ __device__ __forceinline__ void flush_hist(uint32_t *lds, int bins, uint32_t *gl
     __syncthreads();
 }
 
-// Wave-aggregated reservation: every lane asks for `c` (< 32) slots of the
-// counter; returns the lane's first slot.
-__device__ __forceinline__ uint32_t reserve(uint32_t *counter, uint32_t c) {
-    uint32_t wtot;
-    const uint32_t pre = wave_prefix_small(c, wtot);
-    uint32_t base = 0;
-    const int lane = threadIdx.x & (kWave - 1);
-    if (lane == 0 && wtot != 0u) base = atomicAdd(counter, wtot);
-    base = __shfl(base, 0);
-    return base + pre;
+// Selections of a workgroup are staged in LDS and written out in coalesced
+// runs behind one atomic per run (a global atomic per tile would stall every
+// wave for a round trip): payload pairs (index, bits of p) and candidates
+// (bits of p, index) of the current segment.
+constexpr int kStageCap = 496;  // keeps pass1 (with its 32 KiB histogram) at 4 workgroups per CU
+
+struct Stage {
+    uint32_t e_idx[kStageCap];
+    uint32_t e_val[kStageCap];
+    uint2 cand[kStageCap];
+    uint32_t wave[kWaves];
+    uint32_t base;
+};
+
+__device__ __forceinline__ void flush_emit(Stage &sg, uint32_t &fill, SegState *st,
+                                           const SegInfo &inf, int32_t *idx, float *val) {
+    __syncthreads();
+    if (fill == 0u) return;
+    if (threadIdx.x == 0) sg.base = atomicAdd(&st->emit, fill);
+    __syncthreads();
+    const uint32_t base = sg.base;
+    for (uint32_t q = threadIdx.x; q < fill; q += kBlock) {
+        const int64_t slot = int64_t(base) + q;
+        if (slot < inf.k) {
+            idx[inf.kout + slot] = int32_t(sg.e_idx[q]);
+            val[inf.kout + slot] = __uint_as_float(sg.e_val[q]);
+        }
+    }
+    fill = 0u;
+    __syncthreads();
 }
 
-// Appends this thread's elements selected by `emit_mask` to the segment's
-// payload and those in `cand_mask` to its candidate region (slots past the
-// region ends are counted but not written).  zero_e also clears e at the
-// emitted elements.
-__device__ __forceinline__ void append_pairs(const float (&p)[kVecPerThread][4], int64_t block0,
-                                             uint32_t emit_mask, uint32_t cand_mask,
-                                             const SegInfo &inf, SegState *st, const SegWs &ws,
-                                             int32_t *idx, float *val, float *e, bool zero_e) {
-    uint32_t slot = reserve(&st->emit, uint32_t(__popc(emit_mask)));
-    uint32_t cslot = reserve(&st->ccur, uint32_t(__popc(cand_mask)));
-    if ((emit_mask | cand_mask) == 0u) return;
+__device__ __forceinline__ void flush_cand(Stage &sg, uint32_t &fill, SegState *st,
+                                           const SegInfo &inf, uint2 *cand) {
+    __syncthreads();
+    if (fill == 0u) return;
+    if (threadIdx.x == 0) sg.base = atomicAdd(&st->ccur, fill);
+    __syncthreads();
+    const uint32_t base = sg.base;
+    for (uint32_t q = threadIdx.x; q < fill; q += kBlock) {
+        const int64_t slot = int64_t(base) + q;
+        if (slot < inf.ccap) cand[inf.coff + slot] = sg.cand[q];
+    }
+    fill = 0u;
+    __syncthreads();
+}
+
+// Stages this tile's selections (called by every thread of the workgroup):
+// elements of `emit_mask` for the payload (e cleared there when zero_e), of
+// `cand_mask` for the candidates.  When a tile selects more of either than a
+// stage holds (mode all, or many equal keys), its slots are reserved
+// directly with one atomic and written without staging.
+__device__ __forceinline__ void stage_tile(Stage &sg, uint32_t &efill, uint32_t &cfill,
+                                           const float (&p)[kVecPerThread][4], int64_t block0,
+                                           uint32_t emit_mask, uint32_t cand_mask,
+                                           const SegInfo &inf, SegState *st, uint2 *cand,
+                                           int32_t *idx, float *val, float *e, bool zero_e) {
+    const int lane = threadIdx.x & (kWave - 1);
+    const int wave = threadIdx.x / kWave;
+    const uint32_t mine = uint32_t(__popc(emit_mask)) | (uint32_t(__popc(cand_mask)) << 16);
+    const uint32_t incl = wave_incl_u32(mine);
+    if (lane == kWave - 1) sg.wave[wave] = incl;
+    __syncthreads();
+    uint32_t off = 0, tot = 0;
+#pragma unroll
+    for (int q = 0; q < kWaves; ++q) {
+        off += q < wave ? sg.wave[q] : 0u;
+        tot += sg.wave[q];
+    }
+    const uint32_t pre = off + incl - mine;
+    const uint32_t te = tot & 0xffffu, tc = tot >> 16;
+    __syncthreads();  // sg.wave is reused below and by the next tile
+    if (te == 0u && tc == 0u) return;
+    const bool edirect = te > uint32_t(kStageCap);
+    const bool cdirect = tc > uint32_t(kStageCap);
+    if (!edirect && efill + te > uint32_t(kStageCap)) flush_emit(sg, efill, st, inf, idx, val);
+    if (!cdirect && cfill + tc > uint32_t(kStageCap)) flush_cand(sg, cfill, st, inf, cand);
+    uint32_t ebase = 0, cbase = 0;
+    if (edirect || cdirect) {
+        if (threadIdx.x == 0) {
+            if (edirect) sg.wave[0] = atomicAdd(&st->emit, te);
+            if (cdirect) sg.wave[1] = atomicAdd(&st->ccur, tc);
+        }
+        __syncthreads();
+        ebase = sg.wave[0];
+        cbase = sg.wave[1];
+        __syncthreads();
+    }
+    uint32_t ep = pre & 0xffffu, cp = pre >> 16;
 #pragma unroll
     for (int j = 0; j < kVecPerThread; ++j) {
 #pragma unroll
@@ -416,20 +482,34 @@ __device__ __forceinline__ void append_pairs(const float (&p)[kVecPerThread][4],
             const uint32_t bit = 1u << (4 * j + c);
             const int64_t i = tile_elem(block0, j, c);
             if (emit_mask & bit) {
-                if (int64_t(slot) < inf.k) {
-                    idx[inf.kout + slot] = int32_t(i);
-                    val[inf.kout + slot] = p[j][c];
-                    if (zero_e) e[i] = 0.0f;
+                if (edirect) {
+                    const int64_t slot = int64_t(ebase) + ep;
+                    if (slot < inf.k) {
+                        idx[inf.kout + slot] = int32_t(i);
+                        val[inf.kout + slot] = p[j][c];
+                    }
+                } else {
+                    sg.e_idx[efill + ep] = uint32_t(i);
+                    sg.e_val[efill + ep] = __float_as_uint(p[j][c]);
                 }
-                ++slot;
+                if (zero_e) e[i] = 0.0f;
+                ++ep;
             }
             if (cand_mask & bit) {
-                if (int64_t(cslot) < inf.ccap)
-                    ws.cand[inf.coff + cslot] = make_uint2(__float_as_uint(p[j][c]), uint32_t(i));
-                ++cslot;
+                const uint2 v = make_uint2(__float_as_uint(p[j][c]), uint32_t(i));
+                if (cdirect) {
+                    const int64_t slot = int64_t(cbase) + cp;
+                    if (slot < inf.ccap) cand[inf.coff + slot] = v;
+                } else {
+                    sg.cand[cfill + cp] = v;
+                }
+                ++cp;
             }
         }
     }
+    if (!edirect) efill += te;
+    if (!cdirect) cfill += tc;
+    __syncthreads();
 }
 
 template <bool kAligned>
@@ -439,6 +519,7 @@ __global__ __launch_bounds__(kBlock) void seg_pass1_kernel(const float *__restri
                                                            float *__restrict__ val, int32_t nseg,
                                                            SegWs ws, uint32_t tiles_per_wg) {
     __shared__ uint32_t hist[kDigit1];
+    __shared__ Stage sg;
     if (ws.ctl->status != 0u) return;
     const uint32_t T = ws.ctl->tiles;
     const uint32_t t0 = blockIdx.x * tiles_per_wg;
@@ -450,9 +531,14 @@ __global__ __launch_bounds__(kBlock) void seg_pass1_kernel(const float *__restri
     SegInfo inf = ws.info[s];
     SegState *st = ws.st + s;
     uint32_t bracket = st->bracket, lo = st->lo, hi = st->hi;
+    uint32_t efill = 0, cfill = 0;
     __syncthreads();
     for (uint32_t t = t0; t < t1; ++t) {
         if (t >= next) {
+            if (bracket) {
+                flush_emit(sg, efill, st, inf, idx, val);
+                flush_cand(sg, cfill, st, inf, ws.cand);
+            }
             flush_hist(hist, kDigit1, ws.hist1 + int64_t(s) * kDigit1);
             s = segment_of_tile(ws.tile_prefix, nseg, t);
             next = ws.tile_prefix[s + 1];
@@ -518,7 +604,12 @@ __global__ __launch_bounds__(kBlock) void seg_pass1_kernel(const float *__restri
         // keys above the bracket go to the payload (e is cleared only once
         // the bracket is confirmed), keys inside it to the candidates
         if (bracket)
-            append_pairs(p, r.block0, emit_mask, cand_mask, inf, st, ws, idx, val, e, false);
+            stage_tile(sg, efill, cfill, p, r.block0, emit_mask, cand_mask, inf, st, ws.cand, idx,
+                       val, e, false);
+    }
+    if (bracket) {
+        flush_emit(sg, efill, st, inf, idx, val);
+        flush_cand(sg, cfill, st, inf, ws.cand);
     }
     flush_hist(hist, kDigit1, ws.hist1 + int64_t(s) * kDigit1);
 }
@@ -577,6 +668,7 @@ __global__ __launch_bounds__(kBlock) void seg_pass2_kernel(float *__restrict__ e
                                                            float *__restrict__ val, int32_t nseg,
                                                            SegWs ws, uint32_t tiles_per_wg) {
     __shared__ uint32_t hist[kDigit2];
+    __shared__ Stage sg;
     if (ws.ctl->status != 0u || ws.ctl->pass2 == 0u) return;
     const uint32_t T = ws.ctl->tiles;
     const uint32_t t0 = blockIdx.x * tiles_per_wg;
@@ -589,9 +681,12 @@ __global__ __launch_bounds__(kBlock) void seg_pass2_kernel(float *__restrict__ e
     SegState *st = ws.st + s;
     uint32_t mode = st->mode, D1 = st->d1;
     bool dirty = false;
+    uint32_t efill = 0, cfill = 0;
     __syncthreads();
     for (uint32_t t = t0; t < t1; ++t) {
         if (t >= next) {
+            flush_emit(sg, efill, st, inf, idx, val);
+            flush_cand(sg, cfill, st, inf, ws.cand);
             if (dirty) flush_hist(hist, kDigit2, ws.hist2 + int64_t(s) * kDigit2);
             dirty = false;
             s = segment_of_tile(ws.tile_prefix, nseg, t);
@@ -649,8 +744,11 @@ __global__ __launch_bounds__(kBlock) void seg_pass2_kernel(float *__restrict__ e
         }
         dirty = dirty || mode != kModeAll;
         if (mode != kModeScan)
-            append_pairs(p, r.block0, emit_mask, cand_mask, inf, st, ws, idx, val, e, true);
+            stage_tile(sg, efill, cfill, p, r.block0, emit_mask, cand_mask, inf, st, ws.cand, idx,
+                       val, e, true);
     }
+    flush_emit(sg, efill, st, inf, idx, val);
+    flush_cand(sg, cfill, st, inf, ws.cand);
     if (dirty) flush_hist(hist, kDigit2, ws.hist2 + int64_t(s) * kDigit2);
 }
 
@@ -898,7 +996,9 @@ hipError_t launch_topk_segmented(const float *g, float *e, int64_t d, float lr, 
     seg_reset_kernel<<<1 + zero_grid, kBlock, 0, stream>>>(ws, offsets, k, nseg, d, k_total);
 
     const int64_t max_tiles = (d + kTile - 1) / kTile + nseg;
-    const uint32_t grid = balanced_grid(max_tiles, kStageWorkgroupsPerCU);
+    // 8 workgroups per CU requested (pass1's histogram lets 4 be resident):
+    // measured faster than 4 for both streaming passes
+    const uint32_t grid = balanced_grid(max_tiles, kScanWorkgroupsPerCU);
     const uint32_t per_wg = uint32_t((max_tiles + grid - 1) / grid);
     const bool aligned = ((reinterpret_cast<uintptr_t>(g) | reinterpret_cast<uintptr_t>(e)) & 15) == 0;
     if (aligned)
