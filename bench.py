@@ -274,6 +274,21 @@ def main():
     b.record(cur)
     torch.cuda.synchronize()
     copy_us = a.elapsed_time(b) * 1e3 / args.b2b
+    # cold: a 1 GiB write (stream probe) before every launch evicts the 256 MB
+    # Infinity Cache, so g and e come from HBM; events around the launch only
+    flush = torch.empty(1 << 28, dtype=torch.float32, device=dev)
+    cold = []
+    for s in range(args.b2b):
+        efs.stream_probe(flush, flush, 2)
+        a, b = ev(), ev()
+        a.record(cur)
+        efs.ht_compress(pool[s % len(pool)], e_ht, lr, lam, idx, val, ctr)
+        b.record(cur)
+        torch.cuda.synchronize()
+        cold.append(a.elapsed_time(b) * 1e3)
+    del flush
+    ht_cold_us = float(np.median(cold))
+    kt_cold = efs.counter_value(ctr)
     # layer-wise Top-k over the workload's 161 segments, k_s = ceil(0.1 % d_s)
     seg_ks = synth.layerwise_k(stream.bounds, density)
     seg_ktot = int(seg_ks.sum())
@@ -364,6 +379,11 @@ def main():
                        "bytes": 8.0 * d},
         "ops": {
             "ht_compress_telemetry": {"launch_us": round(ht_tel_us, 2)},
+            "ht_compress_cold": {
+                "median_us": round(ht_cold_us, 2), "p10_us": round(float(np.percentile(cold, 10)), 2),
+                "p90_us": round(float(np.percentile(cold, 90)), 2),
+                "gbps": round((12.0 * d + 8.0 * kt_cold) / (ht_cold_us * 1e-6) / 1e9, 1),
+                "vs_warm": round(ht_cold_us / ht_b2b_us, 3)},
             "topk_segmented_compress": {
                 "launch_us": round(seg_us, 2), "segments": int(seg_ks.size), "k_total": seg_ktot,
                 "bracket_segments_last_call": seg_hits,
@@ -394,8 +414,11 @@ def main():
 
 
 def ht_sweep(efs, torch, synth, cur, reps):
-    """Back-to-back hard-threshold launches on the larger workloads (0.1 %
-    first-step density, e carried), two distinct gradients alternating."""
+    """Back-to-back launches on the larger workloads, two distinct gradients
+    alternating, e carried: the hard threshold (0.1 % first-step density),
+    the streaming ceilings, Top-k at the workload's densities and, where the
+    workload has layers, the layer-wise Top-k at 1 %."""
+    import numpy as np
     res = {}
     for wid in (3, 5):
         st = synth.Stream(wid)
@@ -428,8 +451,64 @@ def ht_sweep(efs, torch, synth, cur, reps):
         res[st.w.name] = {"d": d, "launch_us": round(us, 2), "k_t": kt,
                           "gbps": round(gbps, 1), "frac": round(gbps / HBM_PEAK_GBPS, 4),
                           "gelem_s": round(d / (us * 1e-6) / 1e9, 1)}
+        del e, idx, val
+        torch.cuda.empty_cache()
+        # Top-k on the same gradients, its own e from zero: 5 calls, then
+        # `reps` back-to-back calls timed (bytes: 12 per element + 8 per pair
+        # ideal, 16 + 8 per pair for the two-look radix path)
+        dens = (0.01, 0.001, 0.0001) if wid == 3 else (0.001,)
+        res[st.w.name]["topk"] = {}
+        for rho in dens:
+            k = max(1, int(round(rho * d)))
+            e = torch.zeros(d, dtype=torch.float32, device="cuda")
+            tidx = torch.empty(k, dtype=torch.int32, device="cuda")
+            tval = torch.empty(k, dtype=torch.float32, device="cuda")
+            ws = efs.new_topk_workspace(d, k, "cuda")
+            for s in range(5):
+                efs.topk_compress(gs[s % 2], e, synth.LR, k, tidx, tval, ws)
+            torch.cuda.synchronize()
+            a.record(cur)
+            for s in range(reps):
+                efs.topk_compress(gs[s % 2], e, synth.LR, k, tidx, tval, ws)
+            b.record(cur)
+            torch.cuda.synchronize()
+            us = a.elapsed_time(b) * 1e3 / reps
+            res[st.w.name]["topk"]["k=%d" % k] = {
+                "launch_us": round(us, 2), "gelem_s": round(d / (us * 1e-6) / 1e9, 1),
+                "gbps_ideal": round((12.0 * d + 8.0 * k) / (us * 1e-6) / 1e9, 1),
+                "gbps_twolook": round((16.0 * d + 8.0 * k) / (us * 1e-6) / 1e9, 1),
+                "last_call_bracket": efs.topk_took_bracket_path(ws)}
+            del e, tidx, tval, ws
+            torch.cuda.empty_cache()
+        if st.bounds is not None:
+            # layer-wise Top-k over the workload's segments at 1 %
+            ks = synth.layerwise_k(st.bounds, 0.01)
+            kt = int(ks.sum())
+            offd = torch.from_numpy(st.bounds.astype(np.int64)).to("cuda")
+            kd = torch.from_numpy(ks).to("cuda")
+            e = torch.zeros(d, dtype=torch.float32, device="cuda")
+            tidx = torch.empty(kt, dtype=torch.int32, device="cuda")
+            tval = torch.empty(kt, dtype=torch.float32, device="cuda")
+            ws = efs.new_topk_segmented_workspace(ks.size, kt, "cuda")
+            ws.zero_()
+            for s in range(5):
+                efs.topk_segmented_compress(gs[s % 2], e, synth.LR, offd, kd, tidx, tval, ws)
+            torch.cuda.synchronize()
+            a.record(cur)
+            for s in range(reps):
+                efs.topk_segmented_compress(gs[s % 2], e, synth.LR, offd, kd, tidx, tval, ws)
+            b.record(cur)
+            torch.cuda.synchronize()
+            us = a.elapsed_time(b) * 1e3 / reps
+            res[st.w.name]["topk_layerwise_1pct"] = {
+                "segments": int(ks.size), "k_total": kt, "launch_us": round(us, 2),
+                "gelem_s": round(d / (us * 1e-6) / 1e9, 1),
+                "gbps_ideal": round((12.0 * d + 8.0 * kt) / (us * 1e-6) / 1e9, 1),
+                "bracket_segments_last_call": efs.topk_segmented_bracket_segments(ws)}
+            del e, tidx, tval, ws
         # streaming ceilings on the same buffers (whole tiles): copy, read,
-        # write, and two reads + one write (the hard threshold's pattern)
+        # write, and two reads + one write (the hard threshold's pattern);
+        # last, because the write probes overwrite the second gradient
         nt = (d // 4096) * 4096
         ceil = {}
         for mode, name, nbytes in ((0, "copy", 8.0), (1, "read", 4.0), (2, "write", 4.0),
@@ -443,7 +522,7 @@ def ht_sweep(efs, torch, synth, cur, reps):
             ceil[name] = round(nbytes * nt / (pus * 1e-6) / 1e9, 1)
         res[st.w.name]["ceiling_gbps"] = ceil
         print("sweep %s: %s" % (st.w.name, res[st.w.name]), file=sys.stderr, flush=True)
-        del gs, e, idx, val
+        del gs
         torch.cuda.empty_cache()
     return res
 
@@ -528,8 +607,17 @@ def cpu_baseline(pool_host, d, k, lam, lr, steps):
         _, _, e_tk = oracle.topk(g, e_tk, lr, k)
         oracle.accumulate([(ridx, rval)], d)
     dt = time.perf_counter() - t0
+    model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
     return {"value": round(2.0 * d * steps / dt / 1e9, 5), "unit": "G grad-elements/s",
-            "cores": 1, "kind": "oracle",
+            "cores": 1, "kind": "oracle", "cpu_model": model, "host_cpus": os.cpu_count(),
             "sample": "%d full steps (d=%d: hard threshold + Top-k + average) of the same "
                       "workload, single-threaded C oracle, %.1f s" % (steps, d, dt)}
 

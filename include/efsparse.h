@@ -260,6 +260,14 @@ const char *efs_status_string(efs_status status);
 /* Detail of the last non-OK status returned on the calling thread. */
 const char *efs_last_error_message(void);
 
+/* Sticky status for callers that check once after a sequence of calls:
+ * EFS_EHIP when the HIP runtime holds an error left by an earlier
+ * asynchronous launch on this thread (hipPeekAtLastError, not cleared);
+ * otherwise the last non-OK status any call returned on this thread since
+ * the previous efs_last_error (which clears it), or EFS_OK.  Payload
+ * overflow is not an error: compare the count with the capacity. */
+efs_status efs_last_error(void);
+
 #ifdef __cplusplus
 }
 #endif

@@ -87,6 +87,8 @@ def declare(lib):
     lib.efs_status_string.restype = ctypes.c_char_p
     lib.efs_last_error_message.argtypes = []
     lib.efs_last_error_message.restype = ctypes.c_char_p
+    lib.efs_last_error.argtypes = []
+    lib.efs_last_error.restype = ctypes.c_int
     return lib
 
 

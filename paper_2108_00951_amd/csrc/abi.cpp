@@ -17,12 +17,14 @@ static_assert(efs::kMaxSegments == EFS_SEG_MAX, "segment limit differs from the 
 namespace {
 
 thread_local char g_message[256] = "";
+thread_local efs_status g_sticky = EFS_OK;  // last non-OK status on this thread
 
 efs_status fail(efs_status s, const char *fmt, ...) {
     va_list ap;
     va_start(ap, fmt);
     vsnprintf(g_message, sizeof g_message, fmt, ap);
     va_end(ap);
+    g_sticky = s;
     return s;
 }
 
@@ -87,6 +89,13 @@ const char *efs_status_string(efs_status s) {
 }
 
 const char *efs_last_error_message(void) { return g_message; }
+
+efs_status efs_last_error(void) {
+    if (hipPeekAtLastError() != hipSuccess) return EFS_EHIP;
+    const efs_status s = g_sticky;
+    g_sticky = EFS_OK;
+    return s;
+}
 
 static efs_status ht_common(const char *name, const float *g, float *e, int64_t d, float lr,
                             float lambda, int32_t *idx, float *val, int64_t cap, uint32_t *counter,

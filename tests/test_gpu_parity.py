@@ -471,3 +471,19 @@ def test_stream_probes():
     efs.stream_probe(x, y, 2)
     assert torch.equal(y[:8], torch.tensor([1, 2, 3, 4, 1, 2, 3, 4], dtype=torch.float32, device=DEV))
     efs.stream_probe(x, y, 1)
+
+
+def test_sticky_last_error():
+    lib = efs.load_library()
+    g = torch.zeros(8, dtype=torch.float32, device=DEV)
+    idx = torch.empty(8, dtype=torch.int32, device=DEV)
+    val = torch.empty(8, dtype=torch.float32, device=DEV)
+    ctr = efs.new_counter(DEV)
+    lib.efs_last_error()                    # clear
+    efs.ht_compress(g, g.clone(), 0.1, 1e-3, idx, val, ctr)
+    assert lib.efs_last_error() == efs.EFS_OK
+    with pytest.raises(efs.EfsError):
+        efs.ht_compress(g, g.clone(), 0.1, -1.0, idx, val, ctr)   # lambda < 0
+    efs.ht_compress(g, g.clone(), 0.1, 1e-3, idx, val, ctr)       # a good call after it
+    assert lib.efs_last_error() == efs.EFS_EINVAL                # sticky until read
+    assert lib.efs_last_error() == efs.EFS_OK
