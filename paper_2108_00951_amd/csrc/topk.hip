@@ -227,7 +227,7 @@ __device__ void select_bin(const uint32_t *hist, uint32_t need, uint32_t *s_scan
 // Zeroes the control block (except the hints) and every histogram, and
 // forms the bracket: 2^20 keys centred on the threshold predicted from the
 // last two calls (the last threshold plus the last step in key space, the
-// step capped at 2^18 keys; the last threshold alone when only one is
+// step capped at 2^21 keys; the last threshold alone when only one is
 // known).  Grid-stride over the histogram words.
 __global__ __launch_bounds__(kBlock) void topk_reset_kernel(Workspace ws) {
     if (blockIdx.x == 0) {
@@ -238,13 +238,14 @@ __global__ __launch_bounds__(kBlock) void topk_reset_kernel(Workspace ws) {
             TopkCtl *c = ws.ctl;
             c->last = kNoKey;
             if (c->hint_magic == kHintMagic) {
-                // the step since the previous call, capped at a quarter of
-                // the bracket so the last threshold always stays inside it
+                // the step since the previous call, capped at twice the
+                // bracket: a steady drift of up to ~18 % in |p| per call is
+                // followed; a reversal costs one radix-path call
                 const int64_t h1 = int64_t(c->hint_key & 0x7fffffffu);
                 int64_t pred = h1;
                 if (c->prev_magic == kHintMagic) {
                     int64_t step = h1 - int64_t(c->prev_key & 0x7fffffffu);
-                    const int64_t cap = int64_t(kFine / 4);
+                    const int64_t cap = int64_t(kFine) * 2;
                     step = step > cap ? cap : (step < -cap ? -cap : step);
                     pred = h1 + step;
                     if (pred < 0) pred = 0;
@@ -265,6 +266,23 @@ __global__ __launch_bounds__(kBlock) void topk_reset_kernel(Workspace ws) {
     for (size_t i = size_t(blockIdx.x) * kBlock + threadIdx.x; i < n4;
          i += size_t(gridDim.x) * kBlock)
         h4[i] = z;
+}
+
+// Adds 1 to hist[bin] for every active lane of the wave; the lanes that share
+// the first active lane's bin add together with one atomic (a vector of equal
+// magnitudes costs one atomic per wave, not 64).  Called by all lanes.
+__device__ __forceinline__ void wave_aggregated_add(uint32_t *hist, uint32_t bin, bool active) {
+    const uint64_t act = __ballot(active);
+    if (act == 0) return;
+    const int leader = __ffsll(static_cast<unsigned long long>(act)) - 1;
+    const uint32_t lbin = __shfl(bin, leader);
+    const bool same = active && bin == lbin;
+    const uint64_t mates = __ballot(same);
+    if (same) {
+        if (int(threadIdx.x & (kWave - 1)) == leader) atomicAdd(hist + lbin, uint32_t(__popcll(mates)));
+    } else if (active) {
+        atomicAdd(hist + bin, 1u);
+    }
 }
 
 struct Pass1Shared {
@@ -343,11 +361,20 @@ __global__ __launch_bounds__(kBlock) void topk_pass1_kernel(const float *__restr
                         const bool in = key >= lo && key <= hi;
                         m_above |= uint32_t(key > hi) << b;
                         m_inside |= uint32_t(in) << b;
-                        if (in) {
-                            atomicAdd(&sh.coarse[(key - lo) / kFinePerCoarse], 1u);
-                            atomicAdd(ws.fine + (key - lo), 1u);
-                        }
+                        if (in) atomicAdd(&sh.coarse[(key - lo) / kFinePerCoarse], 1u);
                     }
+                }
+            }
+        }
+        if (bracket) {
+            // fine bins in global memory: lanes with equal keys add together
+#pragma unroll
+            for (int j = 0; j < kVecPerThread; ++j) {
+#pragma unroll
+                for (int c = 0; c < 4; ++c) {
+                    const int b = 4 * j + c;
+                    const uint32_t key = magnitude_key(p[j][c]);
+                    wave_aggregated_add(ws.fine, key - lo, (m_inside >> b) & 1u);
                 }
             }
         }
@@ -368,23 +395,6 @@ __global__ __launch_bounds__(kBlock) void topk_pass1_kernel(const float *__restr
     if (bracket)
         for (int b = tid; b < kCoarse; b += kBlock)
             if (sh.coarse[b]) atomicAdd(ws.coarse + b, sh.coarse[b]);
-}
-
-// Adds 1 to hist[bin] for every active lane of the wave; the lanes that share
-// the first active lane's bin add together with one atomic (a vector of equal
-// magnitudes costs one atomic per wave, not 64).  Called by all lanes.
-__device__ __forceinline__ void wave_aggregated_add(uint32_t *hist, uint32_t bin, bool active) {
-    const uint64_t act = __ballot(active);
-    if (act == 0) return;
-    const int leader = __ffsll(static_cast<unsigned long long>(act)) - 1;
-    const uint32_t lbin = __shfl(bin, leader);
-    const bool same = active && bin == lbin;
-    const uint64_t mates = __ballot(same);
-    if (same) {
-        if (int(threadIdx.x & (kWave - 1)) == leader) atomicAdd(hist + lbin, uint32_t(__popcll(mates)));
-    } else if (active) {
-        atomicAdd(hist + bin, 1u);
-    }
 }
 
 // Radix path: histograms of bits 19..0 of the keys whose bits 30..20 equal
