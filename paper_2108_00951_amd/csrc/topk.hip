@@ -82,9 +82,10 @@ struct TopkCtl {
     uint32_t last;             // threshold of the previous call (kNoKey if none)
     uint32_t pad2;
     // Kept across calls (not cleared by reset): the thresholds of the last
-    // two calls, each valid when its magic word is set.
+    // three calls, each valid when its magic word is set.
     uint32_t hint_key, hint_magic;
     uint32_t prev_key, prev_magic;
+    uint32_t prev2_key, prev2_magic;
 };
 static_assert(sizeof(TopkCtl) <= 256, "control block must fit its slot");
 constexpr int kCtlClearWords = offsetof(TopkCtl, hint_key) / 4;
@@ -226,9 +227,9 @@ __device__ void select_bin(const uint32_t *hist, uint32_t need, uint32_t *s_scan
 
 // Zeroes the control block (except the hints) and every histogram, and
 // forms the bracket: 2^20 keys centred on the threshold predicted from the
-// last two calls (the last threshold plus the last step in key space, the
-// step capped at 2^21 keys; the last threshold alone when only one is
-// known).  Grid-stride over the histogram words.
+// last calls (the last threshold plus the last step in key space, the step
+// capped at 2^18 keys, or at 2^21 during a steady drift; the last threshold
+// alone when only one is known).  Grid-stride over the histogram words.
 __global__ __launch_bounds__(kBlock) void topk_reset_kernel(Workspace ws) {
     if (blockIdx.x == 0) {
         uint32_t *w = reinterpret_cast<uint32_t *>(ws.ctl);
@@ -238,14 +239,24 @@ __global__ __launch_bounds__(kBlock) void topk_reset_kernel(Workspace ws) {
             TopkCtl *c = ws.ctl;
             c->last = kNoKey;
             if (c->hint_magic == kHintMagic) {
-                // the step since the previous call, capped at twice the
-                // bracket: a steady drift of up to ~18 % in |p| per call is
-                // followed; a reversal costs one radix-path call
+                // the step since the previous call, capped at a quarter of
+                // the bracket (so the last threshold stays inside it), or
+                // at twice the bracket when the step before went the same
+                // way and at least half as far: a steady drift of up to
+                // ~18 % in |p| per call is then followed
                 const int64_t h1 = int64_t(c->hint_key & 0x7fffffffu);
                 int64_t pred = h1;
                 if (c->prev_magic == kHintMagic) {
-                    int64_t step = h1 - int64_t(c->prev_key & 0x7fffffffu);
-                    const int64_t cap = int64_t(kFine) * 2;
+                    const int64_t h0 = int64_t(c->prev_key & 0x7fffffffu);
+                    int64_t step = h1 - h0;
+                    int64_t cap = int64_t(kFine / 4);
+                    if (c->prev2_magic == kHintMagic) {
+                        const int64_t before = h0 - int64_t(c->prev2_key & 0x7fffffffu);
+                        const bool same_way = (step > 0 && before > 0) || (step < 0 && before < 0);
+                        const int64_t as = step < 0 ? -step : step;
+                        const int64_t ab = before < 0 ? -before : before;
+                        if (same_way && 2 * ab >= as) cap = int64_t(kFine) * 2;
+                    }
                     step = step > cap ? cap : (step < -cap ? -cap : step);
                     pred = h1 + step;
                     if (pred < 0) pred = 0;
@@ -434,6 +445,8 @@ __device__ __forceinline__ void set_threshold(TopkCtl *c, uint32_t T, uint32_t m
     c->m = m;
     c->ties = ties;
     c->tie_mode = m < ties ? 1u : 0u;
+    c->prev2_key = c->prev_key;
+    c->prev2_magic = c->last != kNoKey ? c->prev_magic : 0u;
     c->prev_key = c->last;
     c->prev_magic = c->last != kNoKey ? kHintMagic : 0u;
     c->hint_key = T;
