@@ -26,14 +26,17 @@
 //          top digit from the pass-1 histogram, then histogram bits 19..0 of
 //          the keys under it (a 4 B/element read of p) into 1024 coarse and
 //          2^20 fine bins.
-//   step4  radix path: coarse then fine selection, so T is exact.  Either
-//          path, when ties at T must be split (0 < m < #(key == T)): per-tile
-//          counts of key == T.
+//   step4  radix path: coarse then fine selection, so T is exact.  When
+//          ties at T must be split (0 < m < #(key == T)): on the bracket
+//          path with at most kTieList ties, a list of the tied candidates
+//          (every key equal to T is a candidate); otherwise per-tile counts
+//          of key == T.
 //   emit   radix path: keep key > T and the ties of index rank < m (a read
 //          of p); bracket path: only the ties of rank < m, when some are
-//          dropped.  Tie ranks: exclusive sums of the per-tile counts (each
-//          workgroup sums the tiles before its own), then a block scan in
-//          index order inside the tile.
+//          dropped (from the list: one workgroup selects the m lowest
+//          indices).  Tie ranks over the vector: exclusive sums of the
+//          per-tile counts (each workgroup sums the tiles before its own),
+//          then a block scan in index order inside the tile.
 //
 // Selections made by every workgroup read the same histograms, so they agree;
 // workgroup 0 records them in the control block.  Workgroups exchange data
@@ -80,7 +83,7 @@ struct TopkCtl {
     unsigned long long cand;   // pass 1: bracket candidates
     unsigned long long emit2;  // pairs appended after pass 1 (steps 3 and emit)
     uint32_t last;             // threshold of the previous call (kNoKey if none)
-    uint32_t pad2;
+    uint32_t tie_list;         // bracket path: keys equal to T listed by step 4
     // Kept across calls (not cleared by reset): the thresholds of the last
     // three calls, each valid when its magic word is set.
     uint32_t hint_key, hint_magic;
@@ -106,8 +109,14 @@ struct Workspace {
     uint32_t *hist1, *rcoarse, *rfine, *coarse, *fine, *tile_ties;
     int32_t *cand_idx;
     float *cand_val;
+    int32_t *ties;  // bracket path: indices of the keys equal to T
     uint32_t ccap;
 };
+
+// Bracket path with some keys equal to T dropped: the tied keys are all
+// candidates, so up to this many are ranked from a list instead of a pass
+// over the whole vector.
+constexpr uint32_t kTieList = 16384;
 
 // Candidate buffer size: the bracket around the k-th magnitude of an
 // error-feedback vector holds several times k keys (about 8k measured on the
@@ -137,6 +146,8 @@ Workspace carve(void *ws, int64_t d, int64_t k) {
     w.cand_idx = reinterpret_cast<int32_t *>(b + off);
     off += round256(sizeof(int32_t) * size_t(w.ccap));
     w.cand_val = reinterpret_cast<float *>(b + off);
+    off += round256(sizeof(float) * size_t(w.ccap));
+    w.ties = reinterpret_cast<int32_t *>(b + off);
     return w;
 }
 
@@ -578,6 +589,23 @@ __global__ __launch_bounds__(kBlock) void topk_step4_kernel(const float *__restr
         tie_mode = c->tie_mode;
     }
     if (tie_mode == 0u) return;
+    if (c->fast != 0u && c->ties <= kTieList) {
+        // bracket path: every key equal to T is a candidate; list them
+        const uint32_t n = c->ncand;
+        const uint32_t stride = gridDim.x * kBlock;
+        const uint32_t lane = threadIdx.x & (kWave - 1);
+        for (uint32_t base = blockIdx.x * kBlock; base < n; base += stride) {
+            const uint32_t j = base + threadIdx.x;
+            const bool tie = j < n && magnitude_key(ws.cand_val[j]) == T;
+            const uint64_t mask = __ballot(tie);
+            if (mask == 0) continue;
+            uint32_t slot = 0;
+            if (lane == 0) slot = atomicAdd(&c->tie_list, uint32_t(__popcll(mask)));
+            slot = __shfl(slot, 0) + lanes_below(mask);
+            if (tie && slot < kTieList) ws.ties[slot] = ws.cand_idx[j];
+        }
+        return;
+    }
     for (uint32_t tile = blockIdx.x; tile < ntiles; tile += gridDim.x) {
         const int64_t tile0 = int64_t(tile) * kTile;
         float v[kVecPerThread][4];
@@ -603,6 +631,47 @@ __device__ __forceinline__ uint32_t tie_count_range(const uint32_t *tile_ties, u
     return block_sum(v, s_wave);
 }
 
+// Bracket path, some ties dropped: the m lowest of the n listed tie
+// indices by a radix select on the index (bits 30..20, 19..10, 9..0; bins
+// stored reversed so the top-down select_bin picks from the bottom), then
+// emitted after the pairs already sent.  One workgroup.
+__device__ void emit_listed_ties(const Workspace &ws, uint32_t m, float *e, int32_t *idx,
+                                 float *val, uint64_t cap, PairStage &st, SelectShared &ss) {
+    const int tid = threadIdx.x;
+    const uint32_t n = min(ws.ctl->tie_list, kTieList);
+    uint32_t *h = reinterpret_cast<uint32_t *>(st.idx);  // 2048 words of the unused stage
+    uint32_t prefix = 0, rem = m;
+#pragma unroll 1
+    for (int level = 0; level < 3; ++level) {
+        const int shift = 20 - 10 * level;
+        const uint32_t bins = level == 0 ? 2048u : 1024u;
+        for (uint32_t b = tid; b < 2048u; b += kBlock) h[b] = 0u;
+        __syncthreads();
+        for (uint32_t j = tid; j < n; j += kBlock) {
+            const uint32_t i = uint32_t(ws.ties[j]);
+            if (level > 0 && (i >> (shift + 10)) != prefix) continue;
+            atomicAdd(&h[bins - 1u - ((i >> shift) & (bins - 1u))], 1u);
+        }
+        __syncthreads();
+        if (level == 0) select_bin<2048>(h, rem, ss.scan, ss.sel);
+        else select_bin<1024>(h, rem, ss.scan, ss.sel);
+        prefix = (prefix << (level == 0 ? 11 : 10)) | (bins - 1u - ss.sel[0]);
+        rem -= ss.sel[1];
+        __syncthreads();
+    }
+    const uint32_t imax = prefix;
+    for (uint32_t j = tid; j < n; j += kBlock) {
+        const int32_t i = ws.ties[j];
+        if (uint32_t(i) > imax) continue;
+        const uint64_t o = atomicAdd(&ws.ctl->emit2, 1ull) & kCountMask;
+        if (o < cap) {
+            idx[o] = i;
+            val[o] = e[i];
+        }
+        e[i] = 0.0f;
+    }
+}
+
 // Final emission over the whole vector.  Radix path: every key > T plus the
 // ties of rank < m (all ties when none is dropped).  Bracket path: only the
 // ties of rank < m when some are dropped (everything else is already sent);
@@ -614,6 +683,7 @@ __global__ __launch_bounds__(kBlock) void topk_emit_kernel(float *__restrict__ e
                                                            uint64_t cap, uint32_t ntiles,
                                                            Workspace ws) {
     __shared__ PairStage st;
+    __shared__ SelectShared ss;
     const bool fast = ws.ctl->fast != 0u;
     const bool tie_mode = ws.ctl->tie_mode != 0u;
     if (fast && !tie_mode) return;
@@ -625,6 +695,11 @@ __global__ __launch_bounds__(kBlock) void topk_emit_kernel(float *__restrict__ e
     idx += base;
     val += base;
     cap -= base;
+    if (fast && ws.ctl->ties <= kTieList) {
+        // the ties step 4 listed: workgroup 0 keeps the m lowest indices
+        if (blockIdx.x == 0) emit_listed_ties(ws, m, e, idx, val, cap, st, ss);
+        return;
+    }
     uint32_t fill = 0;
     // ties in the tiles before this workgroup's current tile
     uint32_t ties_before = 0, counted_to = 0;
@@ -688,6 +763,7 @@ size_t topk_workspace_size(int64_t d, int64_t k) {
     const int64_t tiles = d > 0 ? (d + kTile - 1) / kTile : 1;
     const int64_t ccap = candidate_capacity(d, k);
     return kCtlBytes + round256(kHistBytes) + round256(sizeof(uint32_t) * size_t(tiles)) +
+           round256(sizeof(int32_t) * kTieList) +
            round256(sizeof(int32_t) * size_t(ccap)) + round256(sizeof(float) * size_t(ccap));
 }
 

@@ -367,6 +367,30 @@ def test_topk_workspace_reuse_matches_oracle():
     assert st.bracket()
 
 
+@pytest.mark.parametrize("levels", [81, 5])
+def test_topk_bracket_path_splits_ties(levels):
+    # the same quantised vector twice (fresh e): the second call takes the
+    # bracket, and the k-th key is shared by thousands of coordinates of
+    # which only the lowest indices are kept.  81 levels: fewer ties than
+    # the bracket path ranks from a list; 5 levels: more (whole-vector ranks)
+    d = 300_007
+    st = TopkState(d, 20_000)
+    rng = np.random.default_rng(140 + levels)
+    half = levels // 2
+    q = (rng.integers(-half, half + 1, size=d).astype(np.float32) * np.float32(1e-4))
+    k = 7777 if levels > 10 else 150_001
+    st.ws = efs.new_topk_workspace(d, k, DEV)
+    st.idx = torch.empty(k, dtype=torch.int32, device=DEV)
+    st.val = torch.empty(k, dtype=torch.float32, device=DEV)
+    e = np.zeros(d, np.float32)
+    for t in range(2):
+        gi, gv, ge = st.step(q, k, e)
+        ri, rv, re = oracle.topk(q, e, LR, k)
+        assert_payload_equal(gi, gv, ri, rv, "levels %d call %d" % (levels, t))
+        assert_bits_equal(ge, re, "levels %d call %d" % (levels, t))
+    assert st.bracket()
+
+
 def test_topk_workspace_contents_do_not_matter():
     d, k = 200_003, 1500
     g = synth.small_gradient(77, d)
