@@ -58,7 +58,10 @@ constexpr int kCandLds = 18432;  // candidates the final pass holds in LDS (144 
 constexpr int64_t kCandPerK = 16;
 constexpr int64_t kCandExtra = 4096;
 
-enum : uint32_t { kModeNone = 0, kModeAll = 1, kModeCand = 2, kModeScan = 3, kModeFast = 4 };
+enum : uint32_t {
+    kModeNone = 0, kModeAll = 1, kModeCand = 2, kModeScan = 3, kModeFast = 4,
+    kModeDone = 5  // a segment within one tile, selected entirely in pass1
+};
 
 // bracket = prediction -/+ 2^w keys, w adapted per segment between these
 // (2^19 keys is about 4.6 % in |p|, 2^12 about 0.05 %)
@@ -283,13 +286,18 @@ __global__ __launch_bounds__(kBlock) void seg_reset_kernel(SegWs ws, const int64
                                                            const int64_t *__restrict__ kin,
                                                            int32_t nseg, int64_t d, int64_t k_total) {
     if (blockIdx.x > 0) {
-        // zero both histogram arrays (contiguous) with the other workgroups
-        const int64_t words = int64_t(nseg) * (kDigit1 + kDigit2);
-        uint32_t *h = ws.hist1;
-        const int64_t stride = int64_t(gridDim.x - 1) * kBlock;
-        for (int64_t i = int64_t(blockIdx.x - 1) * kBlock + threadIdx.x; i < words; i += stride) {
-            if (i < int64_t(nseg) * kDigit1) h[i] = 0u;
-            else ws.hist2[i - int64_t(nseg) * kDigit1] = 0u;
+        // the other workgroups zero the histograms of the segments that span
+        // more than one tile (a one-tile segment is selected inside pass1);
+        // an invalid layout is rejected by workgroup 0, so what is zeroed for
+        // it does not matter
+        const f32x4 z = {0.0f, 0.0f, 0.0f, 0.0f};
+        for (int32_t sg = int32_t(blockIdx.x) - 1; sg < nseg; sg += int32_t(gridDim.x) - 1) {
+            const int64_t lo = off[sg], size = off[sg + 1] - lo;
+            if (size < 0 || segment_tiles(lo, size) <= 1) continue;
+            f32x4 *h1 = reinterpret_cast<f32x4 *>(ws.hist1 + int64_t(sg) * kDigit1);
+            f32x4 *h2 = reinterpret_cast<f32x4 *>(ws.hist2 + int64_t(sg) * kDigit2);
+            for (int q = threadIdx.x; q < kDigit1 / 4; q += kBlock) h1[q] = z;
+            for (int q = threadIdx.x; q < kDigit2 / 4; q += kBlock) h2[q] = z;
         }
         return;
     }
@@ -310,9 +318,10 @@ __global__ __launch_bounds__(kBlock) void seg_reset_kernel(SegWs ws, const int64
             continue;
         }
         const int64_t keff = kk < size ? kk : size;
+        const int64_t nt = segment_tiles(lo, size);
         sum_k += keff;
-        sum_c += (keff > 0 && keff < size) ? kCandPerK * keff + kCandExtra : 0;
-        sum_t += segment_tiles(lo, size);
+        sum_c += (nt > 1 && keff > 0 && keff < size) ? kCandPerK * keff + kCandExtra : 0;
+        sum_t += nt;
     }
     if (t == 0 && off[0] != 0) bad = true;
     if (t == 0 && off[nseg] != d) bad = true;
@@ -328,8 +337,8 @@ __global__ __launch_bounds__(kBlock) void seg_reset_kernel(SegWs ws, const int64
         for (int32_t s = s0; s < s1; ++s) {
             const int64_t lo = off[s], size = off[s + 1] - lo, kk = kin[s];
             const int64_t keff = kk < size ? kk : size;
-            const int64_t ccap = (keff > 0 && keff < size) ? kCandPerK * keff + kCandExtra : 0;
             const uint32_t nt = uint32_t(segment_tiles(lo, size));
+            const int64_t ccap = (nt > 1 && keff > 0 && keff < size) ? kCandPerK * keff + kCandExtra : 0;
             SegInfo inf;
             inf.off = lo;
             inf.size = size;
@@ -344,7 +353,7 @@ __global__ __launch_bounds__(kBlock) void seg_reset_kernel(SegWs ws, const int64
             ws.tile_prefix[s] = uint32_t(base_t);
             SegState z = {};
             const SegHint h = ws.hint[s];
-            if (keff > 0 && keff < size && h.magic == kHintMagic && h.key <= 0x7fffffffu &&
+            if (nt > 1 && keff > 0 && keff < size && h.magic == kHintMagic && h.key <= 0x7fffffffu &&
                 h.prev <= 0x7fffffffu && h.width >= kWidthMin && h.width <= kWidthMax) {
                 const int64_t half = int64_t(1) << h.width;
                 // last threshold plus the last step (capped): error feedback
@@ -512,6 +521,88 @@ __device__ __forceinline__ void stage_tile(Stage &sg, uint32_t &efill, uint32_t 
     __syncthreads();
 }
 
+// A segment that lies within one tile is selected here, by the workgroup
+// holding it: a radix select on the keys of its elements (bits 30..20,
+// 19..10, 9..0, histograms in LDS), the keys equal to the threshold kept in
+// index order, the pairs written to the segment's payload region and e
+// cleared at them (e already holds p).  `hist` is 2048 words of zeroed
+// LDS, zeroed again on return.  Called by every thread of the workgroup.
+__device__ void select_in_tile(const float (&p)[kVecPerThread][4], uint32_t valid,
+                               int64_t block0, const SegInfo &inf, uint32_t *hist,
+                               uint32_t *s_wave, uint32_t *s_out, int32_t *idx, float *val,
+                               float *e) {
+    const int tid = threadIdx.x;
+    uint32_t key[kVecPerThread][4];
+#pragma unroll
+    for (int j = 0; j < kVecPerThread; ++j)
+#pragma unroll
+        for (int c = 0; c < 4; ++c) key[j][c] = magnitude_key(p[j][c]);
+    uint32_t keep = 0;
+    if (inf.k >= inf.size) {
+        keep = valid;
+    } else if (inf.k > 0) {
+        uint32_t need = uint32_t(inf.k), prefix = 0;
+#pragma unroll 1
+        for (int level = 0; level < 3; ++level) {
+            const int shift = 20 - 10 * level;
+            const uint32_t mask = level == 0 ? 2047u : 1023u;
+#pragma unroll
+            for (int j = 0; j < kVecPerThread; ++j)
+#pragma unroll
+                for (int c = 0; c < 4; ++c)
+                    if (((valid >> (4 * j + c)) & 1u) &&
+                        (level == 0 || (key[j][c] >> (shift + 10)) == prefix))
+                        atomicAdd(&hist[(key[j][c] >> shift) & mask], 1u);
+            __syncthreads();
+            if (level == 0) pick_bin<2048, true>(hist, need, s_wave, s_out);
+            else pick_bin<1024, true>(hist, need, s_wave, s_out);
+            prefix = (prefix << (level == 0 ? 11 : 10)) | s_out[0];
+            need -= s_out[1];
+            for (int b = tid; b < 2048; b += kBlock) hist[b] = 0u;
+            __syncthreads();
+        }
+        const uint32_t T = prefix;  // need = keys equal to T to keep
+        uint32_t tie = 0;
+#pragma unroll
+        for (int j = 0; j < kVecPerThread; ++j)
+#pragma unroll
+            for (int c = 0; c < 4; ++c) {
+                const uint32_t bit = 1u << (4 * j + c);
+                if (!(valid & bit)) continue;
+                if (key[j][c] > T) keep |= bit;
+                else if (key[j][c] == T) tie |= bit;
+            }
+        // tie ranks in index order: vector slot j, then thread, then c
+        uint32_t rank = 0;
+#pragma unroll
+        for (int j = 0; j < kVecPerThread; ++j) {
+            const uint32_t tj = (tie >> (4 * j)) & 0xfu;
+            uint32_t slot_total;
+            uint32_t r = rank + block_prefix_small(uint32_t(__popc(tj)), s_wave, slot_total);
+#pragma unroll
+            for (int c = 0; c < 4; ++c)
+                if ((tj >> c) & 1u) {
+                    keep |= uint32_t(r < need) << (4 * j + c);
+                    ++r;
+                }
+            rank += slot_total;
+        }
+    }
+    uint32_t total;
+    int64_t slot = inf.kout + block_prefix_small(uint32_t(__popc(keep)), s_wave, total);
+#pragma unroll
+    for (int j = 0; j < kVecPerThread; ++j)
+#pragma unroll
+        for (int c = 0; c < 4; ++c)
+            if ((keep >> (4 * j + c)) & 1u) {
+                const int64_t i = tile_elem(block0, j, c);
+                idx[slot] = int32_t(i);
+                val[slot] = p[j][c];
+                e[i] = 0.0f;
+                ++slot;
+            }
+}
+
 template <bool kAligned>
 __global__ __launch_bounds__(kBlock) void seg_pass1_kernel(const float *__restrict__ g,
                                                            float *__restrict__ e, float lr,
@@ -520,6 +611,8 @@ __global__ __launch_bounds__(kBlock) void seg_pass1_kernel(const float *__restri
                                                            SegWs ws, uint32_t tiles_per_wg) {
     __shared__ uint32_t hist[kDigit1];
     __shared__ Stage sg;
+    __shared__ uint32_t s_wave[kWaves];
+    __shared__ uint32_t s_out[3];
     if (ws.ctl->status != 0u) return;
     const uint32_t T = ws.ctl->tiles;
     const uint32_t t0 = blockIdx.x * tiles_per_wg;
@@ -588,6 +681,10 @@ __global__ __launch_bounds__(kBlock) void seg_pass1_kernel(const float *__restri
                 }
             }
         }
+        if (inf.ntiles == 1) {
+            select_in_tile(p, valid, r.block0, inf, hist, s_wave, s_out, idx, val, e);
+            continue;
+        }
         uint32_t emit_mask = 0, cand_mask = 0;
 #pragma unroll
         for (int j = 0; j < kVecPerThread; ++j) {
@@ -625,6 +722,10 @@ __global__ __launch_bounds__(kBlock) void seg_select1_kernel(SegWs ws) {
     const int32_t s = blockIdx.x;
     const SegInfo inf = ws.info[s];
     SegState *st = ws.st + s;
+    if (inf.ntiles <= 1) {  // selected in pass1 (or empty)
+        if (threadIdx.x == 0) st->mode = kModeDone;
+        return;
+    }
     if (inf.k == 0 || inf.k == inf.size) {
         if (threadIdx.x == 0) {
             st->mode = inf.k == 0 ? kModeNone : kModeAll;
@@ -696,7 +797,7 @@ __global__ __launch_bounds__(kBlock) void seg_pass2_kernel(float *__restrict__ e
             mode = st->mode;
             D1 = st->d1;
         }
-        if (mode == kModeNone || mode == kModeFast) {
+        if (mode == kModeNone || mode == kModeFast || mode == kModeDone) {
             t = next - 1;  // nothing to do in this segment: skip its tiles
             continue;
         }
@@ -990,9 +1091,7 @@ hipError_t launch_topk_segmented(const float *g, float *e, int64_t d, float lr, 
     ws.cand = reinterpret_cast<uint2 *>(base + L.cand);
     ws.ccap_total = L.ccap_total;
 
-    const int64_t hist_words = int64_t(nseg) * (kDigit1 + kDigit2);
-    const uint32_t zero_grid = persistent_grid((hist_words + int64_t(kBlock) * 4 - 1) /
-                                               (int64_t(kBlock) * 4));
+    const uint32_t zero_grid = persistent_grid(nseg);  // one segment's histograms per pass
     seg_reset_kernel<<<1 + zero_grid, kBlock, 0, stream>>>(ws, offsets, k, nseg, d, k_total);
 
     const int64_t max_tiles = (d + kTile - 1) / kTile + nseg;

@@ -285,3 +285,21 @@ def test_segmented_bracket_from_another_scale_falls_back():
         hits.append(efs.topk_segmented_bracket_segments(ws))
     assert hits[0] == 0 and hits[1] == 0
     assert hits[2] == ks.size
+
+
+@pytest.mark.parametrize("levels", [4, 1000])
+def test_segmented_many_small_layers(levels):
+    # hundreds of layers that fit in one 4096-element tile (selected inside
+    # pass 1) mixed with a few large ones; few magnitudes -> ties at nearly
+    # every threshold, split by index
+    rng = np.random.default_rng(600 + levels)
+    sizes = rng.integers(1, 4097, size=700)
+    sizes[rng.choice(700, 5, replace=False)] = rng.integers(5000, 60000, size=5)
+    off = np.concatenate([[0], np.cumsum(sizes)]).astype(np.int64)
+    d = int(off[-1])
+    half = levels // 2
+    g = (rng.integers(-half, half + 1, size=d) * np.float32(0.125)).astype(np.float32)
+    e = np.zeros(d, np.float32)
+    ks = np.ceil(sizes * rng.uniform(0.0, 1.2, size=sizes.size)).astype(np.int64)
+    say("segmented many small layers levels=%d d=%d" % (levels, d))
+    check(g, e, off, ks, lr=np.float32(1.0), what="small layers")
