@@ -6,36 +6,42 @@
 //
 // Work is cut into tiles: the 4096-element blocks of the vector, clipped to
 // each segment, so every tile belongs to one segment and every whole tile is
-// 16-byte aligned.  Five launches:
+// 16-byte aligned.  The two sweeps take short slices of consecutive tiles in
+// turn across the vector.  Five launches:
 //
 //   reset    one workgroup checks the layout and forms the per-segment
-//            tables (tile ranges, payload offsets, candidate regions); the
-//            others zero the per-segment histograms.
+//            tables (tile ranges, payload offsets, candidate regions, the
+//            bracket); the others zero the per-segment histograms.
 //   pass1    p = e + lr*g written into e (12 B/element); LDS histogram of key
 //            bits 30..18 (8192 bins) per segment, flushed (non-zero bins) to
-//            the segment's global histogram.  With a bracket [lo, hi] around
-//            the segment's threshold predicted from its last two calls on this
-//            workspace (error feedback moves it little; the bracket's width,
-//            2^13..2^20 keys, adapts per segment to how many keys it caught
-//            and whether it missed), keys above hi go straight to the payload
-//            and keys inside it to the candidates.
+//            the segment's global histogram.  A segment within one tile is
+//            selected right there.  With a bracket [lo, hi] around the
+//            segment's threshold predicted from its last three calls on this
+//            workspace (error feedback moves it little and smoothly; the
+//            bracket reaches 2^wl keys below the prediction and 2^wh above,
+//            each 2^12..2^19, adapted per segment), keys above hi go straight
+//            to the payload, keys inside it to the candidates and to a
+//            1024-bin histogram of the bracket.
 //   select1  one workgroup per segment: when pass1 had a bracket and its
-//            counts prove the k-th key inside it, the segment selects from
-//            the bracket (below).  Otherwise the digit D1 holding the k-th
-//            key and the mode: none (k = 0), all (k = size), candidates (the
-//            keys in D1 fit the segment's candidate region) or scan (they do
-//            not: a large set of equal or nearly equal magnitudes).
-//   pass2    radix path only, a read of p (4 B/element): keys above D1 go to
-//            the payload and
-//            their e to +0 (mode all: every key); keys in D1 are appended to
-//            the candidate region and histogrammed by bits 17..8.
-//   final    one workgroup per segment selects among its candidates: bits
-//            17..8, then 7..0 (the exact threshold T; from the bracket: bits
-//            19..10 then 9..0 of key - lo), then, when only some keys equal to
-//            T are kept, the lowest indices among them by a radix select on
-//            the index; emits, clears e, and keeps T as the next hint.  Scan
-//            mode does the same over the segment's elements.  Results never
-//            depend on the hint.
+//            counts prove the k-th key inside it, the bracket bin da holding
+//            it, and pass2's work items for the segment.  Otherwise the digit
+//            D1 holding the k-th key and the mode: none (k = 0), all
+//            (k = size), candidates (the keys in D1 fit the segment's
+//            candidate region) or scan (they do not: a large set of equal or
+//            nearly equal magnitudes).
+//   pass2    radix path, a read of p (4 B/element): keys above D1 go to the
+//            payload and their e to +0 (mode all: every key); keys in D1 are
+//            appended to the candidate region and histogrammed by bits 17..8.
+//            Bracket path, spread over the whole grid: e cleared at the pairs
+//            above the bracket; candidates in bins above da to the payload,
+//            those in bin da listed after the candidates.
+//   final    one workgroup per segment: among its candidates (radix path)
+//            bits 17..8, then 7..0 give the exact threshold T; among the keys
+//            of bin da (bracket path) the low bits of key - lo give it.  Then,
+//            when only some keys equal to T are kept, the lowest indices among
+//            them by a radix select on the index; emits, clears e, and keeps
+//            T as the next hint.  Scan mode does the same over the segment's
+//            elements.  Results never depend on the hint.
 //
 // Payload: segment s's pairs at [kout[s], kout[s] + min(k[s], size)), kout the
 // exclusive prefix of those counts; order within a segment unspecified.
@@ -66,15 +72,30 @@ enum : uint32_t {
 // bracket = prediction -/+ 2^w keys, w adapted per segment between these
 // (2^19 keys is about 4.6 % in |p|, 2^12 about 0.05 %)
 constexpr uint32_t kWidthMax = 19, kWidthMin = 12, kWidthStart = 17;
-constexpr int64_t kMaxStep = 1 << 18;          // cap on the extrapolated step, in keys
+// cap on the extrapolated step, in keys: wide when the last two steps agree
+// (a steady drift), narrow otherwise (a jump is not repeated)
+constexpr int64_t kMaxStep = 1 << 22, kMaxStepUnsure = 1 << 18;
+constexpr int kFineBins = 1024;                // bracket histogram: the bracket in 1024 bins
+constexpr uint32_t kChunk = 2048;              // pass2 work item: payload slots or candidates
+// The sweeps take slices of `slice` consecutive tiles (at most
+// kSliceTilesMax), slice b + i * grid for workgroup b: the resident
+// workgroups stream one compact window of the vector at a time (measured
+// faster than one long range per workgroup), and a slice is long enough to
+// amortise its flushes.
+constexpr int64_t kSliceTilesMax = 4;
+constexpr int kSliceWorkgroupsPerCU = 4;
+constexpr uint32_t kNoBin = 0xffffffffu;
+static_assert(kFineBins == kDigit2, "the bracket histogram lives in a segment's second histogram");
+static_assert(kWidthMax <= 19, "a bracket spans under 2^20 keys, so a bin at most 1024");
 constexpr uint32_t kHintMagic = 0x53454748u;
 
 struct SegCtl {
     uint32_t status;   // 0: layout accepted; 1: rejected (the call changed nothing)
     uint32_t tiles;    // tiles of all segments
     uint32_t bracket;  // segments that selected from the bracket (a diagnostic)
-    uint32_t pass2;    // segments that need pass2
-    uint32_t pad[60];
+    uint32_t pass2;    // segments that need pass2's tile sweep
+    uint32_t nwork;    // entries of the work list (bracket path, for pass2)
+    uint32_t pad[59];
 };
 static_assert(sizeof(SegCtl) == 256, "control block is 256 bytes");
 
@@ -91,15 +112,48 @@ struct SegState {
     uint32_t ccur;     // candidates appended (pass1 with a bracket, or pass2)
     uint32_t bracket;  // 1: pass1 collects keys in [lo, hi], emits keys above hi
     uint32_t lo, hi;
-    uint32_t pad[7];
+    uint32_t shift;    // bracket bin of a key: (key - lo) >> shift, 1024 bins
+    uint32_t da;       // bracket path: the bin holding the k-th key (kNoBin: none needed)
+    uint32_t needa;    // keys of bin da to keep
+    uint32_t ca;       // keys in bin da
+    uint32_t ecut;     // pairs above the bracket (payload slots 0 .. ecut-1)
+    uint32_t tcur;     // keys of bin da listed by pass2 after the candidates
+    uint32_t miss;     // bracket not used: 1 threshold below it, 2 above it, 3 too many keys in it
 };
 static_assert(sizeof(SegState) == 64, "segment state is 64 bytes");
 
 // Threshold of the last call on this workspace, kept across calls (the
 // reset does not touch it); it only decides the bracket, never a result.
 struct SegHint {
-    uint32_t key, prev, magic, width;  // last threshold, the one before, validity, log2 half-width
+    uint32_t key, prev, prev2;  // the last three thresholds
+    uint32_t magic, width;      // validity; bracket widths (packed, see below)
+    uint32_t pad[3];
 };
+
+// A bracket reaches 2^wl keys below the predicted threshold and 2^wh above
+// it; the two are adapted separately, since under error feedback the keys
+// crowd just below the threshold and are sparse above it.  Packed as
+// wl | wh << 8.
+__device__ __forceinline__ uint32_t width_lo(uint32_t w) { return w & 0xffu; }
+__device__ __forceinline__ uint32_t width_hi(uint32_t w) { return (w >> 8) & 0xffu; }
+__device__ __forceinline__ uint32_t make_widths(uint32_t wl, uint32_t wh) { return wl | (wh << 8); }
+__device__ __forceinline__ bool widths_ok(uint32_t w) {
+    return (w >> 16) == 0u && width_lo(w) >= kWidthMin && width_lo(w) <= kWidthMax &&
+           width_hi(w) >= kWidthMin && width_hi(w) <= kWidthMax;
+}
+static_assert(sizeof(SegHint) == 32, "hint is 32 bytes");
+
+// The hint after a call whose threshold was T.
+__device__ __forceinline__ SegHint next_hint(const SegHint &old, uint32_t T, uint32_t width) {
+    const bool ok = old.magic == kHintMagic;
+    SegHint h = {};
+    h.key = T;
+    h.prev = ok ? old.key : T;
+    h.prev2 = ok ? old.prev : T;
+    h.magic = kHintMagic;
+    h.width = width;
+    return h;
+}
 
 struct SegWs {
     SegCtl *ctl;
@@ -108,14 +162,16 @@ struct SegWs {
     uint32_t *tile_prefix;  // [nseg + 1]
     SegState *st;
     uint32_t *hist1;        // [nseg][kDigit1]
-    uint32_t *hist2;        // [nseg][kDigit2]
+    uint32_t *hist2;        // [nseg][kDigit2]; on the bracket path, the bracket histogram
     uint2 *cand;            // (bits of p, index)
+    uint2 *work;            // pass2 work list: (segment | kind << 31, first slot)
     int64_t ccap_total;
+    uint32_t work_cap;
 };
 
 struct SegLayout {
-    size_t info, tile_prefix, st, hint, hist1, hist2, cand, bytes;
-    int64_t ccap_total;
+    size_t info, tile_prefix, st, hint, hist1, hist2, cand, work, bytes;
+    int64_t ccap_total, work_cap;
 };
 
 size_t round256(size_t b) { return (b + 255) & ~size_t(255); }
@@ -138,6 +194,10 @@ SegLayout seg_layout(int32_t nseg, int64_t k_total) {
     o += round256(4 * size_t(kDigit2) * size_t(nseg));
     L.cand = o;
     o += round256(8 * size_t(L.ccap_total));
+    // one entry per kChunk payload slots or candidates of a segment
+    L.work_cap = (k_total + L.ccap_total) / kChunk + 2 * int64_t(nseg) + 1;
+    L.work = o;
+    o += round256(8 * size_t(L.work_cap));
     L.bytes = o;
     return L;
 }
@@ -354,15 +414,22 @@ __global__ __launch_bounds__(kBlock) void seg_reset_kernel(SegWs ws, const int64
             SegState z = {};
             const SegHint h = ws.hint[s];
             if (nt > 1 && keff > 0 && keff < size && h.magic == kHintMagic && h.key <= 0x7fffffffu &&
-                h.prev <= 0x7fffffffu && h.width >= kWidthMin && h.width <= kWidthMax) {
-                const int64_t half = int64_t(1) << h.width;
+                h.prev <= 0x7fffffffu && h.prev2 <= 0x7fffffffu && widths_ok(h.width)) {
                 // last threshold plus the last step (capped): error feedback
                 // makes thresholds drift smoothly from call to call
-                const int64_t step = max(-kMaxStep, min(kMaxStep, int64_t(h.key) - int64_t(h.prev)));
+                const int64_t last = int64_t(h.key) - int64_t(h.prev);
+                const int64_t before = int64_t(h.prev) - int64_t(h.prev2);
+                const int64_t al = last < 0 ? -last : last, ab = before < 0 ? -before : before;
+                const bool steady = (last >= 0) == (before >= 0) && 2 * ab >= al && 2 * al >= ab;
+                const int64_t cap = steady ? kMaxStep : kMaxStepUnsure;
+                const int64_t step = max(-cap, min(cap, last));
                 const int64_t pred = max(int64_t(0), min(int64_t(0x7fffffff), int64_t(h.key) + step));
                 z.bracket = 1u;
-                z.lo = uint32_t(max(int64_t(0), pred - half));
-                z.hi = uint32_t(min(int64_t(z.lo) + 2 * half - 1, int64_t(0x7fffffff)));
+                z.lo = uint32_t(max(int64_t(0), pred - (int64_t(1) << width_lo(h.width))));
+                z.hi = uint32_t(min(pred + (int64_t(1) << width_hi(h.width)) - 1, int64_t(0x7fffffff)));
+                // hi - lo + 1 <= 2^20 keys in kFineBins bins
+                const uint32_t span_bits = 32u - uint32_t(__clz(int(z.hi - z.lo) | 1));
+                z.shift = span_bits > 10u ? span_bits - 10u : 0u;
             }
             ws.st[s] = z;
             base_k += keff;
@@ -373,6 +440,7 @@ __global__ __launch_bounds__(kBlock) void seg_reset_kernel(SegWs ws, const int64
     if (t == 0) {
         ws.ctl->bracket = 0u;
         ws.ctl->pass2 = 0u;
+        ws.ctl->nwork = 0u;
         ws.ctl->status = reject ? 1u : 0u;
         ws.ctl->tiles = reject ? 0u : uint32_t(tot_t);
         if (!reject) ws.tile_prefix[nseg] = uint32_t(tot_t);
@@ -427,8 +495,19 @@ __device__ __forceinline__ void flush_emit(Stage &sg, uint32_t &fill, SegState *
     __syncthreads();
 }
 
+// Bracket histogram of a segment: a candidate key (in [lo, hi]) counted in
+// its bin (global memory: pass1 keeps the digit-1 histogram in LDS).
+struct Fine {
+    uint32_t *hist;  // nullptr: not counted
+    uint32_t lo, shift;
+};
+
+__device__ __forceinline__ void count_fine(const Fine &f, uint32_t bits) {
+    if (f.hist) atomicAdd(&f.hist[(((bits & 0x7fffffffu) - f.lo) >> f.shift) & (kFineBins - 1)], 1u);
+}
+
 __device__ __forceinline__ void flush_cand(Stage &sg, uint32_t &fill, SegState *st,
-                                           const SegInfo &inf, uint2 *cand) {
+                                           const SegInfo &inf, uint2 *cand, const Fine &fine) {
     __syncthreads();
     if (fill == 0u) return;
     if (threadIdx.x == 0) sg.base = atomicAdd(&st->ccur, fill);
@@ -436,7 +515,9 @@ __device__ __forceinline__ void flush_cand(Stage &sg, uint32_t &fill, SegState *
     const uint32_t base = sg.base;
     for (uint32_t q = threadIdx.x; q < fill; q += kBlock) {
         const int64_t slot = int64_t(base) + q;
-        if (slot < inf.ccap) cand[inf.coff + slot] = sg.cand[q];
+        const uint2 v = sg.cand[q];
+        if (slot < inf.ccap) cand[inf.coff + slot] = v;
+        count_fine(fine, v.x);
     }
     fill = 0u;
     __syncthreads();
@@ -444,14 +525,16 @@ __device__ __forceinline__ void flush_cand(Stage &sg, uint32_t &fill, SegState *
 
 // Stages this tile's selections (called by every thread of the workgroup):
 // elements of `emit_mask` for the payload (e cleared there when zero_e), of
-// `cand_mask` for the candidates.  When a tile selects more of either than a
-// stage holds (mode all, or many equal keys), its slots are reserved
-// directly with one atomic and written without staging.
+// `cand_mask` for the candidates (counted in `fine` when it has a
+// histogram).  When a tile selects more of either than a stage holds (mode
+// all, or many equal keys), its slots are reserved directly with one atomic
+// and written without staging.
 __device__ __forceinline__ void stage_tile(Stage &sg, uint32_t &efill, uint32_t &cfill,
                                            const float (&p)[kVecPerThread][4], int64_t block0,
                                            uint32_t emit_mask, uint32_t cand_mask,
                                            const SegInfo &inf, SegState *st, uint2 *cand,
-                                           int32_t *idx, float *val, float *e, bool zero_e) {
+                                           int32_t *idx, float *val, float *e, bool zero_e,
+                                           const Fine &fine) {
     const int lane = threadIdx.x & (kWave - 1);
     const int wave = threadIdx.x / kWave;
     const uint32_t mine = uint32_t(__popc(emit_mask)) | (uint32_t(__popc(cand_mask)) << 16);
@@ -471,7 +554,7 @@ __device__ __forceinline__ void stage_tile(Stage &sg, uint32_t &efill, uint32_t 
     const bool edirect = te > uint32_t(kStageCap);
     const bool cdirect = tc > uint32_t(kStageCap);
     if (!edirect && efill + te > uint32_t(kStageCap)) flush_emit(sg, efill, st, inf, idx, val);
-    if (!cdirect && cfill + tc > uint32_t(kStageCap)) flush_cand(sg, cfill, st, inf, cand);
+    if (!cdirect && cfill + tc > uint32_t(kStageCap)) flush_cand(sg, cfill, st, inf, cand, fine);
     uint32_t ebase = 0, cbase = 0;
     if (edirect || cdirect) {
         if (threadIdx.x == 0) {
@@ -509,6 +592,7 @@ __device__ __forceinline__ void stage_tile(Stage &sg, uint32_t &efill, uint32_t 
                 if (cdirect) {
                     const int64_t slot = int64_t(cbase) + cp;
                     if (slot < inf.ccap) cand[inf.coff + slot] = v;
+                    count_fine(fine, v.x);
                 } else {
                     sg.cand[cfill + cp] = v;
                 }
@@ -603,34 +687,26 @@ __device__ void select_in_tile(const float (&p)[kVecPerThread][4], uint32_t vali
             }
 }
 
+// Tiles [t0, t1) of pass1; every selection, count and histogram is flushed
+// before it returns (the LDS histogram is left zero).
 template <bool kAligned>
-__global__ __launch_bounds__(kBlock) void seg_pass1_kernel(const float *__restrict__ g,
-                                                           float *__restrict__ e, float lr,
-                                                           int32_t *__restrict__ idx,
-                                                           float *__restrict__ val, int32_t nseg,
-                                                           SegWs ws, uint32_t tiles_per_wg) {
-    __shared__ uint32_t hist[kDigit1];
-    __shared__ Stage sg;
-    __shared__ uint32_t s_wave[kWaves];
-    __shared__ uint32_t s_out[3];
-    if (ws.ctl->status != 0u) return;
-    const uint32_t T = ws.ctl->tiles;
-    const uint32_t t0 = blockIdx.x * tiles_per_wg;
-    if (t0 >= T) return;
-    const uint32_t t1 = min(T, t0 + tiles_per_wg);
-    for (int b = threadIdx.x; b < kDigit1; b += kBlock) hist[b] = 0u;
+__device__ void pass1_slice(const float *__restrict__ g, float *__restrict__ e, float lr,
+                            int32_t *__restrict__ idx, float *__restrict__ val, int32_t nseg,
+                            const SegWs &ws, uint32_t t0, uint32_t t1, uint32_t *hist, Stage &sg,
+                            uint32_t *s_wave, uint32_t *s_out) {
     int32_t s = segment_of_tile(ws.tile_prefix, nseg, t0);
     uint32_t next = ws.tile_prefix[s + 1];
     SegInfo inf = ws.info[s];
     SegState *st = ws.st + s;
     uint32_t bracket = st->bracket, lo = st->lo, hi = st->hi;
+    Fine fine = {ws.hist2 + int64_t(s) * kDigit2, lo, st->shift};
     uint32_t efill = 0, cfill = 0;
     __syncthreads();
     for (uint32_t t = t0; t < t1; ++t) {
         if (t >= next) {
             if (bracket) {
                 flush_emit(sg, efill, st, inf, idx, val);
-                flush_cand(sg, cfill, st, inf, ws.cand);
+                flush_cand(sg, cfill, st, inf, ws.cand, fine);
             }
             flush_hist(hist, kDigit1, ws.hist1 + int64_t(s) * kDigit1);
             s = segment_of_tile(ws.tile_prefix, nseg, t);
@@ -640,6 +716,7 @@ __global__ __launch_bounds__(kBlock) void seg_pass1_kernel(const float *__restri
             bracket = st->bracket;
             lo = st->lo;
             hi = st->hi;
+            fine = Fine{ws.hist2 + int64_t(s) * kDigit2, lo, st->shift};
         }
         const TileRange r = tile_range(inf, t);
         float p[kVecPerThread][4];
@@ -699,21 +776,61 @@ __global__ __launch_bounds__(kBlock) void seg_pass1_kernel(const float *__restri
             }
         }
         // keys above the bracket go to the payload (e is cleared only once
-        // the bracket is confirmed), keys inside it to the candidates
+        // the bracket is confirmed), keys inside it to the candidates and
+        // the bracket histogram
         if (bracket)
             stage_tile(sg, efill, cfill, p, r.block0, emit_mask, cand_mask, inf, st, ws.cand, idx,
-                       val, e, false);
+                       val, e, false, fine);
     }
     if (bracket) {
         flush_emit(sg, efill, st, inf, idx, val);
-        flush_cand(sg, cfill, st, inf, ws.cand);
+        flush_cand(sg, cfill, st, inf, ws.cand, fine);
     }
     flush_hist(hist, kDigit1, ws.hist1 + int64_t(s) * kDigit1);
+}
+
+template <bool kAligned>
+__global__ __launch_bounds__(kBlock) void seg_pass1_kernel(const float *__restrict__ g,
+                                                           float *__restrict__ e, float lr,
+                                                           int32_t *__restrict__ idx,
+                                                           float *__restrict__ val, int32_t nseg,
+                                                           SegWs ws, uint32_t slice) {
+    __shared__ uint32_t hist[kDigit1];
+    __shared__ Stage sg;
+    __shared__ uint32_t s_wave[kWaves];
+    __shared__ uint32_t s_out[3];
+    if (ws.ctl->status != 0u) return;
+    const uint32_t T = ws.ctl->tiles;
+    for (int b = threadIdx.x; b < kDigit1; b += kBlock) hist[b] = 0u;
+    for (uint32_t t0 = blockIdx.x * slice; t0 < T; t0 += gridDim.x * slice)
+        pass1_slice<kAligned>(g, e, lr, idx, val, nseg, ws, t0, min(T, t0 + slice), hist, sg,
+                              s_wave, s_out);
 }
 
 // ---------------------------------------------------------------------------
 // select1: per segment, the digit of the k-th key and the mode
 // ---------------------------------------------------------------------------
+
+// Radix path of segment s (0 < k < size): from its digit-1 histogram, the
+// digit D1 holding the k-th key, the keys still needed inside it, and the
+// mode (none, candidates, or scan when the keys in D1 overflow the segment's
+// candidate region).  Called by every thread of the workgroup.
+__device__ void choose_digit1(const SegWs &ws, int32_t s, const SegInfo &inf, SegState *st,
+                              uint32_t *s_wave, uint32_t *s_out) {
+    pick_bin<kDigit1, true>(ws.hist1 + int64_t(s) * kDigit1, uint32_t(inf.k), s_wave, s_out);
+    if (threadIdx.x == 0) {
+        // the radix path emits and collects from scratch in pass2
+        st->emit = 0u;
+        st->ccur = 0u;
+        const uint32_t c1 = s_out[2];
+        st->d1 = s_out[0];
+        st->need1 = uint32_t(inf.k) - s_out[1];
+        st->c1 = c1;
+        st->mode = c1 == 0u ? kModeNone : (int64_t(c1) <= inf.ccap ? kModeCand : kModeScan);
+        if (c1 != 0u) atomicAdd(&ws.ctl->pass2, 1u);
+    }
+    __syncthreads();  // s_out is reused by the caller
+}
 
 __global__ __launch_bounds__(kBlock) void seg_select1_kernel(SegWs ws) {
     __shared__ uint32_t s_wave[kWaves];
@@ -734,47 +851,74 @@ __global__ __launch_bounds__(kBlock) void seg_select1_kernel(SegWs ws) {
         return;
     }
     // bracket confirmed when #(key > hi) <= k <= #(key >= lo) and every key in
-    // the bracket was collected: the selection continues among candidates
+    // the bracket was collected: the bracket histogram then names the bin da
+    // holding the k-th key; keys in higher bins are kept, keys in lower bins
+    // dropped, and only bin da is ranked (by the final pass, from a list that
+    // pass2 writes after the candidates, so it must fit there)
     const SegState cur = *st;
+    uint32_t *fine = ws.hist2 + int64_t(s) * kDigit2;
+    __syncthreads();  // every thread has read the state before it changes
     if (cur.bracket && int64_t(cur.emit) <= inf.k && int64_t(cur.emit) + cur.ccur >= inf.k &&
         int64_t(cur.ccur) <= inf.ccap) {
-        if (threadIdx.x == 0) {
-            st->mode = kModeFast;
-            st->need1 = uint32_t(inf.k) - cur.emit;
-            atomicAdd(&ws.ctl->bracket, 1u);
+        const uint32_t need = uint32_t(inf.k) - cur.emit;
+        uint32_t da = kNoBin, needa = 0u, ca = 0u;
+        if (need > 0u) {
+            pick_bin<kFineBins, true>(fine, need, s_wave, s_out);
+            da = s_out[0];
+            needa = need - s_out[1];
+            ca = s_out[2];
         }
-        return;
+        if (int64_t(cur.ccur) + ca <= inf.ccap) {
+            // pass2's work: clear e at the pairs above the bracket, and sort
+            // the candidates into kept, dropped and bin da
+            const uint32_t na = (cur.emit + kChunk - 1) / kChunk;
+            const uint32_t nc = need > 0u ? (cur.ccur + kChunk - 1) / kChunk : 0u;
+            __syncthreads();  // s_out is read above by every thread
+            if (threadIdx.x == 0) {
+                st->mode = kModeFast;
+                st->need1 = need;
+                st->da = da;
+                st->needa = needa;
+                st->ca = ca;
+                st->ecut = cur.emit;
+                st->tcur = 0u;
+                s_out[0] = atomicAdd(&ws.ctl->nwork, na + nc);
+                atomicAdd(&ws.ctl->bracket, 1u);
+            }
+            __syncthreads();
+            const uint32_t base = s_out[0];
+            for (uint32_t q = threadIdx.x; q < na + nc; q += kBlock) {
+                const uint32_t w = base + q;
+                if (w < ws.work_cap)
+                    ws.work[w] = q < na ? make_uint2(uint32_t(s), q * kChunk)
+                                        : make_uint2(uint32_t(s) | 0x80000000u, (q - na) * kChunk);
+            }
+            return;
+        }
     }
-    pick_bin<kDigit1, true>(ws.hist1 + int64_t(s) * kDigit1, uint32_t(inf.k), s_wave, s_out);
-    if (threadIdx.x == 0) {
-        // the radix path emits and collects from scratch in pass2
-        st->emit = 0u;
-        st->ccur = 0u;
-        const uint32_t c1 = s_out[2];
-        st->d1 = s_out[0];
-        st->need1 = uint32_t(inf.k) - s_out[1];
-        st->c1 = c1;
-        st->mode = c1 == 0u ? kModeNone : (int64_t(c1) <= inf.ccap ? kModeCand : kModeScan);
-        if (c1 != 0u) atomicAdd(&ws.ctl->pass2, 1u);
+    if (cur.bracket) {
+        // missed: the radix path follows; the bracket histogram shares the
+        // memory pass2 counts in
+        f32x4 *h = reinterpret_cast<f32x4 *>(fine);
+        const f32x4 z = {0.0f, 0.0f, 0.0f, 0.0f};
+        for (int q = threadIdx.x; q < kDigit2 / 4; q += kBlock) h[q] = z;
+        if (threadIdx.x == 0)
+            st->miss = int64_t(cur.emit) > inf.k ? 2u
+                       : (int64_t(cur.emit) + cur.ccur < inf.k ? 1u : 3u);
     }
+    choose_digit1(ws, s, inf, st, s_wave, s_out);
 }
 
 // ---------------------------------------------------------------------------
 // pass2: keys above D1 to the payload, keys in D1 to the candidates
 // ---------------------------------------------------------------------------
 
+// The radix path's sweep over tiles [t0, t1).
 template <bool kAligned>
-__global__ __launch_bounds__(kBlock) void seg_pass2_kernel(float *__restrict__ e,
-                                                           int32_t *__restrict__ idx,
-                                                           float *__restrict__ val, int32_t nseg,
-                                                           SegWs ws, uint32_t tiles_per_wg) {
-    __shared__ uint32_t hist[kDigit2];
-    __shared__ Stage sg;
-    if (ws.ctl->status != 0u || ws.ctl->pass2 == 0u) return;
-    const uint32_t T = ws.ctl->tiles;
-    const uint32_t t0 = blockIdx.x * tiles_per_wg;
-    if (t0 >= T) return;
-    const uint32_t t1 = min(T, t0 + tiles_per_wg);
+__device__ void pass2_tiles(float *__restrict__ e, int32_t *__restrict__ idx,
+                            float *__restrict__ val, int32_t nseg, const SegWs &ws, uint32_t t0,
+                            uint32_t t1, uint32_t *hist, Stage &sg) {
+    const Fine nofine = {nullptr, 0u, 0u};
     for (int b = threadIdx.x; b < kDigit2; b += kBlock) hist[b] = 0u;
     int32_t s = segment_of_tile(ws.tile_prefix, nseg, t0);
     uint32_t next = ws.tile_prefix[s + 1];
@@ -787,7 +931,7 @@ __global__ __launch_bounds__(kBlock) void seg_pass2_kernel(float *__restrict__ e
     for (uint32_t t = t0; t < t1; ++t) {
         if (t >= next) {
             flush_emit(sg, efill, st, inf, idx, val);
-            flush_cand(sg, cfill, st, inf, ws.cand);
+            flush_cand(sg, cfill, st, inf, ws.cand, nofine);
             if (dirty) flush_hist(hist, kDigit2, ws.hist2 + int64_t(s) * kDigit2);
             dirty = false;
             s = segment_of_tile(ws.tile_prefix, nseg, t);
@@ -846,11 +990,88 @@ __global__ __launch_bounds__(kBlock) void seg_pass2_kernel(float *__restrict__ e
         dirty = dirty || mode != kModeAll;
         if (mode != kModeScan)
             stage_tile(sg, efill, cfill, p, r.block0, emit_mask, cand_mask, inf, st, ws.cand, idx,
-                       val, e, true);
+                       val, e, true, nofine);
     }
     flush_emit(sg, efill, st, inf, idx, val);
-    flush_cand(sg, cfill, st, inf, ws.cand);
+    flush_cand(sg, cfill, st, inf, ws.cand, nofine);
     if (dirty) flush_hist(hist, kDigit2, ws.hist2 + int64_t(s) * kDigit2);
+}
+
+// One work item of a segment on the bracket path (select1 lists them):
+//   kind 0: payload slots [first, first + kChunk) of the pairs above the
+//           bracket: their e is cleared (pass1 left it for a fallback);
+//   kind 1: candidates [first, first + kChunk): bins above da to the payload
+//           (e cleared), bin da appended to the list after the candidates.
+__device__ void bracket_work(uint2 item, float *__restrict__ e, int32_t *__restrict__ idx,
+                             float *__restrict__ val, const SegWs &ws, Stage &sg) {
+    const int32_t s = int32_t(item.x & 0x7fffffffu);
+    const uint32_t first = item.y;
+    const SegInfo inf = ws.info[s];
+    SegState *st = ws.st + s;
+    if (!(item.x >> 31)) {
+        const uint32_t end = min(first + kChunk, st->ecut);
+        for (uint32_t q = first + threadIdx.x; q < end; q += kBlock) e[idx[inf.kout + q]] = 0.0f;
+        return;
+    }
+    constexpr int kPer = kChunk / kBlock;
+    const uint32_t lo = st->lo, shift = st->shift, da = st->da, ccur = st->ccur;
+    const uint32_t end = min(first + kChunk, ccur);
+    const uint2 *cand = ws.cand + inf.coff;
+    uint2 v[kPer];
+    uint32_t keep = 0u, tie = 0u;
+#pragma unroll
+    for (int u = 0; u < kPer; ++u) {
+        const uint32_t q = first + uint32_t(u * kBlock) + threadIdx.x;
+        v[u] = make_uint2(0u, 0u);
+        if (q < end) {
+            v[u] = cand[q];
+            const uint32_t bin = ((v[u].x & 0x7fffffffu) - lo) >> shift;
+            keep |= uint32_t(bin > da) << u;
+            tie |= uint32_t(bin == da) << u;
+        }
+    }
+    uint32_t tk, tt;
+    uint32_t pk = block_prefix_small(uint32_t(__popc(keep)), sg.wave, tk);
+    uint32_t pt = block_prefix_small(uint32_t(__popc(tie)), sg.wave, tt);
+    if (threadIdx.x == 0) {
+        sg.wave[0] = tk ? atomicAdd(&st->emit, tk) : 0u;
+        sg.wave[1] = tt ? atomicAdd(&st->tcur, tt) : 0u;
+    }
+    __syncthreads();
+    pk += sg.wave[0];
+    pt += sg.wave[1];
+    __syncthreads();  // sg.wave is reused by the next item
+#pragma unroll
+    for (int u = 0; u < kPer; ++u) {
+        if ((keep >> u) & 1u) {
+            if (int64_t(pk) < inf.k) {
+                idx[inf.kout + pk] = int32_t(v[u].y);
+                val[inf.kout + pk] = __uint_as_float(v[u].x);
+                e[v[u].y] = 0.0f;
+            }
+            ++pk;
+        }
+        if ((tie >> u) & 1u) {
+            if (int64_t(ccur) + pt < inf.ccap) ws.cand[inf.coff + ccur + pt] = v[u];
+            ++pt;
+        }
+    }
+}
+
+template <bool kAligned>
+__global__ __launch_bounds__(kBlock) void seg_pass2_kernel(float *__restrict__ e,
+                                                           int32_t *__restrict__ idx,
+                                                           float *__restrict__ val, int32_t nseg,
+                                                           SegWs ws, uint32_t slice) {
+    __shared__ uint32_t hist[kDigit2];
+    __shared__ Stage sg;
+    if (ws.ctl->status != 0u) return;
+    const uint32_t T = ws.ctl->tiles;
+    if (ws.ctl->pass2 != 0u)
+        for (uint32_t t0 = blockIdx.x * slice; t0 < T; t0 += gridDim.x * slice)
+            pass2_tiles<kAligned>(e, idx, val, nseg, ws, t0, min(T, t0 + slice), hist, sg);
+    const uint32_t nwork = min(ws.ctl->nwork, ws.work_cap);
+    for (uint32_t w = blockIdx.x; w < nwork; w += gridDim.x) bracket_work(ws.work[w], e, idx, val, ws, sg);
 }
 
 // ---------------------------------------------------------------------------
@@ -940,8 +1161,7 @@ __device__ void finish(FinalShared &sh, const SegInfo &inf, const uint2 *cand, i
         }
     });
     if (tid == 0) {
-        const SegHint old = *hint;
-        *hint = SegHint{T, old.magic == kHintMagic ? old.key : T, kHintMagic, width};
+        *hint = next_hint(*hint, T, width);
     }
 }
 
@@ -976,41 +1196,37 @@ __device__ void final_select(FinalShared &sh, const SegInfo &inf, const SegState
                         kMode == kModeCand ? st.emit : 0u, hint, width);
 }
 
-// Bracket path: pass1 put the keys above hi in the payload (e not yet
-// cleared) and the keys in [lo, hi] (at most 2^20 keys) in the candidates;
-// select the remaining need1 among them by (key - lo) bits 19..10, then 9..0.
+// Bracket path: pass1 put the keys above the bracket in the payload,
+// pass2 cleared their e, emitted the candidates of the bracket bins above
+// da and listed the `ca` candidates of bin da; rank those by the low
+// `shift` bits of key - lo (the exact threshold T), then by index among
+// keys equal to T, and emit the `needa` kept ones into the last slots.
 template <bool kLds>
-__device__ void final_bracket(FinalShared &sh, const SegInfo &inf, const SegState &st,
-                              const uint2 *cand, int64_t n, float *e, int32_t *idx, float *val,
-                              SegHint *hint, uint32_t width) {
+__device__ void final_fast(FinalShared &sh, const SegInfo &inf, const SegState &st,
+                           const uint2 *list, int64_t n, float *e, int32_t *idx, float *val,
+                           SegHint *hint, uint32_t width) {
     const int tid = threadIdx.x;
-    const uint32_t above = min(st.emit, uint32_t(inf.k));
-    for (uint32_t j = tid; j < above; j += kBlock) e[idx[inf.kout + j]] = 0.0f;
-    const uint32_t need = st.need1;
-    if (need == 0u) return;
-    const uint32_t lo = st.lo;
-    for (int b = tid; b < 1024; b += kBlock) sh.hist[b] = 0u;
+    if (st.needa == 0u) {  // the pairs above the bracket were exactly k
+        if (tid == 0) {
+            *hint = next_hint(*hint, min(st.hi, 0x7ffffffeu) + 1u, width);
+        }
+        return;
+    }
+    const uint32_t lo = st.lo, shift = st.shift;
+    const uint32_t sub_mask = (1u << shift) - 1u;
+    for (int b = tid; b < kIdxBins; b += kBlock) sh.hist[b] = 0u;
     __syncthreads();
-    for_items<kModeCand, kLds>(sh, cand, e, inf, n, [&](uint32_t key, uint32_t, uint32_t) {
-        atomicAdd(&sh.hist[((key - lo) >> 10) & 1023u], 1u);
+    for_items<kModeCand, kLds>(sh, list, e, inf, n, [&](uint32_t key, uint32_t, uint32_t) {
+        atomicAdd(&sh.hist[(key - lo) & sub_mask], 1u);
     });
     __syncthreads();
-    pick_bin<1024, true>(sh.hist, need, sh.wave, sh.out);
-    const uint32_t DA = sh.out[0];
-    const uint32_t needA = need - sh.out[1];
-    __syncthreads();
-    for (int b = tid; b < 1024; b += kBlock) sh.hist[b] = 0u;
-    __syncthreads();
-    for_items<kModeCand, kLds>(sh, cand, e, inf, n, [&](uint32_t key, uint32_t, uint32_t) {
-        if (((key - lo) >> 10) == DA) atomicAdd(&sh.hist[(key - lo) & 1023u], 1u);
-    });
-    __syncthreads();
-    pick_bin<1024, true>(sh.hist, needA, sh.wave, sh.out);
-    const uint32_t T = lo + ((DA << 10) | sh.out[0]);
-    const uint32_t need3 = needA - sh.out[1];
+    pick_bin<kIdxBins, true>(sh.hist, st.needa, sh.wave, sh.out);
+    const uint32_t T = lo + ((st.da << shift) | sh.out[0]);
+    const uint32_t need3 = st.needa - sh.out[1];
     const uint32_t ties = sh.out[2];
     __syncthreads();
-    finish<kModeCand, kLds>(sh, inf, cand, n, e, idx, val, T, need3, ties, above, hint, width);
+    finish<kModeCand, kLds>(sh, inf, list, n, e, idx, val, T, need3, ties,
+                            uint32_t(inf.k) - st.needa, hint, width);
 }
 
 __global__ __launch_bounds__(kBlock) void seg_final_kernel(float *__restrict__ e,
@@ -1023,23 +1239,32 @@ __global__ __launch_bounds__(kBlock) void seg_final_kernel(float *__restrict__ e
     if (st.mode != kModeCand && st.mode != kModeScan && st.mode != kModeFast) return;
     const SegInfo inf = ws.info[s];
     SegHint *hint = ws.hint + s;
-    // next bracket width: narrower after a bracket that held many more keys
-    // than needed, wider after one that missed the k-th key
+    // next bracket widths: the lower side narrower after a bracket that held
+    // many more keys below the threshold than the segment keeps, or more than
+    // it can hold; both sides wider after the threshold fell outside it
     const SegHint oh = *hint;
-    uint32_t width = (oh.magic == kHintMagic && oh.width >= kWidthMin && oh.width <= kWidthMax)
-                         ? oh.width : kWidthStart;
+    const uint32_t w0 = oh.magic == kHintMagic && widths_ok(oh.width)
+                            ? oh.width : make_widths(kWidthStart, kWidthStart);
+    uint32_t wl = width_lo(w0), wh = width_hi(w0);
     if (st.mode == kModeFast) {
-        if (int64_t(st.ccur) > 4 * inf.k + 1024 && width > kWidthMin) --width;
-    } else if (st.bracket && width < kWidthMax) {
-        ++width;
+        if (int64_t(st.ccur) - int64_t(st.need1) > inf.k + 1024 && wl > kWidthMin) --wl;
+    } else if (st.bracket && st.miss == 3u) {
+        if (wl > kWidthMin) --wl;
+    } else if (st.bracket) {
+        wl = min(wl + 1u, kWidthMax);
+        wh = min(wh + 1u, kWidthMax);
     }
+    const uint32_t width = make_widths(wl, wh);
     const uint32_t *h2 = ws.hist2 + int64_t(s) * kDigit2;
     if (st.mode == kModeScan) {
         final_select<kModeScan, false>(sh, inf, st, nullptr, inf.size, e, idx, val, h2, hint, width);
         return;
     }
-    const int64_t n = min(int64_t(st.ccur), inf.ccap);
-    const uint2 *cand = ws.cand + inf.coff;
+    // the candidates, or on the bracket path the list of bin da after them
+    const bool fast = st.mode == kModeFast;
+    const int64_t n = fast ? int64_t(st.needa ? min(st.ca, st.tcur) : 0u)
+                           : min(int64_t(st.ccur), inf.ccap);
+    const uint2 *cand = ws.cand + inf.coff + (fast ? st.ccur : 0u);
     const bool lds = n <= kCandLds;
     if (lds) {
         for (int64_t base = 0; base < n; base += int64_t(kUnroll) * kBlock) {
@@ -1057,9 +1282,9 @@ __global__ __launch_bounds__(kBlock) void seg_final_kernel(float *__restrict__ e
         }
         __syncthreads();
     }
-    if (st.mode == kModeFast) {
-        if (lds) final_bracket<true>(sh, inf, st, cand, n, e, idx, val, hint, width);
-        else final_bracket<false>(sh, inf, st, cand, n, e, idx, val, hint, width);
+    if (fast) {
+        if (lds) final_fast<true>(sh, inf, st, cand, n, e, idx, val, hint, width);
+        else final_fast<false>(sh, inf, st, cand, n, e, idx, val, hint, width);
     } else {
         if (lds) final_select<kModeCand, true>(sh, inf, st, cand, n, e, idx, val, h2, hint, width);
         else final_select<kModeCand, false>(sh, inf, st, cand, n, e, idx, val, h2, hint, width);
@@ -1080,7 +1305,7 @@ hipError_t launch_topk_segmented(const float *g, float *e, int64_t d, float lr, 
                                  int32_t *idx, float *val, void *workspace, hipStream_t stream) {
     const SegLayout L = seg_layout(nseg, k_total);
     char *base = static_cast<char *>(workspace);
-    SegWs ws;
+    SegWs ws = {};
     ws.ctl = reinterpret_cast<SegCtl *>(base);
     ws.info = reinterpret_cast<SegInfo *>(base + L.info);
     ws.tile_prefix = reinterpret_cast<uint32_t *>(base + L.tile_prefix);
@@ -1089,26 +1314,28 @@ hipError_t launch_topk_segmented(const float *g, float *e, int64_t d, float lr, 
     ws.hist1 = reinterpret_cast<uint32_t *>(base + L.hist1);
     ws.hist2 = reinterpret_cast<uint32_t *>(base + L.hist2);
     ws.cand = reinterpret_cast<uint2 *>(base + L.cand);
+    ws.work = reinterpret_cast<uint2 *>(base + L.work);
     ws.ccap_total = L.ccap_total;
+    ws.work_cap = uint32_t(L.work_cap);
 
     const uint32_t zero_grid = persistent_grid(nseg);  // one segment's histograms per pass
     seg_reset_kernel<<<1 + zero_grid, kBlock, 0, stream>>>(ws, offsets, k, nseg, d, k_total);
 
     const int64_t max_tiles = (d + kTile - 1) / kTile + nseg;
-    // 8 workgroups per CU requested (pass1's histogram lets 4 be resident):
-    // measured faster than 4 for both streaming passes
-    const uint32_t grid = balanced_grid(max_tiles, kScanWorkgroupsPerCU);
-    const uint32_t per_wg = uint32_t((max_tiles + grid - 1) / grid);
+    // slices: at least two per workgroup of a full grid, at most kSliceTilesMax tiles
+    const int64_t wgs = int64_t(device_cu_count()) * kSliceWorkgroupsPerCU;
+    const int64_t slice = max(int64_t(1), min(kSliceTilesMax, max_tiles / (2 * wgs)));
+    const uint32_t grid = uint32_t(min(wgs, (max_tiles + slice - 1) / slice));
     const bool aligned = ((reinterpret_cast<uintptr_t>(g) | reinterpret_cast<uintptr_t>(e)) & 15) == 0;
     if (aligned)
-        seg_pass1_kernel<true><<<grid, kBlock, 0, stream>>>(g, e, lr, idx, val, nseg, ws, per_wg);
+        seg_pass1_kernel<true><<<grid, kBlock, 0, stream>>>(g, e, lr, idx, val, nseg, ws, uint32_t(slice));
     else
-        seg_pass1_kernel<false><<<grid, kBlock, 0, stream>>>(g, e, lr, idx, val, nseg, ws, per_wg);
+        seg_pass1_kernel<false><<<grid, kBlock, 0, stream>>>(g, e, lr, idx, val, nseg, ws, uint32_t(slice));
     seg_select1_kernel<<<uint32_t(nseg), kBlock, 0, stream>>>(ws);
     if (aligned)
-        seg_pass2_kernel<true><<<grid, kBlock, 0, stream>>>(e, idx, val, nseg, ws, per_wg);
+        seg_pass2_kernel<true><<<grid, kBlock, 0, stream>>>(e, idx, val, nseg, ws, uint32_t(slice));
     else
-        seg_pass2_kernel<false><<<grid, kBlock, 0, stream>>>(e, idx, val, nseg, ws, per_wg);
+        seg_pass2_kernel<false><<<grid, kBlock, 0, stream>>>(e, idx, val, nseg, ws, uint32_t(slice));
     seg_final_kernel<<<uint32_t(nseg), kBlock, 0, stream>>>(e, idx, val, ws);
     return hipGetLastError();
 }
