@@ -63,6 +63,8 @@ constexpr int kFinePerCoarse = int(kFine) / kCoarse;
 constexpr uint32_t kHintMagic = 0x48494e54u;
 constexpr int kStagePairs = 1024;
 constexpr uint32_t kNoKey = 0xffffffffu;            // larger than every 31-bit key
+constexpr uint32_t kCandChunkMax = 4096;           // bracket candidates per step-3 work unit, at most
+constexpr uint32_t kStep3Chunks = 512;             // step-3 work units aimed for
 
 // Fields are written by workgroup 0 of one launch and read by later
 // launches only, never by other workgroups of the launch that writes them.
@@ -532,35 +534,51 @@ __global__ __launch_bounds__(kBlock) void topk_step3_kernel(float *__restrict__ 
     // pairs pass 1 sent: zero their residuals (above <= k, so all were written)
     for (uint32_t j = blockIdx.x * kBlock + tid; j < uint32_t(above); j += gridDim.x * kBlock)
         e[idx[j]] = 0.0f;
-    // candidates: one block-wide prefix and one atomic per round
+    // candidates: chunks of `per` candidates per thread, one block-wide prefix
+    // and one atomic on the shared payload counter per chunk; `per` grows
+    // with the candidate count so that about kStep3Chunks chunks take it (an
+    // atomic per workgroup per kBlock candidates serialises on that one
+    // address at millions of candidates, while too few chunks leave most
+    // workgroups idle)
+    constexpr int kPer = kCandChunkMax / kBlock;
     const uint32_t n = uint32_t(inside);
-    const uint32_t stride = gridDim.x * kBlock;
-    const uint32_t rounds = (n + stride - 1) / stride;
-    for (uint32_t r = 0; r < rounds; ++r) {
-        const uint32_t j = r * stride + blockIdx.x * kBlock + tid;
-        bool keep = false;
-        int32_t i = 0;
-        float v = 0.0f;
-        if (j < n) {
-            i = ws.cand_idx[j];
-            v = ws.cand_val[j];
-            const uint32_t key = magnitude_key(v);
-            keep = key > T || (all_ties && key == T);
+    const uint32_t per = min(uint32_t(kPer), max(1u, (n + kStep3Chunks * kBlock - 1) /
+                                                         (kStep3Chunks * kBlock)));
+    const uint32_t chunk = per * kBlock;
+    for (uint32_t base = blockIdx.x * chunk; base < n; base += gridDim.x * chunk) {
+        int32_t ci[kPer];
+        float cv[kPer];
+        uint32_t keep = 0;
+#pragma unroll
+        for (int u = 0; u < kPer; ++u) {
+            const uint32_t j = base + uint32_t(u * kBlock + tid);
+            ci[u] = 0;
+            cv[u] = 0.0f;
+            if (uint32_t(u) < per && j < n) {
+                ci[u] = ws.cand_idx[j];
+                cv[u] = ws.cand_val[j];
+                const uint32_t key = magnitude_key(cv[u]);
+                keep |= uint32_t(key > T || (all_ties && key == T)) << u;
+            }
         }
         uint32_t total;
-        const uint32_t pos = block_prefix_small(keep ? 1u : 0u, s_wave, total);
+        const uint32_t pos = block_prefix_small(uint32_t(__popc(keep)), s_wave, total);
         if (total == 0) continue;
         if (tid == 0) s_base = atomicAdd(&c->emit2, (unsigned long long)total) & kCountMask;
         __syncthreads();
-        if (keep) {
-            const uint64_t o = above + s_base + pos;
-            if (o < k) {
-                idx[o] = i;
-                val[o] = v;
+        uint64_t o = above + s_base + pos;
+#pragma unroll
+        for (int u = 0; u < kPer; ++u) {
+            if ((keep >> u) & 1u) {
+                if (o < k) {
+                    idx[o] = ci[u];
+                    val[o] = cv[u];
+                }
+                e[ci[u]] = 0.0f;
+                ++o;
             }
-            e[i] = 0.0f;
         }
-        __syncthreads();
+        __syncthreads();  // s_base is reused by the next chunk
     }
 }
 
