@@ -263,6 +263,77 @@ def test_segmented_workspace_contents_do_not_matter():
         assert_bits_equal(ge, re)
 
 
+def _two_calls(gs, off, ks):
+    """Calls on one zeroed workspace, e from zero each time; each call
+    checked against the oracle.  Returns the bracket count of each call."""
+    ws = efs.new_topk_segmented_workspace(len(ks), int(np.sum(ks)), DEV)
+    ws.zero_()
+    hits = []
+    for g in gs:
+        e = np.zeros(g.size, np.float32)
+        gi, gv, ge, _ = run_gpu(g, e, off, ks, ws=ws)
+        ri, rv, re = oracle.topk_segmented(g, e, LR, off, ks)
+        np.testing.assert_array_equal(np.sort(gi), np.sort(ri))
+        assert_bits_equal(np.sort(gv), np.sort(rv))
+        assert_bits_equal(ge, re)
+        hits.append(efs.topk_segmented_bracket_segments(ws))
+    return hits
+
+
+def test_segmented_bracket_exactly_k_above():
+    # the first call puts the threshold at |p| = 1.0; on the second exactly k
+    # keys (1.05) lie above the bracket around it and three more (1.0)
+    # inside: the bracket is confirmed with nothing left to take from the
+    # candidates
+    rng = np.random.default_rng(660)
+    d0, k0 = 3 * 4096, 10
+    off = np.array([0, d0, d0 + 20_000], dtype=np.int64)
+    ks = np.array([k0, 0], dtype=np.int64)
+    tiny = lambda n: rng.uniform(-1e-2, 1e-2, size=n).astype(np.float32)
+    pos = rng.choice(d0, 13, replace=False)
+    g1 = np.concatenate([tiny(d0), synth.small_gradient(661, 20_000)])
+    g1[pos[:10]] = np.float32(10.0)
+    g2 = np.concatenate([tiny(d0), synth.small_gradient(662, 20_000)])
+    g2[pos[:10]] = np.float32(-10.5)
+    g2[pos[10:]] = np.float32(10.0)
+    say("segmented bracket with exactly k pairs above it")
+    hits = _two_calls([g1, g2], off, ks)
+    assert hits == [0, 1]
+
+
+def test_segmented_bracket_bin_too_large_falls_back():
+    # 2,200 keys tied at the threshold share one bracket bin; with the
+    # candidates they exceed the segment's candidate region (16 k + 4096), so
+    # the bin cannot be listed and the radix path takes over
+    rng = np.random.default_rng(670)
+    d0, k0 = 2 * 4096, 10
+    off = np.array([0, d0], dtype=np.int64)
+    ks = np.array([k0], dtype=np.int64)
+    g = rng.uniform(-1e-2, 1e-2, size=d0).astype(np.float32)
+    pos = rng.choice(d0, 2205, replace=False)
+    g[pos[:2200]] = np.float32(10.0)
+    g[pos[2200:]] = np.float32(10.1)
+    say("segmented bracket bin too large for the list")
+    hits = _two_calls([g, g], off, ks)
+    assert hits == [0, 0]
+
+
+def test_segmented_bracket_bin_listed():
+    # the same shape with 2,000 tied keys: the bin fits after the candidates,
+    # is listed by pass 2 and ranked by index in the final pass
+    rng = np.random.default_rng(680)
+    d0, k0 = 2 * 4096, 10
+    off = np.array([0, d0], dtype=np.int64)
+    ks = np.array([k0], dtype=np.int64)
+    g = rng.uniform(-1e-2, 1e-2, size=d0).astype(np.float32)
+    pos = rng.choice(d0, 2005, replace=False)
+    g[pos[:2000]] = np.float32(10.0)
+    g[pos[2000:]] = np.float32(-10.1)
+    say("segmented bracket bin listed")
+    hits = _two_calls([g, g], off, ks)
+    assert hits == [0, 1]
+
+
 def test_segmented_bracket_from_another_scale_falls_back():
     # hints learned on one scale make a bracket that misses the next call's
     # thresholds (50x larger): the radix path takes over, results exact; the
