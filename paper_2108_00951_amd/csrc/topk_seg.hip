@@ -85,6 +85,7 @@ constexpr uint32_t kChunk = 2048;              // pass2 work item: payload slots
 constexpr int64_t kSliceTilesMax = 4;
 constexpr int kSliceWorkgroupsPerCU = 4;
 constexpr uint32_t kNoBin = 0xffffffffu;
+constexpr uint32_t kNoWork = 0xffffffffu;      // work-list slot not in use this call
 static_assert(kFineBins == kDigit2, "the bracket histogram lives in a segment's second histogram");
 static_assert(kWidthMax <= 19, "a bracket spans under 2^20 keys, so a bin at most 1024");
 constexpr uint32_t kHintMagic = 0x53454748u;
@@ -93,8 +94,8 @@ struct SegCtl {
     uint32_t status;   // 0: layout accepted; 1: rejected (the call changed nothing)
     uint32_t tiles;    // tiles of all segments
     uint32_t bracket;  // segments that selected from the bracket (a diagnostic)
-    uint32_t pass2;    // segments that need pass2's tile sweep
-    uint32_t nwork;    // entries of the work list (bracket path, for pass2)
+    uint32_t pass2;    // nonzero when some segment needs pass2's tile sweep
+    uint32_t wtotal;   // work-list slots of all segments (bracket path, for pass2)
     uint32_t pad[59];
 };
 static_assert(sizeof(SegCtl) == 256, "control block is 256 bytes");
@@ -102,7 +103,7 @@ static_assert(sizeof(SegCtl) == 256, "control block is 256 bytes");
 struct SegInfo {
     int64_t off, size, kout, k, coff, ccap;
     uint32_t tile0, ntiles;
-    uint32_t pad[2];
+    uint32_t wbase, wmax;  // the segment's work-list slots (bracket path)
 };
 static_assert(sizeof(SegInfo) == 64, "segment info is 64 bytes");
 
@@ -313,6 +314,13 @@ __device__ __forceinline__ int32_t segment_of_tile(const uint32_t *tp, int32_t n
     return lo;
 }
 
+// The segment holding tile t when the segment s before it ended at t
+// (t == tp[s + 1]): usually the next one, else a search past empty ones.
+__device__ __forceinline__ int32_t segment_after(const uint32_t *tp, int32_t nseg, int32_t s,
+                                                 uint32_t t) {
+    return tp[s + 2] > t ? s + 1 : segment_of_tile(tp, nseg, t);
+}
+
 // Element (j, c) of this thread in the 4096-element block starting at
 // `block0` (index block0 + (j * kBlock + tid) * 4 + c, the hard threshold's
 // map).
@@ -342,9 +350,69 @@ __device__ __forceinline__ TileRange tile_range(const SegInfo &inf, uint32_t t) 
 // reset
 // ---------------------------------------------------------------------------
 
-__global__ __launch_bounds__(kBlock) void seg_reset_kernel(SegWs ws, const int64_t *__restrict__ off,
-                                                           const int64_t *__restrict__ kin,
-                                                           int32_t nseg, int64_t d, int64_t k_total) {
+// The reset runs 512-thread workgroups: workgroup 0 forms the tables in
+// chunks of 512 segments (one block-wide scan per chunk, the next chunk's
+// loads in flight meanwhile), the others zero histograms.
+constexpr int kResetBlock = 512;
+constexpr int kResetWaves = kResetBlock / kWave;
+
+struct Sums {
+    int64_t k, c, t, w;  // pairs, candidate slots, tiles, work-list slots
+};
+
+// Exclusive prefix of v over the workgroup's threads in order; `total` gets
+// the sum.  Two barriers.
+__device__ __forceinline__ Sums reset_scan(Sums v, Sums *s_wave, Sums &total) {
+    const int lane = threadIdx.x & (kWave - 1);
+    const int wave = threadIdx.x / kWave;
+    const Sums incl = {wave_incl_i64(v.k), wave_incl_i64(v.c), wave_incl_i64(v.t),
+                       wave_incl_i64(v.w)};
+    if (lane == kWave - 1) s_wave[wave] = incl;
+    __syncthreads();
+    Sums off = {0, 0, 0, 0}, tot = {0, 0, 0, 0};
+#pragma unroll
+    for (int q = 0; q < kResetWaves; ++q) {
+        const Sums x = s_wave[q];
+        if (q < wave) {
+            off.k += x.k;
+            off.c += x.c;
+            off.t += x.t;
+            off.w += x.w;
+        }
+        tot.k += x.k;
+        tot.c += x.c;
+        tot.t += x.t;
+        tot.w += x.w;
+    }
+    __syncthreads();
+    total = tot;
+    return Sums{off.k + incl.k - v.k, off.c + incl.c - v.c, off.t + incl.t - v.t,
+                off.w + incl.w - v.w};
+}
+
+// What the reset reads of one segment.
+struct SegIn {
+    int64_t lo, hi, k;
+    SegHint h;
+};
+
+__device__ __forceinline__ SegIn load_seg(const int64_t *off, const int64_t *kin,
+                                          const SegHint *hint, int32_t s, int32_t nseg) {
+    SegIn in = {};
+    if (s < nseg) {
+        in.lo = off[s];
+        in.hi = off[s + 1];
+        in.k = kin[s];
+        in.h = hint[s];
+    }
+    return in;
+}
+
+__global__ __launch_bounds__(kResetBlock) void seg_reset_kernel(SegWs ws,
+                                                                const int64_t *__restrict__ off,
+                                                                const int64_t *__restrict__ kin,
+                                                                int32_t nseg, int64_t d,
+                                                                int64_t k_total) {
     if (blockIdx.x > 0) {
         // the other workgroups zero the histograms of the segments that span
         // more than one tile (a one-tile segment is selected inside pass1);
@@ -356,64 +424,58 @@ __global__ __launch_bounds__(kBlock) void seg_reset_kernel(SegWs ws, const int64
             if (size < 0 || segment_tiles(lo, size) <= 1) continue;
             f32x4 *h1 = reinterpret_cast<f32x4 *>(ws.hist1 + int64_t(sg) * kDigit1);
             f32x4 *h2 = reinterpret_cast<f32x4 *>(ws.hist2 + int64_t(sg) * kDigit2);
-            for (int q = threadIdx.x; q < kDigit1 / 4; q += kBlock) h1[q] = z;
-            for (int q = threadIdx.x; q < kDigit2 / 4; q += kBlock) h2[q] = z;
+            for (int q = threadIdx.x; q < kDigit1 / 4; q += kResetBlock) h1[q] = z;
+            for (int q = threadIdx.x; q < kDigit2 / 4; q += kResetBlock) h2[q] = z;
         }
         return;
     }
-    __shared__ int64_t s_wave[kWaves];
+    __shared__ Sums s_wave[kResetWaves];
     __shared__ uint32_t s_bad;
     const int t = threadIdx.x;
     if (t == 0) s_bad = 0u;
     __syncthreads();
-    const int32_t per = (nseg + kBlock - 1) / kBlock;
-    const int32_t s0 = min(nseg, t * per), s1 = min(nseg, s0 + per);
-    int64_t sum_k = 0, sum_c = 0, sum_t = 0;
     bool bad = false;
-    for (int32_t s = s0; s < s1; ++s) {
-        const int64_t lo = off[s], hi = off[s + 1], kk = kin[s];
-        const int64_t size = hi - lo;
-        if (size < 0 || kk < 0 || lo < 0 || hi > d) {
-            bad = true;
-            continue;
+    Sums carry = {0, 0, 0, 0};
+    // the tables are written as the chunks go; a rejected layout leaves them
+    // meaningless, and every later kernel then returns at once
+    SegIn nxt = load_seg(off, kin, ws.hint, t, nseg);
+    for (int32_t c0 = 0; c0 < nseg; c0 += kResetBlock) {
+        const int32_t s = c0 + t;
+        const SegIn in = nxt;
+        nxt = load_seg(off, kin, ws.hint, s + kResetBlock, nseg);  // next chunk, in flight
+        const int64_t size = in.hi - in.lo;
+        int64_t keff = 0, ccap = 0, wmax = 0;
+        uint32_t nt = 0u;
+        if (s < nseg) {
+            if (size < 0 || in.k < 0 || in.lo < 0 || in.hi > d) bad = true;
+            if (size >= 0 && in.k >= 0) {
+                keff = in.k < size ? in.k : size;
+                nt = uint32_t(segment_tiles(in.lo, size));
+                ccap = (nt > 1u && keff > 0 && keff < size) ? kCandPerK * keff + kCandExtra : 0;
+                // bracket path: the pairs above the bracket (at most k) and
+                // the candidates (at most ccap), kChunk per work item
+                wmax = ccap > 0 ? (keff + kChunk - 1) / kChunk + (ccap + kChunk - 1) / kChunk : 0;
+            }
         }
-        const int64_t keff = kk < size ? kk : size;
-        const int64_t nt = segment_tiles(lo, size);
-        sum_k += keff;
-        sum_c += (nt > 1 && keff > 0 && keff < size) ? kCandPerK * keff + kCandExtra : 0;
-        sum_t += nt;
-    }
-    if (t == 0 && off[0] != 0) bad = true;
-    if (t == 0 && off[nseg] != d) bad = true;
-    if (bad) atomicOr(&s_bad, 1u);
-    int64_t tot_k, tot_c, tot_t;
-    int64_t base_k = block_excl_i64(sum_k, s_wave, tot_k);
-    int64_t base_c = block_excl_i64(sum_c, s_wave, tot_c);
-    int64_t base_t = block_excl_i64(sum_t, s_wave, tot_t);
-    // the barriers above also publish s_bad
-    const bool reject = s_bad != 0u || tot_k > k_total || tot_c > ws.ccap_total ||
-                        tot_t > int64_t(UINT32_MAX);
-    if (!reject) {
-        for (int32_t s = s0; s < s1; ++s) {
-            const int64_t lo = off[s], size = off[s + 1] - lo, kk = kin[s];
-            const int64_t keff = kk < size ? kk : size;
-            const uint32_t nt = uint32_t(segment_tiles(lo, size));
-            const int64_t ccap = (nt > 1 && keff > 0 && keff < size) ? kCandPerK * keff + kCandExtra : 0;
+        Sums tot;
+        const Sums ex = reset_scan(Sums{keff, ccap, int64_t(nt), wmax}, s_wave, tot);
+        if (s < nseg) {
             SegInfo inf;
-            inf.off = lo;
+            inf.off = in.lo;
             inf.size = size;
-            inf.kout = base_k;
+            inf.kout = carry.k + ex.k;
             inf.k = keff;
-            inf.coff = base_c;
+            inf.coff = carry.c + ex.c;
             inf.ccap = ccap;
-            inf.tile0 = uint32_t(base_t);
+            inf.tile0 = uint32_t(carry.t + ex.t);
             inf.ntiles = nt;
-            inf.pad[0] = inf.pad[1] = 0u;
+            inf.wbase = uint32_t(carry.w + ex.w);
+            inf.wmax = uint32_t(wmax);
             ws.info[s] = inf;
-            ws.tile_prefix[s] = uint32_t(base_t);
+            ws.tile_prefix[s] = uint32_t(carry.t + ex.t);
             SegState z = {};
-            const SegHint h = ws.hint[s];
-            if (nt > 1 && keff > 0 && keff < size && h.magic == kHintMagic && h.key <= 0x7fffffffu &&
+            const SegHint h = in.h;
+            if (nt > 1u && keff > 0 && keff < size && h.magic == kHintMagic && h.key <= 0x7fffffffu &&
                 h.prev <= 0x7fffffffu && h.prev2 <= 0x7fffffffu && widths_ok(h.width)) {
                 // last threshold plus the last step (capped): error feedback
                 // makes thresholds drift smoothly from call to call
@@ -432,18 +494,25 @@ __global__ __launch_bounds__(kBlock) void seg_reset_kernel(SegWs ws, const int64
                 z.shift = span_bits > 10u ? span_bits - 10u : 0u;
             }
             ws.st[s] = z;
-            base_k += keff;
-            base_c += ccap;
-            base_t += nt;
         }
+        carry.k += tot.k;
+        carry.c += tot.c;
+        carry.t += tot.t;
+        carry.w += tot.w;
     }
+    if (t == 0 && off[0] != 0) bad = true;
+    if (t == 0 && off[nseg] != d) bad = true;
+    if (bad) atomicOr(&s_bad, 1u);
+    __syncthreads();
+    const bool reject = s_bad != 0u || carry.k > k_total || carry.c > ws.ccap_total ||
+                        carry.t > int64_t(UINT32_MAX) || carry.w > int64_t(ws.work_cap);
     if (t == 0) {
         ws.ctl->bracket = 0u;
         ws.ctl->pass2 = 0u;
-        ws.ctl->nwork = 0u;
+        ws.ctl->wtotal = reject ? 0u : uint32_t(carry.w);
         ws.ctl->status = reject ? 1u : 0u;
-        ws.ctl->tiles = reject ? 0u : uint32_t(tot_t);
-        if (!reject) ws.tile_prefix[nseg] = uint32_t(tot_t);
+        ws.ctl->tiles = reject ? 0u : uint32_t(carry.t);
+        if (!reject) ws.tile_prefix[nseg] = uint32_t(carry.t);
     }
 }
 
@@ -708,8 +777,9 @@ __device__ void pass1_slice(const float *__restrict__ g, float *__restrict__ e, 
                 flush_emit(sg, efill, st, inf, idx, val);
                 flush_cand(sg, cfill, st, inf, ws.cand, fine);
             }
-            flush_hist(hist, kDigit1, ws.hist1 + int64_t(s) * kDigit1);
-            s = segment_of_tile(ws.tile_prefix, nseg, t);
+            // a one-tile segment leaves the LDS histogram zero
+            if (inf.ntiles > 1) flush_hist(hist, kDigit1, ws.hist1 + int64_t(s) * kDigit1);
+            s = segment_after(ws.tile_prefix, nseg, s, t);
             next = ws.tile_prefix[s + 1];
             inf = ws.info[s];
             st = ws.st + s;
@@ -786,7 +856,8 @@ __device__ void pass1_slice(const float *__restrict__ g, float *__restrict__ e, 
         flush_emit(sg, efill, st, inf, idx, val);
         flush_cand(sg, cfill, st, inf, ws.cand, fine);
     }
-    flush_hist(hist, kDigit1, ws.hist1 + int64_t(s) * kDigit1);
+    if (inf.ntiles > 1) flush_hist(hist, kDigit1, ws.hist1 + int64_t(s) * kDigit1);
+    __syncthreads();  // the next slice starts with another segment's state
 }
 
 template <bool kAligned>
@@ -827,16 +898,14 @@ __device__ void choose_digit1(const SegWs &ws, int32_t s, const SegInfo &inf, Se
         st->need1 = uint32_t(inf.k) - s_out[1];
         st->c1 = c1;
         st->mode = c1 == 0u ? kModeNone : (int64_t(c1) <= inf.ccap ? kModeCand : kModeScan);
-        if (c1 != 0u) atomicAdd(&ws.ctl->pass2, 1u);
+        // a flag, stored (an atomic per segment on one word serialises when
+        // thousands of segments take this path)
+        if (c1 != 0u) ws.ctl->pass2 = 1u;
     }
     __syncthreads();  // s_out is reused by the caller
 }
 
-__global__ __launch_bounds__(kBlock) void seg_select1_kernel(SegWs ws) {
-    __shared__ uint32_t s_wave[kWaves];
-    __shared__ uint32_t s_out[3];
-    if (ws.ctl->status != 0u) return;
-    const int32_t s = blockIdx.x;
+__device__ void select1_segment(const SegWs &ws, int32_t s, uint32_t *s_wave, uint32_t *s_out) {
     const SegInfo inf = ws.info[s];
     SegState *st = ws.st + s;
     if (inf.ntiles <= 1) {  // selected in pass1 (or empty)
@@ -846,7 +915,7 @@ __global__ __launch_bounds__(kBlock) void seg_select1_kernel(SegWs ws) {
     if (inf.k == 0 || inf.k == inf.size) {
         if (threadIdx.x == 0) {
             st->mode = inf.k == 0 ? kModeNone : kModeAll;
-            if (inf.k != 0) atomicAdd(&ws.ctl->pass2, 1u);
+            if (inf.k != 0) ws.ctl->pass2 = 1u;
         }
         return;
     }
@@ -882,20 +951,21 @@ __global__ __launch_bounds__(kBlock) void seg_select1_kernel(SegWs ws) {
                 st->ca = ca;
                 st->ecut = cur.emit;
                 st->tcur = 0u;
-                s_out[0] = atomicAdd(&ws.ctl->nwork, na + nc);
-                atomicAdd(&ws.ctl->bracket, 1u);
             }
-            __syncthreads();
-            const uint32_t base = s_out[0];
-            for (uint32_t q = threadIdx.x; q < na + nc; q += kBlock) {
-                const uint32_t w = base + q;
+            // the items go to the segment's own slots, the rest of them marked
+            // unused: every slot of the list is written every call
+            for (uint32_t q = threadIdx.x; q < inf.wmax; q += kBlock) {
+                const uint32_t w = inf.wbase + q;
                 if (w < ws.work_cap)
                     ws.work[w] = q < na ? make_uint2(uint32_t(s), q * kChunk)
-                                        : make_uint2(uint32_t(s) | 0x80000000u, (q - na) * kChunk);
+                                 : q < na + nc ? make_uint2(uint32_t(s) | 0x80000000u, (q - na) * kChunk)
+                                               : make_uint2(kNoWork, 0u);
             }
             return;
         }
     }
+    for (uint32_t q = threadIdx.x; q < inf.wmax; q += kBlock)
+        if (inf.wbase + q < ws.work_cap) ws.work[inf.wbase + q] = make_uint2(kNoWork, 0u);
     if (cur.bracket) {
         // missed: the radix path follows; the bracket histogram shares the
         // memory pass2 counts in
@@ -907,6 +977,15 @@ __global__ __launch_bounds__(kBlock) void seg_select1_kernel(SegWs ws) {
                        : (int64_t(cur.emit) + cur.ccur < inf.k ? 1u : 3u);
     }
     choose_digit1(ws, s, inf, st, s_wave, s_out);
+}
+
+// One workgroup per segment (a loop over segments per workgroup serialises
+// their latencies: measured slower with thousands of segments).
+__global__ __launch_bounds__(kBlock) void seg_select1_kernel(SegWs ws) {
+    __shared__ uint32_t s_wave[kWaves];
+    __shared__ uint32_t s_out[3];
+    if (ws.ctl->status != 0u) return;
+    select1_segment(ws, int32_t(blockIdx.x), s_wave, s_out);
 }
 
 // ---------------------------------------------------------------------------
@@ -934,7 +1013,7 @@ __device__ void pass2_tiles(float *__restrict__ e, int32_t *__restrict__ idx,
             flush_cand(sg, cfill, st, inf, ws.cand, nofine);
             if (dirty) flush_hist(hist, kDigit2, ws.hist2 + int64_t(s) * kDigit2);
             dirty = false;
-            s = segment_of_tile(ws.tile_prefix, nseg, t);
+            s = segment_after(ws.tile_prefix, nseg, s, t);
             next = ws.tile_prefix[s + 1];
             inf = ws.info[s];
             st = ws.st + s;
@@ -1070,8 +1149,29 @@ __global__ __launch_bounds__(kBlock) void seg_pass2_kernel(float *__restrict__ e
     if (ws.ctl->pass2 != 0u)
         for (uint32_t t0 = blockIdx.x * slice; t0 < T; t0 += gridDim.x * slice)
             pass2_tiles<kAligned>(e, idx, val, nseg, ws, t0, min(T, t0 + slice), hist, sg);
-    const uint32_t nwork = min(ws.ctl->nwork, ws.work_cap);
-    for (uint32_t w = blockIdx.x; w < nwork; w += gridDim.x) bracket_work(ws.work[w], e, idx, val, ws, sg);
+    // work list: workgroup b owns slots b, b + grid, b + 2 grid, ... (a
+    // segment's items are consecutive slots, so they spread over workgroups);
+    // its threads read those slots together, then the workgroup runs the
+    // items in use (select1 writes every slot each call).
+    const uint32_t W = min(ws.ctl->wtotal, ws.work_cap);
+    const uint32_t per = (W + gridDim.x - 1) / gridDim.x;
+    uint2 *list = sg.cand;  // staging is flushed: its candidate area holds the slots in use
+    for (uint32_t r0 = 0; r0 < per; r0 += kBlock) {
+        const uint32_t r = r0 + threadIdx.x;
+        const uint32_t w = blockIdx.x + r * gridDim.x;
+        uint2 item = make_uint2(0u, 0u);
+        bool use = false;
+        if (r < per && w < W) {
+            item = ws.work[w];
+            use = item.x != kNoWork && (item.x & 0x7fffffffu) < uint32_t(nseg);
+        }
+        uint32_t n_use;
+        const uint32_t pos = block_prefix_small(use ? 1u : 0u, sg.wave, n_use);
+        if (use) list[pos] = item;
+        __syncthreads();
+        for (uint32_t q = 0; q < n_use; ++q) bracket_work(list[q], e, idx, val, ws, sg);
+        __syncthreads();  // the list is rewritten by the next round
+    }
 }
 
 // ---------------------------------------------------------------------------
@@ -1229,12 +1329,9 @@ __device__ void final_fast(FinalShared &sh, const SegInfo &inf, const SegState &
                             uint32_t(inf.k) - st.needa, hint, width);
 }
 
-__global__ __launch_bounds__(kBlock) void seg_final_kernel(float *__restrict__ e,
-                                                           int32_t *__restrict__ idx,
-                                                           float *__restrict__ val, SegWs ws) {
-    __shared__ FinalShared sh;
-    if (ws.ctl->status != 0u) return;
-    const int32_t s = blockIdx.x;
+__device__ void final_segment(float *__restrict__ e, int32_t *__restrict__ idx,
+                              float *__restrict__ val, const SegWs &ws, int32_t s,
+                              FinalShared &sh) {
     const SegState st = ws.st[s];
     if (st.mode != kModeCand && st.mode != kModeScan && st.mode != kModeFast) return;
     const SegInfo inf = ws.info[s];
@@ -1291,6 +1388,23 @@ __global__ __launch_bounds__(kBlock) void seg_final_kernel(float *__restrict__ e
     }
 }
 
+// One workgroup per CU at most (the LDS candidate buffer), looping over the
+// segments; most return at once (one tile, none, all, or nothing to rank).
+__global__ __launch_bounds__(kBlock) void seg_final_kernel(float *__restrict__ e,
+                                                           int32_t *__restrict__ idx,
+                                                           float *__restrict__ val, SegWs ws,
+                                                           int32_t nseg) {
+    __shared__ FinalShared sh;
+    if (ws.ctl->status != 0u) return;
+    uint32_t fast = 0;  // segments of this workgroup resolved from the bracket
+    for (int32_t s = blockIdx.x; s < nseg; s += gridDim.x) {
+        __syncthreads();  // LDS of the previous segment is free
+        fast += ws.st[s].mode == kModeFast ? 1u : 0u;
+        final_segment(e, idx, val, ws, s, sh);
+    }
+    if (threadIdx.x == 0 && fast != 0u) atomicAdd(&ws.ctl->bracket, fast);
+}
+
 }  // namespace
 
 size_t topk_segmented_workspace_size(int32_t nseg, int64_t k_total) {
@@ -1319,7 +1433,7 @@ hipError_t launch_topk_segmented(const float *g, float *e, int64_t d, float lr, 
     ws.work_cap = uint32_t(L.work_cap);
 
     const uint32_t zero_grid = persistent_grid(nseg);  // one segment's histograms per pass
-    seg_reset_kernel<<<1 + zero_grid, kBlock, 0, stream>>>(ws, offsets, k, nseg, d, k_total);
+    seg_reset_kernel<<<1 + zero_grid, kResetBlock, 0, stream>>>(ws, offsets, k, nseg, d, k_total);
 
     const int64_t max_tiles = (d + kTile - 1) / kTile + nseg;
     // slices: at least two per workgroup of a full grid, at most kSliceTilesMax tiles
@@ -1336,7 +1450,8 @@ hipError_t launch_topk_segmented(const float *g, float *e, int64_t d, float lr, 
         seg_pass2_kernel<true><<<grid, kBlock, 0, stream>>>(e, idx, val, nseg, ws, uint32_t(slice));
     else
         seg_pass2_kernel<false><<<grid, kBlock, 0, stream>>>(e, idx, val, nseg, ws, uint32_t(slice));
-    seg_final_kernel<<<uint32_t(nseg), kBlock, 0, stream>>>(e, idx, val, ws);
+    seg_final_kernel<<<uint32_t(min(int64_t(nseg), int64_t(device_cu_count()))), kBlock, 0, stream>>>(
+        e, idx, val, ws, nseg);
     return hipGetLastError();
 }
 
