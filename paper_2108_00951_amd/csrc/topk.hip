@@ -63,6 +63,8 @@ constexpr int kFinePerCoarse = int(kFine) / kCoarse;
 constexpr uint32_t kHintMagic = 0x48494e54u;
 constexpr int kStagePairs = 1024;
 constexpr uint32_t kNoKey = 0xffffffffu;            // larger than every 31-bit key
+// pass 1 workgroups per CU (measured: 3 beats 2 and 4 at 25.6e6 and 110e6)
+constexpr int kPass1WorkgroupsPerCU = 3;
 constexpr uint32_t kCandChunkMax = 4096;           // bracket candidates per step-3 work unit, at most
 constexpr uint32_t kStep3Chunks = 512;             // step-3 work units aimed for
 
@@ -791,15 +793,16 @@ hipError_t launch_topk(const float *g, float *e, int64_t d, float lr, int64_t k,
     const uint32_t ntiles = uint32_t((d + kTile - 1) / kTile);
     const uint32_t grid = balanced_grid(ntiles, kScanWorkgroupsPerCU);
     const uint32_t sgrid = balanced_grid(ntiles, kStageWorkgroupsPerCU);
+    const uint32_t pgrid = balanced_grid(ntiles, kPass1WorkgroupsPerCU);
     const Workspace ws = carve(workspace, d, k);
     const uint32_t kk = uint32_t(k);
     const bool vec = ((reinterpret_cast<uintptr_t>(g) | reinterpret_cast<uintptr_t>(e)) & 15u) == 0;
 
     topk_reset_kernel<<<persistent_grid(64), kBlock, 0, stream>>>(ws);
     if (vec)
-        topk_pass1_kernel<true><<<sgrid, kBlock, 0, stream>>>(g, e, d, lr, ntiles, kk, idx, val, ws);
+        topk_pass1_kernel<true><<<pgrid, kBlock, 0, stream>>>(g, e, d, lr, ntiles, kk, idx, val, ws);
     else
-        topk_pass1_kernel<false><<<sgrid, kBlock, 0, stream>>>(g, e, d, lr, ntiles, kk, idx, val, ws);
+        topk_pass1_kernel<false><<<pgrid, kBlock, 0, stream>>>(g, e, d, lr, ntiles, kk, idx, val, ws);
     if (k == 0) return hipGetLastError();
     if (vec) {
         topk_step3_kernel<true><<<grid, kBlock, 0, stream>>>(e, d, ntiles, kk, idx, val, ws);
