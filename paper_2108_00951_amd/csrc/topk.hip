@@ -193,15 +193,30 @@ __device__ __forceinline__ int64_t elem_index(int64_t tile0, int j, int c) {
     return tile0 + int64_t(j * kBlock + int(threadIdx.x)) * 4 + c;
 }
 
+// Inclusive sum of v over the lanes of the wave up to this one.
+__device__ __forceinline__ uint32_t wave_inclusive_sum(uint32_t v) {
+    const int lane = threadIdx.x & (kWave - 1);
+#pragma unroll
+    for (int off = 1; off < kWave; off <<= 1) {
+        const uint32_t o = __shfl_up(v, off);
+        if (lane >= off) v += o;
+    }
+    return v;
+}
+
 // Called by every thread of one workgroup.  Bins are ranked from the top
 // (highest bin first); finds the bin where the running count first reaches
 // `need` (1 <= need <= sum of bins) and writes {bin, count above the bin,
-// count in the bin} to s_out ({0, 0, 0} if no bin qualifies).
+// count in the bin} to s_out ({0, 0, 0} if no bin qualifies).  A wave scan
+// of per-thread sums, then one exchange of wave totals: two barriers.
 template <int kBins>
 __device__ void select_bin(const uint32_t *hist, uint32_t need, uint32_t *s_scan,
                            uint32_t *s_out) {
     constexpr int kPer = kBins / kBlock;
+    static_assert(kPer >= 1 && kBins % kBlock == 0, "whole bins per thread");
     const int t = threadIdx.x;
+    const int lane = t & (kWave - 1);
+    const int wave = t / kWave;
     if (t == 0) {
         s_out[0] = 0u;
         s_out[1] = 0u;
@@ -214,15 +229,13 @@ __device__ void select_bin(const uint32_t *hist, uint32_t need, uint32_t *s_scan
         c[i] = hist[kBins - 1 - (t * kPer + i)];
         tot += c[i];
     }
-    s_scan[t] = tot;
+    const uint32_t incl_w = wave_inclusive_sum(tot);
+    if (lane == kWave - 1) s_scan[wave] = incl_w;
     __syncthreads();
-    for (int off = 1; off < kBlock; off <<= 1) {
-        const uint32_t add = t >= off ? s_scan[t - off] : 0u;
-        __syncthreads();
-        s_scan[t] += add;
-        __syncthreads();
-    }
-    const uint32_t incl = s_scan[t];
+    uint32_t off = 0;
+#pragma unroll
+    for (int q = 0; q < kWaves; ++q) off += q < wave ? s_scan[q] : 0u;
+    const uint32_t incl = off + incl_w;
     const uint32_t excl = incl - tot;
     if (excl < need && incl >= need) {
         uint32_t run = excl;
