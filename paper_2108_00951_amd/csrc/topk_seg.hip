@@ -83,7 +83,7 @@ constexpr uint32_t kChunk = 2048;              // pass2 work item: payload slots
 // faster than one long range per workgroup), and a slice is long enough to
 // amortise its flushes.
 constexpr int64_t kSliceTilesMax = 4;
-constexpr int kSliceWorkgroupsPerCU = 4;
+constexpr int kSliceWorkgroupsPerCU = 8;
 constexpr uint32_t kNoBin = 0xffffffffu;
 constexpr uint32_t kNoWork = 0xffffffffu;      // work-list slot not in use this call
 static_assert(kFineBins == kDigit2, "the bracket histogram lives in a segment's second histogram");
@@ -1436,9 +1436,10 @@ hipError_t launch_topk_segmented(const float *g, float *e, int64_t d, float lr, 
     seg_reset_kernel<<<1 + zero_grid, kResetBlock, 0, stream>>>(ws, offsets, k, nseg, d, k_total);
 
     const int64_t max_tiles = (d + kTile - 1) / kTile + nseg;
-    // slices: at least two per workgroup of a full grid, at most kSliceTilesMax tiles
+    // slices: the tiles spread over kSliceWorkgroupsPerCU workgroups per CU
+    // (4 resident), at most kSliceTilesMax tiles each
     const int64_t wgs = int64_t(device_cu_count()) * kSliceWorkgroupsPerCU;
-    const int64_t slice = max(int64_t(1), min(kSliceTilesMax, max_tiles / (2 * wgs)));
+    const int64_t slice = max(int64_t(1), min(kSliceTilesMax, (max_tiles + wgs - 1) / wgs));
     const uint32_t grid = uint32_t(min(wgs, (max_tiles + slice - 1) / slice));
     const bool aligned = ((reinterpret_cast<uintptr_t>(g) | reinterpret_cast<uintptr_t>(e)) & 15) == 0;
     if (aligned)
