@@ -6,7 +6,9 @@
 //            (i, v) of that payload.  Indices are distinct within a payload,
 //            so no two lanes of one launch touch the same coordinate and no
 //            atomics are needed; stream order between launches fixes the
-//            summation order, so the result is the same on every run.
+//            summation order, so the result is the same on every run.  The
+//            first launch knows out[i] is +0 and stores +0 + v without
+//            reading it.
 //   scale    out = out / n (IEEE division), skipped for n == 1.
 //
 // Also the streaming copy probe used to measure the bandwidth ceiling.
@@ -27,6 +29,7 @@ __global__ __launch_bounds__(kBlock) void fill_zero_kernel(float *__restrict__ o
     if (blockIdx.x == 0 && t < d) out[t] = 0.0f;
 }
 
+template <bool kFirst>
 __global__ __launch_bounds__(kBlock) void scatter_add_kernel(const int32_t *__restrict__ idx,
                                                              const float *__restrict__ val,
                                                              const uint32_t *__restrict__ count,
@@ -37,7 +40,8 @@ __global__ __launch_bounds__(kBlock) void scatter_add_kernel(const int32_t *__re
     const int64_t stride = int64_t(gridDim.x) * kBlock;
     for (int64_t j = int64_t(blockIdx.x) * kBlock + threadIdx.x; j < n; j += stride) {
         const int32_t i = idx[j];
-        if (i >= 0 && int64_t(i) < d) out[i] = __fadd_rn(out[i], val[j]);
+        if (i >= 0 && int64_t(i) < d)
+            out[i] = __fadd_rn(kFirst ? 0.0f : out[i], val[j]);
     }
 }
 
@@ -127,12 +131,17 @@ hipError_t launch_accumulate(const int32_t *const *idx, const float *const *val,
     // aligned by the ABI layer.
     const uint32_t dense_grid = stream_grid(d / 4 + 1);
     fill_zero_kernel<<<dense_grid, kBlock, 0, stream>>>(out, d);
+    bool first = true;
     for (int32_t w = 0; w < n; ++w) {
         const int64_t cap = caps[w];
         if (cap <= 0) continue;
         const uint32_t grid = persistent_grid((cap + kTile - 1) / kTile);
         const uint32_t *cnt = counts != nullptr ? counts[w] : nullptr;
-        scatter_add_kernel<<<grid, kBlock, 0, stream>>>(idx[w], val[w], cnt, cap, d, out);
+        if (first)
+            scatter_add_kernel<true><<<grid, kBlock, 0, stream>>>(idx[w], val[w], cnt, cap, d, out);
+        else
+            scatter_add_kernel<false><<<grid, kBlock, 0, stream>>>(idx[w], val[w], cnt, cap, d, out);
+        first = false;
     }
     if (n > 1) scale_kernel<<<dense_grid, kBlock, 0, stream>>>(out, d, float(n));
     return hipGetLastError();
