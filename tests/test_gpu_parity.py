@@ -391,6 +391,23 @@ def test_topk_bracket_path_splits_ties(levels):
     assert st.bracket()
 
 
+def test_topk_bracket_with_many_candidates():
+    # |p| uniform in [0.9, 1.1]: the bracket around the previous threshold
+    # (the 90th percentile) holds ~40 % of the vector, so the bracket path
+    # moves its candidates several per thread per chunk
+    d, k = 1 << 20, 100_000
+    st = TopkState(d, k)
+    rng = np.random.default_rng(150)
+    for t in range(2):
+        g = (rng.uniform(9.0, 11.0, size=d) * rng.choice([-1.0, 1.0], size=d)).astype(np.float32)
+        e = np.zeros(d, np.float32)
+        gi, gv, ge = st.step(g, k, e)
+        ri, rv, re = oracle.topk(g, e, LR, k)
+        assert_payload_equal(gi, gv, ri, rv, "call %d" % t)
+        assert_bits_equal(ge, re, "call %d" % t)
+    assert st.bracket()
+
+
 def test_topk_workspace_contents_do_not_matter():
     d, k = 200_003, 1500
     g = synth.small_gradient(77, d)
