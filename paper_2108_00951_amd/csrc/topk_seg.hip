@@ -69,8 +69,9 @@ enum : uint32_t {
     kModeDone = 5  // a segment within one tile, selected entirely in pass1
 };
 
-// bracket = prediction -/+ 2^w keys, w adapted per segment between these
-// (2^19 keys is about 4.6 % in |p|, 2^12 about 0.05 %)
+// log2 of how far the bracket reaches below and above the predicted
+// threshold, each adapted per segment between these (2^19 keys are 3-6 % of
+// |p|, 2^12 keys 0.02-0.05 %)
 constexpr uint32_t kWidthMax = 19, kWidthMin = 12, kWidthStart = 17;
 // cap on the extrapolated step, in keys: wide when the last two steps agree
 // (a steady drift), narrow otherwise (a jump is not repeated)
@@ -123,8 +124,9 @@ struct SegState {
 };
 static_assert(sizeof(SegState) == 64, "segment state is 64 bytes");
 
-// Threshold of the last call on this workspace, kept across calls (the
-// reset does not touch it); it only decides the bracket, never a result.
+// Thresholds of the last calls on this workspace and the bracket widths,
+// kept across calls (the reset only reads them); they decide the bracket,
+// never a result.
 struct SegHint {
     uint32_t key, prev, prev2;  // the last three thresholds
     uint32_t magic, width;      // validity; bracket widths (packed, see below)
@@ -879,7 +881,7 @@ __global__ __launch_bounds__(kBlock) void seg_pass1_kernel(const float *__restri
 }
 
 // ---------------------------------------------------------------------------
-// select1: per segment, the digit of the k-th key and the mode
+// select1: per segment, the bracket bin or the digit of the k-th key, and the mode
 // ---------------------------------------------------------------------------
 
 // Radix path of segment s (0 < k < size): from its digit-1 histogram, the
@@ -989,7 +991,8 @@ __global__ __launch_bounds__(kBlock) void seg_select1_kernel(SegWs ws) {
 }
 
 // ---------------------------------------------------------------------------
-// pass2: keys above D1 to the payload, keys in D1 to the candidates
+// pass2: keys above D1 to the payload, keys in D1 to the candidates; the
+// bracket path's work items
 // ---------------------------------------------------------------------------
 
 // The radix path's sweep over tiles [t0, t1).
@@ -1175,7 +1178,7 @@ __global__ __launch_bounds__(kBlock) void seg_pass2_kernel(float *__restrict__ e
 }
 
 // ---------------------------------------------------------------------------
-// final: exact selection inside D1 for each segment
+// final: each segment's exact threshold, its ties, the last pairs
 // ---------------------------------------------------------------------------
 
 struct FinalShared {
