@@ -358,8 +358,12 @@ __device__ __forceinline__ TileRange tile_range(const SegInfo &inf, uint32_t t) 
 constexpr int kResetBlock = 512;
 constexpr int kResetWaves = kResetBlock / kWave;
 
+// Tiles and work-list slots stay far below 2^32 for any accepted layout
+// (sizes >= 0 summing to d < 2^31); a layout breaking that is rejected by
+// its per-segment checks, whatever its sums.
 struct Sums {
-    int64_t k, c, t, w;  // pairs, candidate slots, tiles, work-list slots
+    int64_t k, c;   // pairs, candidate slots
+    uint32_t t, w;  // tiles, work-list slots
 };
 
 // Exclusive prefix of v over the workgroup's threads in order; `total` gets
@@ -367,11 +371,11 @@ struct Sums {
 __device__ __forceinline__ Sums reset_scan(Sums v, Sums *s_wave, Sums &total) {
     const int lane = threadIdx.x & (kWave - 1);
     const int wave = threadIdx.x / kWave;
-    const Sums incl = {wave_incl_i64(v.k), wave_incl_i64(v.c), wave_incl_i64(v.t),
-                       wave_incl_i64(v.w)};
+    const Sums incl = {wave_incl_i64(v.k), wave_incl_i64(v.c), wave_incl_u32(v.t),
+                       wave_incl_u32(v.w)};
     if (lane == kWave - 1) s_wave[wave] = incl;
     __syncthreads();
-    Sums off = {0, 0, 0, 0}, tot = {0, 0, 0, 0};
+    Sums off = {0, 0, 0u, 0u}, tot = {0, 0, 0u, 0u};
 #pragma unroll
     for (int q = 0; q < kResetWaves; ++q) {
         const Sums x = s_wave[q];
@@ -392,20 +396,18 @@ __device__ __forceinline__ Sums reset_scan(Sums v, Sums *s_wave, Sums &total) {
                 off.w + incl.w - v.w};
 }
 
-// What the reset reads of one segment.
+// What the reset reads of one segment's layout.
 struct SegIn {
     int64_t lo, hi, k;
-    SegHint h;
 };
 
-__device__ __forceinline__ SegIn load_seg(const int64_t *off, const int64_t *kin,
-                                          const SegHint *hint, int32_t s, int32_t nseg) {
+__device__ __forceinline__ SegIn load_seg(const int64_t *off, const int64_t *kin, int32_t s,
+                                          int32_t nseg) {
     SegIn in = {};
     if (s < nseg) {
         in.lo = off[s];
         in.hi = off[s + 1];
         in.k = kin[s];
-        in.h = hint[s];
     }
     return in;
 }
@@ -437,14 +439,16 @@ __global__ __launch_bounds__(kResetBlock) void seg_reset_kernel(SegWs ws,
     if (t == 0) s_bad = 0u;
     __syncthreads();
     bool bad = false;
-    Sums carry = {0, 0, 0, 0};
+    Sums carry = {0, 0, 0u, 0u};
     // the tables are written as the chunks go; a rejected layout leaves them
     // meaningless, and every later kernel then returns at once
-    SegIn nxt = load_seg(off, kin, ws.hint, t, nseg);
+    SegIn nxt = load_seg(off, kin, t, nseg);
     for (int32_t c0 = 0; c0 < nseg; c0 += kResetBlock) {
         const int32_t s = c0 + t;
         const SegIn in = nxt;
-        nxt = load_seg(off, kin, ws.hint, s + kResetBlock, nseg);  // next chunk, in flight
+        nxt = load_seg(off, kin, s + kResetBlock, nseg);  // next chunk, in flight
+        SegHint h = {};
+        if (s < nseg) h = ws.hint[s];  // used after the scan
         const int64_t size = in.hi - in.lo;
         int64_t keff = 0, ccap = 0, wmax = 0;
         uint32_t nt = 0u;
@@ -460,7 +464,7 @@ __global__ __launch_bounds__(kResetBlock) void seg_reset_kernel(SegWs ws,
             }
         }
         Sums tot;
-        const Sums ex = reset_scan(Sums{keff, ccap, int64_t(nt), wmax}, s_wave, tot);
+        const Sums ex = reset_scan(Sums{keff, ccap, nt, uint32_t(wmax)}, s_wave, tot);
         if (s < nseg) {
             SegInfo inf;
             inf.off = in.lo;
@@ -476,7 +480,6 @@ __global__ __launch_bounds__(kResetBlock) void seg_reset_kernel(SegWs ws,
             ws.info[s] = inf;
             ws.tile_prefix[s] = uint32_t(carry.t + ex.t);
             SegState z = {};
-            const SegHint h = in.h;
             if (nt > 1u && keff > 0 && keff < size && h.magic == kHintMagic && h.key <= 0x7fffffffu &&
                 h.prev <= 0x7fffffffu && h.prev2 <= 0x7fffffffu && widths_ok(h.width)) {
                 // last threshold plus the last step (capped): error feedback
@@ -507,14 +510,14 @@ __global__ __launch_bounds__(kResetBlock) void seg_reset_kernel(SegWs ws,
     if (bad) atomicOr(&s_bad, 1u);
     __syncthreads();
     const bool reject = s_bad != 0u || carry.k > k_total || carry.c > ws.ccap_total ||
-                        carry.t > int64_t(UINT32_MAX) || carry.w > int64_t(ws.work_cap);
+                        carry.w > ws.work_cap;
     if (t == 0) {
         ws.ctl->bracket = 0u;
         ws.ctl->pass2 = 0u;
-        ws.ctl->wtotal = reject ? 0u : uint32_t(carry.w);
+        ws.ctl->wtotal = reject ? 0u : carry.w;
         ws.ctl->status = reject ? 1u : 0u;
-        ws.ctl->tiles = reject ? 0u : uint32_t(carry.t);
-        if (!reject) ws.tile_prefix[nseg] = uint32_t(carry.t);
+        ws.ctl->tiles = reject ? 0u : carry.t;
+        if (!reject) ws.tile_prefix[nseg] = carry.t;
     }
 }
 
