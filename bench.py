@@ -27,6 +27,7 @@ import csv
 import glob
 import json
 import os
+import re
 import sys
 import time
 
@@ -79,6 +80,11 @@ def parse():
                     help="steps of the CPU oracle for the baseline (0 to skip)")
     ap.add_argument("--traffic", type=str, default=TRAFFIC_FILE,
                     help="summary written by --parse-pmc (HBM bytes per hard-threshold launch)")
+    ap.add_argument("--parse-trace", metavar="TRACE_DIR",
+                    help="print the kernel statistics of a rocprofv3 --kernel-trace --stats "
+                         "run of this script (run_kernel_stats.csv, run_kernel_trace.csv), "
+                         "with the average of the back-to-back hard-threshold launches that "
+                         "roofline.launch_us times")
     ap.add_argument("--parse-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
                     help="summarise two rocprofv3 --pmc output folders and exit")
     ap.add_argument("--no-apply", action="store_true",
@@ -123,6 +129,52 @@ def parse_pmc(fetch_dir, write_dir, d):
     return out
 
 
+def _short_kernel_name(name):
+    name = name.replace("efs::(anonymous namespace)::", "").replace("efs::", "")
+    name = name.replace("void ", "")
+    return re.sub(r"\(.*", "", name)[:34]
+
+
+def parse_trace(folder, b2b):
+    """Per-kernel statistics of a rocprofv3 kernel trace, and the average of
+    the `b2b` consecutive dispatches of the hard-threshold kernel (its plain
+    variant) that no other kernel interrupts: the launches roofline.launch_us
+    times with HIP events."""
+    import csv
+    stats = list(csv.DictReader(open(os.path.join(folder, "run_kernel_stats.csv"))))
+    trace = list(csv.DictReader(open(os.path.join(folder, "run_kernel_trace.csv"))))
+    trace.sort(key=lambda r: int(r["Start_Timestamp"]))
+    total = sum(float(r["TotalDurationNs"]) for r in stats)
+    lines = ["%-36s %6s %9s %9s %9s %7s" % ("kernel", "calls", "avg_us", "min_us", "max_us", "pct")]
+    for r in sorted(stats, key=lambda r: -float(r["TotalDurationNs"])):
+        if float(r["TotalDurationNs"]) / total < 0.0005:
+            continue
+        lines.append("%-36s %6s %9.2f %9.2f %9.2f %7.2f" % (
+            _short_kernel_name(r["Name"]), r["Calls"], float(r["AverageNs"]) / 1e3,
+            float(r["MinNs"]) / 1e3, float(r["MaxNs"]) / 1e3,
+            100 * float(r["TotalDurationNs"]) / total))
+    plain = HT_KERNEL + "<true, false>"
+    runs, cur = [], []
+    for r in trace:
+        if plain in r["Kernel_Name"]:
+            cur.append((int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3)
+        else:
+            if cur:
+                runs.append(cur)
+            cur = []
+    if cur:
+        runs.append(cur)
+    b2b_runs = [x for x in runs if len(x) == b2b]
+    lines.append("")
+    if b2b_runs:
+        x = b2b_runs[0]
+        lines.append("# %s, the %d back-to-back launches timed for roofline.launch_us: "
+                     "avg %.2f us, min %.2f, max %.2f" % (plain, b2b, sum(x) / len(x), min(x), max(x)))
+    else:
+        lines.append("# no run of %d back-to-back %s dispatches in the trace" % (b2b, plain))
+    return "\n".join(lines) + "\n"
+
+
 def format_traffic(res):
     lines = ["# HBM traffic of %s per launch from rocprofv3 counters" % HT_KERNEL,
              "# (KiB per dispatch, averaged over the kernel's dispatches; each counter",
@@ -152,6 +204,9 @@ def main():
     d, k, density = wl.d, wl.topk_k[0], wl.densities[0]
     if args.parse_pmc:
         sys.stdout.write(format_traffic(parse_pmc(args.parse_pmc[0], args.parse_pmc[1], d)))
+        return
+    if args.parse_trace:
+        sys.stdout.write(parse_trace(args.parse_trace, args.b2b))
         return
 
     import torch
