@@ -319,7 +319,8 @@ def prepare_sparse_apply(payloads: Sequence[Tuple], d: int, mode: int, x, worksp
                          beta: float = 0.0, gamma: float = 0.0, stream=None):
     """Marshal the arguments of sparse_apply once and return a callable that
     issues the call with them (for loops that repeat the same call on the
-    same buffers: the per-call cost is then one C call)."""
+    same buffers: the per-call cost is then one C call).  The stream is fixed
+    here too: `stream`, else the current stream at this call."""
     import torch
     lib = load_library()
     _require(x, torch.float32, "x")
