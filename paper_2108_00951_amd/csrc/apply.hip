@@ -23,6 +23,11 @@
 //
 // Indices are distinct within a payload, so no two lanes adding one
 // worker's pairs touch the same LDS word; a barrier separates workers.
+//
+// With one worker the sum is a single term, so grouping buys nothing: the
+// average is the plain fill-and-scatter of sparse_accumulate, and the SGD
+// update one scatter x[i] = x[i] - (+0 + v) over the payload (the same bits:
+// the sum starts from +0 and the division by 1 is exact).
 #include "device_common.hpp"
 #include "launch.hpp"
 
@@ -334,6 +339,22 @@ __global__ __launch_bounds__(kBlock) void apply_range_kernel(const uint32_t *__r
     }
 }
 
+// One worker's SGD update: x[i] -= (+0 + v) for each pair (i, v); indices
+// outside [0, d) are ignored, as everywhere.
+__global__ __launch_bounds__(kBlock) void apply_sgd_one_kernel(const int32_t *__restrict__ idx,
+                                                               const float *__restrict__ val,
+                                                               const uint32_t *__restrict__ count,
+                                                               int64_t cap, int64_t d,
+                                                               float *__restrict__ x) {
+    int64_t n = cap;
+    if (count != nullptr) n = min(int64_t(*count), cap);
+    const int64_t stride = int64_t(gridDim.x) * kBlock;
+    for (int64_t j = int64_t(blockIdx.x) * kBlock + threadIdx.x; j < n; j += stride) {
+        const int32_t i = idx[j];
+        if (i >= 0 && int64_t(i) < d) x[i] = __fsub_rn(x[i], __fadd_rn(0.0f, val[j]));
+    }
+}
+
 }  // namespace
 
 size_t apply_workspace_size(int32_t n, int64_t d, int64_t total_cap) {
@@ -345,6 +366,15 @@ hipError_t launch_apply(const int32_t *const *idx, const float *const *val,
                         int64_t d, int mode, float *x, float *m, float beta, float gamma,
                         void *workspace, hipStream_t stream) {
     if (d == 0) return hipSuccess;
+    if (n == 1 && mode == 0) return launch_accumulate(idx, val, counts, caps, 1, d, x, stream);
+    if (n == 1 && mode == 1) {
+        if (caps[0] > 0) {
+            const uint32_t grid = persistent_grid((caps[0] + kTile - 1) / kTile);
+            apply_sgd_one_kernel<<<grid, kBlock, 0, stream>>>(
+                idx[0], val[0], counts != nullptr ? counts[0] : nullptr, caps[0], d, x);
+        }
+        return hipGetLastError();
+    }
     Payloads p{};
     int64_t total = 0, max_cap = 0;
     for (int32_t w = 0; w < n; ++w) {

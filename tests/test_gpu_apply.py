@@ -175,6 +175,30 @@ def test_apply_ignores_out_of_range_indices():
     check_all_modes(p_dev, p_ref, d, 9)
 
 
+def test_apply_one_worker_signed_zeros():
+    # one worker: x - (+0 + v), never x - v (they differ for x = -0, v = -0),
+    # and out-of-range indices ignored
+    d = 9000
+    idx = np.array([0, 1, 2, 3, 4, -5, 9000, 8191, 8192], dtype=np.int32)
+    val = np.array([-0.0, 0.0, -1e-45, 2e-39, -0.0, 1.0, 2.0, 3.5, -0.0], dtype=np.float32)
+    keep = (idx >= 0) & (idx < d)
+    x0, m0 = host_state(d, 21)
+    x0[4] = np.float32(-0.0)
+    x0[8192] = np.float32(-0.0)
+    p_dev = [(dev(idx), dev(val))]
+    p_ref = [(idx[keep], val[keep])]
+    got, _ = run_apply(p_dev, d, efs.APPLY_SGD, x0)
+    want, _ = oracle.update(p_ref, x0, 1)
+    assert_bits_equal(got, want)
+    assert got[4].view(np.uint32) == np.float32(-0.0).view(np.uint32)
+    got, _ = run_apply(p_dev, d, efs.APPLY_AVERAGE, np.full(d, 7.0, np.float32))
+    assert_bits_equal(got, oracle.accumulate(p_ref, d))
+    got_x, got_m = run_apply(p_dev, d, efs.APPLY_MOMENTUM, x0, m0)
+    want_x, want_m = oracle.update(p_ref, x0, 2, m=m0, beta=BETA, gamma=GAMMA)
+    assert_bits_equal(got_m, want_m)
+    assert_bits_equal(got_x, want_x)
+
+
 def test_apply_count_larger_than_capacity():
     # a counter above the capacity (an overflowed payload) uses caps[w] pairs
     d = 20_000
