@@ -132,6 +132,41 @@ def _check_segments(acc, bounds, ks, gi, gv, e_next):
         pos += n
 
 
+def _bracket_eligible(bounds, ks):
+    """Segments that can select from a bracket: more than one 4096-element
+    tile and 0 < k < size."""
+    lo, hi = np.asarray(bounds[:-1], np.int64), np.asarray(bounds[1:], np.int64)
+    size = hi - lo
+    tiles = np.where(size > 0, (hi - 1) // 4096 - lo // 4096 + 1, 0)
+    return int(np.sum((tiles > 1) & (ks > 0) & (ks < size)))
+
+
+def _repeat_from_the_bracket(g_dev, b, ks, bounds):
+    """Runs the call of `b` again from e = 0 on the same workspace: the
+    threshold of each segment is the one the last call recorded, so the
+    segments select from the bracket; the result must equal the last call's
+    bit for bit (results never depend on the path)."""
+    first_i, first_v, first_e = (b["idx"].cpu().numpy(), b["val"].cpu().numpy(),
+                                 b["e"].cpu().numpy())
+    b["e"].zero_()
+    efs.topk_segmented_compress(g_dev, b["e"], LR, b["off"], b["k"], b["idx"], b["val"], b["ws"])
+    assert efs.topk_segmented_status(b["ws"]) == 0
+    hits = efs.topk_segmented_bracket_segments(b["ws"])
+    gi, gv, ge = b["idx"].cpu().numpy(), b["val"].cpu().numpy(), b["e"].cpu().numpy()
+    pos = 0
+    for s in range(len(ks)):
+        n = int(ks[s])
+        o1, o2 = np.argsort(first_i[pos:pos + n]), np.argsort(gi[pos:pos + n])
+        np.testing.assert_array_equal(gi[pos:pos + n][o2], first_i[pos:pos + n][o1],
+                                      "segment %d" % s)
+        assert_bits_equal(gv[pos:pos + n][o2], first_v[pos:pos + n][o1], "segment %d" % s)
+        pos += n
+    assert_bits_equal(ge, first_e, "e' from the bracket")
+    eligible = _bracket_eligible(bounds, ks)
+    say("  repeated from the bracket: %d of %d eligible segments" % (hits, eligible))
+    assert hits >= 0.9 * eligible
+
+
 def test_workload2_layerwise_topk():
     # layer-wise Top-k over the 161 segments, k_s = ceil(0.1 % of d_s), e
     # carried for three steps: the oracle at t = 0 and 1, properties after
@@ -157,8 +192,11 @@ def test_workload2_layerwise_topk():
                 pos += n
             assert_bits_equal(ge, re, "layer-wise e' t=%d" % t)
         _check_segments(acc, st.bounds, ks, gi, gv, ge)
-        e_ref = ge
         say("workload 2 layer-wise t=%d: %d pairs in %d segments ok" % (t, ks.sum(), ks.size))
+        if t == 0:
+            # the oracle-checked first call, repeated from the bracket
+            _repeat_from_the_bracket(torch.from_numpy(g).to(DEV), b, ks, st.bounds)
+        e_ref = b["e"].cpu().numpy()
 
 
 def test_workload3_layerwise_topk():
@@ -177,6 +215,7 @@ def test_workload3_layerwise_topk():
         _check_segments(acc, st.bounds, ks, b["idx"].cpu().numpy(), b["val"].cpu().numpy(),
                         b["e"].cpu().numpy())
         say("workload 3 layer-wise rho=%g: %d pairs ok" % (rho, ks.sum()))
+        _repeat_from_the_bracket(g_dev, b, ks, st.bounds)
         del b
         torch.cuda.empty_cache()
 
