@@ -33,6 +33,22 @@ def say(*a):
     print("[%6.1fs]" % (time.time() - T0), *a, flush=True)
 
 
+def _repeat_topk_from_the_bracket(tk, g_dev, k):
+    """Repeats the last Top-k call of `tk` from e = 0 on the same workspace
+    (its threshold is recorded there, so the call selects from the bracket)
+    and checks the result equals the last call's bit for bit."""
+    first_i, first_v = tk.payload(k)
+    first_e = tk.e.cpu().numpy()
+    tk.e.zero_()
+    tk.topk(g_dev, k)
+    assert efs.topk_took_bracket_path(tk.ws)
+    gi, gv = tk.payload(k)
+    o1, o2 = np.argsort(first_i), np.argsort(gi)
+    np.testing.assert_array_equal(gi[o2], first_i[o1])
+    assert_bits_equal(gv[o2], first_v[o1], "values from the bracket")
+    assert_bits_equal(tk.e.cpu().numpy(), first_e, "e' from the bracket")
+
+
 class Worker:
     """Hard-threshold and Top-k EF state of one worker on the device."""
 
@@ -109,6 +125,7 @@ def test_workload2_segments_25m():
             ri, rv, re = oracle.topk(g, np.zeros(w.d, np.float32), LR, k)
             assert_payload_equal(gi, gv, ri, rv, "topk t=0 vs oracle")
             assert_bits_equal(e_tk, re, "topk e' t=0")
+            _repeat_topk_from_the_bracket(tk, g_dev, k)
         check_topk_properties(acc, k, gi, gv, e_tk)
         say("workload 2 t=%d: ht k_t=%d, topk ok" % (t, n))
 
@@ -241,6 +258,7 @@ def test_workload3_student_t_110m():
         acc = oracle.ht(gs[0], np.zeros(w.d, np.float32), LR, np.inf)[2]
         tk.topk(g_devs[0], k)
         check_topk_properties(acc, k, *tk.payload(k), tk.e.cpu().numpy())
+        _repeat_topk_from_the_bracket(tk, g_devs[0], k)
         del tk, acc
         say("workload 3 rho=%g: ht k_t=%d, topk k=%d ok" % (density, n, k))
 
