@@ -374,3 +374,46 @@ def test_segmented_many_small_layers(levels):
     ks = np.ceil(sizes * rng.uniform(0.0, 1.2, size=sizes.size)).astype(np.int64)
     say("segmented many small layers levels=%d d=%d" % (levels, d))
     check(g, e, off, ks, lr=np.float32(1.0), what="small layers")
+
+
+@pytest.mark.parametrize("seed", range(8))
+def test_segmented_randomised_ef_loops(seed):
+    # random layouts (empty, one-tile and multi-tile layers), random budgets,
+    # six EF steps on one workspace with the gradient scale sometimes jumping
+    # and some steps quantised (heavy ties): every step against the oracle,
+    # whichever path each layer takes
+    rng = np.random.default_rng(900 + seed)
+    d = int(rng.integers(20_000, 300_000))
+    nseg = int(rng.integers(1, 80))
+    off = random_layout(rng, d, nseg)
+    sizes = np.diff(off)
+    ks = np.ceil(sizes * 10.0 ** rng.uniform(-3.0, -0.3, size=nseg)).astype(np.int64)
+    ks[rng.random(nseg) < 0.1] = 0
+    ks[rng.random(nseg) < 0.05] = 10 ** 9  # more than the layer holds: all kept
+    k_total = int(np.minimum(ks, sizes).sum())
+    ws = efs.new_topk_segmented_workspace(nseg, k_total, DEV)
+    ws.zero_()
+    e = np.zeros(d, np.float32)
+    hits = []
+    say("segmented randomised seed=%d d=%d nseg=%d" % (seed, d, nseg))
+    for t in range(6):
+        scale = np.float32(10.0 ** rng.choice([0.0, 0.0, 0.0, 1.5, -1.0]))
+        g = (synth.small_gradient(910 + 10 * seed + t, d) * scale).astype(np.float32)
+        if rng.random() < 0.3:
+            g = (np.round(g / np.float32(2e-3)) * np.float32(2e-3)).astype(np.float32)
+        gi, gv, ge, _ = run_gpu(g, e, off, ks, k_total=k_total, ws=ws)
+        assert efs.topk_segmented_status(ws) == 0
+        ri, rv, re = oracle.topk_segmented(g, e, LR, off, ks)
+        pos = 0
+        for s in range(nseg):
+            n = int(min(ks[s], sizes[s]))
+            o = np.argsort(gi[pos:pos + n], kind="stable")
+            np.testing.assert_array_equal(gi[pos:pos + n][o], ri[pos:pos + n],
+                                          "seed %d t=%d segment %d" % (seed, t, s))
+            assert_bits_equal(gv[pos:pos + n][o], rv[pos:pos + n],
+                              "seed %d t=%d segment %d" % (seed, t, s))
+            pos += n
+        assert_bits_equal(ge, re, "seed %d t=%d e'" % (seed, t))
+        hits.append(efs.topk_segmented_bracket_segments(ws))
+        e = re
+    say("  bracket segments per step: %s" % hits)
