@@ -408,6 +408,30 @@ def test_topk_bracket_with_many_candidates():
     assert st.bracket()
 
 
+@pytest.mark.parametrize("seed", range(6))
+def test_topk_randomised_ef_loops(seed):
+    # random size and k, six EF steps on one workspace with scale jumps and
+    # quantised steps: every step against the oracle, whichever path it takes
+    rng = np.random.default_rng(950 + seed)
+    d = int(rng.integers(10_000, 400_000))
+    k = int(np.ceil(d * 10.0 ** rng.uniform(-3.5, -0.5)))
+    st = TopkState(d, k)
+    e = np.zeros(d, np.float32)
+    paths = []
+    for t in range(6):
+        scale = np.float32(10.0 ** rng.choice([0.0, 0.0, 0.0, 1.5, -1.0]))
+        g = (synth.small_gradient(960 + 10 * seed + t, d) * scale).astype(np.float32)
+        if rng.random() < 0.3:
+            g = (np.round(g / np.float32(2e-3)) * np.float32(2e-3)).astype(np.float32)
+        gi, gv, ge = st.step(g, k, e)
+        ri, rv, re = oracle.topk(g, e, LR, k)
+        assert_payload_equal(gi, gv, ri, rv, "seed %d t=%d" % (seed, t))
+        assert_bits_equal(ge, re, "seed %d t=%d e'" % (seed, t))
+        paths.append(int(st.bracket()))
+        e = re
+    say("topk randomised seed=%d d=%d k=%d: bracket path per step %s" % (seed, d, k, paths))
+
+
 def test_topk_workspace_contents_do_not_matter():
     d, k = 200_003, 1500
     g = synth.small_gradient(77, d)
