@@ -229,29 +229,10 @@ __device__ __forceinline__ int64_t wave_incl_i64(int64_t v) {
     return v;
 }
 
-// Exclusive prefix of v over the workgroup's threads in order; `total` gets
-// the sum.  Uses kWaves int64 of LDS; two barriers.
-__device__ __forceinline__ int64_t block_excl_i64(int64_t v, int64_t *s_wave, int64_t &total) {
-    const int lane = threadIdx.x & (kWave - 1);
-    const int wave = threadIdx.x / kWave;
-    const int64_t incl = wave_incl_i64(v);
-    if (lane == kWave - 1) s_wave[wave] = incl;
-    __syncthreads();
-    int64_t off = 0, tot = 0;
-#pragma unroll
-    for (int q = 0; q < kWaves; ++q) {
-        off += q < wave ? s_wave[q] : 0;
-        tot += s_wave[q];
-    }
-    __syncthreads();
-    total = tot;
-    return off + incl - v;
-}
-
-// In a histogram of kBins bins (LDS), ranked from the top (kFromTop) or from
-// the bottom, the bin where the running count first reaches `need`
-// (1 <= need <= sum).  s_out gets {bin, count before the bin, count in the
-// bin}; {0, 0, 0} when no bin qualifies.  Three barriers.
+// In a histogram of kBins bins (LDS or global), ranked from the top
+// (kFromTop) or from the bottom, the bin where the running count first
+// reaches `need` (1 <= need <= sum).  s_out gets {bin, count before the bin,
+// count in the bin}; {0, 0, 0} when no bin qualifies.  Two barriers.
 template <int kBins, bool kFromTop>
 __device__ void pick_bin(const uint32_t *hist, uint32_t need, uint32_t *s_wave, uint32_t *s_out) {
     constexpr int kPer = kBins / kBlock;
