@@ -17,7 +17,10 @@ from a second pass over the same steps with events between the operations.
 
 The roofline entry is for the hard-threshold kernel: algorithmic bytes
 (12 per element + 8 per kept pair) over its launch duration, from HIP events
-around back-to-back launches.  --traffic takes the counter-derived HBM
+around back-to-back launches on four error-feedback states taken in turn, so
+that g and e come from HBM as they do inside the step (ops also reports one
+state carried from launch to launch, where part of e stays in the Infinity
+Cache, and launches after a cache flush).  --traffic takes the counter-derived HBM
 bytes per launch written by --parse-pmc from two rocprofv3 --pmc runs of this
 script (FETCH_SIZE, then WRITE_SIZE), scaled by what the same counters read
 for the copy probe of known size.
@@ -137,9 +140,9 @@ def _short_kernel_name(name):
 
 def parse_trace(folder, b2b):
     """Per-kernel statistics of a rocprofv3 kernel trace, and the average of
-    the `b2b` consecutive dispatches of the hard-threshold kernel (its plain
-    variant) that no other kernel interrupts: the launches roofline.launch_us
-    times with HIP events."""
+    the first `b2b` consecutive dispatches of the hard-threshold kernel (its
+    plain variant) that no other kernel interrupts: the launches
+    roofline.launch_us times with HIP events."""
     import csv
     stats = list(csv.DictReader(open(os.path.join(folder, "run_kernel_stats.csv"))))
     trace = list(csv.DictReader(open(os.path.join(folder, "run_kernel_trace.csv"))))
@@ -299,10 +302,52 @@ def main():
         bracket_hits += efs.topk_took_bracket_path(ws)
 
     # ---- kernel durations: back-to-back launches -------------------------
-    # Hard threshold continuing the EF trajectory from the end of the timed
-    # region, then the copy probe on the same number of elements.
+    # Hard threshold on four error-feedback states continuing from the end of
+    # the timed region, taken in turn, each with its own gradient sequence:
+    # g and e of every launch come from HBM, as inside the step, where the
+    # other operations evict them from the 256 MB Infinity Cache.
+    e_rot = [e_ht_end.clone() for _ in range(4)]
+    ctr_rot = [efs.new_counter(dev) for _ in range(4)]
+
+    def ht_rot(s, telemetry=None):
+        r = s % 4
+        g = pool[(s + s // 4) % len(pool)]
+        if telemetry is None:
+            efs.ht_compress(g, e_rot[r], lr, lam, idx, val, ctr_rot[r])
+        else:
+            efs.ht_compress_telemetry(g, e_rot[r], lr, lam, idx, val, ctr_rot[r], telemetry)
+
+    a, b = ev(), ev()
+    torch.cuda.synchronize()
+    a.record(cur)
+    for s in range(args.b2b):
+        ht_rot(s)
+    b.record(cur)
+    torch.cuda.synchronize()
+    ht_b2b_us = a.elapsed_time(b) * 1e3 / args.b2b
+    kt_b2b = float(np.mean([efs.counter_value(c) for c in ctr_rot]))
+    # the same with the fused telemetry (total error, pairs sent, max |e'|)
+    tel = efs.new_telemetry(dev)
+    a, b = ev(), ev()
+    torch.cuda.synchronize()
+    a.record(cur)
+    for s in range(args.b2b):
+        ht_rot(s, tel)
+    b.record(cur)
+    torch.cuda.synchronize()
+    ht_tel_us = a.elapsed_time(b) * 1e3 / args.b2b
+    # copy probe over the same element count, destinations in turn
+    a, b = ev(), ev()
+    a.record(cur)
+    for s in range(args.b2b):
+        efs.copy_probe(pool[s % len(pool)], e_rot[(s + 1) % 4])
+    b.record(cur)
+    torch.cuda.synchronize()
+    copy_us = a.elapsed_time(b) * 1e3 / args.b2b
+    del e_rot
+    # one state carried from launch to launch (an EF loop with nothing in
+    # between): part of e then stays in the Infinity Cache
     e_ht.copy_(e_ht_end)
-    e_tk.copy_(e_tk_end)
     a, b = ev(), ev()
     torch.cuda.synchronize()
     a.record(cur)
@@ -310,25 +355,8 @@ def main():
         efs.ht_compress(pool[s % len(pool)], e_ht, lr, lam, idx, val, ctr)
     b.record(cur)
     torch.cuda.synchronize()
-    ht_b2b_us = a.elapsed_time(b) * 1e3 / args.b2b
-    kt_b2b = efs.counter_value(ctr)
-    # the same with the fused telemetry (total error, pairs sent, max |e'|)
-    tel = efs.new_telemetry(dev)
-    a, b = ev(), ev()
-    torch.cuda.synchronize()
-    a.record(cur)
-    for s in range(args.b2b):
-        efs.ht_compress_telemetry(pool[s % len(pool)], e_ht, lr, lam, idx, val, ctr, tel)
-    b.record(cur)
-    torch.cuda.synchronize()
-    ht_tel_us = a.elapsed_time(b) * 1e3 / args.b2b
-    a, b = ev(), ev()
-    a.record(cur)
-    for s in range(args.b2b):
-        efs.copy_probe(pool[s % len(pool)], out)
-    b.record(cur)
-    torch.cuda.synchronize()
-    copy_us = a.elapsed_time(b) * 1e3 / args.b2b
+    ht_one_us = a.elapsed_time(b) * 1e3 / args.b2b
+    kt_one = efs.counter_value(ctr)
     # cold: a 1 GiB write (stream probe) before every launch evicts the 256 MB
     # Infinity Cache, so g and e come from HBM; events around the launch only
     flush = torch.empty(1 << 28, dtype=torch.float32, device=dev)
@@ -434,11 +462,14 @@ def main():
                        "bytes": 8.0 * d},
         "ops": {
             "ht_compress_telemetry": {"launch_us": round(ht_tel_us, 2)},
+            "ht_compress_one_state": {
+                "launch_us": round(ht_one_us, 2), "k_t": kt_one,
+                "gbps": round((12.0 * d + 8.0 * kt_one) / (ht_one_us * 1e-6) / 1e9, 1)},
             "ht_compress_cold": {
                 "median_us": round(ht_cold_us, 2), "p10_us": round(float(np.percentile(cold, 10)), 2),
                 "p90_us": round(float(np.percentile(cold, 90)), 2),
                 "gbps": round((12.0 * d + 8.0 * kt_cold) / (ht_cold_us * 1e-6) / 1e9, 1),
-                "vs_warm": round(ht_cold_us / ht_b2b_us, 3)},
+                "vs_b2b": round(ht_cold_us / ht_b2b_us, 3)},
             "topk_segmented_compress": {
                 "launch_us": round(seg_us, 2), "segments": int(seg_ks.size), "k_total": seg_ktot,
                 "bracket_segments_last_call": seg_hits,
@@ -458,8 +489,7 @@ def main():
     }
 
     if not args.no_apply:
-        line["sparse_apply"] = apply_bench(efs, torch, synth, cur, args.b2b, (idx, val, ctr), d,
-                                           out)
+        line["sparse_apply"] = apply_bench(efs, torch, synth, cur, args.b2b, (idx, val, ctr), d)
     if args.sweep:
         del pool, e_tk, out, ws
         line["ht_sweep"] = ht_sweep(efs, torch, synth, cur, args.b2b)
@@ -582,23 +612,25 @@ def ht_sweep(efs, torch, synth, cur, reps):
     return res
 
 
-def apply_bench(efs, torch, synth, cur, reps, ht_payload, d, out):
+def apply_bench(efs, torch, synth, cur, reps, ht_payload, d):
     """Back-to-back sparse_apply launches in each mode: on the step's own
     hard-threshold payload (1 worker), and on 8 workers' payloads of the
     8-worker workload (same d and segment layout, 0.1 % first-step density),
-    next to sparse_accumulate on the same payloads.  Algorithmic bytes:
+    next to sparse_accumulate on the same payloads; the launches take four
+    output sets in turn.  Algorithmic bytes:
     average 8 per pair + 4 d; sgd 8 per pair + 8 per touched coordinate;
     momentum 8 per pair + 16 d."""
     import numpy as np
 
-    def timed(fn):
+    def timed(fns):
         a = torch.cuda.Event(enable_timing=True)
         b = torch.cuda.Event(enable_timing=True)
-        fn()
+        for fn in fns:
+            fn()
         torch.cuda.synchronize()
         a.record(cur)
-        for _ in range(reps):
-            fn()
+        for s in range(reps):
+            fns[s % len(fns)]()
         b.record(cur)
         torch.cuda.synchronize()
         return a.elapsed_time(b) * 1e3 / reps
@@ -608,19 +640,21 @@ def apply_bench(efs, torch, synth, cur, reps, ht_payload, d, out):
         touched = int(torch.unique(torch.cat(
             [p[0][:efs.counter_value(p[2])] for p in payloads])).numel())
         ws = efs.new_apply_workspace(payloads, d, "cuda")
-        x = torch.zeros(d, dtype=torch.float32, device="cuda")
-        m = torch.zeros(d, dtype=torch.float32, device="cuda")
+        # four (x, m) sets taken in turn, so that they come from HBM as the
+        # parameters and momentum of a training step would
+        xs = [torch.zeros(d, dtype=torch.float32, device="cuda") for _ in range(4)]
+        ms = [torch.zeros(d, dtype=torch.float32, device="cuda") for _ in range(4)]
         res = {"pairs": pairs, "touched": touched, "workspace_mb": round(ws.numel() / 2 ** 20, 1)}
         for mode, name, nbytes in (
                 (efs.APPLY_AVERAGE, "average", 8.0 * pairs + 4.0 * d),
                 (efs.APPLY_SGD, "sgd", 8.0 * pairs + 8.0 * touched),
                 (efs.APPLY_MOMENTUM, "momentum", 8.0 * pairs + 16.0 * d)):
-            us = timed(efs.prepare_sparse_apply(payloads, d, mode, x, ws, m=m, beta=0.9,
-                                                gamma=0.05))
+            us = timed([efs.prepare_sparse_apply(payloads, d, mode, xs[r], ws, m=ms[r], beta=0.9,
+                                                 gamma=0.05) for r in range(4)])
             res[name] = {"us": round(us, 2), "gbps": round(nbytes / (us * 1e-6) / 1e9, 1)}
-        us = timed(efs.prepare_sparse_accumulate(payloads, d, out))
+        us = timed([efs.prepare_sparse_accumulate(payloads, d, x) for x in xs])
         res["sparse_accumulate_us"] = round(us, 2)
-        del ws, x, m
+        del ws, xs, ms
         return res
 
     res = {"workers_1": measure([ht_payload])}

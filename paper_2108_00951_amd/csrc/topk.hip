@@ -12,7 +12,8 @@
 //          [lo, hi] of 2^20 keys (about 3..6 % in magnitude either side)
 //          around the threshold predicted from the previous two calls on
 //          this workspace.
-//   pass1  p = e + lr*g written into e (12 B/element); LDS histogram of key
+//   pass1  p = e + lr*g written into e (12 B/element, streamed with the
+//          non-temporal hint); LDS histogram of key
 //          bits 30..20; with a bracket, keys above it go straight to the
 //          payload and keys inside it to a candidate buffer (staged
 //          compaction) and into coarse (1024) and fine (2^20) histograms of
@@ -358,7 +359,7 @@ __global__ __launch_bounds__(kBlock) void topk_pass1_kernel(const float *__restr
 #pragma unroll
             for (int j = 0; j < kVecPerThread; ++j) {
                 gv[j] = __builtin_nontemporal_load(g4 + j * kBlock + tid);
-                ev[j] = e4[j * kBlock + tid];
+                ev[j] = __builtin_nontemporal_load(e4 + j * kBlock + tid);
             }
 #pragma unroll
             for (int j = 0; j < kVecPerThread; ++j) {
@@ -368,7 +369,7 @@ __global__ __launch_bounds__(kBlock) void topk_pass1_kernel(const float *__restr
                     o[c] = ef_accumulate(ev[j][c], lr, gv[j][c]);
                     p[j][c] = o[c];
                 }
-                e4[j * kBlock + tid] = o;
+                __builtin_nontemporal_store(o, e4 + j * kBlock + tid);
             }
             valid = 0xffffu;
         } else {

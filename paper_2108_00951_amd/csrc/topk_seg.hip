@@ -12,7 +12,8 @@
 //   reset    one workgroup checks the layout and forms the per-segment
 //            tables (tile ranges, payload offsets, candidate regions, the
 //            bracket); the others zero the per-segment histograms.
-//   pass1    p = e + lr*g written into e (12 B/element); LDS histogram of key
+//   pass1    p = e + lr*g written into e (12 B/element, streamed with the
+//            non-temporal hint); LDS histogram of key
 //            bits 30..18 (8192 bins) per segment, flushed (non-zero bins) to
 //            the segment's global histogram.  A segment within one tile is
 //            selected right there.  With a bracket [lo, hi] around the
@@ -784,7 +785,7 @@ __device__ void pass1_slice(const float *__restrict__ g, float *__restrict__ e, 
 #pragma unroll
             for (int j = 0; j < kVecPerThread; ++j) {
                 gv[j] = __builtin_nontemporal_load(g4 + j * kBlock + threadIdx.x);
-                ev[j] = e4[j * kBlock + threadIdx.x];
+                ev[j] = __builtin_nontemporal_load(e4 + j * kBlock + threadIdx.x);
             }
 #pragma unroll
             for (int j = 0; j < kVecPerThread; ++j) {
@@ -794,7 +795,7 @@ __device__ void pass1_slice(const float *__restrict__ g, float *__restrict__ e, 
                     pv[c] = ef_accumulate(ev[j][c], lr, gv[j][c]);
                     p[j][c] = pv[c];
                 }
-                e4[j * kBlock + threadIdx.x] = pv;
+                __builtin_nontemporal_store(pv, e4 + j * kBlock + threadIdx.x);
             }
             valid = 0xffffu;
         } else {
