@@ -128,6 +128,11 @@ def parse_pmc(fetch_dir, write_dir, d):
         out[name] = {"ht_kib_per_launch": ht_b / 1024, "copy_kib_per_launch": cp_b / 1024,
                      "copy_expected_kib": 4.0 * d / 1024, "scale": scale,
                      "ht_bytes_scaled": ht_b * scale, "launches": len(ht)}
+        # every other kernel of the run, the same scale applied
+        by = {}
+        for k, v in rows:
+            by.setdefault(_short_kernel_name(k), []).append(v)
+        out[name]["kernels"] = {k: (1024.0 * sum(v) / len(v) * scale, len(v)) for k, v in by.items()}
     out["ht_bytes_per_launch"] = out["FETCH_SIZE"]["ht_bytes_scaled"] + out["WRITE_SIZE"]["ht_bytes_scaled"]
     return out
 
@@ -187,6 +192,16 @@ def format_traffic(res):
         lines.append("# %s: kernel %.1f KiB, copy probe %.1f KiB (expected %.1f), scale %.5f, "
                      "%d launches" % (name, r["ht_kib_per_launch"], r["copy_kib_per_launch"],
                                       r["copy_expected_kib"], r["scale"], r["launches"]))
+    fk, wk = res["FETCH_SIZE"].get("kernels", {}), res["WRITE_SIZE"].get("kernels", {})
+    if fk or wk:
+        lines.append("# every kernel of the run, scaled the same way: MB fetched + MB written per "
+                     "launch (launches)")
+        names = sorted(set(fk) | set(wk),
+                       key=lambda n: -(fk.get(n, (0.0, 0))[0] + wk.get(n, (0.0, 0))[0]))
+        for n in names:
+            f, nf = fk.get(n, (0.0, 0))
+            w, nw = wk.get(n, (0.0, 0))
+            lines.append("#   %-34s %9.2f + %9.2f MB  (%d)" % (n, f / 1e6, w / 1e6, max(nf, nw)))
     lines.append("ht_bytes_per_launch %d" % round(res["ht_bytes_per_launch"]))
     lines.append("kernel_source_sha256 %s" % kernel_source_digest())
     return "\n".join(lines) + "\n"

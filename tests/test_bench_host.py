@@ -85,6 +85,11 @@ def test_parse_pmc_scales_by_the_copy_probe(tmp_path):
     assert res["ht_bytes_per_launch"] == pytest.approx(16384 * 1024 * 0.5 + 4096 * 1024)
     text = bench.format_traffic(res)
     assert "ht_bytes_per_launch %d" % round(res["ht_bytes_per_launch"]) in text
+    # the other kernels get the same scales: topk_step3 fetched nothing, wrote 1 KiB
+    step3 = [x for x in text.splitlines() if "topk_step3_kernel" in x]
+    assert len(step3) == 1 and "0.00 +      0.00 MB  (1)" in step3[0]
+    ht_line = [x for x in text.splitlines() if "ht_fused_kernel<true, false>" in x][0]
+    assert "%9.2f + %9.2f MB" % (16384 * 1024 * 0.5 / 1e6, 4096 * 1024 / 1e6) in ht_line
     assert "kernel_source_sha256 " + bench.kernel_source_digest() in text
 
 
