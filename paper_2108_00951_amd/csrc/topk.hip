@@ -325,6 +325,32 @@ __device__ __forceinline__ void wave_aggregated_add(uint32_t *hist, uint32_t bin
     }
 }
 
+// Adds 1 to fine[(key - sub) mod 2^20] for every element (j, c) of this
+// thread selected by bit 4*j + c of `mask`.  Each round takes the lowest
+// remaining selected element of every lane, so a wave runs as many rounds as
+// its fullest lane has selected elements (usually none or a few) instead of
+// one per element slot.  Called by all lanes.
+__device__ __forceinline__ void fine_add_masked(uint32_t *fine, uint32_t mask,
+                                                const float (&p)[kVecPerThread][4],
+                                                uint32_t sub) {
+    while (__ballot(mask != 0u) != 0ull) {
+        const bool act = mask != 0u;
+        uint32_t key = 0u;
+        if (act) {
+            const int b = __ffs(mask) - 1;
+            mask &= mask - 1u;
+            float x = 0.0f;
+#pragma unroll
+            for (int j = 0; j < kVecPerThread; ++j)
+#pragma unroll
+                for (int c = 0; c < 4; ++c)
+                    if (b == 4 * j + c) x = p[j][c];
+            key = magnitude_key(x);
+        }
+        wave_aggregated_add(fine, (key - sub) & (kFine - 1), act);
+    }
+}
+
 struct Pass1Shared {
     uint32_t h[kBins1];
     uint32_t coarse[kCoarse];
@@ -406,18 +432,8 @@ __global__ __launch_bounds__(kBlock) void topk_pass1_kernel(const float *__restr
                 }
             }
         }
-        if (bracket) {
-            // fine bins in global memory: lanes with equal keys add together
-#pragma unroll
-            for (int j = 0; j < kVecPerThread; ++j) {
-#pragma unroll
-                for (int c = 0; c < 4; ++c) {
-                    const int b = 4 * j + c;
-                    const uint32_t key = magnitude_key(p[j][c]);
-                    wave_aggregated_add(ws.fine, key - lo, (m_inside >> b) & 1u);
-                }
-            }
-        }
+        // fine bins in global memory: lanes with equal keys add together
+        if (bracket) fine_add_masked(ws.fine, m_inside, p, lo);
         if (bracket) {
             stage_mask(sh.above, fill_above, m_above, p, tile0, &ws.ctl->emit, k, idx, val);
             stage_mask(sh.inside, fill_inside, m_inside, p, tile0, &ws.ctl->cand, ws.ccap,
@@ -451,6 +467,7 @@ __device__ void radix_refine20(const float *__restrict__ e, int64_t d, uint32_t 
         float v[kVecPerThread][4];
         uint32_t valid;
         load_tile<kVector>(e, tile0, d, v, valid);
+        uint32_t under = 0;  // elements whose key lies under the top digit
 #pragma unroll
         for (int j = 0; j < kVecPerThread; ++j) {
 #pragma unroll
@@ -458,9 +475,10 @@ __device__ void radix_refine20(const float *__restrict__ e, int64_t d, uint32_t 
                 const uint32_t key = magnitude_key(v[j][c]);
                 const bool in = ((valid >> (4 * j + c)) & 1u) && (key >> 20) == prefix;
                 if (in) atomicAdd(&h[(key >> 10) & (kCoarse - 1)], 1u);
-                wave_aggregated_add(fine, key & (kFine - 1), in);
+                under |= uint32_t(in) << (4 * j + c);
             }
         }
+        fine_add_masked(fine, under, v, 0u);
     }
     __syncthreads();
     for (int b = tid; b < kCoarse; b += kBlock)
