@@ -78,9 +78,10 @@ efs_status ht_compress(const float *g, float *e, int64_t d, float lr, float lamb
 
 /* A telemetry object: EFS_TELEMETRY_BYTES of device memory, 8-byte aligned,
  * zero-filled by the caller before the first call; every call adds to it:
- *   double   err2_total    sum over calls of ||e_{t+1}||^2, the total error
- *                          of Remark 4 (section 3) when the calls are the
- *                          iterations t = 0..T-1;
+ *   double   err2_part[32] partial sums whose total is the sum over calls of
+ *                          ||e_{t+1}||^2, the total error of Remark 4
+ *                          (section 3) when the calls are the iterations
+ *                          t = 0..T-1 (sum the 32 values to read it);
  *   double   sent_total    sum over calls of k_t (average density =
  *                          sent_total / (calls * d), the measure of data
  *                          volume used in section 6);
@@ -89,10 +90,11 @@ efs_status ht_compress(const float *g, float *e, int64_t d, float lr, float lamb
  *                          below lambda: the absolute-compressor bound of
  *                          section 5);
  *   uint32_t calls         number of calls accumulated;
- *   8 bytes reserved.
- * The norm is summed in binary64 by one atomic per workgroup, so its last
- * bits can vary with the order of the additions. */
-#define EFS_TELEMETRY_BYTES 32
+ *   16 bytes reserved.
+ * The norm is summed in binary64, each workgroup adding its share into one
+ * of the 32 parts with an atomic (one word for all of them serialises), so
+ * its last bits can vary with the order of the additions. */
+#define EFS_TELEMETRY_BYTES 288
 
 /* ht_compress, and in the same pass the telemetry above added to
  * `telemetry` (device pointer, see EFS_TELEMETRY_BYTES). */

@@ -146,7 +146,7 @@ def ht_compress(g, e, lr: float, lam: float, idx, val, counter, stream=None) -> 
     _check(lib, rc)
 
 
-TELEMETRY_BYTES = 32
+TELEMETRY_BYTES = 288
 
 
 def new_telemetry(device="cuda"):
@@ -159,8 +159,12 @@ def read_telemetry(tel) -> dict:
     """Decode a telemetry object (synchronises with the device)."""
     import numpy as np
     raw = tel.cpu().numpy().tobytes()
-    err2, sent = np.frombuffer(raw[:16], dtype="<f8")
-    max_bits, calls = np.frombuffer(raw[16:24], dtype="<u4")
+    parts = np.frombuffer(raw[:256], dtype="<f8")
+    err2 = 0.0
+    for x in parts:  # the total error is the sum of the 32 parts
+        err2 += float(x)
+    (sent,) = np.frombuffer(raw[256:264], dtype="<f8")
+    max_bits, calls = np.frombuffer(raw[264:272], dtype="<u4")
     return {"err2_total": float(err2), "sent_total": float(sent),
             "max_abs": float(np.array([max_bits], dtype=np.uint32).view(np.float32)[0]),
             "max_abs_bits": int(max_bits), "calls": int(calls)}

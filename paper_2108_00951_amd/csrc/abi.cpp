@@ -10,9 +10,11 @@
 
 #include "../../include/efsparse.h"
 #include "launch.hpp"
+#include "device_common.hpp"
 
 static_assert(efs::kMaxApplyWorkers == EFS_APPLY_MAX_WORKERS, "worker limit differs from the header");
 static_assert(efs::kMaxSegments == EFS_SEG_MAX, "segment limit differs from the header");
+static_assert(sizeof(efs::Telemetry) == EFS_TELEMETRY_BYTES, "telemetry layout differs from the header");
 
 namespace {
 

@@ -140,16 +140,20 @@ using PairStage = PairStageN<kTile>;
 // to zero for the next call.  Slots at or past `cap` are not written.
 // Called by every thread of the workgroup; contains barriers.
 // Error-feedback telemetry accumulated across calls (layout of the C ABI's
-// telemetry object): total error sum_t ||e_{t+1}||^2, total pairs sent
-// sum_t k_t, running max of |e_{t+1}| as a bit pattern, number of calls.
+// telemetry object): the total error sum_t ||e_{t+1}||^2 as kTelemetryParts
+// partial sums (workgroup b adds into part b mod kTelemetryParts: one binary64
+// atomic per workgroup on a single word serialises at the end of the pass),
+// total pairs sent sum_t k_t, running max of |e_{t+1}| as a bit pattern,
+// number of calls.
+constexpr int kTelemetryParts = 32;
 struct Telemetry {
-    double err2_total;
+    double err2_part[kTelemetryParts];
     double sent_total;
     uint32_t max_abs_bits;
     uint32_t calls;
-    uint64_t reserved;
+    uint64_t reserved[2];
 };
-static_assert(sizeof(Telemetry) == 32, "telemetry object is 32 bytes");
+static_assert(sizeof(Telemetry) == 288, "telemetry object layout");
 
 template <int N>
 __device__ __forceinline__ void stage_flush(PairStageN<N> &st, uint32_t fill, bool last,

@@ -26,7 +26,8 @@ namespace efs {
 
 // With kStats, every workgroup also sums ||e'||^2 (binary64) and the max of
 // |e'| over its elements and adds them to the telemetry object with one
-// atomic each; the last workgroup adds k_t and counts the call.
+// atomic each (the sum into one of the 32 partial sums, spreading the
+// atomics over 32 words); the last workgroup adds k_t and counts the call.
 template <bool kVector, bool kStats>
 __global__ __launch_bounds__(kBlock) void ht_fused_kernel(
     const float *__restrict__ g, float *__restrict__ e, int64_t d, float lr, float lambda,
@@ -121,7 +122,7 @@ __global__ __launch_bounds__(kBlock) void ht_fused_kernel(
         const double wg_err2 = block_sum_f64(err2, s_f64);
         const uint32_t wg_max = block_max(max_bits, st.wave);
         if (tid == 0) {
-            atomicAdd(&tel->err2_total, wg_err2);
+            atomicAdd(&tel->err2_part[blockIdx.x % kTelemetryParts], wg_err2);
             atomicMax(&tel->max_abs_bits, wg_max);
         }
     }

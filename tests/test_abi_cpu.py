@@ -220,3 +220,9 @@ def test_topk_segmented_rejects_bad_arguments(lib):
                                        None) == binding.EFS_OK
     assert lib.topk_segmented_workspace_bytes(0, 1) == 0
     assert lib.topk_segmented_workspace_bytes(1, -1) == 0
+
+
+def test_binding_sizes_match_the_header():
+    text = open(os.path.join(ROOT, "include", "efsparse.h")).read()
+    defs = dict(re.findall(r"#define (EFS_\w+) (\d+)", text))
+    assert int(defs["EFS_TELEMETRY_BYTES"]) == binding.TELEMETRY_BYTES
