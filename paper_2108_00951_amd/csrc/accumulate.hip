@@ -9,8 +9,10 @@
 //            summation order, so the result is the same on every run.  The
 //            first launch knows out[i] is +0 and stores +0 + v without
 //            reading it.
-//   scale    out = out / n (IEEE division, non-temporal loads and stores),
-//            skipped for n == 1.
+//   scale    out = out / n (IEEE division), skipped for n == 1.  A zero
+//            divided by n is the same zero, so only the non-zero
+//            coordinates (those some payload touched) are rewritten: a read
+//            of out and a few scattered writes instead of a full rewrite.
 //
 // Also the streaming copy probe used to measure the bandwidth ceiling.
 #include "device_common.hpp"
@@ -52,13 +54,16 @@ __global__ __launch_bounds__(kBlock) void scale_kernel(float *__restrict__ out, 
     const int64_t nvec = d / 4;
     f32x4 *o4 = reinterpret_cast<f32x4 *>(out);
     for (int64_t v = int64_t(blockIdx.x) * kBlock + threadIdx.x; v < nvec; v += stride) {
-        f32x4 x = __builtin_nontemporal_load(o4 + v);
+        const f32x4 x = __builtin_nontemporal_load(o4 + v);
 #pragma unroll
-        for (int c = 0; c < 4; ++c) x[c] = __fdiv_rn(x[c], n);
-        __builtin_nontemporal_store(x, o4 + v);
+        for (int c = 0; c < 4; ++c)
+            if (x[c] != 0.0f) out[4 * v + c] = __fdiv_rn(x[c], n);
     }
     const int64_t t = nvec * 4 + int64_t(blockIdx.x) * kBlock + threadIdx.x;
-    if (blockIdx.x == 0 && t < d) out[t] = __fdiv_rn(out[t], n);
+    if (blockIdx.x == 0 && t < d) {
+        const float x = out[t];
+        if (x != 0.0f) out[t] = __fdiv_rn(x, n);
+    }
 }
 
 // Same tile shape, grid sizing and cache hints as the hard-threshold kernel:

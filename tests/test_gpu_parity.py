@@ -503,6 +503,38 @@ def test_accumulate_topk_payloads_and_tail():
     assert_bits_equal(out.cpu().numpy(), oracle.accumulate(ps_ref, d))
 
 
+@pytest.mark.parametrize("n", [3, 8])
+def test_accumulate_special_values(n):
+    # signed zeros, sums that cancel to zero, infinities, NaN and subnormals,
+    # also at the ragged tail: the division by n leaves every zero as it is
+    # and must divide everything else with one IEEE rounding
+    d = 4096 * 2 + 3
+    tiny = np.float32(1e-45)
+    base = [(5, -0.0), (6, 0.0), (8, np.inf), (9, -np.inf), (10, np.nan),
+            (11, tiny), (12, -3 * tiny), (d - 1, 2.5), (d - 2, -0.0)]
+    ps_dev, ps_ref = [], []
+    for w in range(n):
+        pairs = list(base) + [(200 + w, float(w) - 1.25)]
+        # workers 0 and 1 alone touch 7 and d - 3, with opposite values: the
+        # sums there are +0
+        if w == 0:
+            pairs += [(7, 1.5), (d - 3, 7.0)]
+        if w == 1:
+            pairs = [(7, -1.5), (d - 3, -7.0), (100 + w, 1.0)]
+        idx = np.array([i for i, _ in pairs], dtype=np.int32)
+        val = np.array([v for _, v in pairs], dtype=np.float32)
+        ps_dev.append((to_dev(idx), to_dev(val)))
+        ps_ref.append((idx, val))
+    out = torch.full((d,), 9.0, dtype=torch.float32, device=DEV)
+    efs.sparse_accumulate(ps_dev, d, out)
+    got = out.cpu().numpy()
+    ref = oracle.accumulate(ps_ref, d)
+    nan = np.isnan(ref)
+    assert np.array_equal(np.isnan(got), nan)
+    assert_bits_equal(got[~nan], ref[~nan])
+    assert bits(got[7]) == 0 and bits(got[d - 3]) == 0  # cancelled sums are +0
+
+
 def test_accumulate_ignores_out_of_range_indices():
     d = 1000
     idx = np.array([3, -1, 999, 1000, 7], dtype=np.int32)
