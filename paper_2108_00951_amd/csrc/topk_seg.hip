@@ -1377,19 +1377,36 @@ __device__ void final_segment(float *__restrict__ e, int32_t *__restrict__ idx,
 }
 
 // One workgroup per CU at most (the LDS candidate buffer), looping over the
-// segments; most return at once (one tile, none, all, or nothing to rank).
+// segments b, b + grid, ...  Most need nothing here (one tile, none, all), so
+// the workgroup first reads the modes of up to kBlock of its segments at once
+// and then runs only those with something to rank (one dependent read per
+// segment in turn was the larger cost with thousands of segments).
 __global__ __launch_bounds__(kBlock) void seg_final_kernel(float *__restrict__ e,
                                                            int32_t *__restrict__ idx,
                                                            float *__restrict__ val, SegWs ws,
                                                            int32_t nseg) {
     __shared__ FinalShared sh;
+    __shared__ int32_t s_list[kBlock];
+    __shared__ uint32_t s_wave[kWaves];
     if (ws.ctl->status != 0u) return;
-    uint32_t fast = 0;  // segments of this workgroup resolved from the bracket
-    for (int32_t s = blockIdx.x; s < nseg; s += gridDim.x) {
-        __syncthreads();  // LDS of the previous segment is free
-        fast += ws.st[s].mode == kModeFast ? 1u : 0u;
-        final_segment(e, idx, val, ws, s, sh);
+    uint32_t fast = 0;  // segments resolved from the bracket, counted per thread
+    const int32_t per = (nseg - int32_t(blockIdx.x) + int32_t(gridDim.x) - 1) / int32_t(gridDim.x);
+    for (int32_t g0 = 0; g0 < per; g0 += kBlock) {
+        const int32_t q = g0 + int32_t(threadIdx.x);
+        const int32_t s = int32_t(blockIdx.x) + q * int32_t(gridDim.x);
+        const uint32_t mode = q < per ? ws.st[s].mode : uint32_t(kModeNone);
+        fast += mode == kModeFast ? 1u : 0u;
+        const bool work = mode == kModeCand || mode == kModeScan || mode == kModeFast;
+        uint32_t n_work;
+        const uint32_t pos = block_prefix_small(work ? 1u : 0u, s_wave, n_work);
+        if (work) s_list[pos] = s;
+        __syncthreads();
+        for (uint32_t i = 0; i < n_work; ++i) {
+            final_segment(e, idx, val, ws, s_list[i], sh);
+            __syncthreads();  // the LDS of this segment is free
+        }
     }
+    fast = block_sum(fast, s_wave);
     if (threadIdx.x == 0 && fast != 0u) atomicAdd(&ws.ctl->bracket, fast);
 }
 
