@@ -1,0 +1,71 @@
+"""The 25,557,032-element, 161-layer workload over 30 error-feedback steps
+with a fresh gradient each step: hard threshold, flat Top-k and layer-wise
+Top-k, every step's payload and residual bit-exact against the oracle.  The
+oracle's Top-k sorts the whole vector, so the run takes a few minutes: it
+runs when EFS_LONG_TESTS=1 is set, and is skipped otherwise."""
+import os
+
+import numpy as np
+import pytest
+
+from paper_2108_00951_amd import synth
+from tests._checks import assert_bits_equal, assert_payload_equal
+
+pytestmark = [pytest.mark.gpu,
+              pytest.mark.skipif(os.environ.get("EFS_LONG_TESTS") != "1",
+                                 reason="long run; set EFS_LONG_TESTS=1")]
+
+torch = pytest.importorskip("torch")
+import oracle  # noqa: E402
+from paper_2108_00951_amd import binding as efs  # noqa: E402
+
+DEV = "cuda"
+
+
+@pytest.mark.timeout(1200)
+def test_thirty_ef_steps_of_the_benchmark_workload():
+    T = 30
+    st = synth.Stream(2)
+    d, k = st.w.d, st.w.topk_k[0]
+    g0 = st.gradient(0, threads=16)
+    lam = synth.calibrate_lambda(g0, 0.001)
+    ks = synth.layerwise_k(st.bounds, 0.001)
+    kt = int(ks.sum())
+    e_ht, e_tk, e_sg = (torch.zeros(d, device=DEV) for _ in range(3))
+    idx = torch.empty(d, dtype=torch.int32, device=DEV)
+    val = torch.empty(d, device=DEV)
+    ctr = efs.new_counter(DEV)
+    tidx = torch.empty(k, dtype=torch.int32, device=DEV)
+    tval = torch.empty(k, device=DEV)
+    ws = efs.new_topk_workspace(d, k, DEV)
+    ws.zero_()
+    sidx = torch.empty(kt, dtype=torch.int32, device=DEV)
+    sval = torch.empty(kt, device=DEV)
+    sws = efs.new_topk_segmented_workspace(ks.size, kt, DEV)
+    sws.zero_()
+    offd = torch.from_numpy(st.bounds.astype(np.int64)).to(DEV)
+    kd = torch.from_numpy(ks).to(DEV)
+    r_ht, r_tk, r_sg = (np.zeros(d, np.float32) for _ in range(3))
+    bracket_steps = 0
+    for t in range(T):
+        g = g0 if t == 0 else st.gradient(t, threads=16)
+        gd = torch.from_numpy(g).to(DEV)
+        efs.ht_compress(gd, e_ht, synth.LR, lam, idx, val, ctr)
+        efs.topk_compress(gd, e_tk, synth.LR, k, tidx, tval, ws)
+        efs.topk_segmented_compress(gd, e_sg, synth.LR, offd, kd, sidx, sval, sws)
+        n = efs.counter_value(ctr)
+        ri, rv, r_ht, rk = oracle.ht(g, r_ht, synth.LR, lam)
+        assert n == rk, t
+        assert_payload_equal(idx[:n].cpu().numpy(), val[:n].cpu().numpy(), ri, rv, "ht t=%d" % t)
+        assert_bits_equal(e_ht.cpu().numpy(), r_ht, "ht e t=%d" % t)
+        ti, tv, r_tk = oracle.topk(g, r_tk, synth.LR, k)
+        assert_payload_equal(tidx.cpu().numpy(), tval.cpu().numpy(), ti, tv, "topk t=%d" % t)
+        assert_bits_equal(e_tk.cpu().numpy(), r_tk, "topk e t=%d" % t)
+        si, sv, r_sg = oracle.topk_segmented(g, r_sg, synth.LR, st.bounds.astype(np.int64), ks)
+        assert_payload_equal(sidx.cpu().numpy(), sval.cpu().numpy(), si, sv, "layer-wise t=%d" % t)
+        assert_bits_equal(e_sg.cpu().numpy(), r_sg, "layer-wise e t=%d" % t)
+        bracket_steps += efs.topk_took_bracket_path(ws)
+        print("step %d bit-exact (k_t %d, Top-k bracket %d, layers from the bracket %d)"
+              % (t, n, efs.topk_took_bracket_path(ws), efs.topk_segmented_bracket_segments(sws)),
+              flush=True)
+    assert bracket_steps >= T // 2
