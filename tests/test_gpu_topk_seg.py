@@ -376,6 +376,38 @@ def test_segmented_many_small_layers(levels):
     check(g, e, off, ks, lr=np.float32(1.0), what="small layers")
 
 
+def test_segmented_thousands_of_layers_ef_loop():
+    # 5,000 layers (the reset scans the layer table 512 layers at a time: ten
+    # chunks), mostly within one tile, some spanning many; three EF steps
+    rng = np.random.default_rng(990)
+    sizes = np.exp(rng.uniform(np.log(1), np.log(2000), size=5000)).astype(np.int64)
+    sizes[rng.choice(5000, 40, replace=False)] = rng.integers(8000, 40000, size=40)
+    off = np.concatenate([[0], np.cumsum(sizes)]).astype(np.int64)
+    d = int(off[-1])
+    ks = synth.layerwise_k(off, 0.01)
+    k_total = int(ks.sum())
+    e_ref = np.zeros(d, np.float32)
+    ed = torch.zeros(d, dtype=torch.float32, device=DEV)
+    idx = torch.empty(k_total, dtype=torch.int32, device=DEV)
+    val = torch.empty(k_total, dtype=torch.float32, device=DEV)
+    ws = efs.new_topk_segmented_workspace(ks.size, k_total, DEV)
+    ws.zero_()
+    offd, kd = dev(off), dev(ks)
+    say("segmented thousands of layers d=%d nseg=%d k=%d" % (d, ks.size, k_total))
+    for t in range(3):
+        g = synth.small_gradient(995 + t, d)
+        efs.topk_segmented_compress(dev(g), ed, LR, offd, kd, idx, val, ws)
+        assert efs.topk_segmented_status(ws) == 0
+        ri, rv, e_ref = oracle.topk_segmented(g, e_ref, LR, off, ks)
+        gi, gv = idx.cpu().numpy(), val.cpu().numpy()
+        # layer regions in order: sort each region by index, then compare
+        order = np.lexsort((gi, np.repeat(np.arange(ks.size), ks)))
+        np.testing.assert_array_equal(gi[order], ri, "t=%d indices" % t)
+        assert_bits_equal(gv[order], rv, "t=%d values" % t)
+        assert_bits_equal(ed.cpu().numpy(), e_ref, "e' t=%d" % t)
+        say("  step %d ok (bracket in %d layers)" % (t, efs.topk_segmented_bracket_segments(ws)))
+
+
 @pytest.mark.parametrize("seed", range(8))
 def test_segmented_randomised_ef_loops(seed):
     # random layouts (empty, one-tile and multi-tile layers), random budgets,
