@@ -206,6 +206,34 @@ def test_ht_telemetry_totals(unaligned):
     assert abs(got["err2_total"] - err2) <= 1e-9 * err2
 
 
+def test_ht_telemetry_object_shared_by_calls_of_different_sizes():
+    # one telemetry object for vectors of 1 tile, 40 tiles and 4000 tiles:
+    # the calls run 1, 40 and hundreds of workgroups, so they fill different
+    # sets of the 32 partial sums, whose total must still be every call's sum
+    tel = efs.new_telemetry(DEV)
+    err2, sent, maxbits, calls = 0.0, 0, 0, 0
+    for d, seed in ((4093, 31), (4096 * 40, 32), (4096 * 4000 + 7, 33)):
+        g = synth.small_gradient(seed, d)
+        lam = synth.calibrate_lambda(g, 0.01)
+        st = HT(d)
+        for t in range(2):
+            gt = g if t == 0 else synth.small_gradient(seed + 100, d)
+            efs.ht_compress_telemetry(to_dev(gt), st.e, LR, lam, st.idx, st.val, st.ctr, tel)
+            e_prev = np.zeros(d, np.float32) if t == 0 else e_ref
+            _, _, e_ref, rk = oracle.ht(gt, e_prev, LR, lam)
+            err2 += float(np.sum(e_ref.astype(np.float64) ** 2))
+            sent += rk
+            maxbits = max(maxbits, int(np.max(bits(e_ref) & np.uint32(0x7FFFFFFF))))
+            calls += 1
+        assert_bits_equal(st.e.cpu().numpy(), e_ref, "e' d=%d" % d)
+    got = efs.read_telemetry(tel)
+    assert got["calls"] == calls and got["sent_total"] == sent
+    assert got["max_abs_bits"] == maxbits
+    assert abs(got["err2_total"] - err2) <= 1e-9 * err2
+    parts = np.frombuffer(tel.cpu().numpy().tobytes()[:256], dtype="<f8")
+    assert np.count_nonzero(parts) == 32  # the large call reaches every part
+
+
 def test_ht_telemetry_empty_and_all_sent():
     st = HT(4096 * 3 + 1)
     tel = efs.new_telemetry(DEV)
