@@ -500,7 +500,7 @@ def test_topk_ef_loop_matches_oracle_each_step():
 # n-worker average
 # ---------------------------------------------------------------------------
 
-@pytest.mark.parametrize("n", [1, 2, 3, 8])
+@pytest.mark.parametrize("n", [1, 2, 3, 8, 40])
 def test_accumulate_matches_oracle(n):
     d = 400_009
     lam = np.float32(2.2e-4)
