@@ -1,8 +1,9 @@
-"""The 25,557,032-element, 161-layer workload over 30 error-feedback steps
-with a fresh gradient each step: hard threshold, flat Top-k and layer-wise
-Top-k, every step's payload and residual bit-exact against the oracle.  The
-oracle's Top-k sorts the whole vector, so the run takes a few minutes: it
-runs when EFS_LONG_TESTS=1 is set, and is skipped otherwise."""
+"""Long error-feedback runs at full size, every step's payload and residual
+bit-exact against the oracle: the 25,557,032-element, 161-layer workload over
+30 steps (hard threshold, flat and layer-wise Top-k), and the 110e6-element
+heavy-tailed workload over 6 steps at k = 1 % (flat and layer-wise Top-k).
+The oracle's Top-k sorts the whole vector, so each takes a few minutes: they
+run when EFS_LONG_TESTS=1 is set, and are skipped otherwise."""
 import os
 
 import numpy as np
@@ -69,3 +70,42 @@ def test_thirty_ef_steps_of_the_benchmark_workload():
               % (t, n, efs.topk_took_bracket_path(ws), efs.topk_segmented_bracket_segments(sws)),
               flush=True)
     assert bracket_steps >= T // 2
+
+
+@pytest.mark.timeout(1200)
+def test_six_ef_steps_of_the_heavy_tailed_110m_workload_at_one_percent():
+    # 110e6 Student-t gradients in 200 layers: flat Top-k at k = 1.1 M and
+    # layer-wise Top-k at 1 % per layer, e carried over six steps (large k:
+    # millions of bracket candidates), every step bit-exact
+    T = 6
+    st = synth.Stream(3)
+    d = st.w.d
+    k = st.w.topk_k[0]
+    ks = synth.layerwise_k(st.bounds, 0.01)
+    kt = int(ks.sum())
+    e_tk, e_sg = (torch.zeros(d, device=DEV) for _ in range(2))
+    tidx = torch.empty(k, dtype=torch.int32, device=DEV)
+    tval = torch.empty(k, device=DEV)
+    ws = efs.new_topk_workspace(d, k, DEV)
+    ws.zero_()
+    sidx = torch.empty(kt, dtype=torch.int32, device=DEV)
+    sval = torch.empty(kt, device=DEV)
+    sws = efs.new_topk_segmented_workspace(ks.size, kt, DEV)
+    sws.zero_()
+    offd = torch.from_numpy(st.bounds.astype(np.int64)).to(DEV)
+    kd = torch.from_numpy(ks).to(DEV)
+    r_tk, r_sg = (np.zeros(d, np.float32) for _ in range(2))
+    for t in range(T):
+        g = st.gradient(t, threads=16)
+        gd = torch.from_numpy(g).to(DEV)
+        efs.topk_compress(gd, e_tk, synth.LR, k, tidx, tval, ws)
+        efs.topk_segmented_compress(gd, e_sg, synth.LR, offd, kd, sidx, sval, sws)
+        ti, tv, r_tk = oracle.topk(g, r_tk, synth.LR, k)
+        assert_payload_equal(tidx.cpu().numpy(), tval.cpu().numpy(), ti, tv, "topk t=%d" % t)
+        assert_bits_equal(e_tk.cpu().numpy(), r_tk, "topk e t=%d" % t)
+        si, sv, r_sg = oracle.topk_segmented(g, r_sg, synth.LR, st.bounds.astype(np.int64), ks)
+        assert_payload_equal(sidx.cpu().numpy(), sval.cpu().numpy(), si, sv, "layer-wise t=%d" % t)
+        assert_bits_equal(e_sg.cpu().numpy(), r_sg, "layer-wise e t=%d" % t)
+        print("step %d bit-exact (Top-k bracket %d, layers from the bracket %d)"
+              % (t, efs.topk_took_bracket_path(ws), efs.topk_segmented_bracket_segments(sws)),
+              flush=True)
