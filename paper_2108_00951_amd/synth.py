@@ -2,9 +2,12 @@
 
 This module holds no part of the compression arithmetic: it only draws the
 inputs (gradients g_t, per worker and iteration) with numpy's counter-free
-PCG64 generator keyed by a SeedSequence, and picks the parameters (lambda, k)
-that the workloads are quoted at.  Both the HIP path and the CPU oracle are
-fed from here.
+PCG64 generator keyed by a SeedSequence, and holds the workload parameters
+(sizes, densities, k, the layer-wise budgets).  Both the HIP path and the
+CPU oracle are fed from here.  The threshold lambda that gives a workload's
+first-step density is a selection on fl(lr * g_0), so it is computed by the
+oracle (a committed script stores each workload's value, read by
+`stored_lambda`).
 
 The paper trains real models (Table 1 of Appendix C lists ResNet-18 with
 11,173,962 parameters, an LSTM with 28,949,319 and NCF with 31,832,577);
@@ -197,19 +200,24 @@ def small_gradient(seed: int, d: int, scale: float = 1e-3) -> np.ndarray:
     return (rng.standard_normal(d, dtype=np.float32) * np.float32(scale))
 
 
-def calibrate_lambda(g0: np.ndarray, density: float, lr=LR) -> np.float32:
-    """Threshold giving the requested density at the first iteration.
+LAMBDA_FILE = "workload_lambdas.json"
 
-    With e_0 = 0 the first compressed vector is a = fl(lr * g_0).  For
-    K = round(density * d) the threshold is the K-th largest |a|, the upper
-    end of the interval (A_(K+1), A_(K)] of Lemma 3, so the first iteration
-    keeps exactly K coordinates when that magnitude is not tied.
-    """
-    a = np.abs(np.float32(lr) * g0.astype(np.float32, copy=False))
-    d = a.size
-    K = int(round(density * d))
-    K = min(max(K, 1), d)
-    return np.float32(np.partition(a, d - K)[d - K])
+
+def stored_lambda(workload_id: int, density: float, worker: int = 0) -> np.float32:
+    """The threshold of a workload at a first-step density, as stored by the
+    oracle's calibration script (the K-th largest |fl(lr * g_0)| of that
+    workload's first gradient, K = round(density * d)), bit for bit."""
+    import json
+    import os
+    path = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))),
+                        "tests", "golden", LAMBDA_FILE)
+    with open(path) as f:
+        table = json.load(f)
+    key = "%d/%g/%d" % (workload_id, density, worker)
+    if key not in table["lambda_bits"]:
+        raise KeyError("no stored threshold for workload %d at density %g (worker %d)"
+                       % (workload_id, density, worker))
+    return np.array([table["lambda_bits"][key]], dtype=np.uint32).view(np.float32)[0]
 
 
 def lambda_from_k(k: int) -> float:

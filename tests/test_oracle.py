@@ -606,7 +606,7 @@ def test_lambda_rule_matches_table5():
 
 def test_calibrated_lambda_gives_density():
     g = synth.small_gradient(3, 400_000)
-    lam = synth.calibrate_lambda(g, 0.01)
+    lam = oracle.calibrate_lambda(g, 0.01)
     _, _, _, k = oracle.ht(g, np.zeros_like(g), float(synth.LR), lam)
     assert k == 4000
 
@@ -619,3 +619,63 @@ def test_segment_layout_and_chunked_streams():
     part = st.gradient(0, start=123_457, stop=987_654)
     np.testing.assert_array_equal(full[123_457:987_654], part)
     assert abs(float(np.std(full)) - 1e-3) < 2e-5
+
+
+# ---------------------------------------------------------------------------
+# the multi-core variant returns the single-threaded oracle's bits
+# ---------------------------------------------------------------------------
+
+LR = np.float32(0.1)
+
+
+def _special_vector(d, seed):
+    rng = np.random.default_rng(seed)
+    g = (rng.standard_normal(d) * 1e-3).astype(np.float32)
+    if d >= 8:
+        g[:8] = np.array([np.nan, np.inf, -np.inf, -0.0, 0.0, 1e-45, -1e-45, 5e-39], np.float32)
+    q = (rng.integers(-6, 7, size=d) * 1e-4).astype(np.float32)   # many exact ties
+    return g, q
+
+
+@pytest.mark.parametrize("d", [0, 1, 5, 7, 4097, 100_003, 1_000_003])
+def test_multicore_oracle_matches_single_threaded(d):
+    assert oracle.mt_threads() >= 1
+    g, q = _special_vector(d, 900 + d)
+    e = np.zeros(d, np.float32)
+    e[::3] = np.float32(2e-5)
+    for vec in (g, q):
+        for lam in (np.float32(0.0), np.float32(2e-4), np.float32(np.inf)):
+            for cap in (None, d // 7):
+                a = oracle.ht(vec, e, LR, lam, cap=cap)
+                b = oracle.ht(vec, e, LR, lam, cap=cap, mt=True)
+                assert a[3] == b[3]
+                np.testing.assert_array_equal(a[0], b[0])
+                np.testing.assert_array_equal(bits(a[1]), bits(b[1]))
+                np.testing.assert_array_equal(bits(a[2]), bits(b[2]))
+        for k in sorted({0, 1, d // 3, d}):
+            a = oracle.topk(vec, e, LR, k)
+            b = oracle.topk(vec, e, LR, k, mt=True)
+            np.testing.assert_array_equal(a[0], b[0])
+            np.testing.assert_array_equal(bits(a[1]), bits(b[1]))
+            np.testing.assert_array_equal(bits(a[2]), bits(b[2]))
+    if d >= 7:
+        off = np.array([0, 1, d // 3, d // 3, d - 2, d], np.int64)
+        ks = np.array([1, d // 50 + 1, 3, 5, 10], np.int64)
+        for vec in (g, q):
+            a = oracle.topk_segmented(vec, e, LR, off, ks)
+            b = oracle.topk_segmented(vec, e, LR, off, ks, mt=True)
+            np.testing.assert_array_equal(a[0], b[0])
+            np.testing.assert_array_equal(bits(a[1]), bits(b[1]))
+            np.testing.assert_array_equal(bits(a[2]), bits(b[2]))
+        payloads = [oracle.ht(v, e, LR, np.float32(1e-4))[:2] for v in (g, q, g[::-1].copy())]
+        np.testing.assert_array_equal(bits(oracle.accumulate(payloads, d)),
+                                      bits(oracle.accumulate(payloads, d, mt=True)))
+
+
+def test_multicore_oracle_rejects_what_the_oracle_rejects():
+    with pytest.raises(ValueError):
+        oracle.accumulate([(np.array([5], np.int32), np.array([1.0], np.float32))], 5, mt=True)
+    with pytest.raises(ValueError):
+        oracle.topk_segmented(np.zeros(4, np.float32), np.zeros(4, np.float32), LR,
+                              np.array([0, 3, 2, 4], np.int64), np.array([1, 1, 1], np.int64),
+                              mt=True)
