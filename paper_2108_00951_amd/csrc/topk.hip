@@ -20,7 +20,9 @@
 //          key - lo.
 //   step3  every workgroup first decides the path: the bracket path only
 //          when the counts prove the k-th key lies inside the bracket
-//          (#(key > hi) <= k <= #(key >= lo), every bracket key collected).
+//          (#(key > hi) <= k <= #(key >= lo), every bracket key collected),
+//          and not when T is the key of zero with more ties to split than
+//          the tie list holds (see below).
 //          Bracket path: select T from the coarse then fine histogram, append
 //          the candidates with key > T (all key == T too when no tie is
 //          dropped), zero e at every kept coordinate.  Radix path: select the
@@ -522,8 +524,27 @@ __global__ __launch_bounds__(kBlock) void topk_step3_kernel(float *__restrict__ 
     const bool lead = blockIdx.x == 0 && tid == 0;
     const uint64_t above = c->emit & kCountMask;
     const uint64_t inside = c->cand & kCountMask;
-    const bool fast = c->bracket_on != 0u && above <= k && above + inside >= k &&
-                      inside <= ws.ccap;
+    bool fast = c->bracket_on != 0u && above <= k && above + inside >= k && inside <= ws.ccap;
+
+    // Bracket path: rank `need` among the candidates, coarse then fine.
+    const uint32_t need = fast ? k - uint32_t(above) : 0u;
+    uint32_t T = kNoKey, m = 0u, ties = 0u;
+    if (need > 0u) {
+        select_bin<kCoarse>(ws.coarse, need, ss.scan, ss.sel);
+        const uint32_t cb = ss.sel[0], above_c = ss.sel[1];
+        __syncthreads();
+        select_bin<kFinePerCoarse>(ws.fine + size_t(cb) * kFinePerCoarse, need - above_c, ss.scan,
+                                   ss.sel);
+        T = c->lo + cb * uint32_t(kFinePerCoarse) + ss.sel[0];
+        m = need - above_c - ss.sel[1];
+        ties = ss.sel[2];
+        __syncthreads();  // ss.sel is rewritten below
+        // Ties beyond the list are ranked by a scan of e after this kernel,
+        // and this kernel sets e to +0 at every pair it keeps; when T is the
+        // key of zero those cleared coordinates would read as ties.  The
+        // radix path ranks the ties before anything is cleared.
+        if (T == 0u && m < ties && ties > kTieList) fast = false;
+    }
     if (!fast) {
         // the pairs pass 1 sent are ignored: the radix path writes the whole
         // payload from slot 0 in the emit launch
@@ -538,19 +559,6 @@ __global__ __launch_bounds__(kBlock) void topk_step3_kernel(float *__restrict__ 
         return;
     }
 
-    // Bracket path: rank `need` among the candidates, coarse then fine.
-    const uint32_t need = k - uint32_t(above);
-    uint32_t T = kNoKey, m = 0u, ties = 0u;
-    if (need > 0u) {
-        select_bin<kCoarse>(ws.coarse, need, ss.scan, ss.sel);
-        const uint32_t cb = ss.sel[0], above_c = ss.sel[1];
-        __syncthreads();
-        select_bin<kFinePerCoarse>(ws.fine + size_t(cb) * kFinePerCoarse, need - above_c, ss.scan,
-                                   ss.sel);
-        T = c->lo + cb * uint32_t(kFinePerCoarse) + ss.sel[0];
-        m = need - above_c - ss.sel[1];
-        ties = ss.sel[2];
-    }
     const bool all_ties = m >= ties;
     if (lead) {
         c->fast = 1u;
