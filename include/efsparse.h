@@ -177,30 +177,61 @@ efs_status topk_segmented_compress(const float *g, float *e, int64_t d, float lr
                                    int32_t *idx, float *val, void *workspace,
                                    size_t workspace_bytes, void *stream);
 
-/* Exchange-and-average of n workers' payloads on one device (Algorithm 1):
+/* Exchange-and-average of n workers' payloads on one device (Algorithm 1:
+ * the average (1/n) sum_i Delta_i of the compressed updates; App. C.6.2,
+ * Algorithm 2: DECOMPRESS then AGGREGATE):
  *     out = (sum over w = 0..n-1, in that order, of decompress(payload_w)) / n
- * with fp32 adds in worker order and one IEEE division by (float)n.
+ * with fp32 adds in worker order and one IEEE division by (float)n at every
+ * coordinate (untouched coordinates are +0).
  *
  *   idx, val   HOST arrays of n_workers device pointers; payload w has
  *              indices idx[w][0..c_w) (distinct within one payload) and
  *              values val[w][0..c_w).
  *   counts     HOST array of n_workers device pointers to the uint32 count of
- *              each payload (word 0 of ht_compress's counter object), or NULL
- *              entries / a NULL array meaning c_w = caps[w].
- *   caps       HOST array of n_workers capacities; c_w = min(*counts[w], caps[w]).
- *   d          length of out.
+ *              each payload (word 0 of ht_compress's counter object, which
+ *              stays on the device), or NULL entries / a NULL array meaning
+ *              c_w = caps[w].
+ *   caps       HOST array of n_workers capacities; c_w = min(*counts[w],
+ *              caps[w]).  A count above its capacity (a truncated
+ *              hard-threshold payload) is averaged over its caps[w] pairs and
+ *              reported in the status word (EFS_SPARSE_TRUNCATED).
+ *   n_workers  1 <= n_workers <= EFS_MAX_WORKERS; sum of caps <= 2^32 - 1.
+ *   d          length of out; d == 0 is a no-op.
  *   out        [d] fp32, 16-byte aligned, overwritten.
- * Payload entries with an index outside [0, d) are ignored. */
+ *   workspace  device memory of at least
+ *              sparse_accumulate_workspace_bytes(n_workers, d, sum of caps)
+ *              bytes, 16-byte aligned: a 256-byte control block, an 8-byte
+ *              counter and a 4-byte segment start per (range of 8192
+ *              coordinates, worker), and 8 bytes per payload slot for the
+ *              pairs grouped by range.  Contents need no initialisation: each
+ *              counter carries the 40-bit epoch of the call that wrote it
+ *              (the control block's epoch, advanced by every call), so a
+ *              counter of an earlier call reads as zero, as does arbitrary
+ *              content except when its epoch bits equal the current epoch
+ *              (probability 2^-40 per counter for random bytes).  Not
+ *              shareable between concurrent calls.
+ * Payload entries with an index outside [0, d) are skipped and reported in
+ * the status word (EFS_SPARSE_BAD_INDEX).  The status word is the uint32 at
+ * sparse_status_offset() in the workspace: the EFS_SPARSE_* bits of the last
+ * completed call (0: every payload was whole and in range).  The counts are
+ * read on the device, so these are reported there and not as an efs_status. */
+#define EFS_MAX_WORKERS 64
+#define EFS_SPARSE_TRUNCATED 1u
+#define EFS_SPARSE_BAD_INDEX 2u
+size_t sparse_accumulate_workspace_bytes(int32_t n_workers, int64_t d, int64_t total_cap);
+size_t sparse_status_offset(void);
 efs_status sparse_accumulate(const int32_t *const *idx, const float *const *val,
                              const uint32_t *const *counts, const int64_t *caps,
-                             int32_t n_workers, int64_t d, float *out, void *stream);
+                             int32_t n_workers, int64_t d, float *out, void *workspace,
+                             size_t workspace_bytes, void *stream);
 
 /* Exchange-and-average fused with the model update that follows it.
  *
  *   avg = (sum over w = 0..n-1, in that order, of decompress(payload_w)) / n
  * exactly as sparse_accumulate computes it (fp32 adds in worker order, one
  * IEEE division by (float)n), then, by mode:
- *   EFS_APPLY_AVERAGE   x = avg at every coordinate (x is the output).
+ *   EFS_APPLY_AVERAGE   x = avg at every coordinate (x is the output; the
+ *                       same call as sparse_accumulate).
  *   EFS_APPLY_SGD       x = x - avg (Algorithm 1, model update).  Only
  *                       coordinates that some payload touches are written;
  *                       the others keep x, which equals x - (+0) for every
@@ -213,25 +244,16 @@ efs_status sparse_accumulate(const int32_t *const *idx, const float *const *val,
  * Every operation is one separately rounded fp32 operation, in the order
  * written (no fused multiply-add).
  *
- *   idx, val, counts, caps, n_workers   as for sparse_accumulate, with
- *              1 <= n_workers <= EFS_APPLY_MAX_WORKERS and
- *              sum of caps <= 2^32 - 1.  Entries with an index outside
- *              [0, d) are ignored.
+ *   idx, val, counts, caps, n_workers, d, workspace, status word
+ *              as for sparse_accumulate (the same workspace layout).
  *   x          [d] fp32, 16-byte aligned, read and written in place (mode
  *              EFS_APPLY_AVERAGE only writes it).  Must not overlap a payload.
  *   m          [d] fp32 momentum, 16-byte aligned, read and written in place;
  *              used by EFS_APPLY_MOMENTUM only (may be NULL otherwise).
  *   beta, gamma  momentum factor and learning rate (finite); used by
  *              EFS_APPLY_MOMENTUM only.
- *   workspace  device memory of at least
- *              sparse_apply_workspace_bytes(n_workers, d, sum of caps) bytes,
- *              16-byte aligned: one counter per range of 8192
- *              coordinates, and 8 bytes per payload slot for the pairs
- *              grouped by range.  Results never depend on its prior
- *              contents.  Not shareable between concurrent calls.
  * Returns EFS_ESPACE if the workspace is too small, EFS_EINVAL on any other
  * invalid argument; nothing is launched then.  d == 0 is a no-op. */
-#define EFS_APPLY_MAX_WORKERS 32
 enum { EFS_APPLY_AVERAGE = 0, EFS_APPLY_SGD = 1, EFS_APPLY_MOMENTUM = 2 };
 
 /* Workspace bytes for sparse_apply; 0 if the arguments are out of range. */
@@ -268,8 +290,10 @@ const char *efs_last_error_message(void);
  * EFS_EHIP when the HIP runtime holds an error left by an earlier
  * asynchronous launch on this thread (hipPeekAtLastError, not cleared);
  * otherwise the last non-OK status any call returned on this thread since
- * the previous efs_last_error (which clears it), or EFS_OK.  Payload
- * overflow is not an error: compare the count with the capacity. */
+ * the previous efs_last_error (which clears it), or EFS_OK.  Conditions
+ * that only the device sees are reported on the device: a hard-threshold
+ * count above the capacity in the counter object (compare it with cap), a
+ * truncated payload or an index out of range in the average's status word. */
 efs_status efs_last_error(void);
 
 #ifdef __cplusplus

@@ -17,6 +17,7 @@ LIB_PATH = os.path.join(HERE, "libefsparse.so")
 
 EFS_OK, EFS_EINVAL, EFS_ESPACE, EFS_EHIP = 0, 1, 2, 3
 COUNTER_WORDS = 4
+MAX_WORKERS = 64
 
 _lib = None
 
@@ -62,8 +63,12 @@ def declare(lib):
     lib.topk_compress.argtypes = [vp, vp, i64, f32, i64, vp, vp, vp, ctypes.c_size_t, vp]
     lib.topk_compress.restype = ctypes.c_int
     lib.sparse_accumulate.argtypes = [ctypes.POINTER(vp), ctypes.POINTER(vp), ctypes.POINTER(vp),
-                                      ctypes.POINTER(i64), i32, i64, vp, vp]
+                                      ctypes.POINTER(i64), i32, i64, vp, vp, ctypes.c_size_t, vp]
     lib.sparse_accumulate.restype = ctypes.c_int
+    lib.sparse_accumulate_workspace_bytes.argtypes = [i32, i64, i64]
+    lib.sparse_accumulate_workspace_bytes.restype = ctypes.c_size_t
+    lib.sparse_status_offset.argtypes = []
+    lib.sparse_status_offset.restype = ctypes.c_size_t
     lib.topk_segmented_workspace_bytes.argtypes = [i32, i64]
     lib.topk_segmented_workspace_bytes.restype = ctypes.c_size_t
     lib.topk_segmented_status_offset.argtypes = []
@@ -296,12 +301,23 @@ def _payload_arrays(payloads: Sequence[Tuple]):
     return idx_arr, val_arr, cnt_arr, caps
 
 
-def sparse_accumulate(payloads: Sequence[Tuple], d: int, out, stream=None) -> None:
+def sparse_accumulate(payloads: Sequence[Tuple], d: int, out, workspace, stream=None) -> None:
     """Average of n payloads into out; see sparse_accumulate in include/efsparse.h.
 
-    payloads: sequence of (idx, val, counter_or_None).
+    payloads: sequence of (idx, val, counter_or_None); workspace from
+    new_apply_workspace (the average and the fused update share its layout).
     """
-    prepare_sparse_accumulate(payloads, d, out, stream)()
+    prepare_sparse_accumulate(payloads, d, out, workspace, stream)()
+
+
+SPARSE_TRUNCATED, SPARSE_BAD_INDEX = 1, 2
+
+
+def sparse_status(workspace) -> int:
+    """EFS_SPARSE_* bits of the last completed sparse_accumulate / sparse_apply
+    on this workspace (synchronises)."""
+    off = int(load_library().sparse_status_offset())
+    return int(workspace[off:off + 4].cpu().numpy().view("<u4")[0])
 
 
 APPLY_AVERAGE, APPLY_SGD, APPLY_MOMENTUM = 0, 1, 2
@@ -312,7 +328,8 @@ def sparse_apply_workspace_bytes(n_workers: int, d: int, total_cap: int) -> int:
 
 
 def new_apply_workspace(payloads: Sequence[Tuple], d: int, device="cuda"):
-    """A workspace for sparse_apply over payloads of these capacities."""
+    """A workspace for sparse_accumulate or sparse_apply over payloads of
+    these capacities."""
     import torch
     total = sum(int(p[0].numel()) for p in payloads)
     nbytes = sparse_apply_workspace_bytes(len(payloads), d, total)
@@ -352,17 +369,18 @@ def sparse_apply(payloads: Sequence[Tuple], d: int, mode: int, x, workspace, m=N
     prepare_sparse_apply(payloads, d, mode, x, workspace, m, beta, gamma, stream)()
 
 
-def prepare_sparse_accumulate(payloads: Sequence[Tuple], d: int, out, stream=None):
+def prepare_sparse_accumulate(payloads: Sequence[Tuple], d: int, out, workspace, stream=None):
     """sparse_accumulate with its arguments marshalled once (see
     prepare_sparse_apply)."""
     import torch
     lib = load_library()
     _require(out, torch.float32, "out")
+    _require(workspace, torch.uint8, "workspace")
     if out.numel() != d:
         raise ValueError("out must have d elements")
     idx_arr, val_arr, cnt_arr, caps = _payload_arrays(payloads)
-    args = (idx_arr, val_arr, cnt_arr, caps, len(payloads), int(d), _ptr(out),
-            _stream_handle(stream))
+    args = (idx_arr, val_arr, cnt_arr, caps, len(payloads), int(d), _ptr(out), _ptr(workspace),
+            workspace.numel(), _stream_handle(stream))
     fn = lib.sparse_accumulate
 
     def call():

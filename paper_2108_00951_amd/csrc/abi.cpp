@@ -12,7 +12,9 @@
 #include "launch.hpp"
 #include "device_common.hpp"
 
-static_assert(efs::kMaxApplyWorkers == EFS_APPLY_MAX_WORKERS, "worker limit differs from the header");
+static_assert(efs::kMaxApplyWorkers == EFS_MAX_WORKERS, "worker limit differs from the header");
+static_assert(efs::kSparseTruncated == EFS_SPARSE_TRUNCATED, "status bit differs from the header");
+static_assert(efs::kSparseBadIndex == EFS_SPARSE_BAD_INDEX, "status bit differs from the header");
 static_assert(efs::kMaxSegments == EFS_SEG_MAX, "segment limit differs from the header");
 static_assert(sizeof(efs::Telemetry) == EFS_TELEMETRY_BYTES, "telemetry layout differs from the header");
 
@@ -158,30 +160,6 @@ efs_status topk_compress(const float *g, float *e, int64_t d, float lr, int64_t 
                         "topk_compress");
 }
 
-efs_status sparse_accumulate(const int32_t *const *idx, const float *const *val,
-                             const uint32_t *const *counts, const int64_t *caps,
-                             int32_t n_workers, int64_t d, float *out, void *stream) {
-    if (n_workers < 1) return fail(EFS_EINVAL, "sparse_accumulate: n_workers=%d < 1", n_workers);
-    if (d < 0 || d > kMaxLen) return fail(EFS_EINVAL, "sparse_accumulate: d=%lld outside [0, 2^31-1]", (long long)d);
-    if (idx == nullptr || val == nullptr || caps == nullptr)
-        return fail(EFS_EINVAL, "sparse_accumulate: idx, val and caps must be host arrays");
-    if (d > 0 && (out == nullptr || !aligned(out, 16)))
-        return fail(EFS_EINVAL, "sparse_accumulate: out must be non-NULL and 16-byte aligned");
-    for (int32_t w = 0; w < n_workers; ++w) {
-        if (caps[w] < 0 || caps[w] > kMaxLen)
-            return fail(EFS_EINVAL, "sparse_accumulate: caps[%d]=%lld outside [0, 2^31-1]", w, (long long)caps[w]);
-        if (caps[w] > 0 && (idx[w] == nullptr || val[w] == nullptr))
-            return fail(EFS_EINVAL, "sparse_accumulate: payload %d has a NULL pointer", w);
-        if (!aligned(idx[w], 4) || !aligned(val[w], 4))
-            return fail(EFS_EINVAL, "sparse_accumulate: payload %d is not 4-byte aligned", w);
-        if (counts != nullptr && counts[w] != nullptr && !aligned(counts[w], 4))
-            return fail(EFS_EINVAL, "sparse_accumulate: count %d is not 4-byte aligned", w);
-    }
-    return check_launch(efs::launch_accumulate(idx, val, counts, caps, n_workers, d, out,
-                                               static_cast<hipStream_t>(stream)),
-                        "sparse_accumulate");
-}
-
 size_t topk_segmented_workspace_bytes(int32_t nseg, int64_t k_total) {
     if (nseg < 1 || nseg > efs::kMaxSegments || k_total < 0 || k_total > kMaxLen) return 0;
     return efs::topk_segmented_workspace_size(nseg, k_total);
@@ -225,47 +203,78 @@ size_t sparse_apply_workspace_bytes(int32_t n_workers, int64_t d, int64_t total_
     return efs::apply_workspace_size(n_workers, d, total_cap);
 }
 
+size_t sparse_accumulate_workspace_bytes(int32_t n_workers, int64_t d, int64_t total_cap) {
+    return sparse_apply_workspace_bytes(n_workers, d, total_cap);
+}
+
+size_t sparse_status_offset(void) { return efs::apply_status_offset(); }
+
+// Checks shared by sparse_accumulate and sparse_apply: the payload arrays,
+// the output (x), the workspace.  Returns EFS_OK when the call may proceed.
+static efs_status check_payloads(const char *name, const int32_t *const *idx,
+                                 const float *const *val, const uint32_t *const *counts,
+                                 const int64_t *caps, int32_t n_workers, int64_t d, const float *x,
+                                 const void *workspace, size_t workspace_bytes) {
+    if (n_workers < 1 || n_workers > efs::kMaxApplyWorkers)
+        return fail(EFS_EINVAL, "%s: n_workers=%d outside [1, %d]", name, n_workers,
+                    efs::kMaxApplyWorkers);
+    if (d < 0 || d > kMaxLen) return fail(EFS_EINVAL, "%s: d=%lld outside [0, 2^31-1]", name, (long long)d);
+    if (idx == nullptr || val == nullptr || caps == nullptr)
+        return fail(EFS_EINVAL, "%s: idx, val and caps must be host arrays", name);
+    if (d > 0 && (x == nullptr || !aligned(x, 16)))
+        return fail(EFS_EINVAL, "%s: the output must be non-NULL and 16-byte aligned", name);
+    int64_t total = 0;
+    for (int32_t w = 0; w < n_workers; ++w) {
+        if (caps[w] < 0 || caps[w] > kMaxLen)
+            return fail(EFS_EINVAL, "%s: caps[%d]=%lld outside [0, 2^31-1]", name, w, (long long)caps[w]);
+        if (caps[w] > 0 && (idx[w] == nullptr || val[w] == nullptr))
+            return fail(EFS_EINVAL, "%s: payload %d has a NULL pointer", name, w);
+        if (!aligned(idx[w], 4) || !aligned(val[w], 4))
+            return fail(EFS_EINVAL, "%s: payload %d is not 4-byte aligned", name, w);
+        if (counts != nullptr && counts[w] != nullptr && !aligned(counts[w], 4))
+            return fail(EFS_EINVAL, "%s: count %d is not 4-byte aligned", name, w);
+        total += caps[w];
+    }
+    if (total > int64_t(UINT32_MAX))
+        return fail(EFS_EINVAL, "%s: total capacity %lld exceeds 2^32-1 pairs", name, (long long)total);
+    if (d == 0) return EFS_OK;
+    if (workspace == nullptr || !aligned(workspace, 16))
+        return fail(EFS_EINVAL, "%s: workspace must be non-NULL and 16-byte aligned", name);
+    const size_t need = efs::apply_workspace_size(n_workers, d, total);
+    if (workspace_bytes < need)
+        return fail(EFS_ESPACE, "%s: workspace has %zu bytes, needs %zu", name, workspace_bytes, need);
+    return EFS_OK;
+}
+
+efs_status sparse_accumulate(const int32_t *const *idx, const float *const *val,
+                             const uint32_t *const *counts, const int64_t *caps,
+                             int32_t n_workers, int64_t d, float *out, void *workspace,
+                             size_t workspace_bytes, void *stream) {
+    const efs_status s = check_payloads("sparse_accumulate", idx, val, counts, caps, n_workers, d,
+                                        out, workspace, workspace_bytes);
+    if (s != EFS_OK || d == 0) return s;
+    return check_launch(efs::launch_apply(idx, val, counts, caps, n_workers, d, EFS_APPLY_AVERAGE,
+                                          out, nullptr, 0.0f, 0.0f, workspace,
+                                          static_cast<hipStream_t>(stream)),
+                        "sparse_accumulate");
+}
+
 efs_status sparse_apply(const int32_t *const *idx, const float *const *val,
                         const uint32_t *const *counts, const int64_t *caps, int32_t n_workers,
                         int64_t d, int mode, float *x, float *m, float beta, float gamma,
                         void *workspace, size_t workspace_bytes, void *stream) {
-    if (n_workers < 1 || n_workers > efs::kMaxApplyWorkers)
-        return fail(EFS_EINVAL, "sparse_apply: n_workers=%d outside [1, %d]", n_workers,
-                    efs::kMaxApplyWorkers);
-    if (d < 0 || d > kMaxLen) return fail(EFS_EINVAL, "sparse_apply: d=%lld outside [0, 2^31-1]", (long long)d);
     if (mode < EFS_APPLY_AVERAGE || mode > EFS_APPLY_MOMENTUM)
         return fail(EFS_EINVAL, "sparse_apply: mode %d is not one of EFS_APPLY_*", mode);
-    if (idx == nullptr || val == nullptr || caps == nullptr)
-        return fail(EFS_EINVAL, "sparse_apply: idx, val and caps must be host arrays");
-    if (d > 0 && (x == nullptr || !aligned(x, 16)))
-        return fail(EFS_EINVAL, "sparse_apply: x must be non-NULL and 16-byte aligned");
-    if (mode == EFS_APPLY_MOMENTUM) {
-        if (d > 0 && (m == nullptr || !aligned(m, 16)))
+    if (mode == EFS_APPLY_MOMENTUM && d > 0) {
+        if (m == nullptr || !aligned(m, 16))
             return fail(EFS_EINVAL, "sparse_apply: m must be non-NULL and 16-byte aligned");
-        if (d > 0 && m == x) return fail(EFS_EINVAL, "sparse_apply: m and x must not alias");
-        if (!std::isfinite(beta) || !std::isfinite(gamma))
-            return fail(EFS_EINVAL, "sparse_apply: beta and gamma must be finite");
+        if (m == x) return fail(EFS_EINVAL, "sparse_apply: m and x must not alias");
     }
-    int64_t total = 0;
-    for (int32_t w = 0; w < n_workers; ++w) {
-        if (caps[w] < 0 || caps[w] > kMaxLen)
-            return fail(EFS_EINVAL, "sparse_apply: caps[%d]=%lld outside [0, 2^31-1]", w, (long long)caps[w]);
-        if (caps[w] > 0 && (idx[w] == nullptr || val[w] == nullptr))
-            return fail(EFS_EINVAL, "sparse_apply: payload %d has a NULL pointer", w);
-        if (!aligned(idx[w], 4) || !aligned(val[w], 4))
-            return fail(EFS_EINVAL, "sparse_apply: payload %d is not 4-byte aligned", w);
-        if (counts != nullptr && counts[w] != nullptr && !aligned(counts[w], 4))
-            return fail(EFS_EINVAL, "sparse_apply: count %d is not 4-byte aligned", w);
-        total += caps[w];
-    }
-    if (total > int64_t(UINT32_MAX))
-        return fail(EFS_EINVAL, "sparse_apply: total capacity %lld exceeds 2^32-1 pairs", (long long)total);
-    if (d == 0) return EFS_OK;
-    if (workspace == nullptr || !aligned(workspace, 16))
-        return fail(EFS_EINVAL, "sparse_apply: workspace must be non-NULL and 16-byte aligned");
-    const size_t need = efs::apply_workspace_size(n_workers, d, total);
-    if (workspace_bytes < need)
-        return fail(EFS_ESPACE, "sparse_apply: workspace has %zu bytes, needs %zu", workspace_bytes, need);
+    if (mode == EFS_APPLY_MOMENTUM && (!std::isfinite(beta) || !std::isfinite(gamma)))
+        return fail(EFS_EINVAL, "sparse_apply: beta and gamma must be finite");
+    const efs_status s = check_payloads("sparse_apply", idx, val, counts, caps, n_workers, d, x,
+                                        workspace, workspace_bytes);
+    if (s != EFS_OK || d == 0) return s;
     return check_launch(efs::launch_apply(idx, val, counts, caps, n_workers, d, mode, x, m, beta,
                                           gamma, workspace, static_cast<hipStream_t>(stream)),
                         "sparse_apply");

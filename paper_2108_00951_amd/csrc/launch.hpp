@@ -17,10 +17,6 @@ size_t topk_path_flag_offset();
 hipError_t launch_topk(const float *g, float *e, int64_t d, float lr, int64_t k,
                        int32_t *idx, float *val, void *workspace, hipStream_t stream);
 
-hipError_t launch_accumulate(const int32_t *const *idx, const float *const *val,
-                             const uint32_t *const *counts, const int64_t *caps,
-                             int32_t n, int64_t d, float *out, hipStream_t stream);
-
 // Layer-wise Top-k (topk_seg.hip).
 constexpr int32_t kMaxSegments = 1 << 16;
 size_t topk_segmented_workspace_size(int32_t nseg, int64_t k_total);
@@ -30,9 +26,14 @@ hipError_t launch_topk_segmented(const float *g, float *e, int64_t d, float lr, 
                                  const int64_t *offsets, const int64_t *k, int64_t k_total,
                                  int32_t *idx, float *val, void *workspace, hipStream_t stream);
 
-// Exchange-and-average fused with the model update (apply.hip).
-constexpr int kMaxApplyWorkers = 32;
+// Exchange-and-average, alone (mode 0) or fused with the model update
+// (apply.hip).  Status bits of the last call, at apply_status_offset() in the
+// workspace.
+constexpr int kMaxApplyWorkers = 64;
+constexpr uint32_t kSparseTruncated = 1u;   // a count exceeded its payload's capacity
+constexpr uint32_t kSparseBadIndex = 2u;    // an index outside [0, d) was ignored
 size_t apply_workspace_size(int32_t n, int64_t d, int64_t total_cap);
+size_t apply_status_offset();
 hipError_t launch_apply(const int32_t *const *idx, const float *const *val,
                         const uint32_t *const *counts, const int64_t *caps, int32_t n,
                         int64_t d, int mode, float *x, float *m, float beta, float gamma,

@@ -112,13 +112,24 @@ def test_accumulate_rejects_bad_arguments(lib):
     idx = (vp * 2)(fake, fake)
     val = (vp * 2)(fake, fake)
     caps = (ctypes.c_int64 * 2)(5, 5)
-    assert lib.sparse_accumulate(idx, val, None, caps, 0, 10, fake, None) == binding.EFS_EINVAL
-    assert lib.sparse_accumulate(idx, val, None, caps, 2, -1, fake, None) == binding.EFS_EINVAL
-    assert lib.sparse_accumulate(idx, val, None, caps, 2, 10, fake + 4, None) == binding.EFS_EINVAL
-    bad = (ctypes.c_int64 * 2)(5, -1)
-    assert lib.sparse_accumulate(idx, val, None, bad, 2, 10, fake, None) == binding.EFS_EINVAL
-    nul = (vp * 2)(fake, None)
-    assert lib.sparse_accumulate(nul, val, None, caps, 2, 10, fake, None) == binding.EFS_EINVAL
+    need = lib.sparse_accumulate_workspace_bytes(2, 10, 10)
+    assert need > 0 and need == lib.sparse_apply_workspace_bytes(2, 10, 10)
+
+    def call(idx=idx, val=val, caps=caps, n=2, d=10, out=fake, ws=fake, ws_bytes=need):
+        return lib.sparse_accumulate(idx, val, None, caps, n, d, out, ws, ws_bytes, None)
+
+    assert call(n=0) == binding.EFS_EINVAL
+    assert call(n=binding.MAX_WORKERS + 1) == binding.EFS_EINVAL
+    assert call(d=-1) == binding.EFS_EINVAL
+    assert call(out=fake + 4) == binding.EFS_EINVAL
+    assert call(caps=(ctypes.c_int64 * 2)(5, -1)) == binding.EFS_EINVAL
+    assert call(idx=(vp * 2)(fake, None)) == binding.EFS_EINVAL
+    assert call(ws=None) == binding.EFS_EINVAL
+    assert call(ws=fake + 4) == binding.EFS_EINVAL
+    assert call(ws_bytes=need - 1) == binding.EFS_ESPACE
+    assert call(d=0, out=None, ws=None, ws_bytes=0) == binding.EFS_OK   # d == 0: nothing to do
+    assert lib.sparse_accumulate_workspace_bytes(binding.MAX_WORKERS + 1, 10, 10) == 0
+    assert lib.sparse_status_offset() < 256
     assert lib.efs_copy_probe(fake + 4, fake, 8, None) == binding.EFS_EINVAL
 
 
@@ -149,7 +160,7 @@ def test_apply_rejects_bad_arguments(lib):
 
     cases = [
         (dict(n=0), binding.EFS_EINVAL),
-        (dict(n=33), binding.EFS_EINVAL),
+        (dict(n=binding.MAX_WORKERS + 1), binding.EFS_EINVAL),
         (dict(d=-1), binding.EFS_EINVAL),
         (dict(mode=3), binding.EFS_EINVAL),
         (dict(mode=-1), binding.EFS_EINVAL),
@@ -178,7 +189,7 @@ def test_apply_rejects_bad_arguments(lib):
 
 def test_apply_workspace_size(lib):
     assert lib.sparse_apply_workspace_bytes(0, 100, 10) == 0
-    assert lib.sparse_apply_workspace_bytes(33, 100, 10) == 0
+    assert lib.sparse_apply_workspace_bytes(binding.MAX_WORKERS + 1, 100, 10) == 0
     assert lib.sparse_apply_workspace_bytes(2, -1, 10) == 0
     assert lib.sparse_apply_workspace_bytes(2, 100, 2 ** 32) == 0
     a = lib.sparse_apply_workspace_bytes(8, 25_600_000, 0)
@@ -226,3 +237,4 @@ def test_binding_sizes_match_the_header():
     text = open(os.path.join(ROOT, "include", "efsparse.h")).read()
     defs = dict(re.findall(r"#define (EFS_\w+) (\d+)", text))
     assert int(defs["EFS_TELEMETRY_BYTES"]) == binding.TELEMETRY_BYTES
+    assert int(defs["EFS_MAX_WORKERS"]) == binding.MAX_WORKERS

@@ -173,6 +173,9 @@ def test_apply_ignores_out_of_range_indices():
     p_dev = [(dev(idx), dev(val)), (dev(idx[:1]), dev(val[:1]))]
     p_ref = [(idx[keep], val[keep]), (idx[:1], val[:1])]
     check_all_modes(p_dev, p_ref, d, 9)
+    ws = efs.new_apply_workspace(p_dev, d, DEV)
+    run_apply(p_dev, d, efs.APPLY_SGD, np.zeros(d, np.float32), ws=ws)
+    assert efs.sparse_status(ws) == efs.SPARSE_BAD_INDEX
 
 
 def test_apply_one_worker_signed_zeros():
@@ -208,13 +211,15 @@ def test_apply_count_larger_than_capacity():
     ctr = efs.new_counter(DEV)
     ctr[0] = 100_000
     p_dev = [(dev(idx), dev(val), ctr)]
-    got, _ = run_apply(p_dev, d, efs.APPLY_AVERAGE, np.zeros(d, np.float32))
+    ws = efs.new_apply_workspace(p_dev, d, DEV)
+    got, _ = run_apply(p_dev, d, efs.APPLY_AVERAGE, np.zeros(d, np.float32), ws=ws)
     assert_bits_equal(got, oracle.accumulate([(idx, val)], d))
+    assert efs.sparse_status(ws) == efs.SPARSE_TRUNCATED
 
 
 def test_apply_max_workers():
     d = 8192 + 1000
-    n = 32
+    n = efs.MAX_WORKERS
     rng = np.random.default_rng(13)
     p_dev, p_ref = [], []
     for w in range(n):
@@ -222,7 +227,7 @@ def test_apply_max_workers():
         val = rng.standard_normal(2000).astype(np.float32)
         p_dev.append((dev(idx), dev(val)))
         p_ref.append((idx, val))
-    say("apply n=32")
+    say("apply n=%d" % n)
     check_all_modes(p_dev, p_ref, d, 13)
 
 

@@ -7,6 +7,7 @@ replays."""
 import numpy as np
 import pytest
 
+import oracle
 from paper_2108_00951_amd import synth
 from tests._checks import assert_bits_equal
 
@@ -33,11 +34,12 @@ class Step:
         self.ws = efs.new_topk_workspace(d, k, DEV)
         self.ws.zero_()
         self.out = torch.empty(d, dtype=torch.float32, device=DEV)
+        self.aws = efs.new_apply_workspace([(self.idx, self.val, self.ctr)], d, DEV)
 
     def run(self):
         efs.ht_compress(self.g, self.e_ht, LR, self.lam, self.idx, self.val, self.ctr)
         efs.topk_compress(self.g, self.e_tk, LR, self.k, self.tidx, self.tval, self.ws)
-        efs.sparse_accumulate([(self.idx, self.val, self.ctr)], self.d, self.out)
+        efs.sparse_accumulate([(self.idx, self.val, self.ctr)], self.d, self.out, self.aws)
 
     def result(self):
         n = efs.counter_value(self.ctr)
@@ -52,7 +54,7 @@ class Step:
 def test_step_replays_in_a_graph():
     d, k, steps = 300_007, 3000, 6
     pool = [synth.small_gradient(700 + t, d) for t in range(steps)]
-    lam = synth.calibrate_lambda(pool[0], 0.01)
+    lam = oracle.calibrate_lambda(pool[0], 0.01)
 
     eager = Step(d, k, lam)
     want = []

@@ -77,7 +77,7 @@ SIZES = [1, 3, 63, 64, 65, 1023, 4095, 4096, 4097, 8191, 12_289, 100_003, 1_000_
 def test_ht_ef_loop_matches_oracle(d, unaligned):
     say("ht parity d=%d unaligned=%s" % (d, unaligned))
     gs = [synth.small_gradient(10 + t, d) for t in range(3)]
-    lam = synth.calibrate_lambda(gs[0], 0.01)
+    lam = oracle.calibrate_lambda(gs[0], 0.01)
     st = HT(d, unaligned=unaligned)
     e_ref = np.zeros(d, dtype=np.float32)
     for t in range(3):
@@ -135,7 +135,7 @@ def test_ht_empty_vector():
 def test_ht_capacity_overflow():
     d = 300_007
     g = synth.small_gradient(3, d)
-    lam = synth.calibrate_lambda(g, 0.05)
+    lam = oracle.calibrate_lambda(g, 0.05)
     cap = 1000
     st = HT(d, cap=cap)
     gi, gv, ge, gk = st.step(g, lam)
@@ -165,7 +165,7 @@ def test_ht_counter_returns_to_zero_between_calls():
 def test_ht_repeat_is_deterministic():
     d = 1_000_000
     g = synth.small_gradient(5, d)
-    lam = synth.calibrate_lambda(g, 0.02)
+    lam = oracle.calibrate_lambda(g, 0.02)
     outs = []
     for _ in range(3):
         st = HT(d)
@@ -184,7 +184,7 @@ def test_ht_telemetry_totals(unaligned):
     # |e'|, accumulated over an EF loop, against the oracle's residuals
     d, T = 1_000_003, 6
     gs = [synth.small_gradient(500 + t, d) for t in range(T)]
-    lam = synth.calibrate_lambda(gs[0], 0.005)
+    lam = oracle.calibrate_lambda(gs[0], 0.005)
     st = HT(d, unaligned=unaligned)
     tel = efs.new_telemetry(DEV)
     e_ref = np.zeros(d, dtype=np.float32)
@@ -214,7 +214,7 @@ def test_ht_telemetry_object_shared_by_calls_of_different_sizes():
     err2, sent, maxbits, calls = 0.0, 0, 0, 0
     for d, seed in ((4093, 31), (4096 * 40, 32), (4096 * 4000 + 7, 33)):
         g = synth.small_gradient(seed, d)
-        lam = synth.calibrate_lambda(g, 0.01)
+        lam = oracle.calibrate_lambda(g, 0.01)
         st = HT(d)
         for t in range(2):
             gt = g if t == 0 else synth.small_gradient(seed + 100, d)
@@ -419,6 +419,37 @@ def test_topk_bracket_path_splits_ties(levels):
     assert st.bracket()
 
 
+@pytest.mark.parametrize("neg_zero", [False, True])
+def test_topk_zero_threshold_with_many_ties_on_one_workspace(neg_zero):
+    # fewer than k non-zero entries: the threshold key is that of zero and
+    # ~200k zeros tie at it, far more than the bracket path ranks from a
+    # list.  The second and third calls start from the first call's
+    # threshold (0), so their bracket holds every zero; the ties must still
+    # go to the lowest indices, none of them a coordinate already sent.
+    d, k = 300_007, 150_000
+    st = TopkState(d, k)
+    rng = np.random.default_rng(2024 + neg_zero)
+    e = np.zeros(d, np.float32)
+    if neg_zero:
+        # -0 + lr * -0 is -0: both signs of zero among the tied keys
+        e[rng.random(d) < 0.5] = np.float32(-0.0)
+    paths = []
+    for t in range(3):
+        g = np.zeros(d, np.float32)
+        if neg_zero:
+            g[rng.random(d) < 0.5] = np.float32(-0.0)
+        nz = rng.choice(d, 100_000, replace=False)
+        g[nz] = (rng.standard_normal(nz.size) * 1e-3).astype(np.float32)
+        gi, gv, ge = st.step(g, k, e)
+        ri, rv, re = oracle.topk(g, e, LR, k)
+        assert np.unique(gi).size == k, "call %d: duplicate indices in the payload" % t
+        assert_payload_equal(gi, gv, ri, rv, "zero threshold, call %d" % t)
+        assert_bits_equal(ge, re, "zero threshold, call %d" % t)
+        paths.append(st.bracket())
+        e = re
+    say("zero threshold calls, bracket path per call: %s" % paths)
+
+
 def test_topk_bracket_with_many_candidates():
     # |p| uniform in [0.9, 1.1]: the bracket around the previous threshold
     # (the 90th percentile) holds ~40 % of the vector, so the bracket path
@@ -513,9 +544,11 @@ def test_accumulate_matches_oracle(n):
         payloads_dev.append((st.idx, st.val, st.ctr))
         payloads_ref.append((gi, gv))
     out = torch.empty(d, dtype=torch.float32, device=DEV)
-    efs.sparse_accumulate(payloads_dev, d, out)
+    ws = efs.new_apply_workspace(payloads_dev, d, DEV)
+    efs.sparse_accumulate(payloads_dev, d, out, ws)
     ref = oracle.accumulate(payloads_ref, d)
     assert_bits_equal(out.cpu().numpy(), ref)
+    assert efs.sparse_status(ws) == 0
 
 
 def test_accumulate_topk_payloads_and_tail():
@@ -527,7 +560,7 @@ def test_accumulate_topk_payloads_and_tail():
         ps_dev.append((to_dev(gi), to_dev(gv)))
         ps_ref.append((gi, gv))
     out = torch.empty(d, dtype=torch.float32, device=DEV)
-    efs.sparse_accumulate(ps_dev, d, out)
+    efs.sparse_accumulate(ps_dev, d, out, efs.new_apply_workspace(ps_dev, d, DEV))
     assert_bits_equal(out.cpu().numpy(), oracle.accumulate(ps_ref, d))
 
 
@@ -554,7 +587,7 @@ def test_accumulate_special_values(n):
         ps_dev.append((to_dev(idx), to_dev(val)))
         ps_ref.append((idx, val))
     out = torch.full((d,), 9.0, dtype=torch.float32, device=DEV)
-    efs.sparse_accumulate(ps_dev, d, out)
+    efs.sparse_accumulate(ps_dev, d, out, efs.new_apply_workspace(ps_dev, d, DEV))
     got = out.cpu().numpy()
     ref = oracle.accumulate(ps_ref, d)
     nan = np.isnan(ref)
@@ -563,15 +596,45 @@ def test_accumulate_special_values(n):
     assert bits(got[7]) == 0 and bits(got[d - 3]) == 0  # cancelled sums are +0
 
 
-def test_accumulate_ignores_out_of_range_indices():
+def test_accumulate_reports_out_of_range_indices():
+    # indices outside [0, d) are skipped and the status word says so; the
+    # next call on the same workspace with a clean payload reports 0 again
     d = 1000
     idx = np.array([3, -1, 999, 1000, 7], dtype=np.int32)
     val = np.array([1.0, 5.0, 2.0, 6.0, 3.0], dtype=np.float32)
     out = torch.empty(d, dtype=torch.float32, device=DEV)
-    efs.sparse_accumulate([(to_dev(idx), to_dev(val)), (to_dev(idx[:1]), to_dev(val[:1]))], d, out)
+    ps = [(to_dev(idx), to_dev(val)), (to_dev(idx[:1]), to_dev(val[:1]))]
+    ws = efs.new_apply_workspace(ps, d, DEV)
+    efs.sparse_accumulate(ps, d, out, ws)
     keep = (idx >= 0) & (idx < d)
     ref = oracle.accumulate([(idx[keep], val[keep]), (idx[:1], val[:1])], d)
     assert_bits_equal(out.cpu().numpy(), ref)
+    assert efs.sparse_status(ws) == efs.SPARSE_BAD_INDEX
+    clean = [(to_dev(idx[keep]), to_dev(val[keep])), ps[1]]
+    efs.sparse_accumulate(clean, d, out, ws)
+    assert_bits_equal(out.cpu().numpy(), ref)
+    assert efs.sparse_status(ws) == 0
+
+
+def test_accumulate_reports_a_truncated_hard_threshold_payload():
+    # a hard-threshold call whose k_t exceeds the payload capacity: the
+    # average uses the cap pairs written and the status word reports the
+    # truncation (the error of the dropped coordinates is already +0)
+    d = 300_007
+    g = synth.small_gradient(3, d)
+    lam = oracle.calibrate_lambda(g, 0.05)
+    full, short = HT(d), HT(d, cap=1000)
+    gi, gv, _, gk = full.step(g, lam)
+    si, sv, _, sk = short.step(g, lam)
+    assert sk == gk > 1000 and si.size == 1000
+    out = torch.empty(d, dtype=torch.float32, device=DEV)
+    ps = [(full.idx, full.val, full.ctr), (short.idx, short.val, short.ctr)]
+    ws = efs.new_apply_workspace(ps, d, DEV)
+    efs.sparse_accumulate(ps, d, out, ws)
+    assert efs.sparse_status(ws) == efs.SPARSE_TRUNCATED
+    assert_bits_equal(out.cpu().numpy(), oracle.accumulate([(gi, gv), (si, sv)], d))
+    efs.sparse_accumulate(ps[:1], d, out, ws)
+    assert efs.sparse_status(ws) == 0
 
 
 def test_copy_probe_copies():

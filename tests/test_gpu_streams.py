@@ -28,11 +28,12 @@ def _step(d, k, lam, g, stream=None):
     tv = torch.empty(k, device=DEV)
     ws = efs.new_topk_workspace(d, k, DEV)
     out = torch.empty(d, device=DEV)
+    aws = efs.new_apply_workspace([(idx, val, ctr)], d, DEV)
     if stream is not None:
         torch.cuda.synchronize()  # the inputs above are ready before the side stream runs
     efs.ht_compress(gd, e_ht, LR, lam, idx, val, ctr, stream=stream)
     efs.topk_compress(gd, e_tk, LR, k, ti, tv, ws, stream=stream)
-    efs.sparse_accumulate([(idx, val, ctr)], d, out, stream=stream)
+    efs.sparse_accumulate([(idx, val, ctr)], d, out, aws, stream=stream)
     return e_ht, e_tk, idx, val, ctr, ti, tv, out
 
 
@@ -53,7 +54,7 @@ def _check(d, k, lam, g, res, sync):
 def test_calls_run_on_the_current_side_stream():
     d, k = 300_007, 3000
     g = synth.small_gradient(41, d)
-    lam = synth.calibrate_lambda(g, 0.01)
+    lam = oracle.calibrate_lambda(g, 0.01)
     s = torch.cuda.Stream()
     torch.cuda.synchronize()
     with torch.cuda.stream(s):
@@ -64,7 +65,7 @@ def test_calls_run_on_the_current_side_stream():
 def test_calls_run_on_an_explicit_stream():
     d, k = 300_007, 3000
     g = synth.small_gradient(42, d)
-    lam = synth.calibrate_lambda(g, 0.01)
+    lam = oracle.calibrate_lambda(g, 0.01)
     s = torch.cuda.Stream()
     res = _step(d, k, lam, g, stream=s)
     _check(d, k, lam, g, res, s.synchronize)
