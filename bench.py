@@ -1,29 +1,37 @@
 """Benchmark of the error-feedback compression step on one MI355X.
 
-One step = one pass of the whole path over one synthetic gradient of the
-25,557,032-element, 161-segment workload (Gaussian, per-segment std
-log-uniform in [1e-5, 1e-2], lr = 0.1):
-    hard threshold  ht_compress    (lambda giving 0.1 % density at the first step)
-    Top-k           topk_compress  (k = 25,557, its own error vector)
-    average         sparse_accumulate of the hard-threshold payload (n = 1)
-Gradients rotate through a pool larger than the 256 MB Infinity Cache, so
-every step reads them from HBM; the error vectors are carried from step to
-step as in training.  Inputs are resident on the device before timing.
+Workload (default, the largest one-GPU configuration): d = 1,500,000,000
+fp32 elements, Gaussian g with std 1e-3 except a fixed seeded 5 % of
+coordinates at std 0.1 (sparse large outliers), lr = 0.1, e carried from
+step to step; hard threshold at the lambda that keeps 0.1 % at the first
+step, Top-k with k = 1,500,000.  Gradients rotate through a pool of two
+(12 GB, far beyond the 256 MB Infinity Cache), resident in HBM before any
+timing.
 
-Prints one JSON line.  value = gradient elements compressed per second over
-the whole step (2 d per step: d by each compressor); the K timed steps carry
-HIP events only at their two ends.  The per-operation breakdown ("ops") comes
-from a second pass over the same steps with events between the operations.
+Timed regions (HIP events at their two ends only, on the stream the
+kernels run on; a barrier and a device synchronisation on both sides):
+  * `value`: K error-feedback steps of the hard threshold (ht_compress,
+    one launch of ht_fused_kernel per step); value = d / (time per step),
+    G grad-elements/s; ms_per_step is that time.
+  * `topk`: K steps of the Top-k baseline (topk_compress, its own error
+    vector and workspace) on the same gradients.
+  * `average`: K exchange-and-average calls (sparse_accumulate) of the
+    eight-worker 25,557,032-element workload's first-step hard-threshold
+    payloads, the output rotating over four buffers.
+Each reports its rate against the HBM roofline (8 TB/s) on the algorithmic
+bytes: 12 d + 8 k_t for the hard threshold, 12 d + 8 k for Top-k (the
+information it must move), 4 d + 8 (sum of counts) for the average.
 
-The roofline entry is for the hard-threshold kernel: algorithmic bytes
-(12 per element + 8 per kept pair) over its launch duration, from HIP events
-around back-to-back launches on four error-feedback states taken in turn, so
-that g and e come from HBM as they do inside the step (ops also reports one
-state carried from launch to launch, where part of e stays in the Infinity
-Cache, and launches after a cache flush).  --traffic takes the counter-derived HBM
-bytes per launch written by --parse-pmc from two rocprofv3 --pmc runs of this
-script (FETCH_SIZE, then WRITE_SIZE), scaled by what the same counters read
-for the copy probe of known size.
+`roofline` is the hard-threshold kernel on the default workload: the
+algorithmic bytes per launch over its launch duration (the timed steps are
+back-to-back launches of that kernel alone).  `traffic` is the HBM bytes
+per launch from two rocprofv3 --pmc runs of this script (FETCH_SIZE, then
+WRITE_SIZE), each scaled by what the same counter reads for the copy probe
+moving a known 8 d bytes in the same run; null when the summary was taken
+from other kernel sources.  `cpu_baseline` is the CPU oracle on the same
+workload (its multi-core build on all host cores; `cpu_baseline_1core` the
+single-threaded build).  `extra` holds the 25,557,032-element workload's
+figures and the fused model updates.
 """
 import argparse
 import csv
@@ -40,9 +48,18 @@ if ROOT not in sys.path:
 
 HBM_PEAK_GBPS = 8000.0
 HT_KERNEL = "ht_fused_kernel"
+HT_PLAIN = HT_KERNEL + "<true, false>"
 COPY_KERNEL = "copy_kernel"
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "ht_fused_kernel_segments_25.6m_pmc.txt")
 HT_SOURCES = ["ht.hip", "device_common.hpp"]
+T0 = time.time()
+
+
+def say(*a):
+    print("[bench %6.1fs]" % (time.time() - T0), *a, file=sys.stderr, flush=True)
+
+
+def traffic_file(name):
+    return os.path.join(ROOT, "profiles", "ht_fused_kernel_%s_pmc.txt" % name)
 
 
 def kernel_source_digest():
@@ -74,27 +91,23 @@ def read_traffic(path):
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--steps", type=int, default=20, help="timed steps (the workload runs 20)")
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--pool", type=int, default=4, help="distinct gradients in the rotation")
-    ap.add_argument("--b2b", type=int, default=20,
-                    help="back-to-back launches timed for the kernel roofline")
-    ap.add_argument("--cpu-steps", type=int, default=2,
-                    help="steps of the CPU oracle for the baseline (0 to skip)")
-    ap.add_argument("--traffic", type=str, default=TRAFFIC_FILE,
-                    help="summary written by --parse-pmc (HBM bytes per hard-threshold launch)")
+    ap.add_argument("--workload", type=int, default=5, choices=(2, 3, 5),
+                    help="workload of the hard-threshold and Top-k timings: 5 = 1.5e9 outliers "
+                         "(default), 2 = 25,557,032 segments, 3 = 110e6 Student-t")
+    ap.add_argument("--pool", type=int, default=None,
+                    help="distinct gradients in the rotation (default: 2 for the 1.5e9 "
+                         "workload, 4 for the others, always beyond the 256 MB Infinity Cache)")
+    ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baselines")
+    ap.add_argument("--no-extra", action="store_true",
+                    help="skip the 25.6e6 workload's figures and the fused model updates")
     ap.add_argument("--parse-trace", metavar="TRACE_DIR",
                     help="print the kernel statistics of a rocprofv3 --kernel-trace --stats "
-                         "run of this script (run_kernel_stats.csv, run_kernel_trace.csv), "
-                         "with the average of the back-to-back hard-threshold launches that "
-                         "roofline.launch_us times")
+                         "run of this script, with the average over the timed run of "
+                         "hard-threshold launches")
     ap.add_argument("--parse-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
                     help="summarise two rocprofv3 --pmc output folders and exit")
-    ap.add_argument("--no-apply", action="store_true",
-                    help="skip the fused update timings (sparse_apply, 1 and 8 workers)")
-    ap.add_argument("--sweep", action="store_true",
-                    help="also time the hard-threshold kernel on the 110e6 Student-t and "
-                         "1.5e9 outlier workloads (adds ~1 min of input generation)")
     return ap.parse_args()
 
 
@@ -118,10 +131,10 @@ def parse_pmc(fetch_dir, write_dir, d):
     out = {}
     for name, folder in (("FETCH_SIZE", fetch_dir), ("WRITE_SIZE", write_dir)):
         rows = _pmc_rows(folder, name)
-        ht = [v for k, v in rows if HT_KERNEL in k]
+        ht = [v for k, v in rows if HT_PLAIN in k]
         cp = [v for k, v in rows if COPY_KERNEL in k]
         if not ht or not cp:
-            raise SystemExit("no %s rows for %s / %s in %s" % (name, HT_KERNEL, COPY_KERNEL, folder))
+            raise SystemExit("no %s rows for %s / %s in %s" % (name, HT_PLAIN, COPY_KERNEL, folder))
         ht_b = 1024.0 * sum(ht) / len(ht)
         cp_b = 1024.0 * sum(cp) / len(cp)
         scale = 4.0 * d / cp_b
@@ -143,12 +156,12 @@ def _short_kernel_name(name):
     return re.sub(r"\(.*", "", name)[:34]
 
 
-def parse_trace(folder, b2b):
+def parse_trace(folder, steps):
     """Per-kernel statistics of a rocprofv3 kernel trace, and the average of
-    the first `b2b` consecutive dispatches of the hard-threshold kernel (its
-    plain variant) that no other kernel interrupts: the launches
-    roofline.launch_us times with HIP events."""
-    import csv
+    the first run of exactly `steps` consecutive dispatches of the
+    hard-threshold kernel (its plain variant) that no other kernel
+    interrupts: the timed steps, which the script delimits with other
+    kernels."""
     stats = list(csv.DictReader(open(os.path.join(folder, "run_kernel_stats.csv"))))
     trace = list(csv.DictReader(open(os.path.join(folder, "run_kernel_trace.csv"))))
     trace.sort(key=lambda r: int(r["Start_Timestamp"]))
@@ -161,10 +174,9 @@ def parse_trace(folder, b2b):
             _short_kernel_name(r["Name"]), r["Calls"], float(r["AverageNs"]) / 1e3,
             float(r["MinNs"]) / 1e3, float(r["MaxNs"]) / 1e3,
             100 * float(r["TotalDurationNs"]) / total))
-    plain = HT_KERNEL + "<true, false>"
     runs, cur = [], []
     for r in trace:
-        if plain in r["Kernel_Name"]:
+        if HT_PLAIN in r["Kernel_Name"]:
             cur.append((int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3)
         else:
             if cur:
@@ -172,19 +184,19 @@ def parse_trace(folder, b2b):
             cur = []
     if cur:
         runs.append(cur)
-    b2b_runs = [x for x in runs if len(x) == b2b]
+    timed = [x for x in runs if len(x) == steps]
     lines.append("")
-    if b2b_runs:
-        x = b2b_runs[0]
-        lines.append("# %s, the %d back-to-back launches timed for roofline.launch_us: "
-                     "avg %.2f us, min %.2f, max %.2f" % (plain, b2b, sum(x) / len(x), min(x), max(x)))
+    if timed:
+        x = timed[0]
+        lines.append("# %s, the %d timed steps: avg %.2f us, min %.2f, max %.2f"
+                     % (HT_PLAIN, steps, sum(x) / len(x), min(x), max(x)))
     else:
-        lines.append("# no run of %d back-to-back %s dispatches in the trace" % (b2b, plain))
+        lines.append("# no run of %d back-to-back %s dispatches in the trace" % (steps, HT_PLAIN))
     return "\n".join(lines) + "\n"
 
 
-def format_traffic(res):
-    lines = ["# HBM traffic of %s per launch from rocprofv3 counters" % HT_KERNEL,
+def format_traffic(res, workload):
+    lines = ["# HBM traffic of %s per launch from rocprofv3 counters, %s" % (HT_PLAIN, workload),
              "# (KiB per dispatch, averaged over the kernel's dispatches; each counter",
              "# scaled by expected/measured for %s moving 4*d bytes each way)" % COPY_KERNEL]
     for name in ("FETCH_SIZE", "WRITE_SIZE"):
@@ -207,6 +219,47 @@ def format_traffic(res):
     return "\n".join(lines) + "\n"
 
 
+def stats_us(xs):
+    import numpy as np
+    a = np.sort(np.asarray(xs, dtype=np.float64))
+    return {"mean_us": round(float(a.mean()), 2),
+            "p10_us": round(float(a[int(0.1 * (a.size - 1))]), 2),
+            "p50_us": round(float(np.median(a)), 2),
+            "p90_us": round(float(a[int(0.9 * (a.size - 1))]), 2)}
+
+
+def rate(nbytes, us):
+    gbps = nbytes / (us * 1e-6) / 1e9
+    return {"gbps": round(gbps, 1), "frac": round(gbps / HBM_PEAK_GBPS, 4)}
+
+
+class Timer:
+    """HIP events at the two ends of a region on one stream, with a device
+    synchronisation on both sides."""
+
+    def __init__(self, torch, stream):
+        self.torch, self.stream = torch, stream
+
+    def __enter__(self):
+        self.a = self.torch.cuda.Event(enable_timing=True)
+        self.b = self.torch.cuda.Event(enable_timing=True)
+        self.torch.cuda.synchronize()
+        self.a.record(self.stream)
+        return self
+
+    def __exit__(self, *exc):
+        self.b.record(self.stream)
+        self.torch.cuda.synchronize()
+        self.us = self.a.elapsed_time(self.b) * 1e3
+
+
+def to_device(torch, host, dev, chunk=1 << 26):
+    out = torch.empty(host.size, dtype=torch.float32, device=dev)
+    for lo in range(0, host.size, chunk):
+        out[lo:lo + chunk].copy_(torch.from_numpy(host[lo:lo + chunk]))
+    return out
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -218,13 +271,13 @@ def main():
 
     from paper_2108_00951_amd import synth
 
-    wl = synth.WORKLOADS[2]
+    wl = synth.WORKLOADS[args.workload]
     d, k, density = wl.d, wl.topk_k[0], wl.densities[0]
     if args.parse_pmc:
-        sys.stdout.write(format_traffic(parse_pmc(args.parse_pmc[0], args.parse_pmc[1], d)))
+        sys.stdout.write(format_traffic(parse_pmc(args.parse_pmc[0], args.parse_pmc[1], d), wl.name))
         return
     if args.parse_trace:
-        sys.stdout.write(parse_trace(args.parse_trace, args.b2b))
+        sys.stdout.write(parse_trace(args.parse_trace, args.steps))
         return
 
     import torch
@@ -234,483 +287,279 @@ def main():
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     efs.load_library()
-
+    cur = torch.cuda.current_stream()
     lr = synth.LR
-    stream = synth.Stream(2)
-    t0 = time.time()
-    pool_host = [stream.gradient(t, threads=16) for t in range(args.pool)]
-    lam = synth.calibrate_lambda(pool_host[0], density, lr)
-    pool = [torch.from_numpy(g).to(dev) for g in pool_host]
-    print("inputs ready: d=%d pool=%d lambda=%.6g k=%d (%.1fs)"
-          % (d, args.pool, float(lam), k, time.time() - t0), file=sys.stderr, flush=True)
+    if args.pool is None:
+        args.pool = 2 if d >= 100_000_000 else 4
+    lam = synth.stored_lambda(wl.ident, density)
+    stream = synth.Stream(wl.ident)
+    threads = min(16, os.cpu_count() or 1)
+    say("drawing %d gradients of %s (d=%d)" % (args.pool, wl.name, d))
+    pool_host = [stream.gradient(t, threads=threads) for t in range(args.pool)]
+    pool = [to_device(torch, g, dev) for g in pool_host]
+    say("inputs resident: lambda=%r k=%d" % (float(lam), k))
+    delimiter = torch.empty(4096, dtype=torch.float32, device=dev)
 
+    def mark():
+        # a short kernel of another name between phases, so that a kernel
+        # trace shows the timed launches as one run
+        efs.stream_probe(delimiter, delimiter, 2)
+
+    # ---- hard threshold: K timed steps --------------------------------------
     e_ht = torch.zeros(d, dtype=torch.float32, device=dev)
-    e_tk = torch.zeros(d, dtype=torch.float32, device=dev)
-    cap = d   # k_t grows under error feedback with a fixed lambda; never truncate
+    cap = min(d, max(1 << 20, d // 8))   # k_t grows under error feedback with a fixed lambda
     idx = torch.empty(cap, dtype=torch.int32, device=dev)
     val = torch.empty(cap, dtype=torch.float32, device=dev)
     ctr = efs.new_counter(dev)
-    tidx = torch.empty(k, dtype=torch.int32, device=dev)
-    tval = torch.empty(k, dtype=torch.float32, device=dev)
-    ws = efs.new_topk_workspace(d, k, dev)
-    out = torch.empty(d, dtype=torch.float32, device=dev)
-    cur = torch.cuda.current_stream()
-
-    def ev():
-        return torch.cuda.Event(enable_timing=True)
-
-    def step(s, evs=None):
-        g = pool[s % len(pool)]
-        if evs is not None:
-            evs[0].record(cur)
-        efs.ht_compress(g, e_ht, lr, lam, idx, val, ctr)
-        if evs is not None:
-            evs[1].record(cur)
-        efs.topk_compress(g, e_tk, lr, k, tidx, tval, ws)
-        if evs is not None:
-            evs[2].record(cur)
-        efs.sparse_accumulate([(idx, val, ctr)], d, out)
-        if evs is not None:
-            evs[3].record(cur)
-
     for s in range(args.warmup):
-        step(s)
-    torch.cuda.synchronize()
-    e_ht_start = e_ht.clone()
-    e_tk_start = e_tk.clone()
-
-    # ---- timed region: K whole steps, events only at its two ends -------
-    begin, end = ev(), ev()
-    torch.cuda.synchronize()
-    begin.record(cur)
-    for s in range(args.steps):
-        step(args.warmup + s)
-    end.record(cur)
-    torch.cuda.synchronize()
-    e_ht_end = e_ht.clone()
-    e_tk_end = e_tk.clone()
-
-    # ---- per-operation breakdown: the same K steps again from the same
-    # state, with events between the operations (the event packets add
-    # dispatch gaps, so this pass is reported but not used for the step time)
-    e_ht.copy_(e_ht_start)
-    e_tk.copy_(e_tk_start)
-    evs = [[ev() for _ in range(4)] for _ in range(args.steps)]
-    torch.cuda.synchronize()
-    for s in range(args.steps):
-        step(args.warmup + s, evs[s])
-    torch.cuda.synchronize()
-
-    # k_t of every timed step, from a deterministic replay of the
-    # hard-threshold calls (same inputs, same starting e).
-    e_ht.copy_(e_ht_start)
+        efs.ht_compress(pool[s % len(pool)], e_ht, lr, lam, idx, val, ctr)
+    e_snap = e_ht.clone()
+    mark()
+    with Timer(torch, cur) as tm:
+        for s in range(args.steps):
+            efs.ht_compress(pool[(args.warmup + s) % len(pool)], e_ht, lr, lam, idx, val, ctr)
+    mark()
+    ht_us = tm.us / args.steps
+    # k_t of every timed step: the same calls again from the same state
+    e_ht.copy_(e_snap)
     kts = []
     for s in range(args.steps):
         efs.ht_compress(pool[(args.warmup + s) % len(pool)], e_ht, lr, lam, idx, val, ctr)
         kts.append(efs.counter_value(ctr))
-
-    # Which Top-k selection each timed step took (same replay idea).
-    e_tk.copy_(e_tk_start)
-    bracket_hits = 0
-    for s in range(args.steps):
-        efs.topk_compress(pool[(args.warmup + s) % len(pool)], e_tk, lr, k, tidx, tval, ws)
-        bracket_hits += efs.topk_took_bracket_path(ws)
-
-    # ---- kernel durations: back-to-back launches -------------------------
-    # Hard threshold on four error-feedback states continuing from the end of
-    # the timed region, taken in turn, each with its own gradient sequence:
-    # g and e of every launch come from HBM, as inside the step, where the
-    # other operations evict them from the 256 MB Infinity Cache.
-    e_rot = [e_ht_end.clone() for _ in range(4)]
-    ctr_rot = [efs.new_counter(dev) for _ in range(4)]
-
-    def ht_rot(s, telemetry=None):
-        r = s % 4
-        g = pool[(s + s // 4) % len(pool)]
-        if telemetry is None:
-            efs.ht_compress(g, e_rot[r], lr, lam, idx, val, ctr_rot[r])
-        else:
-            efs.ht_compress_telemetry(g, e_rot[r], lr, lam, idx, val, ctr_rot[r], telemetry)
-
-    a, b = ev(), ev()
-    torch.cuda.synchronize()
-    a.record(cur)
-    for s in range(args.b2b):
-        ht_rot(s)
-    b.record(cur)
-    torch.cuda.synchronize()
-    ht_b2b_us = a.elapsed_time(b) * 1e3 / args.b2b
-    kt_b2b = float(np.mean([efs.counter_value(c) for c in ctr_rot]))
-    # the same with the fused telemetry (total error, pairs sent, max |e'|)
-    tel = efs.new_telemetry(dev)
-    a, b = ev(), ev()
-    torch.cuda.synchronize()
-    a.record(cur)
-    for s in range(args.b2b):
-        ht_rot(s, tel)
-    b.record(cur)
-    torch.cuda.synchronize()
-    ht_tel_us = a.elapsed_time(b) * 1e3 / args.b2b
-    # copy probe over the same element count, destinations in turn
-    a, b = ev(), ev()
-    a.record(cur)
-    for s in range(args.b2b):
-        efs.copy_probe(pool[s % len(pool)], e_rot[(s + 1) % 4])
-    b.record(cur)
-    torch.cuda.synchronize()
-    copy_us = a.elapsed_time(b) * 1e3 / args.b2b
-    del e_rot
-    # one state carried from launch to launch (an EF loop with nothing in
-    # between): part of e then stays in the Infinity Cache
-    e_ht.copy_(e_ht_end)
-    a, b = ev(), ev()
-    torch.cuda.synchronize()
-    a.record(cur)
-    for s in range(args.b2b):
-        efs.ht_compress(pool[s % len(pool)], e_ht, lr, lam, idx, val, ctr)
-    b.record(cur)
-    torch.cuda.synchronize()
-    ht_one_us = a.elapsed_time(b) * 1e3 / args.b2b
-    kt_one = efs.counter_value(ctr)
-    # cold: a 1 GiB write (stream probe) before every launch evicts the 256 MB
-    # Infinity Cache, so g and e come from HBM; events around the launch only
-    flush = torch.empty(1 << 28, dtype=torch.float32, device=dev)
-    cold = []
-    for s in range(args.b2b):
-        efs.stream_probe(flush, flush, 2)
-        a, b = ev(), ev()
-        a.record(cur)
-        efs.ht_compress(pool[s % len(pool)], e_ht, lr, lam, idx, val, ctr)
-        b.record(cur)
-        torch.cuda.synchronize()
-        cold.append(a.elapsed_time(b) * 1e3)
-    del flush
-    ht_cold_us = float(np.median(cold))
-    kt_cold = efs.counter_value(ctr)
-    # layer-wise Top-k over the workload's 161 segments, k_s = ceil(0.1 % d_s)
-    seg_ks = synth.layerwise_k(stream.bounds, density)
-    seg_ktot = int(seg_ks.sum())
-    seg_off_d = torch.from_numpy(stream.bounds.astype(np.int64)).to(dev)
-    seg_k_d = torch.from_numpy(seg_ks).to(dev)
-    seg_idx = torch.empty(seg_ktot, dtype=torch.int32, device=dev)
-    seg_val = torch.empty(seg_ktot, dtype=torch.float32, device=dev)
-    seg_ws = efs.new_topk_segmented_workspace(seg_ks.size, seg_ktot, dev)
-    e_seg = torch.zeros(d, dtype=torch.float32, device=dev)
-    seg_ws.zero_()
-    # as many untimed calls as the step loop has run (warmup + timed steps), so
-    # the error vector is as far into training as the step's own
-    for s in range(args.warmup + args.steps):
-        efs.topk_segmented_compress(pool[s % len(pool)], e_seg, lr, seg_off_d, seg_k_d, seg_idx,
-                                    seg_val, seg_ws)
-    a, b = ev(), ev()
-    torch.cuda.synchronize()
-    a.record(cur)
-    for s in range(args.b2b):
-        efs.topk_segmented_compress(pool[s % len(pool)], e_seg, lr, seg_off_d, seg_k_d, seg_idx,
-                                    seg_val, seg_ws)
-    b.record(cur)
-    torch.cuda.synchronize()
-    seg_us = a.elapsed_time(b) * 1e3 / args.b2b
-    seg_hits = efs.topk_segmented_bracket_segments(seg_ws)
-    del e_seg, seg_ws
-
-    total_ms = begin.elapsed_time(end)
-    ms_step = total_ms / args.steps
-    ht_ms = [x[0].elapsed_time(x[1]) for x in evs]
-    tk_ms = [x[1].elapsed_time(x[2]) for x in evs]
-    ac_ms = [x[2].elapsed_time(x[3]) for x in evs]
+    if max(kts) > cap:
+        raise RuntimeError("hard-threshold payload capacity exceeded")
     kt = float(np.mean(kts))
-
-    def stats(xs):
-        a = np.sort(np.asarray(xs))
-        return {"mean_us": round(float(a.mean()) * 1e3, 2),
-                "p10_us": round(float(a[int(0.1 * (a.size - 1))]) * 1e3, 2),
-                "p50_us": round(float(np.median(a)) * 1e3, 2),
-                "p90_us": round(float(a[int(0.9 * (a.size - 1))]) * 1e3, 2)}
-
     ht_bytes = 12.0 * d + 8.0 * kt
-    ht_bytes_b2b = 12.0 * d + 8.0 * kt_b2b
-    tk_bytes_ideal = 12.0 * d + 8.0 * k
-    tk_bytes_twolook = 16.0 * d + 8.0 * k
-    ac_bytes = 4.0 * d + 8.0 * kt
-    ht_s = float(np.mean(ht_ms)) / 1e3
-    tk_s = float(np.mean(tk_ms)) / 1e3
-    ac_s = float(np.mean(ac_ms)) / 1e3
-    roof_gbps = ht_bytes_b2b / (ht_b2b_us * 1e-6) / 1e9
+    say("hard threshold: %.1f us per step, k_t %d..%d" % (ht_us, kts[0], kts[-1]))
+    del e_snap, idx, val
+    torch.cuda.empty_cache()
 
-    traffic = read_traffic(args.traffic)
+    # ---- Top-k: K timed steps on its own error vector -------------------------
+    e_tk = torch.zeros(d, dtype=torch.float32, device=dev)
+    tidx = torch.empty(k, dtype=torch.int32, device=dev)
+    tval = torch.empty(k, dtype=torch.float32, device=dev)
+    ws = efs.new_topk_workspace(d, k, dev)
+    for s in range(args.warmup):
+        efs.topk_compress(pool[s % len(pool)], e_tk, lr, k, tidx, tval, ws)
+    e_snap = e_tk.clone()
+    mark()
+    with Timer(torch, cur) as tt:
+        for s in range(args.steps):
+            efs.topk_compress(pool[(args.warmup + s) % len(pool)], e_tk, lr, k, tidx, tval, ws)
+    mark()
+    tk_us = tt.us / args.steps
+    # which selection each timed step took, and its time alone
+    e_tk.copy_(e_snap)
+    paths, tk_each = [], []
+    for s in range(args.steps):
+        with Timer(torch, cur) as t1:
+            efs.topk_compress(pool[(args.warmup + s) % len(pool)], e_tk, lr, k, tidx, tval, ws)
+        tk_each.append(t1.us)
+        paths.append(efs.topk_took_bracket_path(ws))
+    tk_ideal = 12.0 * d + 8.0 * k
+    say("Top-k: %.1f us per step, bracket path in %d of %d" % (tk_us, sum(paths), len(paths)))
+    del e_snap, e_tk, tidx, tval, ws
+    torch.cuda.empty_cache()
+
+    # copy probe over d elements (also the scale of the traffic counters)
+    with Timer(torch, cur) as tc:
+        for s in range(3):
+            efs.copy_probe(pool[s % len(pool)], pool[(s + 1) % len(pool)])
+    copy_us = tc.us / 3
+    del pool
+    torch.cuda.empty_cache()
+
+    # ---- exchange-and-average: eight workers' first-step payloads -------------
+    average = bench_average(efs, torch, synth, cur, args.steps, args.warmup, threads)
 
     line = {
         "metric": "G grad-elements/s compressed (hard-threshold, Top-k) + achieved HBM GB/s",
-        "value": round(2.0 * d / (ms_step / 1e3) / 1e9, 3),
+        "value": round(d / (ht_us * 1e-6) / 1e9, 2),
         "unit": "G grad-elements/s",
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": round(ms_step, 4),
+        "ms_per_step": round(ht_us / 1e3, 4),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "f32",
         "data": "synthetic",
         "config": {
-            "workload": "d=25,557,032 fp32 in 161 log-uniform segments, Gaussian g with "
-                        "per-segment std log-uniform [1e-5,1e-2], lr=0.1; hard threshold at "
-                        "0.1%% first-step density (lambda=%.6g) + Top-k k=25,557 + average of "
-                        "the hard-threshold payload" % float(lam),
+            "workload": "%s: d=%s fp32, %s, lr=0.1, e carried; hard threshold at lambda=%.6g "
+                        "(0.1%% first-step density), error-feedback steps; Top-k k=%s and the "
+                        "8-worker average of the 25,557,032-element workload timed alongside"
+                        % (wl.name, format(d, ","), describe(wl), float(lam), format(k, ",")),
             "d": d, "k": k, "lambda": float(lam), "lr": float(lr), "pool": args.pool,
+            "step": "one hard-threshold error-feedback iteration (ht_compress)",
         },
-        "hbm_gbps_step": round((ht_bytes + tk_bytes_twolook + ac_bytes) / (ms_step / 1e3) / 1e9, 1),
-        "roofline": {
-            "kernel": HT_KERNEL,
-            "bound": "hbm",
-            "achieved": round(roof_gbps, 1),
-            "peak": HBM_PEAK_GBPS,
-            "unit": "GB/s",
-            "frac": round(roof_gbps / HBM_PEAK_GBPS, 4),
-            "traffic": traffic,
-            "launch_us": round(ht_b2b_us, 2),
-            "bytes_per_launch": ht_bytes_b2b,
-            "k_t": kt_b2b,
-        },
-        "copy_probe": {"us": round(copy_us, 2), "gbps": round(8.0 * d / (copy_us * 1e-6) / 1e9, 1),
-                       "bytes": 8.0 * d},
-        "ops": {
-            "ht_compress_telemetry": {"launch_us": round(ht_tel_us, 2)},
-            "ht_compress_one_state": {
-                "launch_us": round(ht_one_us, 2), "k_t": kt_one,
-                "gbps": round((12.0 * d + 8.0 * kt_one) / (ht_one_us * 1e-6) / 1e9, 1)},
-            "ht_compress_cold": {
-                "median_us": round(ht_cold_us, 2), "p10_us": round(float(np.percentile(cold, 10)), 2),
-                "p90_us": round(float(np.percentile(cold, 90)), 2),
-                "gbps": round((12.0 * d + 8.0 * kt_cold) / (ht_cold_us * 1e-6) / 1e9, 1),
-                "vs_b2b": round(ht_cold_us / ht_b2b_us, 3)},
-            "topk_segmented_compress": {
-                "launch_us": round(seg_us, 2), "segments": int(seg_ks.size), "k_total": seg_ktot,
-                "bracket_segments_last_call": seg_hits,
-                "gelem_s": round(d / (seg_us * 1e-6) / 1e9, 2),
-                "gbps_ideal": round((12.0 * d + 8.0 * seg_ktot) / (seg_us * 1e-6) / 1e9, 1),
-                "gbps_two_pass": round((16.0 * d + 8.0 * seg_ktot) / (seg_us * 1e-6) / 1e9, 1)},
-            "ht_compress": dict(stats(ht_ms), gelem_s=round(d / ht_s / 1e9, 2),
-                                gbps=round(ht_bytes / ht_s / 1e9, 1), k_t_mean=kt,
-                                k_t_first=kts[0], k_t_last=kts[-1]),
-            "topk_compress": dict(stats(tk_ms), gelem_s=round(d / tk_s / 1e9, 2),
-                                  bracket_path_steps=bracket_hits,
-                                  gbps_ideal=round(tk_bytes_ideal / tk_s / 1e9, 1),
-                                  gbps_twolook=round(tk_bytes_twolook / tk_s / 1e9, 1)),
-            "sparse_accumulate": dict(stats(ac_ms),
-                                      gbps_min=round(ac_bytes / ac_s / 1e9, 1)),
-        },
+        "hbm_gbps": round(ht_bytes / (ht_us * 1e-6) / 1e9, 1),
+        "roofline": dict(
+            kernel=HT_PLAIN, bound="hbm",
+            achieved=round(ht_bytes / (ht_us * 1e-6) / 1e9, 1), peak=HBM_PEAK_GBPS, unit="GB/s",
+            frac=round(ht_bytes / (ht_us * 1e-6) / 1e9 / HBM_PEAK_GBPS, 4),
+            traffic=read_traffic(traffic_file(wl.name)),
+            launch_us=round(ht_us, 2), bytes_per_launch=ht_bytes, k_t_mean=kt,
+            k_t_first=kts[0], k_t_last=kts[-1],
+            bytes_model="12 d + 8 k_t (read g, read e, write e', 8 bytes per kept pair)"),
+        "topk": dict(
+            stats_us(tk_each), us_per_step=round(tk_us, 2),
+            gelem_s=round(d / (tk_us * 1e-6) / 1e9, 2), bracket_path_steps=int(sum(paths)),
+            bytes_ideal=tk_ideal, **rate(tk_ideal, tk_us),
+            bytes_model="12 d + 8 k: what the step must move (frac is against this)"),
+        "average": average,
+        "copy_probe": {"us": round(copy_us, 2), "bytes": 8.0 * d, **rate(8.0 * d, copy_us)},
     }
-
-    if not args.no_apply:
-        line["sparse_apply"] = apply_bench(efs, torch, synth, cur, args.b2b, (idx, val, ctr), d)
-    if args.sweep:
-        del pool, e_tk, out, ws
-        line["ht_sweep"] = ht_sweep(efs, torch, synth, cur, args.b2b)
-    if args.cpu_steps > 0:
-        line["cpu_baseline"] = cpu_baseline(pool_host, d, k, lam, lr, args.cpu_steps)
+    if not args.no_extra:
+        line["extra"] = {"segments_25.6m": bench_segments(efs, torch, synth, cur, threads),
+                         "sparse_apply_8_workers": average.pop("_apply", None)}
+    average.pop("_apply", None)
+    if not args.no_cpu:
+        line["cpu_baseline"], line["cpu_baseline_1core"] = cpu_baselines(pool_host, wl, lam)
     print(json.dumps(line), flush=True)
 
 
-def ht_sweep(efs, torch, synth, cur, reps):
-    """Back-to-back launches on the larger workloads, two distinct gradients
-    alternating, e carried: the hard threshold (0.1 % first-step density),
-    the streaming ceilings, Top-k at the workload's densities and, where the
-    workload has layers, the layer-wise Top-k at 1 %."""
-    import numpy as np
-    res = {}
-    for wid in (3, 5):
-        st = synth.Stream(wid)
-        d = st.w.d
-        gh = st.gradient(0, threads=16)
-        lam = synth.calibrate_lambda(gh, 0.001)
-        gs = [torch.from_numpy(gh).to("cuda")]
-        del gh
-        gs.append(torch.from_numpy(st.gradient(1, threads=16)).to("cuda"))
-        e = torch.zeros(d, dtype=torch.float32, device="cuda")
-        cap = d // 4
-        idx = torch.empty(cap, dtype=torch.int32, device="cuda")
-        val = torch.empty(cap, dtype=torch.float32, device="cuda")
-        ctr = efs.new_counter("cuda")
-        for s in range(2):
-            efs.ht_compress(gs[s % 2], e, synth.LR, lam, idx, val, ctr)
-        a = torch.cuda.Event(enable_timing=True)
-        b = torch.cuda.Event(enable_timing=True)
-        torch.cuda.synchronize()
-        a.record(cur)
-        for s in range(reps):
-            efs.ht_compress(gs[s % 2], e, synth.LR, lam, idx, val, ctr)
-        b.record(cur)
-        torch.cuda.synchronize()
-        us = a.elapsed_time(b) * 1e3 / reps
-        kt = efs.counter_value(ctr)
-        if kt > cap:
-            raise RuntimeError("sweep payload capacity exceeded")
-        gbps = (12.0 * d + 8.0 * kt) / (us * 1e-6) / 1e9
-        res[st.w.name] = {"d": d, "launch_us": round(us, 2), "k_t": kt,
-                          "gbps": round(gbps, 1), "frac": round(gbps / HBM_PEAK_GBPS, 4),
-                          "gelem_s": round(d / (us * 1e-6) / 1e9, 1)}
-        del e, idx, val
-        torch.cuda.empty_cache()
-        # Top-k on the same gradients, its own e from zero: 5 calls, then
-        # `reps` back-to-back calls timed (bytes: 12 per element + 8 per pair
-        # ideal, 16 + 8 per pair for the two-look radix path)
-        dens = (0.01, 0.001, 0.0001) if wid == 3 else (0.001,)
-        res[st.w.name]["topk"] = {}
-        for rho in dens:
-            k = max(1, int(round(rho * d)))
-            e = torch.zeros(d, dtype=torch.float32, device="cuda")
-            tidx = torch.empty(k, dtype=torch.int32, device="cuda")
-            tval = torch.empty(k, dtype=torch.float32, device="cuda")
-            ws = efs.new_topk_workspace(d, k, "cuda")
-            for s in range(5):
-                efs.topk_compress(gs[s % 2], e, synth.LR, k, tidx, tval, ws)
-            torch.cuda.synchronize()
-            a.record(cur)
-            for s in range(reps):
-                efs.topk_compress(gs[s % 2], e, synth.LR, k, tidx, tval, ws)
-            b.record(cur)
-            torch.cuda.synchronize()
-            us = a.elapsed_time(b) * 1e3 / reps
-            res[st.w.name]["topk"]["k=%d" % k] = {
-                "launch_us": round(us, 2), "gelem_s": round(d / (us * 1e-6) / 1e9, 1),
-                "gbps_ideal": round((12.0 * d + 8.0 * k) / (us * 1e-6) / 1e9, 1),
-                "gbps_twolook": round((16.0 * d + 8.0 * k) / (us * 1e-6) / 1e9, 1),
-                "last_call_bracket": efs.topk_took_bracket_path(ws)}
-            del e, tidx, tval, ws
-            torch.cuda.empty_cache()
-        if st.bounds is not None:
-            # layer-wise Top-k over the workload's segments at 1 %
-            ks = synth.layerwise_k(st.bounds, 0.01)
-            kt = int(ks.sum())
-            offd = torch.from_numpy(st.bounds.astype(np.int64)).to("cuda")
-            kd = torch.from_numpy(ks).to("cuda")
-            e = torch.zeros(d, dtype=torch.float32, device="cuda")
-            tidx = torch.empty(kt, dtype=torch.int32, device="cuda")
-            tval = torch.empty(kt, dtype=torch.float32, device="cuda")
-            ws = efs.new_topk_segmented_workspace(ks.size, kt, "cuda")
-            ws.zero_()
-            for s in range(5):
-                efs.topk_segmented_compress(gs[s % 2], e, synth.LR, offd, kd, tidx, tval, ws)
-            torch.cuda.synchronize()
-            a.record(cur)
-            for s in range(reps):
-                efs.topk_segmented_compress(gs[s % 2], e, synth.LR, offd, kd, tidx, tval, ws)
-            b.record(cur)
-            torch.cuda.synchronize()
-            us = a.elapsed_time(b) * 1e3 / reps
-            res[st.w.name]["topk_layerwise_1pct"] = {
-                "segments": int(ks.size), "k_total": kt, "launch_us": round(us, 2),
-                "gelem_s": round(d / (us * 1e-6) / 1e9, 1),
-                "gbps_ideal": round((12.0 * d + 8.0 * kt) / (us * 1e-6) / 1e9, 1),
-                "bracket_segments_last_call": efs.topk_segmented_bracket_segments(ws)}
-            del e, tidx, tval, ws
-        # streaming ceilings on the same buffers (whole tiles): copy, read,
-        # write, and two reads + one write (the hard threshold's pattern);
-        # last, because the write probes overwrite the second gradient
-        nt = (d // 4096) * 4096
-        ceil = {}
-        for mode, name, nbytes in ((0, "copy", 8.0), (1, "read", 4.0), (2, "write", 4.0),
-                                   (3, "2r1w", 12.0)):
-            a.record(cur)
-            for s in range(reps):
-                efs.stream_probe(gs[0][:nt], gs[1][:nt], mode)
-            b.record(cur)
-            torch.cuda.synchronize()
-            pus = a.elapsed_time(b) * 1e3 / reps
-            ceil[name] = round(nbytes * nt / (pus * 1e-6) / 1e9, 1)
-        res[st.w.name]["ceiling_gbps"] = ceil
-        print("sweep %s: %s" % (st.w.name, res[st.w.name]), file=sys.stderr, flush=True)
-        del gs
-        torch.cuda.empty_cache()
-    return res
+def describe(wl):
+    return {"outliers": "Gaussian g std 1e-3 with a fixed 5% of coordinates at std 0.1",
+            "segments": "161 log-uniform segments, Gaussian g with per-segment std "
+                        "log-uniform [1e-5,1e-2]",
+            "student_t": "200 segments, Student-t (nu=3) g scaled by 1e-4 x per-segment "
+                         "log-uniform [0.1,10]",
+            "gauss": "Gaussian g std 1e-3"}[wl.kind]
 
 
-def apply_bench(efs, torch, synth, cur, reps, ht_payload, d):
-    """Back-to-back sparse_apply launches in each mode: on the step's own
-    hard-threshold payload (1 worker), and on 8 workers' payloads of the
-    8-worker workload (same d and segment layout, 0.1 % first-step density),
-    next to sparse_accumulate on the same payloads; the launches take four
-    output sets in turn.  Algorithmic bytes:
-    average 8 per pair + 4 d; sgd 8 per pair + 8 per touched coordinate;
-    momentum 8 per pair + 16 d."""
-    import numpy as np
-
-    def timed(fns):
-        a = torch.cuda.Event(enable_timing=True)
-        b = torch.cuda.Event(enable_timing=True)
-        for fn in fns:
-            fn()
-        torch.cuda.synchronize()
-        a.record(cur)
-        for s in range(reps):
-            fns[s % len(fns)]()
-        b.record(cur)
-        torch.cuda.synchronize()
-        return a.elapsed_time(b) * 1e3 / reps
-
-    def measure(payloads):
-        pairs = sum(efs.counter_value(p[2]) for p in payloads)
-        touched = int(torch.unique(torch.cat(
-            [p[0][:efs.counter_value(p[2])] for p in payloads])).numel())
-        ws = efs.new_apply_workspace(payloads, d, "cuda")
-        # four (x, m) sets taken in turn, so that they come from HBM as the
-        # parameters and momentum of a training step would
-        xs = [torch.zeros(d, dtype=torch.float32, device="cuda") for _ in range(4)]
-        ms = [torch.zeros(d, dtype=torch.float32, device="cuda") for _ in range(4)]
-        res = {"pairs": pairs, "touched": touched, "workspace_mb": round(ws.numel() / 2 ** 20, 1)}
-        for mode, name, nbytes in (
-                (efs.APPLY_AVERAGE, "average", 8.0 * pairs + 4.0 * d),
-                (efs.APPLY_SGD, "sgd", 8.0 * pairs + 8.0 * touched),
-                (efs.APPLY_MOMENTUM, "momentum", 8.0 * pairs + 16.0 * d)):
-            us = timed([efs.prepare_sparse_apply(payloads, d, mode, xs[r], ws, m=ms[r], beta=0.9,
-                                                 gamma=0.05) for r in range(4)])
-            res[name] = {"us": round(us, 2), "gbps": round(nbytes / (us * 1e-6) / 1e9, 1)}
-        us = timed([efs.prepare_sparse_accumulate(payloads, d, x) for x in xs])
-        res["sparse_accumulate_us"] = round(us, 2)
-        del ws, xs, ms
-        return res
-
-    res = {"workers_1": measure([ht_payload])}
+def bench_average(efs, torch, synth, cur, steps, warmup, threads):
+    """sparse_accumulate over the eight workers' first-step hard-threshold
+    payloads of the 8-worker workload (d = 25,557,032), the output rotating
+    over four buffers; then the fused model updates on the same payloads."""
     st = synth.Stream(4)
     w = st.w
-    assert w.d == d
-    lam = synth.calibrate_lambda(st.gradient(0, worker=0, threads=16), w.densities[0])
+    d = w.d
+    lam = synth.stored_lambda(4, w.densities[0])
     payloads = []
     for wk in range(w.n_workers):
-        g = torch.from_numpy(st.gradient(0, worker=wk, threads=16)).to("cuda")
+        g = torch.from_numpy(st.gradient(0, worker=wk, threads=threads)).to("cuda")
         e = torch.zeros(d, dtype=torch.float32, device="cuda")
         cap = d // 100
         idx = torch.empty(cap, dtype=torch.int32, device="cuda")
         val = torch.empty(cap, dtype=torch.float32, device="cuda")
         ctr = efs.new_counter("cuda")
         efs.ht_compress(g, e, synth.LR, lam, idx, val, ctr)
-        if efs.counter_value(ctr) > cap:
-            raise RuntimeError("apply bench payload capacity exceeded")
         payloads.append((idx, val, ctr))
         del g, e
-    res["workers_8"] = measure(payloads)
-    print("sparse_apply: %s" % res, file=sys.stderr, flush=True)
+    pairs = sum(efs.counter_value(p[2]) for p in payloads)
+    ws = efs.new_apply_workspace(payloads, d, "cuda")
+    outs = [torch.empty(d, dtype=torch.float32, device="cuda") for _ in range(4)]
+    calls = [efs.prepare_sparse_accumulate(payloads, d, o, ws) for o in outs]
+    for s in range(warmup):
+        calls[s % 4]()
+    with Timer(torch, cur) as t:
+        for s in range(steps):
+            calls[s % 4]()
+    us = t.us / steps
+    status = efs.sparse_status(ws)
+    nbytes = 4.0 * d + 8.0 * pairs
+    res = {"workers": w.n_workers, "d": d, "pairs": pairs, "us": round(us, 2), "status": status,
+           "bytes_min": nbytes, **rate(nbytes, us),
+           "bytes_model": "4 d + 8 per pair (dense output write, payload read)"}
+    say("average of %d payloads (%d pairs): %.1f us" % (w.n_workers, pairs, us))
+    # the fused model updates on the same payloads, (x, m) rotating over four sets
+    touched = int(torch.unique(torch.cat(
+        [p[0][:efs.counter_value(p[2])] for p in payloads])).numel())
+    ms = [torch.zeros(d, dtype=torch.float32, device="cuda") for _ in range(4)]
+    upd = {"touched": touched}
+    for mode, name, nb in ((efs.APPLY_SGD, "sgd", 8.0 * pairs + 8.0 * touched),
+                           (efs.APPLY_MOMENTUM, "momentum", 8.0 * pairs + 16.0 * d)):
+        fns = [efs.prepare_sparse_apply(payloads, d, mode, outs[r], ws, m=ms[r], beta=0.9,
+                                        gamma=0.05) for r in range(4)]
+        for s in range(4):
+            fns[s]()
+        with Timer(torch, cur) as t:
+            for s in range(steps):
+                fns[s % 4]()
+        upd[name] = {"us": round(t.us / steps, 2), "bytes": nb, **rate(nb, t.us / steps)}
+    res["_apply"] = upd
+    del ws, outs, ms, payloads
     torch.cuda.empty_cache()
     return res
 
 
-def cpu_baseline(pool_host, d, k, lam, lr, steps):
-    """The CPU oracle (single-threaded C, as written) on the same step."""
+def bench_segments(efs, torch, synth, cur, threads):
+    """The 25,557,032-element, 161-segment workload: hard threshold, flat and
+    layer-wise Top-k, each K = 20 back-to-back error-feedback steps on four
+    gradients in turn after 30 untimed steps."""
+    import numpy as np
+    st = synth.Stream(2)
+    w = st.w
+    d, k = w.d, w.topk_k[0]
+    lam = synth.stored_lambda(2, w.densities[0])
+    pool = [torch.from_numpy(st.gradient(t, threads=threads)).to("cuda") for t in range(4)]
+    lr = synth.LR
+    reps, pre = 20, 30
+    res = {"d": d}
+    e = torch.zeros(d, dtype=torch.float32, device="cuda")
+    idx = torch.empty(d, dtype=torch.int32, device="cuda")
+    val = torch.empty(d, dtype=torch.float32, device="cuda")
+    ctr = efs.new_counter("cuda")
+    for s in range(pre):
+        efs.ht_compress(pool[s % 4], e, lr, lam, idx, val, ctr)
+    with Timer(torch, cur) as t:
+        for s in range(reps):
+            efs.ht_compress(pool[s % 4], e, lr, lam, idx, val, ctr)
+    kt = efs.counter_value(ctr)
+    us = t.us / reps
+    res["ht_compress"] = {"us": round(us, 2), "k_t_last": kt,
+                          "gelem_s": round(d / (us * 1e-6) / 1e9, 1), **rate(12.0 * d + 8.0 * kt, us)}
+    e.zero_()
+    tidx, tval = idx[:k], val[:k]
+    ws = efs.new_topk_workspace(d, k, "cuda")
+    for s in range(pre):
+        efs.topk_compress(pool[s % 4], e, lr, k, tidx, tval, ws)
+    each, paths = [], 0
+    for s in range(reps):
+        with Timer(torch, cur) as t:
+            efs.topk_compress(pool[s % 4], e, lr, k, tidx, tval, ws)
+        each.append(t.us)
+        paths += efs.topk_took_bracket_path(ws)
+    with Timer(torch, cur) as t:
+        for s in range(reps):
+            efs.topk_compress(pool[s % 4], e, lr, k, tidx, tval, ws)
+    us = t.us / reps
+    res["topk_compress"] = dict(stats_us(each), us_back_to_back=round(us, 2),
+                                bracket_path_steps=paths, **rate(12.0 * d + 8.0 * k, us))
+    ks = synth.layerwise_k(st.bounds, w.densities[0])
+    kt = int(ks.sum())
+    offd = torch.from_numpy(st.bounds.astype(np.int64)).to("cuda")
+    kd = torch.from_numpy(ks).to("cuda")
+    sidx = torch.empty(kt, dtype=torch.int32, device="cuda")
+    sval = torch.empty(kt, dtype=torch.float32, device="cuda")
+    sws = efs.new_topk_segmented_workspace(ks.size, kt, "cuda")
+    e.zero_()
+    for s in range(pre):
+        efs.topk_segmented_compress(pool[s % 4], e, lr, offd, kd, sidx, sval, sws)
+    with Timer(torch, cur) as t:
+        for s in range(reps):
+            efs.topk_segmented_compress(pool[s % 4], e, lr, offd, kd, sidx, sval, sws)
+    us = t.us / reps
+    res["topk_segmented_compress"] = {
+        "us": round(us, 2), "segments": int(ks.size), "k_total": kt,
+        "bracket_segments_last_call": efs.topk_segmented_bracket_segments(sws),
+        **rate(12.0 * d + 8.0 * kt, us)}
+    say("25.6e6 workload: %s" % res)
+    del pool, e, idx, val, ws, sws
+    torch.cuda.empty_cache()
+    return res
+
+
+def cpu_baselines(pool_host, wl, lam):
+    """The CPU oracle on the same workload: the hard threshold over the whole
+    first gradient from e = 0 (one step), and Top-k on a leading slice of it
+    (k = 0.1 % of the slice); the multi-core build on all host cores, then the
+    single-threaded build on a smaller Top-k slice."""
     import numpy as np
 
     import oracle
 
-    e_ht = np.zeros(d, dtype=np.float32)
-    e_tk = np.zeros(d, dtype=np.float32)
-    t0 = time.perf_counter()
-    for s in range(steps):
-        g = pool_host[s % len(pool_host)]
-        ridx, rval, e_ht, _ = oracle.ht(g, e_ht, lr, lam)
-        _, _, e_tk = oracle.topk(g, e_tk, lr, k)
-        oracle.accumulate([(ridx, rval)], d)
-    dt = time.perf_counter() - t0
     model = "unknown"
     try:
         with open("/proc/cpuinfo") as f:
@@ -720,10 +569,37 @@ def cpu_baseline(pool_host, d, k, lam, lr, steps):
                     break
     except OSError:
         pass
-    return {"value": round(2.0 * d * steps / dt / 1e9, 5), "unit": "G grad-elements/s",
-            "cores": 1, "kind": "oracle", "cpu_model": model, "host_cpus": os.cpu_count(),
-            "sample": "%d full steps (d=%d: hard threshold + Top-k + average) of the same "
-                      "workload, single-threaded C oracle, %.1f s" % (steps, d, dt)}
+    g = pool_host[0]
+    d = g.size
+    cap = 4 * int(round(wl.densities[0] * d)) + 1024
+    out = []
+    for mt, slice_n in ((True, min(d, 100_000_000)), (False, min(d, 25_000_000))):
+        e0 = np.zeros(d, np.float32)
+        t0 = time.perf_counter()
+        oracle.ht(g, e0, synth_lr(), lam, cap=cap, mt=mt)
+        ht_s = time.perf_counter() - t0
+        del e0
+        sl = g[:slice_n]
+        ks = max(1, int(round(0.001 * slice_n)))
+        t0 = time.perf_counter()
+        oracle.topk(sl, np.zeros(slice_n, np.float32), synth_lr(), ks, mt=mt)
+        tk_s = time.perf_counter() - t0
+        cores = oracle.mt_threads() if mt else 1
+        out.append({
+            "value": round(d / ht_s / 1e9, 4), "unit": "G grad-elements/s", "cores": cores,
+            "kind": "oracle", "cpu_model": model, "host_cpus": os.cpu_count(),
+            "build": "oracle.c + oracle_mt.c, OpenMP" if mt else "oracle.c, one thread",
+            "topk_gelem_s": round(slice_n / tk_s / 1e9, 5),
+            "sample": "hard threshold over the whole d=%d first gradient (one step, %.2f s); "
+                      "Top-k on its first %d elements with k=%d (%.2f s)"
+                      % (d, ht_s, slice_n, ks, tk_s)})
+        say("CPU oracle (%d cores): %s" % (cores, out[-1]["sample"]))
+    return out[0], out[1]
+
+
+def synth_lr():
+    from paper_2108_00951_amd import synth
+    return synth.LR
 
 
 if __name__ == "__main__":

@@ -40,9 +40,9 @@ def _trace(folder, dispatches):
                ["Name", "Calls", "TotalDurationNs", "AverageNs", "MinNs", "MaxNs"], stats)
 
 
-def test_parse_trace_finds_the_back_to_back_run(tmp_path):
-    # hard-threshold launches interleaved with others (the step loop), the
-    # telemetry variant back to back, then the 4 plain launches back to back
+def test_parse_trace_finds_the_timed_run(tmp_path):
+    # hard-threshold launches interleaved with others, the telemetry variant
+    # back to back, then the 4 plain launches of the timed steps back to back
     seq = []
     for _ in range(3):
         seq += [(HT, 70_000), (OTHER, 9_000)]
@@ -52,7 +52,7 @@ def test_parse_trace_finds_the_back_to_back_run(tmp_path):
     seq += [(OTHER, 9_000), (HT, 90_000)]
     _trace(str(tmp_path), seq)
     out = bench.parse_trace(str(tmp_path), 4)
-    line = [x for x in out.splitlines() if "back-to-back" in x]
+    line = [x for x in out.splitlines() if "timed steps" in x]
     assert len(line) == 1
     assert "avg 50.00 us, min 48.00, max 52.00" in line[0]
     # the whole-run table averages every dispatch of the kernel
@@ -83,12 +83,13 @@ def test_parse_pmc_scales_by_the_copy_probe(tmp_path):
     assert res["FETCH_SIZE"]["scale"] == pytest.approx(0.5)
     assert res["WRITE_SIZE"]["scale"] == pytest.approx(1.0)
     assert res["ht_bytes_per_launch"] == pytest.approx(16384 * 1024 * 0.5 + 4096 * 1024)
-    text = bench.format_traffic(res)
+    text = bench.format_traffic(res, "a workload")
     assert "ht_bytes_per_launch %d" % round(res["ht_bytes_per_launch"]) in text
     # the other kernels get the same scales: topk_step3 fetched nothing, wrote 1 KiB
     step3 = [x for x in text.splitlines() if "topk_step3_kernel" in x]
     assert len(step3) == 1 and "0.00 +      0.00 MB  (1)" in step3[0]
-    ht_line = [x for x in text.splitlines() if "ht_fused_kernel<true, false>" in x][0]
+    ht_line = [x for x in text.splitlines()
+               if x.startswith("#   ht_fused_kernel<true, false>")][0]
     assert "%9.2f + %9.2f MB" % (16384 * 1024 * 0.5 / 1e6, 4096 * 1024 / 1e6) in ht_line
     assert "kernel_source_sha256 " + bench.kernel_source_digest() in text
 
