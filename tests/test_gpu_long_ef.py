@@ -1,10 +1,21 @@
-"""Long error-feedback runs at full size, every step's payload and residual
-bit-exact against the oracle: the 25,557,032-element, 161-layer workload over
-30 steps (hard threshold, flat and layer-wise Top-k), and the 110e6-element
-heavy-tailed workload over 6 steps at k = 1 % (flat and layer-wise Top-k).
-The oracle's Top-k sorts the whole vector, so each takes a few minutes: they
-run when EFS_LONG_TESTS=1 is set, and are skipped otherwise."""
+"""Error-feedback trajectories at full size for as many iterations as the
+workloads specify, every step's payload and residual bit-exact against the
+oracle (its multi-core build, which returns the single-threaded oracle's
+bits):
+
+  * the 25,557,032-element, 161-layer workload: 100 iterations of the hard
+    threshold, the flat Top-k (k = 25,557) and the layer-wise Top-k
+    (k_s = ceil(0.1 % d_s)), e carried in each;
+  * the 110e6-element heavy-tailed workload at 1 %: 50 iterations of the flat
+    Top-k (k = 1.1 M) and the layer-wise Top-k, and the hard threshold at
+    its 1 % lambda;
+  * the eight-worker workload: 25 iterations of eight hard-threshold
+    workers and the average of their payloads (the workload leaves the
+    iteration count open).
+
+Each step prints a line, so a slow step is visible while the test runs."""
 import os
+import time
 
 import numpy as np
 import pytest
@@ -12,100 +23,172 @@ import pytest
 from paper_2108_00951_amd import synth
 from tests._checks import assert_bits_equal, assert_payload_equal
 
-pytestmark = [pytest.mark.gpu,
-              pytest.mark.skipif(os.environ.get("EFS_LONG_TESTS") != "1",
-                                 reason="long run; set EFS_LONG_TESTS=1")]
+pytestmark = pytest.mark.gpu
 
 torch = pytest.importorskip("torch")
 import oracle  # noqa: E402
 from paper_2108_00951_amd import binding as efs  # noqa: E402
 
 DEV = "cuda"
+LR = synth.LR
+THREADS = min(16, os.cpu_count() or 1)
+
+
+def say(t0, *a):
+    print("[%6.1fs]" % (time.time() - t0), *a, flush=True)
+
+
+class Flat:
+    """Flat Top-k state on the device."""
+
+    def __init__(self, d, k):
+        self.k = k
+        self.e = torch.zeros(d, device=DEV)
+        self.idx = torch.empty(k, dtype=torch.int32, device=DEV)
+        self.val = torch.empty(k, device=DEV)
+        self.ws = efs.new_topk_workspace(d, k, DEV)
+
+    def step(self, gd):
+        efs.topk_compress(gd, self.e, LR, self.k, self.idx, self.val, self.ws)
+        return self.idx.cpu().numpy(), self.val.cpu().numpy(), self.e.cpu().numpy()
+
+
+class Layered:
+    """Layer-wise Top-k state on the device."""
+
+    def __init__(self, d, bounds, ks):
+        kt = int(ks.sum())
+        self.e = torch.zeros(d, device=DEV)
+        self.idx = torch.empty(kt, dtype=torch.int32, device=DEV)
+        self.val = torch.empty(kt, device=DEV)
+        self.ws = efs.new_topk_segmented_workspace(ks.size, kt, DEV)
+        self.off = torch.from_numpy(np.asarray(bounds, np.int64)).to(DEV)
+        self.k = torch.from_numpy(np.asarray(ks, np.int64)).to(DEV)
+
+    def step(self, gd):
+        efs.topk_segmented_compress(gd, self.e, LR, self.off, self.k, self.idx, self.val, self.ws)
+        assert efs.topk_segmented_status(self.ws) == 0
+        return self.idx.cpu().numpy(), self.val.cpu().numpy(), self.e.cpu().numpy()
+
+
+class Hard:
+    """Hard-threshold state on the device."""
+
+    def __init__(self, d, cap):
+        self.e = torch.zeros(d, device=DEV)
+        self.idx = torch.empty(cap, dtype=torch.int32, device=DEV)
+        self.val = torch.empty(cap, device=DEV)
+        self.ctr = efs.new_counter(DEV)
+        self.cap = cap
+
+    def step(self, gd, lam):
+        efs.ht_compress(gd, self.e, LR, lam, self.idx, self.val, self.ctr)
+        n = efs.counter_value(self.ctr)
+        assert n <= self.cap, "payload capacity exceeded"
+        return self.idx[:n].cpu().numpy(), self.val[:n].cpu().numpy(), self.e.cpu().numpy(), n
 
 
 @pytest.mark.timeout(1200)
-def test_thirty_ef_steps_of_the_benchmark_workload():
-    T = 30
+def test_workload2_hundred_ef_steps():
+    t0 = time.time()
     st = synth.Stream(2)
-    d, k = st.w.d, st.w.topk_k[0]
-    g0 = st.gradient(0, threads=16)
-    lam = synth.calibrate_lambda(g0, 0.001)
-    ks = synth.layerwise_k(st.bounds, 0.001)
-    kt = int(ks.sum())
-    e_ht, e_tk, e_sg = (torch.zeros(d, device=DEV) for _ in range(3))
-    idx = torch.empty(d, dtype=torch.int32, device=DEV)
-    val = torch.empty(d, device=DEV)
-    ctr = efs.new_counter(DEV)
-    tidx = torch.empty(k, dtype=torch.int32, device=DEV)
-    tval = torch.empty(k, device=DEV)
-    ws = efs.new_topk_workspace(d, k, DEV)
-    ws.zero_()
-    sidx = torch.empty(kt, dtype=torch.int32, device=DEV)
-    sval = torch.empty(kt, device=DEV)
-    sws = efs.new_topk_segmented_workspace(ks.size, kt, DEV)
-    sws.zero_()
-    offd = torch.from_numpy(st.bounds.astype(np.int64)).to(DEV)
-    kd = torch.from_numpy(ks).to(DEV)
+    w = st.w
+    d, k = w.d, w.topk_k[0]
+    g0 = st.gradient(0, threads=THREADS)
+    lam = oracle.calibrate_lambda(g0, w.densities[0])
+    assert lam == synth.stored_lambda(2, w.densities[0])
+    ks = synth.layerwise_k(st.bounds, w.densities[0])
+    bounds = st.bounds.astype(np.int64)
+    ht, flat, lay = Hard(d, d), Flat(d, k), Layered(d, bounds, ks)
+    r_ht, r_tk, r_sg = (np.zeros(d, np.float32) for _ in range(3))
+    bracket_steps, layer_hits = 0, []
+    for t in range(w.iters):
+        g = g0 if t == 0 else st.gradient(t, threads=THREADS)
+        gd = torch.from_numpy(g).to(DEV)
+        gi, gv, ge, n = ht.step(gd, lam)
+        ri, rv, r_ht, rk = oracle.ht(g, r_ht, LR, lam, mt=True)
+        assert n == rk, t
+        assert_payload_equal(gi, gv, ri, rv, "ht t=%d" % t)
+        assert_bits_equal(ge, r_ht, "ht e t=%d" % t)
+        gi, gv, ge = flat.step(gd)
+        ri, rv, r_tk = oracle.topk(g, r_tk, LR, k, mt=True)
+        assert_payload_equal(gi, gv, ri, rv, "topk t=%d" % t)
+        assert_bits_equal(ge, r_tk, "topk e t=%d" % t)
+        gi, gv, ge = lay.step(gd)
+        ri, rv, r_sg = oracle.topk_segmented(g, r_sg, LR, bounds, ks, mt=True)
+        assert_payload_equal(gi, gv, ri, rv, "layer-wise t=%d" % t)
+        assert_bits_equal(ge, r_sg, "layer-wise e t=%d" % t)
+        bracket_steps += efs.topk_took_bracket_path(flat.ws)
+        layer_hits.append(efs.topk_segmented_bracket_segments(lay.ws))
+        say(t0, "workload 2 step %d bit-exact: k_t %d, Top-k bracket %d, layers from the "
+                "bracket %d" % (t, n, efs.topk_took_bracket_path(flat.ws), layer_hits[-1]))
+    assert bracket_steps >= w.iters // 2
+    say(t0, "flat Top-k from the bracket in %d of %d steps" % (bracket_steps, w.iters))
+
+
+@pytest.mark.timeout(1800)
+def test_workload3_fifty_ef_steps_at_one_percent():
+    # 110e6 Student-t gradients in 200 layers at 1 %: millions of pairs and
+    # bracket candidates per call
+    t0 = time.time()
+    st = synth.Stream(3)
+    w = st.w
+    d, k, rho = w.d, w.topk_k[0], w.densities[0]
+    ks = synth.layerwise_k(st.bounds, rho)
+    bounds = st.bounds.astype(np.int64)
+    lam = synth.stored_lambda(3, rho)
+    ht, flat, lay = Hard(d, d // 4), Flat(d, k), Layered(d, bounds, ks)
     r_ht, r_tk, r_sg = (np.zeros(d, np.float32) for _ in range(3))
     bracket_steps = 0
-    for t in range(T):
-        g = g0 if t == 0 else st.gradient(t, threads=16)
+    for t in range(w.iters):
+        g = st.gradient(t, threads=THREADS)
         gd = torch.from_numpy(g).to(DEV)
-        efs.ht_compress(gd, e_ht, synth.LR, lam, idx, val, ctr)
-        efs.topk_compress(gd, e_tk, synth.LR, k, tidx, tval, ws)
-        efs.topk_segmented_compress(gd, e_sg, synth.LR, offd, kd, sidx, sval, sws)
-        n = efs.counter_value(ctr)
-        ri, rv, r_ht, rk = oracle.ht(g, r_ht, synth.LR, lam)
+        gi, gv, ge, n = ht.step(gd, lam)
+        ri, rv, r_ht, rk = oracle.ht(g, r_ht, LR, lam, mt=True)
         assert n == rk, t
-        assert_payload_equal(idx[:n].cpu().numpy(), val[:n].cpu().numpy(), ri, rv, "ht t=%d" % t)
-        assert_bits_equal(e_ht.cpu().numpy(), r_ht, "ht e t=%d" % t)
-        ti, tv, r_tk = oracle.topk(g, r_tk, synth.LR, k)
-        assert_payload_equal(tidx.cpu().numpy(), tval.cpu().numpy(), ti, tv, "topk t=%d" % t)
-        assert_bits_equal(e_tk.cpu().numpy(), r_tk, "topk e t=%d" % t)
-        si, sv, r_sg = oracle.topk_segmented(g, r_sg, synth.LR, st.bounds.astype(np.int64), ks)
-        assert_payload_equal(sidx.cpu().numpy(), sval.cpu().numpy(), si, sv, "layer-wise t=%d" % t)
-        assert_bits_equal(e_sg.cpu().numpy(), r_sg, "layer-wise e t=%d" % t)
-        bracket_steps += efs.topk_took_bracket_path(ws)
-        print("step %d bit-exact (k_t %d, Top-k bracket %d, layers from the bracket %d)"
-              % (t, n, efs.topk_took_bracket_path(ws), efs.topk_segmented_bracket_segments(sws)),
-              flush=True)
-    assert bracket_steps >= T // 2
+        if t == 0:
+            assert n == k   # the stored lambda keeps exactly K at the first step
+        assert_payload_equal(gi, gv, ri, rv, "ht t=%d" % t)
+        assert_bits_equal(ge, r_ht, "ht e t=%d" % t)
+        gi, gv, ge = flat.step(gd)
+        ri, rv, r_tk = oracle.topk(g, r_tk, LR, k, mt=True)
+        assert_payload_equal(gi, gv, ri, rv, "topk t=%d" % t)
+        assert_bits_equal(ge, r_tk, "topk e t=%d" % t)
+        gi, gv, ge = lay.step(gd)
+        ri, rv, r_sg = oracle.topk_segmented(g, r_sg, LR, bounds, ks, mt=True)
+        assert_payload_equal(gi, gv, ri, rv, "layer-wise t=%d" % t)
+        assert_bits_equal(ge, r_sg, "layer-wise e t=%d" % t)
+        bracket_steps += efs.topk_took_bracket_path(flat.ws)
+        say(t0, "workload 3 step %d bit-exact: ht k_t %d, Top-k bracket %d, layers from the "
+                "bracket %d" % (t, n, efs.topk_took_bracket_path(flat.ws),
+                                efs.topk_segmented_bracket_segments(lay.ws)))
+    assert bracket_steps >= 1
 
 
-@pytest.mark.timeout(1200)
-def test_six_ef_steps_of_the_heavy_tailed_110m_workload_at_one_percent():
-    # 110e6 Student-t gradients in 200 layers: flat Top-k at k = 1.1 M and
-    # layer-wise Top-k at 1 % per layer, e carried over six steps (large k:
-    # millions of bracket candidates), every step bit-exact
-    T = 6
-    st = synth.Stream(3)
-    d = st.w.d
-    k = st.w.topk_k[0]
-    ks = synth.layerwise_k(st.bounds, 0.01)
-    kt = int(ks.sum())
-    e_tk, e_sg = (torch.zeros(d, device=DEV) for _ in range(2))
-    tidx = torch.empty(k, dtype=torch.int32, device=DEV)
-    tval = torch.empty(k, device=DEV)
-    ws = efs.new_topk_workspace(d, k, DEV)
-    ws.zero_()
-    sidx = torch.empty(kt, dtype=torch.int32, device=DEV)
-    sval = torch.empty(kt, device=DEV)
-    sws = efs.new_topk_segmented_workspace(ks.size, kt, DEV)
-    sws.zero_()
-    offd = torch.from_numpy(st.bounds.astype(np.int64)).to(DEV)
-    kd = torch.from_numpy(ks).to(DEV)
-    r_tk, r_sg = (np.zeros(d, np.float32) for _ in range(2))
-    for t in range(T):
-        g = st.gradient(t, threads=16)
-        gd = torch.from_numpy(g).to(DEV)
-        efs.topk_compress(gd, e_tk, synth.LR, k, tidx, tval, ws)
-        efs.topk_segmented_compress(gd, e_sg, synth.LR, offd, kd, sidx, sval, sws)
-        ti, tv, r_tk = oracle.topk(g, r_tk, synth.LR, k)
-        assert_payload_equal(tidx.cpu().numpy(), tval.cpu().numpy(), ti, tv, "topk t=%d" % t)
-        assert_bits_equal(e_tk.cpu().numpy(), r_tk, "topk e t=%d" % t)
-        si, sv, r_sg = oracle.topk_segmented(g, r_sg, synth.LR, st.bounds.astype(np.int64), ks)
-        assert_payload_equal(sidx.cpu().numpy(), sval.cpu().numpy(), si, sv, "layer-wise t=%d" % t)
-        assert_bits_equal(e_sg.cpu().numpy(), r_sg, "layer-wise e t=%d" % t)
-        print("step %d bit-exact (Top-k bracket %d, layers from the bracket %d)"
-              % (t, efs.topk_took_bracket_path(ws), efs.topk_segmented_bracket_segments(sws)),
-              flush=True)
+@pytest.mark.timeout(1800)
+def test_workload4_twenty_five_steps_of_eight_workers():
+    t0 = time.time()
+    st = synth.Stream(4)
+    w = st.w
+    d = w.d
+    lam = synth.stored_lambda(4, w.densities[0])
+    workers = [Hard(d, d // 4) for _ in range(w.n_workers)]
+    refs = [np.zeros(d, np.float32) for _ in range(w.n_workers)]
+    out = torch.empty(d, device=DEV)
+    p_dev = [(h.idx, h.val, h.ctr) for h in workers]
+    ws = efs.new_apply_workspace(p_dev, d, DEV)
+    for t in range(25):
+        payloads = []
+        for wk in range(w.n_workers):
+            g = st.gradient(t, worker=wk, threads=THREADS)
+            gi, gv, ge, n = workers[wk].step(torch.from_numpy(g).to(DEV), lam)
+            ri, rv, refs[wk], rk = oracle.ht(g, refs[wk], LR, lam, mt=True)
+            assert n == rk
+            assert_payload_equal(gi, gv, ri, rv, "worker %d t=%d" % (wk, t))
+            assert_bits_equal(ge, refs[wk], "worker %d e t=%d" % (wk, t))
+            payloads.append((gi, gv))   # the device order is what is averaged
+        efs.sparse_accumulate(p_dev, d, out, ws)
+        assert_bits_equal(out.cpu().numpy(), oracle.accumulate(payloads, d, mt=True),
+                          "average t=%d" % t)
+        assert efs.sparse_status(ws) == 0
+        say(t0, "workload 4 step %d bit-exact: k_t %s" % (t, [p[0].size for p in payloads]))

@@ -79,7 +79,7 @@ def test_workload1_gauss_1m_all_iterations():
     st = synth.Stream(1)
     w = st.w
     gs = [st.gradient(t) for t in range(w.iters)]
-    lam = synth.calibrate_lambda(gs[0], w.densities[0])
+    lam = oracle.calibrate_lambda(gs[0], w.densities[0])
     k = w.topk_k[0]
     ht, tk = Worker(w.d, w.d), Worker(w.d, k, k=k)
     e_ht = np.zeros(w.d, np.float32)
@@ -105,7 +105,7 @@ def test_workload2_segments_25m():
     w = st.w
     T = 4
     gs = [st.gradient(t, threads=THREADS) for t in range(T)]
-    lam = synth.calibrate_lambda(gs[0], w.densities[0])
+    lam = oracle.calibrate_lambda(gs[0], w.densities[0])
     k = w.topk_k[0]
     ht, tk = Worker(w.d, w.d), Worker(w.d, k, k=k)
     e_ht = np.zeros(w.d, np.float32)
@@ -244,7 +244,7 @@ def test_workload3_student_t_110m():
     say("workload 3 inputs ready")
     g_devs = [torch.from_numpy(g).to(DEV) for g in gs]
     for density, k in zip(w.densities, w.topk_k):
-        lam = synth.calibrate_lambda(gs[0], density)
+        lam = oracle.calibrate_lambda(gs[0], density)
         ht = Worker(w.d, w.d // 8)
         e_ht = np.zeros(w.d, np.float32)
         for t in range(2):
@@ -266,7 +266,7 @@ def test_workload3_student_t_110m():
 def test_workload4_eight_workers_average():
     st = synth.Stream(4)
     w = st.w
-    lam = synth.calibrate_lambda(st.gradient(0, worker=0, threads=THREADS), w.densities[0])
+    lam = oracle.calibrate_lambda(st.gradient(0, worker=0, threads=THREADS), w.densities[0])
     workers = [Worker(w.d, w.d // 4) for _ in range(w.n_workers)]
     e_ref = [np.zeros(w.d, np.float32) for _ in range(w.n_workers)]
     out = torch.empty(w.d, dtype=torch.float32, device=DEV)
@@ -289,9 +289,10 @@ def test_workload4_eight_workers_average():
             assert_payload_equal(gi, gv, ri, rv, "worker %d t=%d" % (wk, t))
             # the device payload, in its own (unspecified) order, is what is averaged
             payloads.append((gi, gv))
-        efs.sparse_accumulate(p_dev, w.d, out)
+        efs.sparse_accumulate(p_dev, w.d, out, ws)
         ref = oracle.accumulate(payloads, w.d)
         assert_bits_equal(out.cpu().numpy(), ref, "average t=%d" % t)
+        assert efs.sparse_status(ws) == 0
         say("workload 4 t=%d: 8 workers averaged, k_t=%s" % (
             t, [efs.counter_value(o.ctr) for o in workers]))
         x_sgd = x.clone()
@@ -314,7 +315,7 @@ def test_workload5_outliers_1_5b_streamed():
     chunk = 1 << 26
     say("workload 5: drawing g_0 (%d elements)" % d)
     g = st.gradient(0, threads=THREADS)
-    lam = synth.calibrate_lambda(g, w.densities[0])
+    lam = synth.stored_lambda(5, w.densities[0])
     g_dev = torch.empty(d, dtype=torch.float32, device=DEV)
     for lo in range(0, d, chunk):
         g_dev[lo:lo + chunk].copy_(torch.from_numpy(g[lo:lo + chunk]))
@@ -341,18 +342,43 @@ def test_workload5_outliers_1_5b_streamed():
             assert_bits_equal(ht.e[lo:hi].cpu().numpy(), e_chunk, "ht e' t=%d chunk %d" % (t, lo))
             total += rk
         assert n == total
+        if t == 0:
+            assert n == w.topk_k[0]   # the stored lambda keeps exactly K at the first step
         say("workload 5 ht t=%d: k_t=%d matches" % (t, n))
     del ht, e_ref
 
-    # Top-k on g_1 from e = 0 (the acc is then fl(lr * g_1))
+    # Top-k on g_1 from e = 0 (the acc is then fl(lr * g_1)): the radix path
     k = w.topk_k[0]
     tk = Worker(d, k, k=k)
+    tk.ws.zero_()    # no threshold recorded yet
     tk.topk(g_dev, k)
+    assert not efs.topk_took_bracket_path(tk.ws)
     gi, gv = tk.payload(k)
     zeros = np.zeros(chunk, np.float32)
     check_topk_chunked(
         d, k, gi, gv,
-        acc_fn=lambda lo, hi: oracle.ht(g[lo:hi], zeros[:hi - lo], LR, np.inf, cap=0)[2],
+        acc_fn=lambda lo, hi: oracle.ht(g[lo:hi], zeros[:hi - lo], LR, np.inf, cap=0, mt=True)[2],
         e_next_fn=lambda lo, hi: tk.e[lo:hi].cpu().numpy(),
         chunk=chunk)
-    say("workload 5 topk k=%d ok" % k)
+    say("workload 5 topk k=%d ok (radix path)" % k)
+
+    # Error feedback on the same workspace: e carried, the same gradient
+    # again, so the threshold drifts up steadily and a later call selects
+    # from the bracket around the extrapolated threshold (24 M candidate
+    # slots, 64-bit offsets).  That call is checked in full.
+    e_before = torch.empty_like(tk.e)
+    for t in range(1, 9):
+        e_before.copy_(tk.e)
+        tk.topk(g_dev, k)
+        if efs.topk_took_bracket_path(tk.ws):
+            break
+    assert efs.topk_took_bracket_path(tk.ws), "no call took the bracket path"
+    say("workload 5 topk call %d took the bracket path; checking it" % t)
+    gi, gv = tk.payload(k)
+    check_topk_chunked(
+        d, k, gi, gv,
+        acc_fn=lambda lo, hi: oracle.ht(g[lo:hi], e_before[lo:hi].cpu().numpy(), LR, np.inf,
+                                        cap=0, mt=True)[2],
+        e_next_fn=lambda lo, hi: tk.e[lo:hi].cpu().numpy(),
+        chunk=chunk)
+    say("workload 5 topk k=%d ok (bracket path, call %d)" % (k, t))
