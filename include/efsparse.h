@@ -198,18 +198,26 @@ efs_status topk_segmented_compress(const float *g, float *e, int64_t d, float lr
  *   n_workers  1 <= n_workers <= EFS_MAX_WORKERS; sum of caps <= 2^32 - 1.
  *   d          length of out; d == 0 is a no-op.
  *   out        [d] fp32, 16-byte aligned, overwritten.
- *   workspace  device memory of at least
- *              sparse_accumulate_workspace_bytes(n_workers, d, sum of caps)
- *              bytes, 16-byte aligned: a 256-byte control block, an 8-byte
- *              counter and a 4-byte segment start per (range of 8192
- *              coordinates, worker), and 8 bytes per payload slot for the
- *              pairs grouped by range.  Contents need no initialisation: each
- *              counter carries the 40-bit epoch of the call that wrote it
- *              (the control block's epoch, advanced by every call), so a
+ *   workspace  device memory, 16-byte aligned, in one of two layouts chosen
+ *              by workspace_bytes:
+ *                bucketed, when workspace_bytes >=
+ *                sparse_bucket_workspace_bytes(n_workers, d) (about 8 n d
+ *                bytes): a 256-byte control block, an 8-byte counter per
+ *                (range of 4096 coordinates, worker) and a bucket of 4096
+ *                8-byte slots per counter.  Two launches.
+ *                packed, otherwise; needs at least
+ *                sparse_accumulate_workspace_bytes(n_workers, d, sum of caps)
+ *                bytes: the control block, an 8-byte counter and a 4-byte
+ *                segment start per (range, worker), and 8 bytes per payload
+ *                slot for the pairs grouped by range.  Four launches.
+ *              Both give the same bits.  Contents need no initialisation:
+ *              each counter carries the 40-bit epoch of the call that wrote
+ *              it (the control block's epoch, advanced by every call), so a
  *              counter of an earlier call reads as zero, as does arbitrary
  *              content except when its epoch bits equal the current epoch
- *              (probability 2^-40 per counter for random bytes).  Not
- *              shareable between concurrent calls.
+ *              (probability 2^-40 per counter for random bytes).  Calls on
+ *              one workspace must be ordered (one stream, or synchronised
+ *              streams); concurrent calls on one workspace race.
  * Payload entries with an index outside [0, d) are skipped and reported in
  * the status word (EFS_SPARSE_BAD_INDEX).  The status word is the uint32 at
  * sparse_status_offset() in the workspace: the EFS_SPARSE_* bits of the last
@@ -218,7 +226,10 @@ efs_status topk_segmented_compress(const float *g, float *e, int64_t d, float lr
 #define EFS_MAX_WORKERS 64
 #define EFS_SPARSE_TRUNCATED 1u
 #define EFS_SPARSE_BAD_INDEX 2u
+/* Bytes of the packed and of the bucketed workspace layout; 0 if the
+ * arguments are out of range. */
 size_t sparse_accumulate_workspace_bytes(int32_t n_workers, int64_t d, int64_t total_cap);
+size_t sparse_bucket_workspace_bytes(int32_t n_workers, int64_t d);
 size_t sparse_status_offset(void);
 efs_status sparse_accumulate(const int32_t *const *idx, const float *const *val,
                              const uint32_t *const *counts, const int64_t *caps,
@@ -245,7 +256,8 @@ efs_status sparse_accumulate(const int32_t *const *idx, const float *const *val,
  * written (no fused multiply-add).
  *
  *   idx, val, counts, caps, n_workers, d, workspace, status word
- *              as for sparse_accumulate (the same workspace layout).
+ *              as for sparse_accumulate (the same workspace layouts, chosen
+ *              the same way).
  *   x          [d] fp32, 16-byte aligned, read and written in place (mode
  *              EFS_APPLY_AVERAGE only writes it).  Must not overlap a payload.
  *   m          [d] fp32 momentum, 16-byte aligned, read and written in place;
@@ -256,7 +268,8 @@ efs_status sparse_accumulate(const int32_t *const *idx, const float *const *val,
  * invalid argument; nothing is launched then.  d == 0 is a no-op. */
 enum { EFS_APPLY_AVERAGE = 0, EFS_APPLY_SGD = 1, EFS_APPLY_MOMENTUM = 2 };
 
-/* Workspace bytes for sparse_apply; 0 if the arguments are out of range. */
+/* Workspace bytes of sparse_apply's packed layout (the same as
+ * sparse_accumulate_workspace_bytes); 0 if the arguments are out of range. */
 size_t sparse_apply_workspace_bytes(int32_t n_workers, int64_t d, int64_t total_cap);
 
 efs_status sparse_apply(const int32_t *const *idx, const float *const *val,

@@ -67,6 +67,8 @@ def declare(lib):
     lib.sparse_accumulate.restype = ctypes.c_int
     lib.sparse_accumulate_workspace_bytes.argtypes = [i32, i64, i64]
     lib.sparse_accumulate_workspace_bytes.restype = ctypes.c_size_t
+    lib.sparse_bucket_workspace_bytes.argtypes = [i32, i64]
+    lib.sparse_bucket_workspace_bytes.restype = ctypes.c_size_t
     lib.sparse_status_offset.argtypes = []
     lib.sparse_status_offset.restype = ctypes.c_size_t
     lib.topk_segmented_workspace_bytes.argtypes = [i32, i64]
@@ -327,12 +329,27 @@ def sparse_apply_workspace_bytes(n_workers: int, d: int, total_cap: int) -> int:
     return int(load_library().sparse_apply_workspace_bytes(int(n_workers), int(d), int(total_cap)))
 
 
-def new_apply_workspace(payloads: Sequence[Tuple], d: int, device="cuda"):
+def sparse_bucket_workspace_bytes(n_workers: int, d: int) -> int:
+    return int(load_library().sparse_bucket_workspace_bytes(int(n_workers), int(d)))
+
+
+LAYOUTS = ("bucketed", "packed")
+
+
+def new_apply_workspace(payloads: Sequence[Tuple], d: int, device="cuda", layout="bucketed"):
     """A workspace for sparse_accumulate or sparse_apply over payloads of
-    these capacities."""
+    these capacities, in the given layout: "bucketed" (two launches, about
+    8 n d bytes) or "packed" (four launches, about 8 bytes per payload
+    slot).  A call takes the bucketed layout whenever the workspace holds
+    it, so a packed workspace at least that large is used as bucketed."""
     import torch
-    total = sum(int(p[0].numel()) for p in payloads)
-    nbytes = sparse_apply_workspace_bytes(len(payloads), d, total)
+    if layout not in LAYOUTS:
+        raise ValueError("layout must be one of %s" % (LAYOUTS,))
+    if layout == "bucketed":
+        nbytes = sparse_bucket_workspace_bytes(len(payloads), d)
+    else:
+        total = sum(int(p[0].numel()) for p in payloads)
+        nbytes = sparse_apply_workspace_bytes(len(payloads), d, total)
     return torch.empty(max(nbytes, 16), dtype=torch.uint8, device=device)
 
 

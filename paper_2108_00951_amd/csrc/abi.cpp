@@ -207,6 +207,11 @@ size_t sparse_accumulate_workspace_bytes(int32_t n_workers, int64_t d, int64_t t
     return sparse_apply_workspace_bytes(n_workers, d, total_cap);
 }
 
+size_t sparse_bucket_workspace_bytes(int32_t n_workers, int64_t d) {
+    if (n_workers < 1 || n_workers > efs::kMaxApplyWorkers || d < 0 || d > kMaxLen) return 0;
+    return efs::apply_bucket_workspace_size(n_workers, d);
+}
+
 size_t sparse_status_offset(void) { return efs::apply_status_offset(); }
 
 // Checks shared by sparse_accumulate and sparse_apply: the payload arrays,
@@ -240,6 +245,8 @@ static efs_status check_payloads(const char *name, const int32_t *const *idx,
     if (d == 0) return EFS_OK;
     if (workspace == nullptr || !aligned(workspace, 16))
         return fail(EFS_EINVAL, "%s: workspace must be non-NULL and 16-byte aligned", name);
+    // the bucketed layout whenever the workspace holds it, else the packed one
+    if (workspace_bytes >= efs::apply_bucket_workspace_size(n_workers, d)) return EFS_OK;
     const size_t need = efs::apply_workspace_size(n_workers, d, total);
     if (workspace_bytes < need)
         return fail(EFS_ESPACE, "%s: workspace has %zu bytes, needs %zu", name, workspace_bytes, need);
@@ -254,7 +261,7 @@ efs_status sparse_accumulate(const int32_t *const *idx, const float *const *val,
                                         out, workspace, workspace_bytes);
     if (s != EFS_OK || d == 0) return s;
     return check_launch(efs::launch_apply(idx, val, counts, caps, n_workers, d, EFS_APPLY_AVERAGE,
-                                          out, nullptr, 0.0f, 0.0f, workspace,
+                                          out, nullptr, 0.0f, 0.0f, workspace, workspace_bytes,
                                           static_cast<hipStream_t>(stream)),
                         "sparse_accumulate");
 }
@@ -276,7 +283,8 @@ efs_status sparse_apply(const int32_t *const *idx, const float *const *val,
                                         workspace, workspace_bytes);
     if (s != EFS_OK || d == 0) return s;
     return check_launch(efs::launch_apply(idx, val, counts, caps, n_workers, d, mode, x, m, beta,
-                                          gamma, workspace, static_cast<hipStream_t>(stream)),
+                                          gamma, workspace, workspace_bytes,
+                                          static_cast<hipStream_t>(stream)),
                         "sparse_apply");
 }
 

@@ -32,12 +32,15 @@ hipError_t launch_topk_segmented(const float *g, float *e, int64_t d, float lr, 
 constexpr int kMaxApplyWorkers = 64;
 constexpr uint32_t kSparseTruncated = 1u;   // a count exceeded its payload's capacity
 constexpr uint32_t kSparseBadIndex = 2u;    // an index outside [0, d) was ignored
+// Workspace of the packed layout (four launches) and of the bucketed one
+// (two launches, taken whenever the workspace holds it).
 size_t apply_workspace_size(int32_t n, int64_t d, int64_t total_cap);
+size_t apply_bucket_workspace_size(int32_t n, int64_t d);
 size_t apply_status_offset();
 hipError_t launch_apply(const int32_t *const *idx, const float *const *val,
                         const uint32_t *const *counts, const int64_t *caps, int32_t n,
                         int64_t d, int mode, float *x, float *m, float beta, float gamma,
-                        void *workspace, hipStream_t stream);
+                        void *workspace, size_t workspace_bytes, hipStream_t stream);
 
 hipError_t launch_copy(const float *src, float *dst, int64_t n, hipStream_t stream);
 hipError_t launch_stream_probe(const float *x, float *y, int64_t n, int mode, hipStream_t stream);

@@ -196,6 +196,17 @@ def test_apply_workspace_size(lib):
     b = lib.sparse_apply_workspace_bytes(8, 25_600_000, 1000)
     assert b - a == 8000                     # 8 bytes per pair slot
     assert a >= (25_600_000 // 8192) * 4       # one counter per 8192-coordinate range
+    # the bucketed layout: a bucket of 8192 8-byte slots per (range, worker)
+    assert lib.sparse_bucket_workspace_bytes(0, 100) == 0
+    assert lib.sparse_bucket_workspace_bytes(binding.MAX_WORKERS + 1, 100) == 0
+    assert lib.sparse_bucket_workspace_bytes(2, -1) == 0
+    ranges = -(-25_600_000 // 8192)
+    bk = lib.sparse_bucket_workspace_bytes(8, 25_600_000)
+    assert bk >= ranges * 8 * 8192 * 8
+    assert bk - ranges * 8 * 8192 * 8 < 1 << 20   # control block and counters
+    # for payload capacities of d / 4 the bucketed layout is the larger one
+    assert bk > lib.sparse_apply_workspace_bytes(8, 25_600_000, 2 * 25_600_000)
+    assert lib.sparse_bucket_workspace_bytes(1, 1) > lib.sparse_apply_workspace_bytes(1, 1, 1)
 
 
 def test_topk_segmented_rejects_bad_arguments(lib):

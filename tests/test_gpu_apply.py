@@ -62,46 +62,48 @@ def host_state(d, seed):
     return x, m
 
 
-def run_apply(p_dev, d, mode, x_host, m_host=None, ws=None):
+def run_apply(p_dev, d, mode, x_host, m_host=None, ws=None, layout="bucketed"):
     x = dev(x_host)
     m = dev(m_host) if m_host is not None else None
     if ws is None:
-        ws = efs.new_apply_workspace(p_dev, d, DEV)
+        ws = efs.new_apply_workspace(p_dev, d, DEV, layout=layout)
     efs.sparse_apply(p_dev, d, mode, x, ws, m=m, beta=BETA, gamma=GAMMA)
     return x.cpu().numpy(), (m.cpu().numpy() if m is not None else None)
 
 
-def check_all_modes(p_dev, p_ref, d, seed):
+def check_all_modes(p_dev, p_ref, d, seed, layout="bucketed"):
     x0, m0 = host_state(d, seed)
-    say("  average")
-    got, _ = run_apply(p_dev, d, efs.APPLY_AVERAGE, np.full(d, 7.0, np.float32))
+    say("  average (%s)" % layout)
+    got, _ = run_apply(p_dev, d, efs.APPLY_AVERAGE, np.full(d, 7.0, np.float32), layout=layout)
     assert_bits_equal(got, oracle.accumulate(p_ref, d))
     say("  sgd")
-    got, _ = run_apply(p_dev, d, efs.APPLY_SGD, x0)
+    got, _ = run_apply(p_dev, d, efs.APPLY_SGD, x0, layout=layout)
     want, _ = oracle.update(p_ref, x0, 1)
     assert_bits_equal(got, want)
     say("  momentum")
-    got_x, got_m = run_apply(p_dev, d, efs.APPLY_MOMENTUM, x0, m0)
+    got_x, got_m = run_apply(p_dev, d, efs.APPLY_MOMENTUM, x0, m0, layout=layout)
     want_x, want_m = oracle.update(p_ref, x0, 2, m=m0, beta=BETA, gamma=GAMMA)
     assert_bits_equal(got_m, want_m)
     assert_bits_equal(got_x, want_x)
 
 
+@pytest.mark.parametrize("layout", efs.LAYOUTS)
 @pytest.mark.parametrize("n", [1, 2, 3, 8])
-def test_apply_ht_payloads(n):
+def test_apply_ht_payloads(n, layout):
     d = 400_009
     say("apply ht payloads n=%d d=%d" % (n, d))
     p_dev, p_ref = ht_payloads(d, n, np.float32(2.2e-4), 100 + 10 * n)
-    check_all_modes(p_dev, p_ref, d, n)
+    check_all_modes(p_dev, p_ref, d, n, layout)
 
 
+@pytest.mark.parametrize("layout", efs.LAYOUTS)
 @pytest.mark.parametrize("d", [1, 5, 8192, 8192 * 2 + 5])
-def test_apply_dense_payloads(d):
+def test_apply_dense_payloads(d, layout):
     # lambda = 0: every worker sends every coordinate (the densest payload)
     say("apply dense payloads d=%d" % d)
     p_dev, p_ref = ht_payloads(d, 3, np.float32(0.0), 7, cap=d)
     assert all(p[0].size == d for p in p_ref)
-    check_all_modes(p_dev, p_ref, d, 3)
+    check_all_modes(p_dev, p_ref, d, 3, layout)
 
 
 def test_apply_topk_payloads():
@@ -120,7 +122,8 @@ def test_apply_topk_payloads():
     check_all_modes(p_dev, p_ref, d, 4)
 
 
-def test_apply_shuffled_overlapping_payloads():
+@pytest.mark.parametrize("layout", efs.LAYOUTS)
+def test_apply_shuffled_overlapping_payloads(layout):
     # pairs in random order, heavy overlap between workers, values chosen so
     # the worker order of the sum matters
     d = 8192 * 4 + 77
@@ -132,7 +135,7 @@ def test_apply_shuffled_overlapping_payloads():
         p_dev.append((dev(idx), dev(val)))
         p_ref.append((idx, val))
     say("apply shuffled payloads")
-    check_all_modes(p_dev, p_ref, d, 5)
+    check_all_modes(p_dev, p_ref, d, 5, layout)
 
 
 def test_apply_worker_order_decides_rounding():
@@ -145,7 +148,8 @@ def test_apply_worker_order_decides_rounding():
     assert got.view(np.uint32)[4] == 0x3EAAAAAB
 
 
-def test_apply_empty_payloads_and_counts():
+@pytest.mark.parametrize("layout", efs.LAYOUTS)
+def test_apply_empty_payloads_and_counts(layout):
     d = 8192 * 2 + 9
     x0, m0 = host_state(d, 8)
     idx = torch.empty(16, dtype=torch.int32, device=DEV)
@@ -154,26 +158,27 @@ def test_apply_empty_payloads_and_counts():
     empty = torch.empty(0, dtype=torch.int32, device=DEV)
     emptyv = torch.empty(0, dtype=torch.float32, device=DEV)
     p_dev = [(idx, val, ctr), (empty, emptyv)]
-    got, _ = run_apply(p_dev, d, efs.APPLY_AVERAGE, np.full(d, 3.0, np.float32))
+    got, _ = run_apply(p_dev, d, efs.APPLY_AVERAGE, np.full(d, 3.0, np.float32), layout=layout)
     assert np.all(got.view(np.uint32) == 0)
-    got, _ = run_apply(p_dev, d, efs.APPLY_SGD, x0)
+    got, _ = run_apply(p_dev, d, efs.APPLY_SGD, x0, layout=layout)
     assert_bits_equal(got, x0)
-    got_x, got_m = run_apply(p_dev, d, efs.APPLY_MOMENTUM, x0, m0)
+    got_x, got_m = run_apply(p_dev, d, efs.APPLY_MOMENTUM, x0, m0, layout=layout)
     none = (np.zeros(0, np.int32), np.zeros(0, np.float32))
     want_x, want_m = oracle.update([none, none], x0, 2, m=m0, beta=BETA, gamma=GAMMA)
     assert_bits_equal(got_m, want_m)
     assert_bits_equal(got_x, want_x)
 
 
-def test_apply_ignores_out_of_range_indices():
+@pytest.mark.parametrize("layout", efs.LAYOUTS)
+def test_apply_ignores_out_of_range_indices(layout):
     d = 9000
     idx = np.array([3, -1, 8999, 9000, 8192, 2 ** 31 - 1, 7], dtype=np.int32)
     val = np.array([1.0, 5.0, 2.0, 6.0, 3.0, 4.0, 0.5], dtype=np.float32)
     keep = (idx >= 0) & (idx < d)
     p_dev = [(dev(idx), dev(val)), (dev(idx[:1]), dev(val[:1]))]
     p_ref = [(idx[keep], val[keep]), (idx[:1], val[:1])]
-    check_all_modes(p_dev, p_ref, d, 9)
-    ws = efs.new_apply_workspace(p_dev, d, DEV)
+    check_all_modes(p_dev, p_ref, d, 9, layout)
+    ws = efs.new_apply_workspace(p_dev, d, DEV, layout=layout)
     run_apply(p_dev, d, efs.APPLY_SGD, np.zeros(d, np.float32), ws=ws)
     assert efs.sparse_status(ws) == efs.SPARSE_BAD_INDEX
 
@@ -202,7 +207,8 @@ def test_apply_one_worker_signed_zeros():
     assert_bits_equal(got_x, want_x)
 
 
-def test_apply_count_larger_than_capacity():
+@pytest.mark.parametrize("layout", efs.LAYOUTS)
+def test_apply_count_larger_than_capacity(layout):
     # a counter above the capacity (an overflowed payload) uses caps[w] pairs
     d = 20_000
     rng = np.random.default_rng(12)
@@ -211,13 +217,14 @@ def test_apply_count_larger_than_capacity():
     ctr = efs.new_counter(DEV)
     ctr[0] = 100_000
     p_dev = [(dev(idx), dev(val), ctr)]
-    ws = efs.new_apply_workspace(p_dev, d, DEV)
+    ws = efs.new_apply_workspace(p_dev, d, DEV, layout=layout)
     got, _ = run_apply(p_dev, d, efs.APPLY_AVERAGE, np.zeros(d, np.float32), ws=ws)
     assert_bits_equal(got, oracle.accumulate([(idx, val)], d))
     assert efs.sparse_status(ws) == efs.SPARSE_TRUNCATED
 
 
-def test_apply_max_workers():
+@pytest.mark.parametrize("layout", efs.LAYOUTS)
+def test_apply_max_workers(layout):
     d = 8192 + 1000
     n = efs.MAX_WORKERS
     rng = np.random.default_rng(13)
@@ -228,15 +235,16 @@ def test_apply_max_workers():
         p_dev.append((dev(idx), dev(val)))
         p_ref.append((idx, val))
     say("apply n=%d" % n)
-    check_all_modes(p_dev, p_ref, d, 13)
+    check_all_modes(p_dev, p_ref, d, 13, layout)
 
 
-def test_apply_workspace_contents_do_not_matter_and_repeat():
+@pytest.mark.parametrize("layout", efs.LAYOUTS)
+def test_apply_workspace_contents_do_not_matter_and_repeat(layout):
     d = 8192 * 3 + 1
     p_dev, p_ref = ht_payloads(d, 4, np.float32(2.2e-4), 40)
     x0, m0 = host_state(d, 14)
     want_x, want_m = oracle.update(p_ref, x0, 2, m=m0, beta=BETA, gamma=GAMMA)
-    ws = efs.new_apply_workspace(p_dev, d, DEV)
+    ws = efs.new_apply_workspace(p_dev, d, DEV, layout=layout)
     for fill in (0, 255, 0x5A, None):
         if fill is None:
             ws.copy_(torch.randint(0, 256, ws.shape, dtype=torch.uint8, device=DEV))
@@ -247,7 +255,8 @@ def test_apply_workspace_contents_do_not_matter_and_repeat():
         assert_bits_equal(got_x, want_x)
 
 
-def test_apply_ef_momentum_loop():
+@pytest.mark.parametrize("layout", efs.LAYOUTS)
+def test_apply_ef_momentum_loop(layout):
     # Algorithm 2 end to end for 4 steps: every worker compresses g + e with
     # the hard threshold (lr = 1: the learning rate is applied at the update),
     # the payloads are averaged and applied with momentum; x, m and each e
@@ -262,7 +271,7 @@ def test_apply_ef_momentum_loop():
     val = [torch.empty(d, dtype=torch.float32, device=DEV) for _ in range(n)]
     ctr = [efs.new_counter(DEV) for _ in range(n)]
     p_dev = [(idx[w], val[w], ctr[w]) for w in range(n)]
-    ws = efs.new_apply_workspace(p_dev, d, DEV)
+    ws = efs.new_apply_workspace(p_dev, d, DEV, layout=layout)
     for t in range(T):
         say("  momentum loop step", t)
         p_ref = []
@@ -279,9 +288,11 @@ def test_apply_ef_momentum_loop():
         assert_bits_equal(x.cpu().numpy(), x_ref)
 
 
-def test_apply_many_ranges_two_level_scan():
-    # more than 4096 ranges of 8192 coordinates: the range counters are
-    # scanned in several chunks plus a pass over the chunk totals
+@pytest.mark.parametrize("layout", efs.LAYOUTS)
+def test_apply_many_ranges(layout):
+    # more than 4096 ranges of 8192 coordinates: more (range, worker)
+    # counters than one tile of the packed layout's scan (8192), pairs at
+    # both ends and in the last range
     d = 4096 * 8192 + 8192 * 37 + 11
     rng = np.random.default_rng(16)
     p_dev, p_ref = [], []
@@ -291,10 +302,10 @@ def test_apply_many_ranges_two_level_scan():
         val = rng.standard_normal(idx.size).astype(np.float32)
         p_dev.append((dev(idx), dev(val)))
         p_ref.append((idx, val))
-    say("apply two-level scan d=%d" % d)
+    say("apply many ranges d=%d (%s)" % (d, layout))
     x0 = rng.standard_normal(d).astype(np.float32)
-    got, _ = run_apply(p_dev, d, efs.APPLY_SGD, x0)
+    got, _ = run_apply(p_dev, d, efs.APPLY_SGD, x0, layout=layout)
     want, _ = oracle.update(p_ref, x0, 1)
     assert_bits_equal(got, want)
-    got, _ = run_apply(p_dev, d, efs.APPLY_AVERAGE, x0)
+    got, _ = run_apply(p_dev, d, efs.APPLY_AVERAGE, x0, layout=layout)
     assert_bits_equal(got, oracle.accumulate(p_ref, d))

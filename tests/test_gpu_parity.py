@@ -531,8 +531,9 @@ def test_topk_ef_loop_matches_oracle_each_step():
 # n-worker average
 # ---------------------------------------------------------------------------
 
+@pytest.mark.parametrize("layout", efs.LAYOUTS)
 @pytest.mark.parametrize("n", [1, 2, 3, 8, 40])
-def test_accumulate_matches_oracle(n):
+def test_accumulate_matches_oracle(n, layout):
     d = 400_009
     lam = np.float32(2.2e-4)
     payloads_dev, payloads_ref = [], []
@@ -544,11 +545,33 @@ def test_accumulate_matches_oracle(n):
         payloads_dev.append((st.idx, st.val, st.ctr))
         payloads_ref.append((gi, gv))
     out = torch.empty(d, dtype=torch.float32, device=DEV)
-    ws = efs.new_apply_workspace(payloads_dev, d, DEV)
+    ws = efs.new_apply_workspace(payloads_dev, d, DEV, layout=layout)
     efs.sparse_accumulate(payloads_dev, d, out, ws)
     ref = oracle.accumulate(payloads_ref, d)
     assert_bits_equal(out.cpu().numpy(), ref)
     assert efs.sparse_status(ws) == 0
+
+
+def test_accumulate_layouts_alternate_on_one_workspace():
+    # the same memory used as bucketed (whole) and as packed (a shorter view)
+    # in turn, with different payloads each call: both layouts keep the
+    # counters and the control block in the same state between calls
+    d, n = 300_007, 3
+    lam = np.float32(3e-4)
+    states = [HT(d, cap=d // 8) for _ in range(n)]
+    p_dev = [(s.idx, s.val, s.ctr) for s in states]
+    whole = efs.new_apply_workspace(p_dev, d, DEV, layout="bucketed")
+    packed = whole[:efs.sparse_apply_workspace_bytes(n, d, sum(s.cap for s in states))]
+    out = torch.empty(d, dtype=torch.float32, device=DEV)
+    for t in range(6):
+        ref_in = []
+        for w, s in enumerate(states):
+            gi, gv, _, _ = s.step(synth.small_gradient(700 + 10 * t + w, d), lam)
+            ref_in.append((gi, gv))
+        ws = whole if t % 3 != 1 else packed
+        efs.sparse_accumulate(p_dev, d, out, ws)
+        assert_bits_equal(out.cpu().numpy(), oracle.accumulate(ref_in, d), "call %d" % t)
+        assert efs.sparse_status(whole) == 0
 
 
 def test_accumulate_topk_payloads_and_tail():
@@ -564,8 +587,9 @@ def test_accumulate_topk_payloads_and_tail():
     assert_bits_equal(out.cpu().numpy(), oracle.accumulate(ps_ref, d))
 
 
+@pytest.mark.parametrize("layout", efs.LAYOUTS)
 @pytest.mark.parametrize("n", [3, 8])
-def test_accumulate_special_values(n):
+def test_accumulate_special_values(n, layout):
     # signed zeros, sums that cancel to zero, infinities, NaN and subnormals,
     # also at the ragged tail: the division by n leaves every zero as it is
     # and must divide everything else with one IEEE rounding
@@ -587,7 +611,7 @@ def test_accumulate_special_values(n):
         ps_dev.append((to_dev(idx), to_dev(val)))
         ps_ref.append((idx, val))
     out = torch.full((d,), 9.0, dtype=torch.float32, device=DEV)
-    efs.sparse_accumulate(ps_dev, d, out, efs.new_apply_workspace(ps_dev, d, DEV))
+    efs.sparse_accumulate(ps_dev, d, out, efs.new_apply_workspace(ps_dev, d, DEV, layout=layout))
     got = out.cpu().numpy()
     ref = oracle.accumulate(ps_ref, d)
     nan = np.isnan(ref)
@@ -596,7 +620,8 @@ def test_accumulate_special_values(n):
     assert bits(got[7]) == 0 and bits(got[d - 3]) == 0  # cancelled sums are +0
 
 
-def test_accumulate_reports_out_of_range_indices():
+@pytest.mark.parametrize("layout", efs.LAYOUTS)
+def test_accumulate_reports_out_of_range_indices(layout):
     # indices outside [0, d) are skipped and the status word says so; the
     # next call on the same workspace with a clean payload reports 0 again
     d = 1000
@@ -604,7 +629,7 @@ def test_accumulate_reports_out_of_range_indices():
     val = np.array([1.0, 5.0, 2.0, 6.0, 3.0], dtype=np.float32)
     out = torch.empty(d, dtype=torch.float32, device=DEV)
     ps = [(to_dev(idx), to_dev(val)), (to_dev(idx[:1]), to_dev(val[:1]))]
-    ws = efs.new_apply_workspace(ps, d, DEV)
+    ws = efs.new_apply_workspace(ps, d, DEV, layout=layout)
     efs.sparse_accumulate(ps, d, out, ws)
     keep = (idx >= 0) & (idx < d)
     ref = oracle.accumulate([(idx[keep], val[keep]), (idx[:1], val[:1])], d)
@@ -616,7 +641,8 @@ def test_accumulate_reports_out_of_range_indices():
     assert efs.sparse_status(ws) == 0
 
 
-def test_accumulate_reports_a_truncated_hard_threshold_payload():
+@pytest.mark.parametrize("layout", efs.LAYOUTS)
+def test_accumulate_reports_a_truncated_hard_threshold_payload(layout):
     # a hard-threshold call whose k_t exceeds the payload capacity: the
     # average uses the cap pairs written and the status word reports the
     # truncation (the error of the dropped coordinates is already +0)
@@ -629,7 +655,7 @@ def test_accumulate_reports_a_truncated_hard_threshold_payload():
     assert sk == gk > 1000 and si.size == 1000
     out = torch.empty(d, dtype=torch.float32, device=DEV)
     ps = [(full.idx, full.val, full.ctr), (short.idx, short.val, short.ctr)]
-    ws = efs.new_apply_workspace(ps, d, DEV)
+    ws = efs.new_apply_workspace(ps, d, DEV, layout=layout)
     efs.sparse_accumulate(ps, d, out, ws)
     assert efs.sparse_status(ws) == efs.SPARSE_TRUNCATED
     assert_bits_equal(out.cpu().numpy(), oracle.accumulate([(gi, gv), (si, sv)], d))
