@@ -236,6 +236,32 @@ efs_status sparse_accumulate(const int32_t *const *idx, const float *const *val,
                              int32_t n_workers, int64_t d, float *out, void *workspace,
                              size_t workspace_bytes, void *stream);
 
+/* sparse_accumulate for callers that cannot allocate device memory (code
+ * under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc): the same operation with the same bits, the pairs grouped in a
+ * scratch array of EFS_STATIC_SCRATCH_BYTES that the library holds on each
+ * device it runs on (from the library's first use of that device until the
+ * process ends) instead of in a caller's workspace.  The call allocates
+ * nothing.
+ *
+ *   idx, val, counts, caps, n_workers, d, out, stream
+ *              as for sparse_accumulate.
+ * Returns EFS_ESPACE, with nothing launched, when the payloads need more
+ * than EFS_STATIC_SCRATCH_BYTES: the bucketed layout is used when
+ * sparse_bucket_workspace_bytes(n_workers, d) fits in the scratch, else the
+ * packed one, which needs sparse_accumulate_workspace_bytes(n_workers, d,
+ * sum of caps).  EFS_EINVAL on any other invalid argument, EFS_EHIP if the
+ * scratch cannot be found on the current device.  Every call on one device
+ * shares that device's scratch; nothing in it needs clearing between calls
+ * (its counters carry epoch tags), but calls that overlap on one device
+ * (from concurrent streams or host threads) race and must be ordered by the
+ * caller.  The status word of these calls stays in the scratch and is not
+ * reported. */
+#define EFS_STATIC_SCRATCH_BYTES ((size_t)64 << 20)
+efs_status sparse_accumulate_static(const int32_t *const *idx, const float *const *val,
+                                    const uint32_t *const *counts, const int64_t *caps,
+                                    int32_t n_workers, int64_t d, float *out, void *stream);
+
 /* Exchange-and-average fused with the model update that follows it.
  *
  *   avg = (sum over w = 0..n-1, in that order, of decompress(payload_w)) / n

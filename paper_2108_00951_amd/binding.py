@@ -80,6 +80,10 @@ def declare(lib):
     lib.topk_segmented_compress.argtypes = [vp, vp, i64, f32, i32, vp, vp, i64, vp, vp, vp,
                                             ctypes.c_size_t, vp]
     lib.topk_segmented_compress.restype = ctypes.c_int
+    lib.sparse_accumulate_static.argtypes = [ctypes.POINTER(vp), ctypes.POINTER(vp),
+                                             ctypes.POINTER(vp), ctypes.POINTER(i64), i32, i64,
+                                             vp, vp]
+    lib.sparse_accumulate_static.restype = ctypes.c_int
     lib.sparse_apply_workspace_bytes.argtypes = [i32, i64, i64]
     lib.sparse_apply_workspace_bytes.restype = ctypes.c_size_t
     lib.sparse_apply.argtypes = [ctypes.POINTER(vp), ctypes.POINTER(vp), ctypes.POINTER(vp),
@@ -403,6 +407,23 @@ def prepare_sparse_accumulate(payloads: Sequence[Tuple], d: int, out, workspace,
     def call():
         _check(lib, fn(*args))
     return call
+
+
+STATIC_SCRATCH_BYTES = 64 << 20
+
+
+def sparse_accumulate_static(payloads: Sequence[Tuple], d: int, out, stream=None) -> None:
+    """sparse_accumulate with the library's per-device scratch in place of a
+    workspace (no allocation by the call); see sparse_accumulate_static in
+    include/efsparse.h."""
+    import torch
+    lib = load_library()
+    _require(out, torch.float32, "out")
+    if out.numel() != d:
+        raise ValueError("out must have d elements")
+    idx_arr, val_arr, cnt_arr, caps = _payload_arrays(payloads)
+    _check(lib, lib.sparse_accumulate_static(idx_arr, val_arr, cnt_arr, caps, len(payloads), int(d),
+                                             _ptr(out), _stream_handle(stream)))
 
 
 def copy_probe(src, dst, stream=None) -> None:

@@ -16,6 +16,7 @@ static_assert(efs::kMaxApplyWorkers == EFS_MAX_WORKERS, "worker limit differs fr
 static_assert(efs::kSparseTruncated == EFS_SPARSE_TRUNCATED, "status bit differs from the header");
 static_assert(efs::kSparseBadIndex == EFS_SPARSE_BAD_INDEX, "status bit differs from the header");
 static_assert(efs::kMaxSegments == EFS_SEG_MAX, "segment limit differs from the header");
+static_assert(efs::kStaticScratchBytes == EFS_STATIC_SCRATCH_BYTES, "scratch size differs from the header");
 static_assert(sizeof(efs::Telemetry) == EFS_TELEMETRY_BYTES, "telemetry layout differs from the header");
 
 namespace {
@@ -214,12 +215,13 @@ size_t sparse_bucket_workspace_bytes(int32_t n_workers, int64_t d) {
 
 size_t sparse_status_offset(void) { return efs::apply_status_offset(); }
 
-// Checks shared by sparse_accumulate and sparse_apply: the payload arrays,
-// the output (x), the workspace.  Returns EFS_OK when the call may proceed.
-static efs_status check_payloads(const char *name, const int32_t *const *idx,
-                                 const float *const *val, const uint32_t *const *counts,
-                                 const int64_t *caps, int32_t n_workers, int64_t d, const float *x,
-                                 const void *workspace, size_t workspace_bytes) {
+// Checks shared by sparse_accumulate, sparse_accumulate_static and
+// sparse_apply: the payload arrays and the output (x).  Returns EFS_OK when
+// they are valid, with the sum of the capacities in *total.
+static efs_status check_payload_args(const char *name, const int32_t *const *idx,
+                                     const float *const *val, const uint32_t *const *counts,
+                                     const int64_t *caps, int32_t n_workers, int64_t d,
+                                     const float *x, int64_t *total_out) {
     if (n_workers < 1 || n_workers > efs::kMaxApplyWorkers)
         return fail(EFS_EINVAL, "%s: n_workers=%d outside [1, %d]", name, n_workers,
                     efs::kMaxApplyWorkers);
@@ -242,13 +244,31 @@ static efs_status check_payloads(const char *name, const int32_t *const *idx,
     }
     if (total > int64_t(UINT32_MAX))
         return fail(EFS_EINVAL, "%s: total capacity %lld exceeds 2^32-1 pairs", name, (long long)total);
-    if (d == 0) return EFS_OK;
+    *total_out = total;
+    return EFS_OK;
+}
+
+// Bytes the call needs of a workspace of `have` bytes: 0 when it holds the
+// bucketed layout or the packed one, else the packed layout's size.
+static size_t workspace_shortfall(int32_t n_workers, int64_t d, int64_t total, size_t have) {
+    if (have >= efs::apply_bucket_workspace_size(n_workers, d)) return 0;
+    const size_t need = efs::apply_workspace_size(n_workers, d, total);
+    return have >= need ? 0 : need;
+}
+
+// The payload checks plus the workspace (pointer, alignment, size).
+static efs_status check_payloads(const char *name, const int32_t *const *idx,
+                                 const float *const *val, const uint32_t *const *counts,
+                                 const int64_t *caps, int32_t n_workers, int64_t d, const float *x,
+                                 const void *workspace, size_t workspace_bytes) {
+    int64_t total = 0;
+    const efs_status s = check_payload_args(name, idx, val, counts, caps, n_workers, d, x, &total);
+    if (s != EFS_OK || d == 0) return s;
     if (workspace == nullptr || !aligned(workspace, 16))
         return fail(EFS_EINVAL, "%s: workspace must be non-NULL and 16-byte aligned", name);
     // the bucketed layout whenever the workspace holds it, else the packed one
-    if (workspace_bytes >= efs::apply_bucket_workspace_size(n_workers, d)) return EFS_OK;
-    const size_t need = efs::apply_workspace_size(n_workers, d, total);
-    if (workspace_bytes < need)
+    const size_t need = workspace_shortfall(n_workers, d, total, workspace_bytes);
+    if (need != 0)
         return fail(EFS_ESPACE, "%s: workspace has %zu bytes, needs %zu", name, workspace_bytes, need);
     return EFS_OK;
 }
@@ -264,6 +284,29 @@ efs_status sparse_accumulate(const int32_t *const *idx, const float *const *val,
                                           out, nullptr, 0.0f, 0.0f, workspace, workspace_bytes,
                                           static_cast<hipStream_t>(stream)),
                         "sparse_accumulate");
+}
+
+efs_status sparse_accumulate_static(const int32_t *const *idx, const float *const *val,
+                                    const uint32_t *const *counts, const int64_t *caps,
+                                    int32_t n_workers, int64_t d, float *out, void *stream) {
+    const char *name = "sparse_accumulate_static";
+    int64_t total = 0;
+    const efs_status s = check_payload_args(name, idx, val, counts, caps, n_workers, d, out, &total);
+    if (s != EFS_OK || d == 0) return s;
+    const size_t need = workspace_shortfall(n_workers, d, total, efs::kStaticScratchBytes);
+    if (need != 0)
+        return fail(EFS_ESPACE, "%s: the payloads need %zu bytes of scratch; the library holds %zu "
+                    "per device (use sparse_accumulate with a workspace)", name, need,
+                    efs::kStaticScratchBytes);
+    void *scratch = nullptr;
+    const hipError_t err = efs::static_scratch(&scratch);
+    if (err != hipSuccess)
+        return fail(EFS_EHIP, "%s: no scratch on the current device: %s", name, hipGetErrorString(err));
+    return check_launch(efs::launch_apply(idx, val, counts, caps, n_workers, d, EFS_APPLY_AVERAGE,
+                                          out, nullptr, 0.0f, 0.0f, scratch,
+                                          efs::kStaticScratchBytes,
+                                          static_cast<hipStream_t>(stream)),
+                        name);
 }
 
 efs_status sparse_apply(const int32_t *const *idx, const float *const *val,

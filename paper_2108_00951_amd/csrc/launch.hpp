@@ -42,6 +42,11 @@ hipError_t launch_apply(const int32_t *const *idx, const float *const *val,
                         int64_t d, int mode, float *x, float *m, float beta, float gamma,
                         void *workspace, size_t workspace_bytes, hipStream_t stream);
 
+// Scratch held by the library per device for sparse_accumulate_static
+// (scratch.hip): its device address on the current device.
+constexpr size_t kStaticScratchBytes = size_t(64) << 20;
+hipError_t static_scratch(void **ptr);
+
 hipError_t launch_copy(const float *src, float *dst, int64_t n, hipStream_t stream);
 hipError_t launch_stream_probe(const float *x, float *y, int64_t n, int mode, hipStream_t stream);
 

@@ -187,6 +187,38 @@ def test_apply_rejects_bad_arguments(lib):
     assert call(d=0, ws=NULL) == binding.EFS_OK
 
 
+def test_accumulate_static_checks_arguments_before_the_device(lib):
+    # argument errors and payloads too large for the library's scratch are
+    # reported before anything touches a device (no GPU here)
+    vp = ctypes.c_void_p
+    fake = 0x10000
+    idx = (vp * 2)(fake, fake)
+    val = (vp * 2)(fake, fake)
+    caps = (ctypes.c_int64 * 2)(5, 5)
+
+    def call(idx=idx, val=val, caps=caps, n=2, d=10, out=fake):
+        return lib.sparse_accumulate_static(idx, val, None, caps, n, d, out, None)
+
+    assert call(n=0) == binding.EFS_EINVAL
+    assert call(n=binding.MAX_WORKERS + 1) == binding.EFS_EINVAL
+    assert call(d=-1) == binding.EFS_EINVAL
+    assert call(out=fake + 4) == binding.EFS_EINVAL
+    assert call(caps=(ctypes.c_int64 * 2)(5, -1)) == binding.EFS_EINVAL
+    assert call(idx=(vp * 2)(fake, None)) == binding.EFS_EINVAL
+    assert call(d=0, out=None) == binding.EFS_OK   # d == 0: nothing to do
+    # neither layout fits in 64 MiB: 2^30 pair slots, or 8 n d bytes of buckets
+    big = (ctypes.c_int64 * 2)(2 ** 30, 2 ** 30)
+    assert call(caps=big, d=2 ** 31 - 1) == binding.EFS_ESPACE
+    msg = lib.efs_last_error_message().decode()
+    assert "sparse_accumulate_static" in msg and str(binding.STATIC_SCRATCH_BYTES) in msg
+    # the largest packed layout that fits: a capacity one pair above it does not
+    d = 50_000_000
+    per = (binding.STATIC_SCRATCH_BYTES - lib.sparse_accumulate_workspace_bytes(2, d, 0)) // 16
+    assert lib.sparse_accumulate_workspace_bytes(2, d, 2 * per) <= binding.STATIC_SCRATCH_BYTES
+    assert lib.sparse_accumulate_workspace_bytes(2, d, 2 * per + 2) > binding.STATIC_SCRATCH_BYTES
+    assert call(caps=(ctypes.c_int64 * 2)(per + 1, per + 1), d=d) == binding.EFS_ESPACE
+
+
 def test_apply_workspace_size(lib):
     assert lib.sparse_apply_workspace_bytes(0, 100, 10) == 0
     assert lib.sparse_apply_workspace_bytes(binding.MAX_WORKERS + 1, 100, 10) == 0
