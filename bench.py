@@ -112,26 +112,33 @@ def parse():
 
 
 def _pmc_rows(folder, counter):
-    """(kernel name, value) of every dispatch in a rocprofv3 counter CSV."""
+    """(kernel name, value) of every dispatch in a rocprofv3 counter CSV, in
+    dispatch order."""
     rows = []
     for path in glob.glob(os.path.join(folder, "**", "*counter_collection.csv"), recursive=True):
         with open(path) as f:
             for r in csv.DictReader(f):
                 if r.get("Counter_Name") == counter:
-                    rows.append((r["Kernel_Name"], float(r["Counter_Value"])))
-    return rows
+                    rows.append((int(r.get("Dispatch_Id") or 0), r["Kernel_Name"],
+                                 float(r["Counter_Value"])))
+    rows.sort()
+    return [(k, v) for _, k, v in rows]
 
 
-def parse_pmc(fetch_dir, write_dir, d):
+def parse_pmc(fetch_dir, write_dir, d, ht_launches):
     """HBM bytes per launch of the hard-threshold kernel, scaled by the copy probe.
 
     FETCH_SIZE and WRITE_SIZE are in KiB per dispatch.  The copy probe moves
     exactly 4n bytes in and 4n bytes out (n = d); the ratio of those bytes to
-    what the counters report for it is the scale applied to the kernel."""
+    what the counters report for it is the scale applied to the kernel.  The
+    kernel's figure averages its first `ht_launches` dispatches: the
+    hard-threshold phase on the workload (warm-up, timed steps, and the same
+    steps again for k_t); the average's payloads come from later, smaller
+    launches of the same kernel."""
     out = {}
     for name, folder in (("FETCH_SIZE", fetch_dir), ("WRITE_SIZE", write_dir)):
         rows = _pmc_rows(folder, name)
-        ht = [v for k, v in rows if HT_PLAIN in k]
+        ht = [v for k, v in rows if HT_PLAIN in k][:ht_launches]
         cp = [v for k, v in rows if COPY_KERNEL in k]
         if not ht or not cp:
             raise SystemExit("no %s rows for %s / %s in %s" % (name, HT_PLAIN, COPY_KERNEL, folder))
@@ -195,10 +202,13 @@ def parse_trace(folder, steps):
     return "\n".join(lines) + "\n"
 
 
-def format_traffic(res, workload):
+def format_traffic(res, workload, args):
     lines = ["# HBM traffic of %s per launch from rocprofv3 counters, %s" % (HT_PLAIN, workload),
-             "# (KiB per dispatch, averaged over the kernel's dispatches; each counter",
-             "# scaled by expected/measured for %s moving 4*d bytes each way)" % COPY_KERNEL]
+             "# (KiB per dispatch, averaged over the kernel's first %d dispatches, the"
+             % (args.warmup + 2 * args.steps),
+             "# hard-threshold phase with --warmup %d --steps %d; each counter scaled by"
+             % (args.warmup, args.steps),
+             "# expected/measured for %s moving 4*d bytes each way)" % COPY_KERNEL]
     for name in ("FETCH_SIZE", "WRITE_SIZE"):
         r = res[name]
         lines.append("# %s: kernel %.1f KiB, copy probe %.1f KiB (expected %.1f), scale %.5f, "
@@ -206,8 +216,8 @@ def format_traffic(res, workload):
                                       r["copy_expected_kib"], r["scale"], r["launches"]))
     fk, wk = res["FETCH_SIZE"].get("kernels", {}), res["WRITE_SIZE"].get("kernels", {})
     if fk or wk:
-        lines.append("# every kernel of the run, scaled the same way: MB fetched + MB written per "
-                     "launch (launches)")
+        lines.append("# every kernel of the run (all its dispatches, of any size), scaled the same "
+                     "way: MB fetched + MB written per launch (launches)")
         names = sorted(set(fk) | set(wk),
                        key=lambda n: -(fk.get(n, (0.0, 0))[0] + wk.get(n, (0.0, 0))[0]))
         for n in names:
@@ -274,7 +284,8 @@ def main():
     wl = synth.WORKLOADS[args.workload]
     d, k, density = wl.d, wl.topk_k[0], wl.densities[0]
     if args.parse_pmc:
-        sys.stdout.write(format_traffic(parse_pmc(args.parse_pmc[0], args.parse_pmc[1], d), wl.name))
+        res = parse_pmc(args.parse_pmc[0], args.parse_pmc[1], d, args.warmup + 2 * args.steps)
+        sys.stdout.write(format_traffic(res, wl.name, args))
         return
     if args.parse_trace:
         sys.stdout.write(parse_trace(args.parse_trace, args.steps))

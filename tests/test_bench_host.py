@@ -1,6 +1,7 @@
 """Host-side logic of bench.py: the rocprofv3 summary parsers and the
 one-GPU guard (no GPU needed)."""
 import csv
+import argparse
 import os
 import subprocess
 import sys
@@ -66,10 +67,12 @@ def test_parse_trace_says_when_no_run_matches(tmp_path):
 
 
 def _pmc(folder, counter, values):
+    # rows written out of dispatch order: the parser sorts them
     os.makedirs(folder)
-    rows = [{"Kernel_Name": n, "Counter_Name": counter, "Counter_Value": v} for n, v in values]
+    rows = [{"Dispatch_Id": i + 1, "Kernel_Name": n, "Counter_Name": counter, "Counter_Value": v}
+            for i, (n, v) in enumerate(values)]
     _write_csv(os.path.join(folder, "run_counter_collection.csv"),
-               ["Kernel_Name", "Counter_Name", "Counter_Value"], rows)
+               ["Dispatch_Id", "Kernel_Name", "Counter_Name", "Counter_Value"], rows[::-1])
 
 
 def test_parse_pmc_scales_by_the_copy_probe(tmp_path):
@@ -77,20 +80,24 @@ def test_parse_pmc_scales_by_the_copy_probe(tmp_path):
     # the copy probe moves 4d bytes each way; its counters read 2x (fetch)
     # and 1x (write) of that, so the kernel's readings are scaled by 1/2, 1
     fetch, write = str(tmp_path / "f"), str(tmp_path / "w")
-    _pmc(fetch, "FETCH_SIZE", [(HT, 16384.0), (HT, 16384.0), (COPY, 8192.0)])
-    _pmc(write, "WRITE_SIZE", [(HT, 4096.0), (COPY, 4096.0), (OTHER, 1.0)])
-    res = bench.parse_pmc(fetch, write, d)
+    # two hard-threshold launches on the workload, then a later small one
+    # (the average's payloads) that the per-launch figure leaves out
+    _pmc(fetch, "FETCH_SIZE", [(HT, 16384.0), (HT, 16384.0), (COPY, 8192.0), (HT, 8.0)])
+    _pmc(write, "WRITE_SIZE", [(HT, 4096.0), (HT, 4096.0), (COPY, 4096.0), (OTHER, 1.0),
+                               (HT, 4.0)])
+    res = bench.parse_pmc(fetch, write, d, 2)
     assert res["FETCH_SIZE"]["scale"] == pytest.approx(0.5)
     assert res["WRITE_SIZE"]["scale"] == pytest.approx(1.0)
     assert res["ht_bytes_per_launch"] == pytest.approx(16384 * 1024 * 0.5 + 4096 * 1024)
-    text = bench.format_traffic(res, "a workload")
+    text = bench.format_traffic(res, "a workload", argparse.Namespace(warmup=0, steps=1))
     assert "ht_bytes_per_launch %d" % round(res["ht_bytes_per_launch"]) in text
     # the other kernels get the same scales: topk_step3 fetched nothing, wrote 1 KiB
     step3 = [x for x in text.splitlines() if "topk_step3_kernel" in x]
     assert len(step3) == 1 and "0.00 +      0.00 MB  (1)" in step3[0]
     ht_line = [x for x in text.splitlines()
                if x.startswith("#   ht_fused_kernel<true, false>")][0]
-    assert "%9.2f + %9.2f MB" % (16384 * 1024 * 0.5 / 1e6, 4096 * 1024 / 1e6) in ht_line
+    every = ((2 * 16384 + 8) / 3 * 1024 * 0.5 / 1e6, (2 * 4096 + 4) / 3 * 1024 / 1e6)
+    assert "%9.2f + %9.2f MB" % every in ht_line
     assert "kernel_source_sha256 " + bench.kernel_source_digest() in text
 
 
