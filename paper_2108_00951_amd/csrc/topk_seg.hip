@@ -169,12 +169,13 @@ struct SegWs {
     uint32_t *hist2;        // [nseg][kDigit2]; on the bracket path, the bracket histogram
     uint2 *cand;            // (bits of p, index)
     uint2 *work;            // pass2 work list: (segment | kind << 31, first slot)
+    struct ResetChunk *chunks;  // the reset's per-chunk sums (many layers)
     int64_t ccap_total;
     uint32_t work_cap;
 };
 
 struct SegLayout {
-    size_t info, tile_prefix, st, hint, hist1, hist2, cand, work, bytes;
+    size_t info, tile_prefix, st, hint, hist1, hist2, cand, work, chunks, bytes;
     int64_t ccap_total, work_cap;
 };
 
@@ -202,6 +203,9 @@ SegLayout seg_layout(int32_t nseg, int64_t k_total) {
     L.work_cap = (k_total + L.ccap_total) / kChunk + 2 * int64_t(nseg) + 1;
     L.work = o;
     o += round256(8 * size_t(L.work_cap));
+    // the reset's per-chunk sums (layouts of more than kResetSingleMax layers)
+    L.chunks = o;
+    o += round256(32 * ((size_t(nseg) + 511) / 512));
     L.bytes = o;
     return L;
 }
@@ -394,25 +398,124 @@ __device__ __forceinline__ SegIn load_seg(const int64_t *off, const int64_t *kin
     return in;
 }
 
+// The per-layer quantities the tables are built from: pairs kept, candidate
+// slots, tiles and work-list slots; `bad` is set for a layer outside the
+// rules (negative size or k, outside [0, d)).
+__device__ __forceinline__ Sums seg_sums(const SegIn &in, int32_t s, int32_t nseg, int64_t d,
+                                         bool &bad) {
+    Sums v = {0, 0, 0u, 0u};
+    if (s >= nseg) return v;
+    const int64_t size = in.hi - in.lo;
+    if (size < 0 || in.k < 0 || in.lo < 0 || in.hi > d) bad = true;
+    if (size >= 0 && in.k >= 0) {
+        const int64_t keff = in.k < size ? in.k : size;
+        const uint32_t nt = uint32_t(segment_tiles(in.lo, size));
+        const int64_t ccap = (nt > 1u && keff > 0 && keff < size) ? kCandPerK * keff + kCandExtra : 0;
+        // bracket path: the pairs above the bracket (at most k) and the
+        // candidates (at most ccap), kChunk per work item
+        const int64_t wmax = ccap > 0 ? (keff + kChunk - 1) / kChunk + (ccap + kChunk - 1) / kChunk : 0;
+        v = Sums{keff, ccap, nt, uint32_t(wmax)};
+    }
+    return v;
+}
+
+// One chunk of kResetBlock layers, s = c0 + thread: their tables after
+// `carry` (the sums of all layers before the chunk) and their bracket from
+// the hints.  Returns the chunk's sums.  Called by every thread of the
+// workgroup.
+__device__ __forceinline__ Sums reset_chunk(const SegWs &ws, const SegIn &in, int32_t s,
+                                            int32_t nseg, int64_t d, Sums carry, Sums *s_wave,
+                                            bool &bad) {
+    SegHint h = {};
+    if (s < nseg) h = ws.hint[s];  // used after the scan
+    const Sums v = seg_sums(in, s, nseg, d, bad);
+    Sums tot;
+    const Sums ex = reset_scan(v, s_wave, tot);
+    if (s < nseg) {
+        const int64_t size = in.hi - in.lo;
+        const int64_t keff = v.k, ccap = v.c;
+        const uint32_t nt = v.t;
+        SegInfo inf;
+        inf.off = in.lo;
+        inf.size = size;
+        inf.kout = carry.k + ex.k;
+        inf.k = keff;
+        inf.coff = carry.c + ex.c;
+        inf.ccap = ccap;
+        inf.tile0 = uint32_t(carry.t + ex.t);
+        inf.ntiles = nt;
+        inf.wbase = uint32_t(carry.w + ex.w);
+        inf.wmax = v.w;
+        ws.info[s] = inf;
+        ws.tile_prefix[s] = uint32_t(carry.t + ex.t);
+        SegState z = {};
+        if (nt > 1u && keff > 0 && keff < size && h.magic == kHintMagic && h.key <= 0x7fffffffu &&
+            h.prev <= 0x7fffffffu && h.prev2 <= 0x7fffffffu && widths_ok(h.width)) {
+            // last threshold plus the last step (capped): error feedback
+            // makes thresholds drift smoothly from call to call
+            const int64_t last = int64_t(h.key) - int64_t(h.prev);
+            const int64_t before = int64_t(h.prev) - int64_t(h.prev2);
+            const int64_t al = last < 0 ? -last : last, ab = before < 0 ? -before : before;
+            const bool steady = (last >= 0) == (before >= 0) && 2 * ab >= al && 2 * al >= ab;
+            const int64_t cap = steady ? kMaxStep : kMaxStepUnsure;
+            const int64_t step = max(-cap, min(cap, last));
+            const int64_t pred = max(int64_t(0), min(int64_t(0x7fffffff), int64_t(h.key) + step));
+            z.bracket = 1u;
+            z.lo = uint32_t(max(int64_t(0), pred - (int64_t(1) << width_lo(h.width))));
+            z.hi = uint32_t(min(pred + (int64_t(1) << width_hi(h.width)) - 1, int64_t(0x7fffffff)));
+            // hi - lo + 1 <= 2^20 keys in kFineBins bins
+            const uint32_t span_bits = 32u - uint32_t(__clz(int(z.hi - z.lo) | 1));
+            z.shift = span_bits > 10u ? span_bits - 10u : 0u;
+        }
+        ws.st[s] = z;
+    }
+    return tot;
+}
+
+// Zeroes the histograms of the layers that span more than one tile (a
+// one-tile layer is selected inside pass1), workgroup w of nw; an invalid
+// layout is rejected, so what is zeroed for it does not matter.
+__device__ __forceinline__ void reset_zero(const SegWs &ws, const int64_t *off, int32_t nseg,
+                                           int32_t w, int32_t nw) {
+    const f32x4 z = {0.0f, 0.0f, 0.0f, 0.0f};
+    for (int32_t sg = w; sg < nseg; sg += nw) {
+        const int64_t lo = off[sg], size = off[sg + 1] - lo;
+        if (size < 0 || segment_tiles(lo, size) <= 1) continue;
+        f32x4 *h1 = reinterpret_cast<f32x4 *>(ws.hist1 + int64_t(sg) * kDigit1);
+        f32x4 *h2 = reinterpret_cast<f32x4 *>(ws.hist2 + int64_t(sg) * kDigit2);
+        for (int q = threadIdx.x; q < kDigit1 / 4; q += kResetBlock) h1[q] = z;
+        for (int q = threadIdx.x; q < kDigit2 / 4; q += kResetBlock) h2[q] = z;
+    }
+}
+
+// The control block once every layer's tables are formed: the layout is
+// rejected when a layer broke the rules, the offsets do not run from 0 to d,
+// or the sums exceed what the workspace was sized for.  One thread.
+__device__ __forceinline__ void reset_publish(const SegWs &ws, const int64_t *off, int32_t nseg,
+                                              int64_t d, int64_t k_total, Sums total, bool bad) {
+    if (off[0] != 0 || off[nseg] != d) bad = true;
+    const bool reject = bad || total.k > k_total || total.c > ws.ccap_total ||
+                        total.w > ws.work_cap;
+    ws.ctl->bracket = 0u;
+    ws.ctl->pass2 = 0u;
+    ws.ctl->wtotal = reject ? 0u : total.w;
+    ws.ctl->status = reject ? 1u : 0u;
+    ws.ctl->tiles = reject ? 0u : total.t;
+    if (!reject) ws.tile_prefix[nseg] = total.t;
+}
+
+// Up to kResetSingleMax layers: workgroup 0 forms the tables in chunks of
+// kResetBlock layers, the next chunk's loads in flight meanwhile; the other
+// workgroups zero histograms.
+constexpr int32_t kResetSingleMax = 4 * kResetBlock;
+
 __global__ __launch_bounds__(kResetBlock) void seg_reset_kernel(SegWs ws,
                                                                 const int64_t *__restrict__ off,
                                                                 const int64_t *__restrict__ kin,
                                                                 int32_t nseg, int64_t d,
                                                                 int64_t k_total) {
     if (blockIdx.x > 0) {
-        // the other workgroups zero the histograms of the segments that span
-        // more than one tile (a one-tile segment is selected inside pass1);
-        // an invalid layout is rejected by workgroup 0, so what is zeroed for
-        // it does not matter
-        const f32x4 z = {0.0f, 0.0f, 0.0f, 0.0f};
-        for (int32_t sg = int32_t(blockIdx.x) - 1; sg < nseg; sg += int32_t(gridDim.x) - 1) {
-            const int64_t lo = off[sg], size = off[sg + 1] - lo;
-            if (size < 0 || segment_tiles(lo, size) <= 1) continue;
-            f32x4 *h1 = reinterpret_cast<f32x4 *>(ws.hist1 + int64_t(sg) * kDigit1);
-            f32x4 *h2 = reinterpret_cast<f32x4 *>(ws.hist2 + int64_t(sg) * kDigit2);
-            for (int q = threadIdx.x; q < kDigit1 / 4; q += kResetBlock) h1[q] = z;
-            for (int q = threadIdx.x; q < kDigit2 / 4; q += kResetBlock) h2[q] = z;
-        }
+        reset_zero(ws, off, nseg, int32_t(blockIdx.x) - 1, int32_t(gridDim.x) - 1);
         return;
     }
     __shared__ Sums s_wave[kResetWaves];
@@ -429,77 +532,91 @@ __global__ __launch_bounds__(kResetBlock) void seg_reset_kernel(SegWs ws,
         const int32_t s = c0 + t;
         const SegIn in = nxt;
         nxt = load_seg(off, kin, s + kResetBlock, nseg);  // next chunk, in flight
-        SegHint h = {};
-        if (s < nseg) h = ws.hint[s];  // used after the scan
-        const int64_t size = in.hi - in.lo;
-        int64_t keff = 0, ccap = 0, wmax = 0;
-        uint32_t nt = 0u;
-        if (s < nseg) {
-            if (size < 0 || in.k < 0 || in.lo < 0 || in.hi > d) bad = true;
-            if (size >= 0 && in.k >= 0) {
-                keff = in.k < size ? in.k : size;
-                nt = uint32_t(segment_tiles(in.lo, size));
-                ccap = (nt > 1u && keff > 0 && keff < size) ? kCandPerK * keff + kCandExtra : 0;
-                // bracket path: the pairs above the bracket (at most k) and
-                // the candidates (at most ccap), kChunk per work item
-                wmax = ccap > 0 ? (keff + kChunk - 1) / kChunk + (ccap + kChunk - 1) / kChunk : 0;
-            }
-        }
-        Sums tot;
-        const Sums ex = reset_scan(Sums{keff, ccap, nt, uint32_t(wmax)}, s_wave, tot);
-        if (s < nseg) {
-            SegInfo inf;
-            inf.off = in.lo;
-            inf.size = size;
-            inf.kout = carry.k + ex.k;
-            inf.k = keff;
-            inf.coff = carry.c + ex.c;
-            inf.ccap = ccap;
-            inf.tile0 = uint32_t(carry.t + ex.t);
-            inf.ntiles = nt;
-            inf.wbase = uint32_t(carry.w + ex.w);
-            inf.wmax = uint32_t(wmax);
-            ws.info[s] = inf;
-            ws.tile_prefix[s] = uint32_t(carry.t + ex.t);
-            SegState z = {};
-            if (nt > 1u && keff > 0 && keff < size && h.magic == kHintMagic && h.key <= 0x7fffffffu &&
-                h.prev <= 0x7fffffffu && h.prev2 <= 0x7fffffffu && widths_ok(h.width)) {
-                // last threshold plus the last step (capped): error feedback
-                // makes thresholds drift smoothly from call to call
-                const int64_t last = int64_t(h.key) - int64_t(h.prev);
-                const int64_t before = int64_t(h.prev) - int64_t(h.prev2);
-                const int64_t al = last < 0 ? -last : last, ab = before < 0 ? -before : before;
-                const bool steady = (last >= 0) == (before >= 0) && 2 * ab >= al && 2 * al >= ab;
-                const int64_t cap = steady ? kMaxStep : kMaxStepUnsure;
-                const int64_t step = max(-cap, min(cap, last));
-                const int64_t pred = max(int64_t(0), min(int64_t(0x7fffffff), int64_t(h.key) + step));
-                z.bracket = 1u;
-                z.lo = uint32_t(max(int64_t(0), pred - (int64_t(1) << width_lo(h.width))));
-                z.hi = uint32_t(min(pred + (int64_t(1) << width_hi(h.width)) - 1, int64_t(0x7fffffff)));
-                // hi - lo + 1 <= 2^20 keys in kFineBins bins
-                const uint32_t span_bits = 32u - uint32_t(__clz(int(z.hi - z.lo) | 1));
-                z.shift = span_bits > 10u ? span_bits - 10u : 0u;
-            }
-            ws.st[s] = z;
-        }
+        const Sums tot = reset_chunk(ws, in, s, nseg, d, carry, s_wave, bad);
         carry.k += tot.k;
         carry.c += tot.c;
         carry.t += tot.t;
         carry.w += tot.w;
     }
-    if (t == 0 && off[0] != 0) bad = true;
-    if (t == 0 && off[nseg] != d) bad = true;
     if (bad) atomicOr(&s_bad, 1u);
     __syncthreads();
-    const bool reject = s_bad != 0u || carry.k > k_total || carry.c > ws.ccap_total ||
-                        carry.w > ws.work_cap;
-    if (t == 0) {
-        ws.ctl->bracket = 0u;
-        ws.ctl->pass2 = 0u;
-        ws.ctl->wtotal = reject ? 0u : carry.w;
-        ws.ctl->status = reject ? 1u : 0u;
-        ws.ctl->tiles = reject ? 0u : carry.t;
-        if (!reject) ws.tile_prefix[nseg] = carry.t;
+    if (t == 0) reset_publish(ws, off, nseg, d, k_total, carry, s_bad != 0u);
+}
+
+// More layers: the tables in two launches of one workgroup per chunk of
+// kResetBlock layers.  The first sums each chunk (and the workgroups after
+// the chunks zero histograms); the second adds up the sums of the chunks
+// before its own and forms that chunk's tables, and its last workgroup
+// publishes the control block.
+struct ResetChunk {
+    Sums sums;
+    uint32_t bad, pad;
+};
+static_assert(sizeof(ResetChunk) == 32, "a chunk's sums take 32 bytes");
+
+__global__ __launch_bounds__(kResetBlock) void seg_reset_sums_kernel(SegWs ws,
+                                                                     const int64_t *__restrict__ off,
+                                                                     const int64_t *__restrict__ kin,
+                                                                     int32_t nseg, int64_t d,
+                                                                     int32_t nchunks) {
+    if (int32_t(blockIdx.x) >= nchunks) {
+        reset_zero(ws, off, nseg, int32_t(blockIdx.x) - nchunks, int32_t(gridDim.x) - nchunks);
+        return;
+    }
+    __shared__ Sums s_wave[kResetWaves];
+    __shared__ uint32_t s_bad;
+    if (threadIdx.x == 0) s_bad = 0u;
+    __syncthreads();
+    const int32_t s = int32_t(blockIdx.x) * kResetBlock + int32_t(threadIdx.x);
+    bool bad = false;
+    const Sums v = seg_sums(load_seg(off, kin, s, nseg), s, nseg, d, bad);
+    if (bad) atomicOr(&s_bad, 1u);
+    Sums tot;
+    reset_scan(v, s_wave, tot);   // its barriers also order s_bad
+    if (threadIdx.x == 0) {
+        ResetChunk r = {};
+        r.sums = tot;
+        r.bad = s_bad;
+        ws.chunks[blockIdx.x] = r;
+    }
+}
+
+__global__ __launch_bounds__(kResetBlock) void seg_reset_tables_kernel(SegWs ws,
+                                                                       const int64_t *__restrict__ off,
+                                                                       const int64_t *__restrict__ kin,
+                                                                       int32_t nseg, int64_t d,
+                                                                       int64_t k_total,
+                                                                       int32_t nchunks) {
+    __shared__ Sums s_wave[kResetWaves];
+    const int32_t c = int32_t(blockIdx.x);
+    const bool last = c == nchunks - 1;
+    const int32_t s = c * kResetBlock + int32_t(threadIdx.x);
+    const SegIn in = load_seg(off, kin, s, nseg);
+    // the sums of the chunks before this one (all of them, and their flags,
+    // for the last)
+    Sums before = {0, 0, 0u, 0u};
+    uint32_t flags = 0u;
+    for (int32_t q = int32_t(threadIdx.x); q < (last ? nchunks : c); q += kResetBlock) {
+        const ResetChunk r = ws.chunks[q];
+        if (q < c) {
+            before.k += r.sums.k;
+            before.c += r.sums.c;
+            before.t += r.sums.t;
+            before.w += r.sums.w;
+        }
+        flags |= r.bad;
+    }
+    Sums carry;
+    reset_scan(before, s_wave, carry);
+    __shared__ uint32_t s_flags;
+    if (threadIdx.x == 0) s_flags = 0u;
+    __syncthreads();
+    if (flags) atomicOr(&s_flags, 1u);
+    bool unused = false;   // this chunk's flag is in ws.chunks already
+    const Sums tot = reset_chunk(ws, in, s, nseg, d, carry, s_wave, unused);
+    if (last && threadIdx.x == 0) {
+        const Sums all = {carry.k + tot.k, carry.c + tot.c, carry.t + tot.t, carry.w + tot.w};
+        reset_publish(ws, off, nseg, d, k_total, all, s_flags != 0u);
     }
 }
 
@@ -1434,11 +1551,20 @@ hipError_t launch_topk_segmented(const float *g, float *e, int64_t d, float lr, 
     ws.hist2 = reinterpret_cast<uint32_t *>(base + L.hist2);
     ws.cand = reinterpret_cast<uint2 *>(base + L.cand);
     ws.work = reinterpret_cast<uint2 *>(base + L.work);
+    ws.chunks = reinterpret_cast<ResetChunk *>(base + L.chunks);
     ws.ccap_total = L.ccap_total;
     ws.work_cap = uint32_t(L.work_cap);
 
     const uint32_t zero_grid = persistent_grid(nseg);  // one segment's histograms per pass
-    seg_reset_kernel<<<1 + zero_grid, kResetBlock, 0, stream>>>(ws, offsets, k, nseg, d, k_total);
+    if (nseg <= kResetSingleMax) {
+        seg_reset_kernel<<<1 + zero_grid, kResetBlock, 0, stream>>>(ws, offsets, k, nseg, d, k_total);
+    } else {
+        const int32_t nchunks = (nseg + kResetBlock - 1) / kResetBlock;
+        seg_reset_sums_kernel<<<uint32_t(nchunks) + zero_grid, kResetBlock, 0, stream>>>(
+            ws, offsets, k, nseg, d, nchunks);
+        seg_reset_tables_kernel<<<uint32_t(nchunks), kResetBlock, 0, stream>>>(ws, offsets, k, nseg,
+                                                                               d, k_total, nchunks);
+    }
 
     const int64_t max_tiles = (d + kTile - 1) / kTile + nseg;
     // slices: the tiles spread over kSliceWorkgroupsPerCU workgroups per CU

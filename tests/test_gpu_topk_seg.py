@@ -247,6 +247,51 @@ def test_segmented_bad_layout_changes_nothing(case):
     assert_bits_equal(ge, re)
 
 
+@pytest.mark.parametrize("case", ["first_offset", "decreasing_late", "last_offset",
+                                  "negative_k_late", "budget"])
+def test_segmented_bad_layout_of_many_layers_changes_nothing(case):
+    # 3,000 layers: the layer tables are formed by one workgroup per 512
+    # layers in two launches; a defect in a late chunk, at either end of the
+    # offsets or in the totals still rejects the whole call
+    nseg = 3000
+    sizes = (4 + np.arange(nseg) % 7).astype(np.int64)
+    off = np.concatenate([[0], np.cumsum(sizes)]).astype(np.int64)
+    d = int(off[-1])
+    ks = np.ones(nseg, dtype=np.int64)
+    k_total = nseg
+    if case == "first_offset":
+        off[0] = 1
+    elif case == "decreasing_late":
+        off[2900] = off[2899] - 1
+    elif case == "last_offset":
+        off[-1] = d - 1
+    elif case == "negative_k_late":
+        ks[2600] = -1
+    else:
+        k_total = nseg - 1
+    g = synth.small_gradient(496, d)
+    e = synth.small_gradient(497, d)
+    gi, gv, ge, ws = run_gpu(g, e, off, ks, k_total=k_total)
+    assert efs.topk_segmented_status(ws) == 1
+    assert_bits_equal(ge, e)
+    assert np.all(gi == -7)
+
+
+@pytest.mark.parametrize("nseg", [2048, 2049, 2560])
+def test_segmented_layer_count_at_the_table_launch_switch(nseg):
+    # up to 2048 layers one workgroup forms the tables, above that one
+    # workgroup per 512 layers; both must give the same call
+    rng = np.random.default_rng(nseg)
+    sizes = rng.integers(1, 3000, size=nseg).astype(np.int64)
+    sizes[rng.choice(nseg, 8, replace=False)] = 20_000
+    off = np.concatenate([[0], np.cumsum(sizes)]).astype(np.int64)
+    d = int(off[-1])
+    ks = synth.layerwise_k(off, 0.01)
+    say("segmented layer count %d d=%d" % (nseg, d))
+    check(synth.small_gradient(498, d), synth.small_gradient(499, d), off, ks,
+          what="%d layers" % nseg)
+
+
 def test_segmented_workspace_contents_do_not_matter():
     rng = np.random.default_rng(495)
     d = 200_000
