@@ -12,7 +12,10 @@ Timed regions (HIP events at their two ends only, on the stream the
 kernels run on; a barrier and a device synchronisation on both sides):
   * `value`: K error-feedback steps of the hard threshold (ht_compress,
     one launch of ht_fused_kernel per step); value = d / (time per step),
-    G grad-elements/s; ms_per_step is that time.
+    G grad-elements/s; ms_per_step is that time.  `ht_steps` holds the
+    p10 / p50 / p90 of the same steps replayed one call at a time, and
+    `ht_cold` five further calls each after a 1 GiB write that evicts the
+    caches.
   * `topk`: K steps of the Top-k baseline (topk_compress, its own error
     vector and workspace) on the same gradients.
   * `average`: K exchange-and-average calls (sparse_accumulate) of the
@@ -331,14 +334,27 @@ def main():
             efs.ht_compress(pool[(args.warmup + s) % len(pool)], e_ht, lr, lam, idx, val, ctr)
     mark()
     ht_us = tm.us / args.steps
-    # k_t of every timed step: the same calls again from the same state
+    # k_t and the time of every timed step: the same calls again from the
+    # same state, one at a time
     e_ht.copy_(e_snap)
-    kts = []
+    kts, ht_each = [], []
     for s in range(args.steps):
-        efs.ht_compress(pool[(args.warmup + s) % len(pool)], e_ht, lr, lam, idx, val, ctr)
+        with Timer(torch, cur) as t1:
+            efs.ht_compress(pool[(args.warmup + s) % len(pool)], e_ht, lr, lam, idx, val, ctr)
+        ht_each.append(t1.us)
         kts.append(efs.counter_value(ctr))
     if max(kts) > cap:
         raise RuntimeError("hard-threshold payload capacity exceeded")
+    # cold calls: a 1 GiB write before each evicts the caches (the
+    # trajectory continues from the replayed steps)
+    flush = torch.empty(1 << 28, dtype=torch.float32, device=dev)
+    ht_cold = []
+    for s in range(5):
+        flush.fill_(float(s))
+        with Timer(torch, cur) as t1:
+            efs.ht_compress(pool[(args.warmup + s) % len(pool)], e_ht, lr, lam, idx, val, ctr)
+        ht_cold.append(t1.us)
+    del flush
     kt = float(np.mean(kts))
     ht_bytes = 12.0 * d + 8.0 * kt
     say("hard threshold: %.1f us per step, k_t %d..%d" % (ht_us, kts[0], kts[-1]))
@@ -405,6 +421,10 @@ def main():
             "step": "one hard-threshold error-feedback iteration (ht_compress)",
         },
         "hbm_gbps": round(ht_bytes / (ht_us * 1e-6) / 1e9, 1),
+        "ht_steps": dict(stats_us(ht_each), note="each timed step replayed alone, synchronised "
+                         "on both sides"),
+        "ht_cold": dict(stats_us(ht_cold), calls=len(ht_cold),
+                        note="one call after a 1 GiB write that evicts the caches"),
         "roofline": dict(
             kernel=HT_PLAIN, bound="hbm",
             achieved=round(ht_bytes / (ht_us * 1e-6) / 1e9, 1), peak=HBM_PEAK_GBPS, unit="GB/s",
