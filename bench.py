@@ -488,9 +488,20 @@ def bench_average(efs, torch, synth, cur, steps, warmup, threads):
         for s in range(steps):
             calls[s % 4]()
     us = t.us / steps
+    # each call's own time: events between the same back-to-back calls
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
+    torch.cuda.synchronize()
+    evs[0].record(cur)
+    for s in range(steps):
+        calls[s % 4]()
+        evs[s + 1].record(cur)
+    torch.cuda.synchronize()
+    per_call = [evs[i].elapsed_time(evs[i + 1]) * 1e3 for i in range(steps)]
     status = efs.sparse_status(ws)
     nbytes = 4.0 * d + 8.0 * pairs
-    res = {"workers": w.n_workers, "d": d, "pairs": pairs, "us": round(us, 2), "status": status,
+    res = {"workers": w.n_workers, "d": d, "pairs": pairs, "us": round(us, 2),
+           "per_call": dict(stats_us(per_call), note="events between back-to-back calls"),
+           "status": status,
            "bytes_min": nbytes, **rate(nbytes, us),
            "bytes_model": "4 d + 8 per pair (dense output write, payload read)"}
     say("average of %d payloads (%d pairs): %.1f us" % (w.n_workers, pairs, us))
