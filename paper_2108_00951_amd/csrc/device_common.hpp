@@ -22,6 +22,34 @@ constexpr int kHtWorkgroupsPerCU = 2;
 constexpr int kStageWorkgroupsPerCU = 4;
 constexpr int kScanWorkgroupsPerCU = 8;
 
+// The tiles a workgroup of a persistent grid takes: first, first + stride,
+// ... below end.  Plain: tile b, b + G, b + 2G, ... (the resident workgroups
+// sweep one window of the vector together).  By XCD: workgroups b with the
+// same b % 8 run on one XCD (workgroups are dispatched to the 8 XCDs in
+// turn), so each XCD takes a contiguous share of the tiles in proportion to
+// its workgroups, and its workgroups stride through that share.
+constexpr int kXcds = 8;
+// Tiles per workgroup from which a sweep walks the vector by XCD.  Measured
+// on the hard threshold (2 workgroups per CU): by XCD is 1-2 % faster from
+// 6e8 elements (290 tiles per workgroup) up to 1.5e9, and 1-9 % slower at
+// 4e8 and below (110e6: 224.5 against 239.3 us).
+constexpr int kXcdWalkMinTiles = 256;
+
+struct TileWalk {
+    uint32_t first, end, stride;
+};
+
+__device__ __forceinline__ TileWalk tile_walk(uint32_t ntiles, bool by_xcd) {
+    const uint32_t G = gridDim.x, b = blockIdx.x;
+    if (!by_xcd) return TileWalk{b, ntiles, G};
+    const uint32_t x = b % kXcds;
+    const uint32_t n_x = (G - x + kXcds - 1) / kXcds;                 // workgroups on this XCD
+    const uint32_t before = x * (G / kXcds) + min(x, G % kXcds);     // on the XCDs before it
+    const uint32_t lo = uint32_t(uint64_t(ntiles) * before / G);
+    const uint32_t hi = uint32_t(uint64_t(ntiles) * (before + n_x) / G);
+    return TileWalk{lo + b / kXcds, hi, n_x};
+}
+
 // Counter word layout used for single-launch stream compaction: the low 40
 // bits accumulate the number of emitted pairs, the high 24 bits count
 // workgroups that have finished (a ticket, so the last one is known).

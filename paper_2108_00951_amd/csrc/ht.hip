@@ -4,7 +4,8 @@
 // section 4.2, S_lambda(p) = { i : |p_i| >= lambda }:
 //   p = e + lr*g ;  payload = { (i, p_i) : |p_i| >= lambda } ;  e' = p - kept.
 //
-// A persistent grid of workgroups strides over 4096-element tiles.  Per tile
+// A persistent grid of workgroups strides over 4096-element tiles (for
+// long sweeps, each XCD through a contiguous share of them).  Per tile
 // each thread loads four 16-byte vectors of g and of e (every wave
 // instruction covers 1 KiB of contiguous memory), forms p with a separately
 // rounded multiply and add, writes e' straight back, and keeps a 16-bit mask
@@ -32,7 +33,7 @@ template <bool kVector, bool kStats>
 __global__ __launch_bounds__(kBlock) void ht_fused_kernel(
     const float *__restrict__ g, float *__restrict__ e, int64_t d, float lr, float lambda,
     int32_t *__restrict__ idx, float *__restrict__ val, int64_t cap,
-    uint32_t *__restrict__ counter, Telemetry *__restrict__ tel, uint32_t ntiles) {
+    uint32_t *__restrict__ counter, Telemetry *__restrict__ tel, uint32_t ntiles, bool by_xcd) {
     __shared__ PairStage st;
     __shared__ double s_f64[kWaves];
     unsigned long long *word = reinterpret_cast<unsigned long long *>(counter + 2);
@@ -41,7 +42,8 @@ __global__ __launch_bounds__(kBlock) void ht_fused_kernel(
     double err2 = 0.0;  // kStats: sum of e'^2 over this thread's elements
     uint32_t max_bits = 0u;
 
-    for (uint32_t tile = blockIdx.x; tile < ntiles; tile += gridDim.x) {
+    const TileWalk walk = tile_walk(ntiles, by_xcd);
+    for (uint32_t tile = walk.first; tile < walk.end; tile += walk.stride) {
         const int64_t tile0 = int64_t(tile) * kTile;
         float p[kVecPerThread][4];
         uint32_t keep = 0;  // bit 4*j + c: element (j, c) of this thread is sent
@@ -135,22 +137,24 @@ hipError_t launch_ht(const float *g, float *e, int64_t d, float lr, float lambda
     const int64_t tiles = d > 0 ? (d + kTile - 1) / kTile : 1;
     const uint32_t ntiles = uint32_t(tiles);
     const uint32_t grid = balanced_grid(tiles, kHtWorkgroupsPerCU);
+    // long sweeps go XCD by XCD
+    const bool by_xcd = tiles >= int64_t(kXcdWalkMinTiles) * grid;
     const bool vec = ((reinterpret_cast<uintptr_t>(g) | reinterpret_cast<uintptr_t>(e)) & 15u) == 0;
     Telemetry *tel = static_cast<Telemetry *>(telemetry);
     if (tel != nullptr) {
         if (vec)
             ht_fused_kernel<true, true><<<grid, kBlock, 0, stream>>>(g, e, d, lr, lambda, idx, val,
-                                                                    cap, counter, tel, ntiles);
+                                                                    cap, counter, tel, ntiles, by_xcd);
         else
             ht_fused_kernel<false, true><<<grid, kBlock, 0, stream>>>(g, e, d, lr, lambda, idx, val,
-                                                                     cap, counter, tel, ntiles);
+                                                                     cap, counter, tel, ntiles, by_xcd);
     } else {
         if (vec)
             ht_fused_kernel<true, false><<<grid, kBlock, 0, stream>>>(g, e, d, lr, lambda, idx, val,
-                                                                     cap, counter, tel, ntiles);
+                                                                     cap, counter, tel, ntiles, by_xcd);
         else
             ht_fused_kernel<false, false><<<grid, kBlock, 0, stream>>>(g, e, d, lr, lambda, idx,
-                                                                      val, cap, counter, tel, ntiles);
+                                                                      val, cap, counter, tel, ntiles, by_xcd);
     }
     return hipGetLastError();
 }

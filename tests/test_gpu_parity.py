@@ -88,6 +88,25 @@ def test_ht_ef_loop_matches_oracle(d, unaligned):
         assert_bits_equal(ge, e_ref, "e' t=%d" % t)
 
 
+@pytest.mark.parametrize("unaligned", [False, True])
+def test_ht_long_sweep(unaligned):
+    # 34 tiles per workgroup and a ragged last tile (the sweeps of 256 tiles
+    # per workgroup and more, walked XCD by XCD, are checked on the 1.5e9
+    # workload)
+    d = 70_000_003
+    say("ht parity long sweep d=%d unaligned=%s" % (d, unaligned))
+    gs = [synth.small_gradient(20 + t, d) for t in range(2)]
+    lam = oracle.calibrate_lambda(gs[0], 0.001)
+    st = HT(d, cap=d // 8, unaligned=unaligned)
+    e_ref = np.zeros(d, dtype=np.float32)
+    for t in range(2):
+        gi, gv, ge, gk = st.step(gs[t], lam)
+        ri, rv, e_ref, rk = oracle.ht(gs[t], e_ref, LR, lam, mt=True)
+        assert gk == rk
+        assert_payload_equal(gi, gv, ri, rv, "t=%d" % t)
+        assert_bits_equal(ge, e_ref, "e' t=%d" % t)
+
+
 def test_ht_lambda_zero_and_infinity():
     d = 70_001
     g = synth.small_gradient(1, d)
