@@ -152,9 +152,9 @@ size_t topk_path_flag_offset(void);
  *   workspace   >= topk_segmented_workspace_bytes(nseg, k_total) bytes,
  *               16-byte aligned: per-segment tables and histograms (36 KiB per
  *               segment), a candidate region of 16*k_total + 4096*nseg
- *               (key, index) pairs and a work list of one 8-byte entry per
- *               2048 of those pairs or payload slots.  Results never depend
- *               on its contents.
+ *               (key, index) pairs, a work list of one 8-byte entry per
+ *               2048 of those pairs or payload slots, and 32 KiB of flags
+ *               over groups of tiles.  Results never depend on its contents.
  *               Not shareable between concurrent calls.
  * Host-visible arguments are checked before anything is launched (EFS_EINVAL,
  * EFS_ESPACE).  offsets and k live on the device and are checked there: a

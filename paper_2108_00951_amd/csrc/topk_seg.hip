@@ -85,6 +85,13 @@ constexpr uint32_t kChunk = 2048;              // pass2 work item: payload slots
 // faster than one long range per workgroup), and a slice is long enough to
 // amortise its flushes.
 constexpr int64_t kSliceTilesMax = 4;
+// A one-tile segment with k at most kSmallK takes k block-wide maxima
+// instead of the three-level radix select (k barriers instead of about 17).
+constexpr int64_t kSmallK = 8;
+// Flags of groups of consecutive tiles (2^sweep_shift tiles a group, at most
+// kSweepGroups groups): select1 marks the groups of the segments that need
+// pass2's tile sweep, and pass2 skips every slice whose groups are unmarked.
+constexpr int kSweepGroups = 8192;
 constexpr int kSliceWorkgroupsPerCU = 8;
 constexpr uint32_t kNoBin = 0xffffffffu;
 constexpr uint32_t kNoWork = 0xffffffffu;      // work-list slot not in use this call
@@ -170,12 +177,14 @@ struct SegWs {
     uint2 *cand;            // (bits of p, index)
     uint2 *work;            // pass2 work list: (segment | kind << 31, first slot)
     struct ResetChunk *chunks;  // the reset's per-chunk sums (many layers)
+    uint32_t *sweep;        // [kSweepGroups] tile-group flags for pass2's sweep
     int64_t ccap_total;
     uint32_t work_cap;
+    uint32_t sweep_shift;   // tile t is in group t >> sweep_shift
 };
 
 struct SegLayout {
-    size_t info, tile_prefix, st, hint, hist1, hist2, cand, work, chunks, bytes;
+    size_t info, tile_prefix, st, hint, hist1, hist2, cand, work, chunks, sweep, bytes;
     int64_t ccap_total, work_cap;
 };
 
@@ -206,6 +215,8 @@ SegLayout seg_layout(int32_t nseg, int64_t k_total) {
     // the reset's per-chunk sums (layouts of more than kResetSingleMax layers)
     L.chunks = o;
     o += round256(32 * ((size_t(nseg) + 511) / 512));
+    L.sweep = o;
+    o += round256(4 * size_t(kSweepGroups));
     L.bytes = o;
     return L;
 }
@@ -220,6 +231,15 @@ __device__ __forceinline__ uint32_t wave_incl_u32(uint32_t v) {
     for (int off = 1; off < kWave; off <<= 1) {
         const uint32_t o = __shfl_up(v, off);
         if (lane >= off) v += o;
+    }
+    return v;
+}
+
+__device__ __forceinline__ uint64_t wave_max_u64(uint64_t v) {
+#pragma unroll
+    for (int off = kWave / 2; off > 0; off >>= 1) {
+        const uint64_t o = __shfl_xor(v, off);
+        v = o > v ? o : v;
     }
     return v;
 }
@@ -472,12 +492,16 @@ __device__ __forceinline__ Sums reset_chunk(const SegWs &ws, const SegIn &in, in
     return tot;
 }
 
-// Zeroes the histograms of the layers that span more than one tile (a
-// one-tile layer is selected inside pass1), workgroup w of nw; an invalid
-// layout is rejected, so what is zeroed for it does not matter.
+// Zeroes the sweep flags and the histograms of the layers that span more
+// than one tile (a one-tile layer is selected inside pass1), workgroup w of
+// nw; an invalid layout is rejected, so what is zeroed for it does not
+// matter.
 __device__ __forceinline__ void reset_zero(const SegWs &ws, const int64_t *off, int32_t nseg,
                                            int32_t w, int32_t nw) {
     const f32x4 z = {0.0f, 0.0f, 0.0f, 0.0f};
+    f32x4 *fl = reinterpret_cast<f32x4 *>(ws.sweep);
+    for (int q = w * kResetBlock + threadIdx.x; q < kSweepGroups / 4; q += nw * kResetBlock)
+        fl[q] = z;
     for (int32_t sg = w; sg < nseg; sg += nw) {
         const int64_t lo = off[sg], size = off[sg + 1] - lo;
         if (size < 0 || segment_tiles(lo, size) <= 1) continue;
@@ -779,11 +803,13 @@ __device__ __forceinline__ void stage_tile(Stage &sg, uint32_t &efill, uint32_t 
 }
 
 // A segment that lies within one tile is selected here, by the workgroup
-// holding it: a radix select on the keys of its elements (bits 30..20,
-// 19..10, 9..0, histograms in LDS), the keys equal to the threshold kept in
-// index order, the pairs written to the segment's payload region and e
-// cleared at them (e already holds p).  `hist` is 2048 words of zeroed
-// LDS, zeroed again on return.  Called by every thread of the workgroup.
+// holding it: for a small k, k rounds of a block-wide maximum of (key, lower
+// index first); otherwise a radix select on the keys of its elements (bits
+// 30..20, 19..10, 9..0, histograms in LDS), the keys equal to the threshold
+// kept in index order.  The pairs are written to the segment's payload
+// region and e cleared at them (e already holds p).  `hist` is 2048 words
+// of zeroed LDS, zeroed again on return.  Called by every thread of the
+// workgroup.
 __device__ void select_in_tile(const float (&p)[kVecPerThread][4], uint32_t valid,
                                int64_t block0, const SegInfo &inf, uint32_t *hist,
                                uint32_t *s_wave, uint32_t *s_out, int32_t *idx, float *val,
@@ -797,6 +823,43 @@ __device__ void select_in_tile(const float (&p)[kVecPerThread][4], uint32_t vali
     uint32_t keep = 0;
     if (inf.k >= inf.size) {
         keep = valid;
+    } else if (inf.k <= kSmallK) {
+        // k rounds of a block-wide maximum over the elements not yet kept,
+        // of (key, then the lower index): one barrier a round
+        __shared__ uint64_t s_best[2][kWaves];
+        const int lane = tid & (kWave - 1);
+        const int wave = tid / kWave;
+#pragma unroll 1
+        for (int r = 0; r < int(inf.k); ++r) {
+            // this thread's elements in (j, c) order are in index order, so
+            // the first strictly larger key is its best
+            const uint32_t open = valid & ~keep;
+            uint32_t bk = 0, bs = 32;
+#pragma unroll
+            for (int j = 0; j < kVecPerThread; ++j)
+#pragma unroll
+                for (int c = 0; c < 4; ++c)
+                    if (((open >> (4 * j + c)) & 1u) && (bs == 32 || key[j][c] > bk)) {
+                        bk = key[j][c];
+                        bs = uint32_t(4 * j + c);
+                    }
+            uint64_t best = 0;
+            if (bs != 32) {
+                const uint32_t pos = ((bs >> 2) * uint32_t(kBlock) + uint32_t(tid)) * 4u + (bs & 3u);
+                best = (uint64_t(bk) << 32) | (0xffffffffu - pos);
+            }
+            best = wave_max_u64(best);
+            if (lane == 0) s_best[r & 1][wave] = best;
+            __syncthreads();
+            uint64_t all = s_best[r & 1][0];
+#pragma unroll
+            for (int q = 1; q < kWaves; ++q) all = s_best[r & 1][q] > all ? s_best[r & 1][q] : all;
+            // every valid element scores above 0, and k < size of them exist
+            const uint32_t pos = 0xffffffffu - uint32_t(all);
+            const uint32_t quad = pos >> 2;
+            if (int(quad % uint32_t(kBlock)) == tid)
+                keep |= 1u << (4 * (quad / uint32_t(kBlock)) + (pos & 3u));
+        }
     } else if (inf.k > 0) {
         uint32_t need = uint32_t(inf.k), prefix = 0;
 #pragma unroll 1
@@ -986,6 +1049,15 @@ __global__ __launch_bounds__(kBlock) void seg_pass1_kernel(const float *__restri
 // select1: per segment, the bracket bin or the digit of the k-th key, and the mode
 // ---------------------------------------------------------------------------
 
+// Marks the tile groups of segment `inf` for pass2's sweep.  Called by
+// every thread of the workgroup.
+__device__ __forceinline__ void mark_sweep(const SegWs &ws, const SegInfo &inf) {
+    const uint32_t g0 = inf.tile0 >> ws.sweep_shift;
+    const uint32_t g1 = min((inf.tile0 + inf.ntiles - 1u) >> ws.sweep_shift,
+                            uint32_t(kSweepGroups - 1));
+    for (uint32_t q = g0 + threadIdx.x; q <= g1; q += kBlock) ws.sweep[q] = 1u;
+}
+
 // Radix path of segment s (0 < k < size): from its digit-1 histogram, the
 // digit D1 holding the k-th key, the keys still needed inside it, and the
 // mode (none, candidates, or scan when the keys in D1 overflow the segment's
@@ -1006,7 +1078,9 @@ __device__ void choose_digit1(const SegWs &ws, int32_t s, const SegInfo &inf, Se
         // thousands of segments take this path)
         if (c1 != 0u) ws.ctl->pass2 = 1u;
     }
+    const bool sweep = s_out[2] != 0u;
     __syncthreads();  // s_out is reused by the caller
+    if (sweep) mark_sweep(ws, inf);
 }
 
 __device__ void select1_segment(const SegWs &ws, int32_t s, uint32_t *s_wave, uint32_t *s_out) {
@@ -1021,6 +1095,7 @@ __device__ void select1_segment(const SegWs &ws, int32_t s, uint32_t *s_wave, ui
             st->mode = inf.k == 0 ? kModeNone : kModeAll;
             if (inf.k != 0) ws.ctl->pass2 = 1u;
         }
+        if (inf.k != 0) mark_sweep(ws, inf);
         return;
     }
     // bracket confirmed when #(key > hi) <= k <= #(key >= lo) and every key in
@@ -1252,8 +1327,13 @@ __global__ __launch_bounds__(kBlock) void seg_pass2_kernel(float *__restrict__ e
     if (ws.ctl->status != 0u) return;
     const uint32_t T = ws.ctl->tiles;
     if (ws.ctl->pass2 != 0u)
-        for (uint32_t t0 = blockIdx.x * slice; t0 < T; t0 += gridDim.x * slice)
-            pass2_tiles<kAligned>(e, idx, val, nseg, ws, t0, min(T, t0 + slice), hist, sg);
+        for (uint32_t t0 = blockIdx.x * slice; t0 < T; t0 += gridDim.x * slice) {
+            const uint32_t t1 = min(T, t0 + slice);
+            const uint32_t g1 = min((t1 - 1u) >> ws.sweep_shift, uint32_t(kSweepGroups - 1));
+            uint32_t marked = 0u;
+            for (uint32_t q = t0 >> ws.sweep_shift; q <= g1; ++q) marked |= ws.sweep[q];
+            if (marked) pass2_tiles<kAligned>(e, idx, val, nseg, ws, t0, t1, hist, sg);
+        }
     // work list: workgroup b owns slots b, b + grid, b + 2 grid, ... (a
     // segment's items are consecutive slots, so they spread over workgroups);
     // its threads read those slots together, then the workgroup runs the
@@ -1552,8 +1632,13 @@ hipError_t launch_topk_segmented(const float *g, float *e, int64_t d, float lr, 
     ws.cand = reinterpret_cast<uint2 *>(base + L.cand);
     ws.work = reinterpret_cast<uint2 *>(base + L.work);
     ws.chunks = reinterpret_cast<ResetChunk *>(base + L.chunks);
+    ws.sweep = reinterpret_cast<uint32_t *>(base + L.sweep);
     ws.ccap_total = L.ccap_total;
     ws.work_cap = uint32_t(L.work_cap);
+    // every tile index is below ceil(d / kTile) + nseg, so its group is below
+    // kSweepGroups
+    const int64_t max_tiles = (d + kTile - 1) / kTile + nseg;
+    while (((max_tiles - 1) >> ws.sweep_shift) >= kSweepGroups) ++ws.sweep_shift;
 
     const uint32_t zero_grid = persistent_grid(nseg);  // one segment's histograms per pass
     if (nseg <= kResetSingleMax) {
@@ -1566,7 +1651,6 @@ hipError_t launch_topk_segmented(const float *g, float *e, int64_t d, float lr, 
                                                                                d, k_total, nchunks);
     }
 
-    const int64_t max_tiles = (d + kTile - 1) / kTile + nseg;
     // slices: the tiles spread over kSliceWorkgroupsPerCU workgroups per CU
     // (4 resident), at most kSliceTilesMax tiles each
     const int64_t wgs = int64_t(device_cu_count()) * kSliceWorkgroupsPerCU;
