@@ -62,6 +62,10 @@ constexpr int kDigit2 = 1 << (kShift1 - kShift2);
 constexpr int kDigit3 = 1 << kShift2;
 constexpr int kIdxBins = 2048;  // index radix for ties: 11 + 10 + 10 bits
 constexpr int kCandLds = 18432;  // candidates the final pass holds in LDS (144 KiB)
+// ... with more than kFinalWideMin segments: a smaller buffer (30 KiB), so
+// that four workgroups share a CU
+constexpr int kCandLdsSmall = 3840;
+constexpr int kFinalWideMin = 256;
 constexpr int64_t kCandPerK = 16;
 constexpr int64_t kCandExtra = 4096;
 
@@ -1363,9 +1367,11 @@ __global__ __launch_bounds__(kBlock) void seg_pass2_kernel(float *__restrict__ e
 // final: each segment's exact threshold, its ties, the last pairs
 // ---------------------------------------------------------------------------
 
+template <int kCap>
 struct FinalShared {
+    static constexpr int cap = kCap;
     uint32_t hist[kIdxBins];
-    uint2 cand[kCandLds];
+    uint2 cand[kCap];
     uint32_t wave[kWaves];
     uint32_t out[3];
     uint32_t cursor;
@@ -1377,8 +1383,8 @@ constexpr int kUnroll = 8;               // items loaded per thread at a time
 // Calls f(key, index, bits of p) for every item of the segment's selection
 // set: the candidate list (LDS or global), or, in scan mode, every element
 // of the segment.  kUnroll loads per thread are in flight together.
-template <int kMode, bool kLds, typename F>
-__device__ __forceinline__ void for_items(const FinalShared &sh, const uint2 *cand,
+template <int kMode, bool kLds, typename Sh, typename F>
+__device__ __forceinline__ void for_items(const Sh &sh, const uint2 *cand,
                                           const float *e, const SegInfo &inf, int64_t n, F f) {
     for (int64_t base = 0; base < n; base += int64_t(kUnroll) * kBlock) {
         uint2 it[kUnroll];
@@ -1406,8 +1412,8 @@ __device__ __forceinline__ void for_items(const FinalShared &sh, const uint2 *ca
 // index: bits 30..20, 19..10, 9..0, unless all are kept), emit every item
 // above T and the chosen ties from payload slot `cursor0` on, clear their e,
 // and record T as the next call's hint.
-template <int kMode, bool kLds>
-__device__ void finish(FinalShared &sh, const SegInfo &inf, const uint2 *cand, int64_t n,
+template <int kMode, bool kLds, typename Sh>
+__device__ void finish(Sh &sh, const SegInfo &inf, const uint2 *cand, int64_t n,
                        float *e, int32_t *idx, float *val, uint32_t T, uint32_t need3,
                        uint32_t ties, uint32_t cursor0, SegHint *hint, uint32_t width) {
     const int tid = threadIdx.x;
@@ -1453,8 +1459,8 @@ __device__ void finish(FinalShared &sh, const SegInfo &inf, const uint2 *cand, i
 // Radix path: D1 from pass1, digit 2 from pass2's histogram of the keys in
 // D1, digit 3 from a pass over the items.  Scan mode also emits every key
 // above D1 (pass2 left them in place).
-template <int kMode, bool kLds>
-__device__ void final_select(FinalShared &sh, const SegInfo &inf, const SegState &st,
+template <int kMode, bool kLds, typename Sh>
+__device__ void final_select(Sh &sh, const SegInfo &inf, const SegState &st,
                              const uint2 *cand, int64_t n, float *e, int32_t *idx, float *val,
                              const uint32_t *hist2, SegHint *hint, uint32_t width) {
     const int tid = threadIdx.x;
@@ -1486,8 +1492,8 @@ __device__ void final_select(FinalShared &sh, const SegInfo &inf, const SegState
 // da and listed the `ca` candidates of bin da; rank those by the low
 // `shift` bits of key - lo (the exact threshold T), then by index among
 // keys equal to T, and emit the `needa` kept ones into the last slots.
-template <bool kLds>
-__device__ void final_fast(FinalShared &sh, const SegInfo &inf, const SegState &st,
+template <bool kLds, typename Sh>
+__device__ void final_fast(Sh &sh, const SegInfo &inf, const SegState &st,
                            const uint2 *list, int64_t n, float *e, int32_t *idx, float *val,
                            SegHint *hint, uint32_t width) {
     const int tid = threadIdx.x;
@@ -1514,9 +1520,9 @@ __device__ void final_fast(FinalShared &sh, const SegInfo &inf, const SegState &
                             uint32_t(inf.k) - st.needa, hint, width);
 }
 
+template <typename Sh>
 __device__ void final_segment(float *__restrict__ e, int32_t *__restrict__ idx,
-                              float *__restrict__ val, const SegWs &ws, int32_t s,
-                              FinalShared &sh) {
+                              float *__restrict__ val, const SegWs &ws, int32_t s, Sh &sh) {
     const SegState st = ws.st[s];
     if (st.mode != kModeCand && st.mode != kModeScan && st.mode != kModeFast) return;
     const SegInfo inf = ws.info[s];
@@ -1547,7 +1553,7 @@ __device__ void final_segment(float *__restrict__ e, int32_t *__restrict__ idx,
     const int64_t n = fast ? int64_t(st.needa ? min(st.ca, st.tcur) : 0u)
                            : min(int64_t(st.ccur), inf.ccap);
     const uint2 *cand = ws.cand + inf.coff + (fast ? st.ccur : 0u);
-    const bool lds = n <= kCandLds;
+    const bool lds = n <= Sh::cap;
     if (lds) {
         for (int64_t base = 0; base < n; base += int64_t(kUnroll) * kBlock) {
             uint2 v[kUnroll];
@@ -1573,16 +1579,19 @@ __device__ void final_segment(float *__restrict__ e, int32_t *__restrict__ idx,
     }
 }
 
-// One workgroup per CU at most (the LDS candidate buffer), looping over the
-// segments b, b + grid, ...  Most need nothing here (one tile, none, all), so
-// the workgroup first reads the modes of up to kBlock of its segments at once
-// and then runs only those with something to rank (one dependent read per
-// segment in turn was the larger cost with thousands of segments).
+// One workgroup per CU at most with the large candidate buffer, four with
+// the small one (a larger list is ranked from global memory), looping over
+// the segments b, b + grid, ...  Most need nothing here (one tile, none,
+// all), so the workgroup first reads the modes of up to kBlock of its
+// segments at once and then runs only those with something to rank (one
+// dependent read per segment in turn was the larger cost with thousands of
+// segments).
+template <int kCap>
 __global__ __launch_bounds__(kBlock) void seg_final_kernel(float *__restrict__ e,
                                                            int32_t *__restrict__ idx,
                                                            float *__restrict__ val, SegWs ws,
                                                            int32_t nseg) {
-    __shared__ FinalShared sh;
+    __shared__ FinalShared<kCap> sh;
     __shared__ int32_t s_list[kBlock];
     __shared__ uint32_t s_wave[kWaves];
     if (ws.ctl->status != 0u) return;
@@ -1666,8 +1675,13 @@ hipError_t launch_topk_segmented(const float *g, float *e, int64_t d, float lr, 
         seg_pass2_kernel<true><<<grid, kBlock, 0, stream>>>(e, idx, val, nseg, ws, uint32_t(slice));
     else
         seg_pass2_kernel<false><<<grid, kBlock, 0, stream>>>(e, idx, val, nseg, ws, uint32_t(slice));
-    seg_final_kernel<<<uint32_t(min(int64_t(nseg), int64_t(device_cu_count()))), kBlock, 0, stream>>>(
-        e, idx, val, ws, nseg);
+    const int64_t cus = device_cu_count();
+    if (nseg > kFinalWideMin)
+        seg_final_kernel<kCandLdsSmall><<<uint32_t(min(int64_t(nseg), 4 * cus)), kBlock, 0, stream>>>(
+            e, idx, val, ws, nseg);
+    else
+        seg_final_kernel<kCandLds><<<uint32_t(min(int64_t(nseg), cus)), kBlock, 0, stream>>>(
+            e, idx, val, ws, nseg);
     return hipGetLastError();
 }
 

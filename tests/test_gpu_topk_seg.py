@@ -150,6 +150,26 @@ def test_segmented_large_candidate_sets():
     check(g, e, off, ks, what="large")
 
 
+def test_segmented_large_candidate_sets_many_layers():
+    # 400 layers, so the final pass holds at most 3,840 candidates in LDS;
+    # in the two large layers 10,000 and 5,000 distinct magnitudes share
+    # the digit of the k-th key, so their lists are ranked from global memory
+    d = 2_000_000
+    small = 37 + 100 * np.arange(397, dtype=np.int64)
+    off = np.concatenate([[0], small, [1_500_000, d]]).astype(np.int64)
+    ks = np.full(off.size - 1, 2, dtype=np.int64)
+    ks[-2:] = [6000, 3000]
+    rng = np.random.default_rng(441)
+    g = (synth.small_gradient(441, d) * np.float32(1e-3)).astype(np.float32)
+    for lo, hi, n in [(off[-3], off[-2], 10_000), (off[-2], off[-1], 5_000)]:
+        pos = rng.choice(np.arange(lo, hi), n, replace=False)
+        mag = np.float32(1.0) + rng.random(n).astype(np.float32) * np.float32(0.02)
+        g[pos] = np.where(rng.random(n) < 0.5, -mag, mag).astype(np.float32)
+    e = np.zeros(d, np.float32)
+    say("segmented large candidate sets among %d layers" % ks.size)
+    check(g, e, off, ks, lr=np.float32(1.0), what="large, many layers")
+
+
 def test_segmented_special_values():
     d = 5000
     off = np.array([0, 1000, 2500, d], dtype=np.int64)
