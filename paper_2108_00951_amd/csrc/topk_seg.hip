@@ -89,6 +89,12 @@ constexpr uint32_t kChunk = 2048;              // pass2 work item: payload slots
 // faster than one long range per workgroup), and a slice is long enough to
 // amortise its flushes.
 constexpr int64_t kSliceTilesMax = 4;
+// With more segments than a two-round search covers, a slice starts with a
+// third round of dependent reads: the slices are then made as long as the
+// grid allows (up to kSliceTilesMaxMany), so that each workgroup searches
+// once or a few times.
+constexpr int32_t kSearchTwoRounds = kWave * kWave;
+constexpr int64_t kSliceTilesMaxMany = 64;
 // A one-tile segment with k at most kSmallK takes k block-wide maxima
 // instead of the three-level radix select (k barriers instead of about 17).
 constexpr int64_t kSmallK = 8;
@@ -338,6 +344,17 @@ __device__ __forceinline__ int32_t segment_after(const uint32_t *tp, int32_t nse
 // map).
 __device__ __forceinline__ int64_t tile_elem(int64_t block0, int j, int c) {
     return block0 + int64_t(j * kBlock + int(threadIdx.x)) * 4 + c;
+}
+
+// The same element's offset from `block0` (below kTile).
+__device__ __forceinline__ uint32_t tile_off(int j, int c) {
+    return uint32_t(j * kBlock + int(threadIdx.x)) * 4u + uint32_t(c);
+}
+
+// Slice j of every thread's elements covers offsets [j * 1024, (j + 1) * 1024)
+// of the block: whether it meets [lo, hi) (the same for the whole workgroup).
+__device__ __forceinline__ bool slice_meets(int j, uint32_t lo, uint32_t hi) {
+    return uint32_t(j) * (4u * kBlock) < hi && uint32_t(j + 1) * (4u * kBlock) > lo;
 }
 
 // Tiles of a segment: the 4096-element blocks it overlaps.
@@ -819,6 +836,8 @@ __device__ void select_in_tile(const float (&p)[kVecPerThread][4], uint32_t vali
                                uint32_t *s_wave, uint32_t *s_out, int32_t *idx, float *val,
                                float *e) {
     const int tid = threadIdx.x;
+    // slices j >= jn hold none of the segment (its elements start at block0)
+    const int jn = int((uint32_t(inf.size) + 4u * kBlock - 1u) / (4u * kBlock));
     uint32_t key[kVecPerThread][4];
 #pragma unroll
     for (int j = 0; j < kVecPerThread; ++j)
@@ -838,21 +857,25 @@ __device__ void select_in_tile(const float (&p)[kVecPerThread][4], uint32_t vali
             // this thread's elements in (j, c) order are in index order, so
             // the first strictly larger key is its best
             const uint32_t open = valid & ~keep;
-            uint32_t bk = 0, bs = 32;
-#pragma unroll
-            for (int j = 0; j < kVecPerThread; ++j)
-#pragma unroll
-                for (int c = 0; c < 4; ++c)
-                    if (((open >> (4 * j + c)) & 1u) && (bs == 32 || key[j][c] > bk)) {
-                        bk = key[j][c];
-                        bs = uint32_t(4 * j + c);
-                    }
             uint64_t best = 0;
-            if (bs != 32) {
-                const uint32_t pos = ((bs >> 2) * uint32_t(kBlock) + uint32_t(tid)) * 4u + (bs & 3u);
-                best = (uint64_t(bk) << 32) | (0xffffffffu - pos);
+            if (__any(open != 0u)) {  // waves past the segment's end skip this
+                uint32_t bk = 0, bs = 32;
+#pragma unroll
+                for (int j = 0; j < kVecPerThread; ++j)
+                    if (j < jn)
+#pragma unroll
+                        for (int c = 0; c < 4; ++c)
+                            if (((open >> (4 * j + c)) & 1u) && (bs == 32 || key[j][c] > bk)) {
+                                bk = key[j][c];
+                                bs = uint32_t(4 * j + c);
+                            }
+                if (bs != 32) {
+                    const uint32_t pos =
+                        ((bs >> 2) * uint32_t(kBlock) + uint32_t(tid)) * 4u + (bs & 3u);
+                    best = (uint64_t(bk) << 32) | (0xffffffffu - pos);
+                }
+                best = wave_max_u64(best);
             }
-            best = wave_max_u64(best);
             if (lane == 0) s_best[r & 1][wave] = best;
             __syncthreads();
             uint64_t all = s_best[r & 1][0];
@@ -984,28 +1007,38 @@ __device__ void pass1_slice(const float *__restrict__ g, float *__restrict__ e, 
             valid = 0xffffu;
         } else {
             // a segment's first or last block: only its own elements are
-            // read and written (the rest of the block belongs to neighbours)
+            // read and written (the rest of the block belongs to neighbours).
+            // A segment within one block is laid over the threads from its
+            // first element on, so that a small one fills few slices and
+            // waves; slices outside the elements are skipped.
+            const int64_t base = inf.ntiles == 1 ? inf.off : r.block0;
+            const uint32_t lo = uint32_t(r.lo - base), hi = uint32_t(r.hi - base);
+            const float *gb = g + base;
+            float *eb = e + base;
 #pragma unroll
             for (int j = 0; j < kVecPerThread; ++j) {
 #pragma unroll
+                for (int c = 0; c < 4; ++c) p[j][c] = 0.0f;
+                if (!slice_meets(j, lo, hi)) continue;
+#pragma unroll
                 for (int c = 0; c < 4; ++c) {
-                    const int64_t i = tile_elem(r.block0, j, c);
-                    p[j][c] = 0.0f;
-                    if (i >= r.lo && i < r.hi) {
-                        p[j][c] = ef_accumulate(e[i], lr, g[i]);
-                        e[i] = p[j][c];
+                    const uint32_t o = tile_off(j, c);
+                    if (o >= lo && o < hi) {
+                        p[j][c] = ef_accumulate(eb[o], lr, gb[o]);
+                        eb[o] = p[j][c];
                         valid |= 1u << (4 * j + c);
                     }
                 }
             }
-        }
-        if (inf.ntiles == 1) {
-            select_in_tile(p, valid, r.block0, inf, hist, s_wave, s_out, idx, val, e);
-            continue;
+            if (inf.ntiles == 1) {
+                select_in_tile(p, valid, base, inf, hist, s_wave, s_out, idx, val, e);
+                continue;
+            }
         }
         uint32_t emit_mask = 0, cand_mask = 0;
 #pragma unroll
         for (int j = 0; j < kVecPerThread; ++j) {
+            if (!__any(((valid >> (4 * j)) & 0xfu) != 0u)) continue;  // none in this wave
 #pragma unroll
             for (int c = 0; c < 4; ++c) {
                 const uint32_t bit = 1u << (4 * j + c);
@@ -1032,7 +1065,7 @@ __device__ void pass1_slice(const float *__restrict__ g, float *__restrict__ e, 
 }
 
 template <bool kAligned>
-__global__ __launch_bounds__(kBlock) void seg_pass1_kernel(const float *__restrict__ g,
+__global__ __launch_bounds__(kBlock, 4) void seg_pass1_kernel(const float *__restrict__ g,
                                                            float *__restrict__ e, float lr,
                                                            int32_t *__restrict__ idx,
                                                            float *__restrict__ val, int32_t nseg,
@@ -1221,14 +1254,18 @@ __device__ void pass2_tiles(float *__restrict__ e, int32_t *__restrict__ idx,
             }
             valid = 0xffffu;
         } else {
+            const float *eb = e + r.block0;
+            const uint32_t lo = uint32_t(r.lo - r.block0), hi = uint32_t(r.hi - r.block0);
 #pragma unroll
             for (int j = 0; j < kVecPerThread; ++j) {
 #pragma unroll
+                for (int c = 0; c < 4; ++c) p[j][c] = 0.0f;
+                if (!slice_meets(j, lo, hi)) continue;
+#pragma unroll
                 for (int c = 0; c < 4; ++c) {
-                    const int64_t i = tile_elem(r.block0, j, c);
-                    p[j][c] = 0.0f;
-                    if (i >= r.lo && i < r.hi) {
-                        p[j][c] = e[i];
+                    const uint32_t o = tile_off(j, c);
+                    if (o >= lo && o < hi) {
+                        p[j][c] = eb[o];
                         valid |= 1u << (4 * j + c);
                     }
                 }
@@ -1661,9 +1698,11 @@ hipError_t launch_topk_segmented(const float *g, float *e, int64_t d, float lr, 
     }
 
     // slices: the tiles spread over kSliceWorkgroupsPerCU workgroups per CU
-    // (4 resident), at most kSliceTilesMax tiles each
+    // (4 resident), at most kSliceTilesMax tiles each (kSliceTilesMaxMany
+    // with many segments)
     const int64_t wgs = int64_t(device_cu_count()) * kSliceWorkgroupsPerCU;
-    const int64_t slice = max(int64_t(1), min(kSliceTilesMax, (max_tiles + wgs - 1) / wgs));
+    const int64_t slice_max = nseg > kSearchTwoRounds ? kSliceTilesMaxMany : kSliceTilesMax;
+    const int64_t slice = max(int64_t(1), min(slice_max, (max_tiles + wgs - 1) / wgs));
     const uint32_t grid = uint32_t(min(wgs, (max_tiles + slice - 1) / slice));
     const bool aligned = ((reinterpret_cast<uintptr_t>(g) | reinterpret_cast<uintptr_t>(e)) & 15) == 0;
     if (aligned)
