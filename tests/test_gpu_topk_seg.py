@@ -473,6 +473,39 @@ def test_segmented_thousands_of_layers_ef_loop():
         say("  step %d ok (bracket in %d layers)" % (t, efs.topk_segmented_bracket_segments(ws)))
 
 
+def test_segmented_twenty_thousand_layers_ef_steps():
+    # 20,000 layers over 25.6e6 (log-uniform sizes from 1 to 10^4 before
+    # scaling): more layers than two rounds of the tile-to-layer search
+    # cover, so the sweeps take long slices; most layers lie in one tile and
+    # the final pass runs with its small LDS buffer.  Four error-feedback
+    # steps on one workspace (the later ones mostly from the brackets), each
+    # against the oracle
+    d, nseg = 25_600_000, 20_000
+    sizes = synth.segment_sizes(7, nseg, d, lo=1.0, hi=1e4)
+    off = np.concatenate([[0], np.cumsum(sizes)]).astype(np.int64)
+    ks = synth.layerwise_k(off, 0.001)
+    k_total = int(ks.sum())
+    e_ref = np.zeros(d, np.float32)
+    ed = torch.zeros(d, dtype=torch.float32, device=DEV)
+    idx = torch.empty(k_total, dtype=torch.int32, device=DEV)
+    val = torch.empty(k_total, dtype=torch.float32, device=DEV)
+    ws = efs.new_topk_segmented_workspace(nseg, k_total, DEV)
+    offd, kd = dev(off), dev(ks)
+    say("segmented 20,000 layers d=%d k=%d" % (d, k_total))
+    for t in range(4):
+        g = synth.small_gradient(2000 + t, d)
+        efs.topk_segmented_compress(dev(g), ed, LR, offd, kd, idx, val, ws)
+        assert efs.topk_segmented_status(ws) == 0
+        ri, rv, e_ref = oracle.topk_segmented(g, e_ref, LR, off, ks)
+        gi, gv = idx.cpu().numpy(), val.cpu().numpy()
+        order = np.lexsort((gi, np.repeat(np.arange(nseg), ks)))
+        np.testing.assert_array_equal(gi[order], ri, "t=%d indices" % t)
+        assert_bits_equal(gv[order], rv, "t=%d values" % t)
+        assert_bits_equal(ed.cpu().numpy(), e_ref, "e' t=%d" % t)
+        say("  step %d ok (bracket in %d layers)" % (t, efs.topk_segmented_bracket_segments(ws)))
+    assert efs.topk_segmented_bracket_segments(ws) >= 500  # 687 on this input
+
+
 @pytest.mark.parametrize("seed", range(8))
 def test_segmented_randomised_ef_loops(seed):
     # random layouts (empty, one-tile and multi-tile layers), random budgets,
