@@ -117,7 +117,7 @@ size_t topk_workspace_bytes(int64_t d, int64_t k);
  *                 bytes, 16-byte aligned; contents need no initialisation.
  *                 The library keeps the last two thresholds in it: a
  *                 following call on the same workspace whose k-th magnitude
- *                 lies within about 3 to 6 % of their linear extrapolation
+ *                 lies within about 6 to 12 % of their linear extrapolation
  *                 (the error-feedback case) selects from a small candidate
  *                 set instead of three more passes over p.
  *                 Results never depend on what the workspace held.  Not

@@ -9,14 +9,15 @@
 // (work a call does not need returns at once):
 //
 //   reset  zero the control block and histograms; form the key bracket
-//          [lo, hi] of 2^20 keys (about 3..6 % in magnitude either side)
+//          [lo, hi] of 2^20 keys (about 3..6 % in magnitude either side;
+//          2^21 keys for 16 calls after a threshold fell outside it)
 //          around the threshold predicted from the previous two calls on
 //          this workspace.
 //   pass1  p = e + lr*g written into e (12 B/element, streamed with the
 //          non-temporal hint); LDS histogram of key
 //          bits 30..20; with a bracket, keys above it go straight to the
 //          payload and keys inside it to a candidate buffer (staged
-//          compaction) and into coarse (1024) and fine (2^20) histograms of
+//          compaction) and into coarse (1024) and fine (one per key) histograms of
 //          key - lo.
 //   step3  every workgroup first decides the path: the bracket path only
 //          when the counts prove the k-th key lies inside the bracket
@@ -47,7 +48,7 @@
 //
 // Workspace (offsets 256-byte aligned):
 //   control block (256 B) | histograms: 2048 top-digit bins, 1024 + 2^20
-//   radix bins, 1024 + 2^20 bracket bins | per-tile tie counts | candidates
+//   radix bins, 1024 + 2^21 bracket bins | per-tile tie counts | candidates
 //   (int32 index, fp32 value) x ccap.
 #include <stddef.h>
 
@@ -61,8 +62,22 @@ namespace {
 constexpr int kBins1 = 2048;  // bits 30..20
 constexpr int kCoarse = 1024; // coarse bins of a 20-bit range (1024 keys each)
 constexpr int kFineBits = 20;
-constexpr uint32_t kFine = 1u << kFineBits;        // bracket width in keys
+constexpr uint32_t kFine = 1u << kFineBits;        // radix path: bits 19..0
 constexpr int kFinePerCoarse = int(kFine) / kCoarse;
+// Bracket width in keys, one fine bin per key: kBracketNarrow, or
+// kBracketWide for kWideCalls calls after a call whose threshold fell
+// outside its bracket.  Under error feedback the threshold's step from one
+// call to the next wanders by about half its size; a 2^20-key bracket
+// missed it on 1 to 2 of 20 calls on the 25.6e6 and 1.5e9 workloads (each
+// miss costs the radix path), a 2^21-key one on none after the first
+// steps, at the price of twice the candidates (+3 us a call at 25.6e6).
+constexpr uint32_t kBracketNarrow = 1u << 20;
+constexpr uint32_t kBracketWide = 1u << 21;
+constexpr uint32_t kWideCalls = 16;
+// the extrapolated step is capped at kStepCap keys, or at kStepCapSteady
+// when the step before went the same way and at least half as far
+constexpr int64_t kStepCap = int64_t(1) << 18;
+constexpr int64_t kStepCapSteady = int64_t(1) << 21;
 constexpr uint32_t kHintMagic = 0x48494e54u;
 constexpr int kStagePairs = 1024;
 constexpr uint32_t kNoKey = 0xffffffffu;            // larger than every 31-bit key
@@ -85,7 +100,8 @@ struct TopkCtl {
     uint32_t bracket_on;  // pass 1 collected the bracket
     uint32_t above;       // bracket path: pairs pass 1 sent (key > hi)
     uint32_t ncand;       // bracket path: candidates collected
-    uint32_t pad[2];
+    uint32_t wide;        // 1: the bracket is kBracketWide keys wide
+    uint32_t pad;
     unsigned long long emit;   // pass 1: pairs above the bracket (count in the low bits)
     unsigned long long cand;   // pass 1: bracket candidates
     unsigned long long emit2;  // pairs appended after pass 1 (steps 3 and emit)
@@ -96,6 +112,8 @@ struct TopkCtl {
     uint32_t hint_key, hint_magic;
     uint32_t prev_key, prev_magic;
     uint32_t prev2_key, prev2_magic;
+    // calls left with the wide bracket (valid when wide_magic is set)
+    uint32_t wide_left, wide_magic;
 };
 static_assert(sizeof(TopkCtl) <= 256, "control block must fit its slot");
 constexpr int kCtlClearWords = offsetof(TopkCtl, hint_key) / 4;
@@ -104,8 +122,8 @@ static_assert(kCtlClearWords <= kBlock, "reset clears the control block with one
 
 constexpr size_t kCtlBytes = 256;
 // radix path: 1024 coarse + 2^20 fine bins for bits 19..0; bracket path:
-// 1024 coarse + 2^20 fine bins for key - lo
-constexpr size_t kHistWords = kBins1 + 2 * (kCoarse + size_t(kFine));
+// 1024 coarse + up to 2^21 fine bins for key - lo (the fine bins last)
+constexpr size_t kHistWords = kBins1 + 2 * size_t(kCoarse) + size_t(kFine) + size_t(kBracketWide);
 constexpr size_t kHistBytes = sizeof(uint32_t) * kHistWords;
 static_assert(kHistWords % 4 == 0, "histograms are cleared with 16-byte stores");
 
@@ -257,11 +275,16 @@ __device__ void select_bin(const uint32_t *hist, uint32_t need, uint32_t *s_scan
 }
 
 // Zeroes the control block (except the hints) and every histogram, and
-// forms the bracket: 2^20 keys centred on the threshold predicted from the
+// forms the bracket: 2^20 or 2^21 keys centred on the threshold predicted from the
 // last calls (the last threshold plus the last step in key space, the step
 // capped at 2^18 keys, or at 2^21 during a steady drift; the last threshold
 // alone when only one is known).  Grid-stride over the histogram words.
 __global__ __launch_bounds__(kBlock) void topk_reset_kernel(Workspace ws) {
+    // read by every workgroup (kept across calls; this launch writes none
+    // of them)
+    const bool hinted = ws.ctl->hint_magic == kHintMagic;
+    const bool wide = hinted && ws.ctl->wide_magic == kHintMagic && ws.ctl->wide_left > 0u;
+    const uint32_t width = wide ? kBracketWide : kBracketNarrow;
     if (blockIdx.x == 0) {
         uint32_t *w = reinterpret_cast<uint32_t *>(ws.ctl);
         if (int(threadIdx.x) < kCtlClearWords) w[threadIdx.x] = 0u;
@@ -270,9 +293,9 @@ __global__ __launch_bounds__(kBlock) void topk_reset_kernel(Workspace ws) {
             TopkCtl *c = ws.ctl;
             c->last = kNoKey;
             if (c->hint_magic == kHintMagic) {
-                // the step since the previous call, capped at a quarter of
+                // the step since the previous call, capped at an eighth of
                 // the bracket (so the last threshold stays inside it), or
-                // at twice the bracket when the step before went the same
+                // at the bracket's width when the step before went the same
                 // way and at least half as far: a steady drift of up to
                 // ~18 % in |p| per call is then followed
                 const int64_t h1 = int64_t(c->hint_key & 0x7fffffffu);
@@ -280,13 +303,13 @@ __global__ __launch_bounds__(kBlock) void topk_reset_kernel(Workspace ws) {
                 if (c->prev_magic == kHintMagic) {
                     const int64_t h0 = int64_t(c->prev_key & 0x7fffffffu);
                     int64_t step = h1 - h0;
-                    int64_t cap = int64_t(kFine / 4);
+                    int64_t cap = kStepCap;
                     if (c->prev2_magic == kHintMagic) {
                         const int64_t before = h0 - int64_t(c->prev2_key & 0x7fffffffu);
                         const bool same_way = (step > 0 && before > 0) || (step < 0 && before < 0);
                         const int64_t as = step < 0 ? -step : step;
                         const int64_t ab = before < 0 ? -before : before;
-                        if (same_way && 2 * ab >= as) cap = int64_t(kFine) * 2;
+                        if (same_way && 2 * ab >= as) cap = kStepCapSteady;
                     }
                     step = step > cap ? cap : (step < -cap ? -cap : step);
                     pred = h1 + step;
@@ -294,17 +317,20 @@ __global__ __launch_bounds__(kBlock) void topk_reset_kernel(Workspace ws) {
                     if (pred > 0x7fffffff) pred = 0x7fffffff;
                 }
                 const uint32_t p = uint32_t(pred);
-                const uint32_t lo = p > kFine / 2 ? p - kFine / 2 : 0u;
+                const uint32_t lo = p > width / 2 ? p - width / 2 : 0u;
                 c->last = uint32_t(h1);
                 c->lo = lo;
-                c->hi = lo + (kFine - 1);
+                c->hi = lo + (width - 1);
+                c->wide = wide ? 1u : 0u;
                 c->bracket_on = 1u;
             }
         }
     }
+    // the histograms up to the bracket's fine bins, and as many of those as
+    // the bracket has keys
     f32x4 *h4 = reinterpret_cast<f32x4 *>(ws.hist1);
     const f32x4 z = {0.0f, 0.0f, 0.0f, 0.0f};
-    const size_t n4 = kHistWords / 4;
+    const size_t n4 = (kHistWords - kBracketWide + (hinted ? width : 0u)) / 4;
     for (size_t i = size_t(blockIdx.x) * kBlock + threadIdx.x; i < n4;
          i += size_t(gridDim.x) * kBlock)
         h4[i] = z;
@@ -327,11 +353,12 @@ __device__ __forceinline__ void wave_aggregated_add(uint32_t *hist, uint32_t bin
     }
 }
 
-// Adds 1 to fine[(key - sub) mod 2^20] for every element (j, c) of this
+// Adds 1 to fine[(key - sub) mod kBins] for every element (j, c) of this
 // thread selected by bit 4*j + c of `mask`.  Each round takes the lowest
 // remaining selected element of every lane, so a wave runs as many rounds as
 // its fullest lane has selected elements (usually none or a few) instead of
 // one per element slot.  Called by all lanes.
+template <uint32_t kBins>
 __device__ __forceinline__ void fine_add_masked(uint32_t *fine, uint32_t mask,
                                                 const float (&p)[kVecPerThread][4],
                                                 uint32_t sub) {
@@ -349,7 +376,7 @@ __device__ __forceinline__ void fine_add_masked(uint32_t *fine, uint32_t mask,
                     if (b == 4 * j + c) x = p[j][c];
             key = magnitude_key(x);
         }
-        wave_aggregated_add(fine, (key - sub) & (kFine - 1), act);
+        wave_aggregated_add(fine, (key - sub) & (kBins - 1), act);
     }
 }
 
@@ -371,6 +398,8 @@ __global__ __launch_bounds__(kBlock) void topk_pass1_kernel(const float *__restr
     const int tid = threadIdx.x;
     const bool bracket = ws.ctl->bracket_on != 0u;
     const uint32_t lo = ws.ctl->lo, hi = ws.ctl->hi;
+    // coarse bins of 1024 or 2048 keys (kCoarse of them span the bracket)
+    const uint32_t coarse_shift = ws.ctl->wide != 0u ? 11u : 10u;
     for (int b = tid; b < kBins1; b += kBlock) sh.h[b] = 0u;
     for (int b = tid; b < kCoarse; b += kBlock) sh.coarse[b] = 0u;
     __syncthreads();
@@ -429,13 +458,13 @@ __global__ __launch_bounds__(kBlock) void topk_pass1_kernel(const float *__restr
                         const bool in = key >= lo && key <= hi;
                         m_above |= uint32_t(key > hi) << b;
                         m_inside |= uint32_t(in) << b;
-                        if (in) atomicAdd(&sh.coarse[(key - lo) / kFinePerCoarse], 1u);
+                        if (in) atomicAdd(&sh.coarse[(key - lo) >> coarse_shift], 1u);
                     }
                 }
             }
         }
         // fine bins in global memory: lanes with equal keys add together
-        if (bracket) fine_add_masked(ws.fine, m_inside, p, lo);
+        if (bracket) fine_add_masked<kBracketWide>(ws.fine, m_inside, p, lo);
         if (bracket) {
             stage_mask(sh.above, fill_above, m_above, p, tile0, &ws.ctl->emit, k, idx, val);
             stage_mask(sh.inside, fill_inside, m_inside, p, tile0, &ws.ctl->cand, ws.ccap,
@@ -480,7 +509,7 @@ __device__ void radix_refine20(const float *__restrict__ e, int64_t d, uint32_t 
                 under |= uint32_t(in) << (4 * j + c);
             }
         }
-        fine_add_masked(fine, under, v, 0u);
+        fine_add_masked<kFine>(fine, under, v, 0u);
     }
     __syncthreads();
     for (int b = tid; b < kCoarse; b += kBlock)
@@ -525,6 +554,14 @@ __global__ __launch_bounds__(kBlock) void topk_step3_kernel(float *__restrict__ 
     const uint64_t above = c->emit & kCountMask;
     const uint64_t inside = c->cand & kCountMask;
     bool fast = c->bracket_on != 0u && above <= k && above + inside >= k && inside <= ws.ccap;
+    if (lead) {
+        // the next calls' bracket width: wide for kWideCalls calls after the
+        // threshold fell outside this call's bracket
+        const bool outside = c->bracket_on != 0u && (above > k || above + inside < k);
+        const uint32_t left = c->wide_magic == kHintMagic ? c->wide_left : 0u;
+        c->wide_left = outside ? kWideCalls : (left > 0u ? left - 1u : 0u);
+        c->wide_magic = kHintMagic;
+    }
 
     // Bracket path: rank `need` among the candidates, coarse then fine.
     const uint32_t need = fast ? k - uint32_t(above) : 0u;
@@ -533,9 +570,15 @@ __global__ __launch_bounds__(kBlock) void topk_step3_kernel(float *__restrict__ 
         select_bin<kCoarse>(ws.coarse, need, ss.scan, ss.sel);
         const uint32_t cb = ss.sel[0], above_c = ss.sel[1];
         __syncthreads();
-        select_bin<kFinePerCoarse>(ws.fine + size_t(cb) * kFinePerCoarse, need - above_c, ss.scan,
-                                   ss.sel);
-        T = c->lo + cb * uint32_t(kFinePerCoarse) + ss.sel[0];
+        if (c->wide != 0u) {
+            constexpr int kPer = int(kBracketWide) / kCoarse;
+            select_bin<kPer>(ws.fine + size_t(cb) * kPer, need - above_c, ss.scan, ss.sel);
+            T = c->lo + cb * uint32_t(kPer) + ss.sel[0];
+        } else {
+            constexpr int kPer = int(kBracketNarrow) / kCoarse;
+            select_bin<kPer>(ws.fine + size_t(cb) * kPer, need - above_c, ss.scan, ss.sel);
+            T = c->lo + cb * uint32_t(kPer) + ss.sel[0];
+        }
         m = need - above_c - ss.sel[1];
         ties = ss.sel[2];
         __syncthreads();  // ss.sel is rewritten below
