@@ -368,7 +368,9 @@ def main():
     ws = efs.new_topk_workspace(d, k, dev)
     for s in range(args.warmup):
         efs.topk_compress(pool[s % len(pool)], e_tk, lr, k, tidx, tval, ws)
-    e_snap = e_tk.clone()
+    # the error vector and the workspace (its threshold history) as the timed
+    # steps found them, so that the replay below repeats those steps
+    e_snap, ws_snap = e_tk.clone(), ws.clone()
     mark()
     with Timer(torch, cur) as tt:
         for s in range(args.steps):
@@ -377,6 +379,7 @@ def main():
     tk_us = tt.us / args.steps
     # which selection each timed step took, and its time alone
     e_tk.copy_(e_snap)
+    ws.copy_(ws_snap)
     paths, tk_each = [], []
     for s in range(args.steps):
         with Timer(torch, cur) as t1:
@@ -385,7 +388,7 @@ def main():
         paths.append(efs.topk_took_bracket_path(ws))
     tk_ideal = 12.0 * d + 8.0 * k
     say("Top-k: %.1f us per step, bracket path in %d of %d" % (tk_us, sum(paths), len(paths)))
-    del e_snap, e_tk, tidx, tval, ws
+    del e_snap, ws_snap, e_tk, tidx, tval, ws
     torch.cuda.empty_cache()
 
     # copy probe over d elements (also the scale of the traffic counters)
