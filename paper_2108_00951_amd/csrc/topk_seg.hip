@@ -828,9 +828,10 @@ __device__ __forceinline__ void stage_tile(Stage &sg, uint32_t &efill, uint32_t 
 // index first); otherwise a radix select on the keys of its elements (bits
 // 30..20, 19..10, 9..0, histograms in LDS), the keys equal to the threshold
 // kept in index order.  The pairs are written to the segment's payload
-// region and e cleared at them (e already holds p).  `hist` is 2048 words
-// of zeroed LDS, zeroed again on return.  Called by every thread of the
-// workgroup.
+// region and e cleared at them (e already holds p).  Element (j, c) of a
+// thread is index block0 + tile_off(j, c), block0 being the segment's first
+// element.  `hist` is 2048 words of zeroed LDS, zeroed again on return.
+// Called by every thread of the workgroup.
 __device__ void select_in_tile(const float (&p)[kVecPerThread][4], uint32_t valid,
                                int64_t block0, const SegInfo &inf, uint32_t *hist,
                                uint32_t *s_wave, uint32_t *s_out, int32_t *idx, float *val,
