@@ -556,10 +556,12 @@ __global__ __launch_bounds__(kBlock) void topk_step3_kernel(float *__restrict__ 
     bool fast = c->bracket_on != 0u && above <= k && above + inside >= k && inside <= ws.ccap;
     if (lead) {
         // the next calls' bracket width: wide for kWideCalls calls after the
-        // threshold fell outside this call's bracket
+        // threshold fell outside this call's bracket, narrow at once after a
+        // bracket that held more keys than the candidate buffer
         const bool outside = c->bracket_on != 0u && (above > k || above + inside < k);
+        const bool overfull = c->bracket_on != 0u && inside > ws.ccap;
         const uint32_t left = c->wide_magic == kHintMagic ? c->wide_left : 0u;
-        c->wide_left = outside ? kWideCalls : (left > 0u ? left - 1u : 0u);
+        c->wide_left = outside ? kWideCalls : (overfull || left == 0u ? 0u : left - 1u);
         c->wide_magic = kHintMagic;
     }
 
