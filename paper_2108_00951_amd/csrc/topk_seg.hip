@@ -7,7 +7,8 @@
 // Work is cut into tiles: the 4096-element blocks of the vector, clipped to
 // each segment, so every tile belongs to one segment and every whole tile is
 // 16-byte aligned.  The two sweeps take short slices of consecutive tiles in
-// turn across the vector.  Five launches:
+// turn across the vector (longer ones with many segments).  Five launches
+// (six above 2048 segments, where the reset takes two):
 //
 //   reset    one workgroup checks the layout and forms the per-segment
 //            tables (tile ranges, payload offsets, candidate regions, the
@@ -36,9 +37,10 @@
 //            Bracket path, spread over the whole grid: e cleared at the pairs
 //            above the bracket; candidates in bins above da to the payload,
 //            those in bin da listed after the candidates.
-//   final    one workgroup per segment: among its candidates (radix path)
-//            bits 17..8, then 7..0 give the exact threshold T; among the keys
-//            of bin da (bracket path) the low bits of key - lo give it.  Then,
+//   final    per segment with work, by one of a grid of workgroups: among
+//            its candidates (radix path) bits 17..8, then 7..0 give the exact
+//            threshold T; among the keys of bin da (bracket path) the low
+//            bits of key - lo give it.  Then,
 //            when only some keys equal to T are kept, the lowest indices among
 //            them by a radix select on the index; emits, clears e, and keeps
 //            T as the next hint.  Scan mode does the same over the segment's
