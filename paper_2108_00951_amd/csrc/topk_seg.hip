@@ -12,12 +12,14 @@
 //
 //   reset    one workgroup checks the layout and forms the per-segment
 //            tables (tile ranges, payload offsets, candidate regions, the
-//            bracket); the others zero the per-segment histograms.
+//            bracket); the others zero the per-segment histograms (a light
+//            segment, below, only its bracket histogram).
 //   pass1    p = e + lr*g written into e (12 B/element, streamed with the
 //            non-temporal hint); LDS histogram of key
 //            bits 30..18 (8192 bins) per segment, flushed (non-zero bins) to
-//            the segment's global histogram.  A segment within one tile is
-//            selected right there.  With a bracket [lo, hi] around the
+//            the segment's global histogram, except for a light segment (a
+//            bracket and at most kLightTiles tiles).  A segment within one
+//            tile is selected right there.  With a bracket [lo, hi] around the
 //            segment's threshold predicted from its last three calls on this
 //            workspace (error feedback moves it little and smoothly; the
 //            bracket reaches 2^wl keys below the prediction and 2^wh above,
@@ -27,16 +29,18 @@
 //   select1  one workgroup per segment: when pass1 had a bracket and its
 //            counts prove the k-th key inside it, the bracket bin da holding
 //            it, and pass2's work items for the segment.  Otherwise the digit
-//            D1 holding the k-th key and the mode: none (k = 0), all
+//            D1 holding the k-th key (for a light segment from a histogram
+//            select1 forms from its elements) and the mode: none (k = 0), all
 //            (k = size), candidates (the keys in D1 fit the segment's
 //            candidate region) or scan (they do not: a large set of equal or
 //            nearly equal magnitudes).
 //   pass2    radix path, a read of p (4 B/element): keys above D1 go to the
 //            payload and their e to +0 (mode all: every key); keys in D1 are
 //            appended to the candidate region and histogrammed by bits 17..8.
-//            Bracket path, spread over the whole grid: e cleared at the pairs
-//            above the bracket; candidates in bins above da to the payload,
-//            those in bin da listed after the candidates.
+//            Bracket path, spread over the whole grid, one work item per
+//            wave: e cleared at the pairs above the bracket; candidates in
+//            bins above da to the payload, those in bin da listed after the
+//            candidates.
 //   final    per segment with work, by one of a grid of workgroups: among
 //            its candidates (radix path) bits 17..8, then 7..0 give the exact
 //            threshold T; among the keys of bin da (bracket path) the low
@@ -76,6 +80,18 @@ enum : uint32_t {
     kModeDone = 5  // a segment within one tile, selected entirely in pass1
 };
 
+// SegState::bracket: 0 none, kBracketFull a bracket with the digit-1
+// histogram kept as well, kBracketLight a bracket alone.  A segment of at
+// most kLightTiles tiles with a bracket is light: pass1 keeps no digit-1
+// histogram for it and the reset zeroes only its 4 KiB bracket histogram
+// (32 KiB less per layer to clear each call, the larger part of the reset
+// with thousands of layers, and no histogram flush in pass1).  When its
+// bracket misses, select1 forms the digit-1 histogram from the segment's
+// elements (at most kLightTiles * kTile of them, one sweep by the
+// segment's workgroup) and the radix path follows as for any other miss.
+constexpr uint32_t kBracketFull = 1u, kBracketLight = 2u;
+constexpr uint32_t kLightTiles = 4;
+
 // log2 of how far the bracket reaches below and above the predicted
 // threshold, each adapted per segment between these (2^19 keys are 3-6 % of
 // |p|, 2^12 keys 0.02-0.05 %)
@@ -84,7 +100,10 @@ constexpr uint32_t kWidthMax = 19, kWidthMin = 12, kWidthStart = 17;
 // (a steady drift), narrow otherwise (a jump is not repeated)
 constexpr int64_t kMaxStep = 1 << 22, kMaxStepUnsure = 1 << 18;
 constexpr int kFineBins = 1024;                // bracket histogram: the bracket in 1024 bins
-constexpr uint32_t kChunk = 2048;              // pass2 work item: payload slots or candidates
+// pass2 work item: payload slots or candidates, one wave's worth (kWorkPerLane
+// a lane); a workgroup's four waves take four items at once
+constexpr int kWorkPerLane = 8;
+constexpr uint32_t kChunk = kWorkPerLane * kWave;
 // The sweeps take slices of `slice` consecutive tiles (at most
 // kSliceTilesMax), slice b + i * grid for workgroup b: the resident
 // workgroups stream one compact window of the vector at a time (measured
@@ -176,6 +195,19 @@ __device__ __forceinline__ SegHint next_hint(const SegHint &old, uint32_t T, uin
     h.magic = kHintMagic;
     h.width = width;
     return h;
+}
+
+// The reset forms a bracket for a segment from its hint when the segment
+// spans several tiles, keeps some but not all of its elements, and the
+// hint is well formed.
+__device__ __forceinline__ bool hint_usable(const SegHint &h) {
+    return h.magic == kHintMagic && h.key <= 0x7fffffffu && h.prev <= 0x7fffffffu &&
+           h.prev2 <= 0x7fffffffu && widths_ok(h.width);
+}
+__device__ __forceinline__ uint32_t bracket_kind(uint32_t ntiles, int64_t keff, int64_t size,
+                                                 const SegHint &h) {
+    if (!(ntiles > 1u && keff > 0 && keff < size && hint_usable(h))) return 0u;
+    return ntiles <= kLightTiles ? kBracketLight : kBracketFull;
 }
 
 struct SegWs {
@@ -492,8 +524,8 @@ __device__ __forceinline__ Sums reset_chunk(const SegWs &ws, const SegIn &in, in
         ws.info[s] = inf;
         ws.tile_prefix[s] = uint32_t(carry.t + ex.t);
         SegState z = {};
-        if (nt > 1u && keff > 0 && keff < size && h.magic == kHintMagic && h.key <= 0x7fffffffu &&
-            h.prev <= 0x7fffffffu && h.prev2 <= 0x7fffffffu && widths_ok(h.width)) {
+        const uint32_t kind = bracket_kind(nt, keff, size, h);
+        if (kind != 0u) {
             // last threshold plus the last step (capped): error feedback
             // makes thresholds drift smoothly from call to call
             const int64_t last = int64_t(h.key) - int64_t(h.prev);
@@ -503,7 +535,7 @@ __device__ __forceinline__ Sums reset_chunk(const SegWs &ws, const SegIn &in, in
             const int64_t cap = steady ? kMaxStep : kMaxStepUnsure;
             const int64_t step = max(-cap, min(cap, last));
             const int64_t pred = max(int64_t(0), min(int64_t(0x7fffffff), int64_t(h.key) + step));
-            z.bracket = 1u;
+            z.bracket = kind;
             z.lo = uint32_t(max(int64_t(0), pred - (int64_t(1) << width_lo(h.width))));
             z.hi = uint32_t(min(pred + (int64_t(1) << width_hi(h.width)) - 1, int64_t(0x7fffffff)));
             // hi - lo + 1 <= 2^20 keys in kFineBins bins
@@ -517,20 +549,30 @@ __device__ __forceinline__ Sums reset_chunk(const SegWs &ws, const SegIn &in, in
 
 // Zeroes the sweep flags and the histograms of the layers that span more
 // than one tile (a one-tile layer is selected inside pass1), workgroup w of
-// nw; an invalid layout is rejected, so what is zeroed for it does not
-// matter.
-__device__ __forceinline__ void reset_zero(const SegWs &ws, const int64_t *off, int32_t nseg,
-                                           int32_t w, int32_t nw) {
+// nw: the digit-1 histogram unless the layer is light this call (the table
+// workgroup decides that from the same hint), and the bracket or digit-2
+// histogram.  An invalid layout is rejected, so what is zeroed for it does
+// not matter.
+__device__ __forceinline__ void reset_zero(const SegWs &ws, const int64_t *off,
+                                           const int64_t *kin, int32_t nseg, int32_t w,
+                                           int32_t nw) {
     const f32x4 z = {0.0f, 0.0f, 0.0f, 0.0f};
     f32x4 *fl = reinterpret_cast<f32x4 *>(ws.sweep);
     for (int q = w * kResetBlock + threadIdx.x; q < kSweepGroups / 4; q += nw * kResetBlock)
         fl[q] = z;
     for (int32_t sg = w; sg < nseg; sg += nw) {
         const int64_t lo = off[sg], size = off[sg + 1] - lo;
-        if (size < 0 || segment_tiles(lo, size) <= 1) continue;
-        f32x4 *h1 = reinterpret_cast<f32x4 *>(ws.hist1 + int64_t(sg) * kDigit1);
+        if (size < 0) continue;
+        const uint32_t nt = uint32_t(segment_tiles(lo, size));
+        if (nt <= 1u) continue;
+        const int64_t kk = kin[sg];
+        const int64_t keff = kk < size ? kk : size;
+        const bool light = bracket_kind(nt, keff, size, ws.hint[sg]) == kBracketLight;
         f32x4 *h2 = reinterpret_cast<f32x4 *>(ws.hist2 + int64_t(sg) * kDigit2);
-        for (int q = threadIdx.x; q < kDigit1 / 4; q += kResetBlock) h1[q] = z;
+        if (!light) {
+            f32x4 *h1 = reinterpret_cast<f32x4 *>(ws.hist1 + int64_t(sg) * kDigit1);
+            for (int q = threadIdx.x; q < kDigit1 / 4; q += kResetBlock) h1[q] = z;
+        }
         for (int q = threadIdx.x; q < kDigit2 / 4; q += kResetBlock) h2[q] = z;
     }
 }
@@ -562,7 +604,7 @@ __global__ __launch_bounds__(kResetBlock) void seg_reset_kernel(SegWs ws,
                                                                 int32_t nseg, int64_t d,
                                                                 int64_t k_total) {
     if (blockIdx.x > 0) {
-        reset_zero(ws, off, nseg, int32_t(blockIdx.x) - 1, int32_t(gridDim.x) - 1);
+        reset_zero(ws, off, kin, nseg, int32_t(blockIdx.x) - 1, int32_t(gridDim.x) - 1);
         return;
     }
     __shared__ Sums s_wave[kResetWaves];
@@ -607,7 +649,8 @@ __global__ __launch_bounds__(kResetBlock) void seg_reset_sums_kernel(SegWs ws,
                                                                      int32_t nseg, int64_t d,
                                                                      int32_t nchunks) {
     if (int32_t(blockIdx.x) >= nchunks) {
-        reset_zero(ws, off, nseg, int32_t(blockIdx.x) - nchunks, int32_t(gridDim.x) - nchunks);
+        reset_zero(ws, off, kin, nseg, int32_t(blockIdx.x) - nchunks,
+                   int32_t(gridDim.x) - nchunks);
         return;
     }
     __shared__ Sums s_wave[kResetWaves];
@@ -974,8 +1017,9 @@ __device__ void pass1_slice(const float *__restrict__ g, float *__restrict__ e, 
                 flush_emit(sg, efill, st, inf, idx, val);
                 flush_cand(sg, cfill, st, inf, ws.cand, fine);
             }
-            // a one-tile segment leaves the LDS histogram zero
-            if (inf.ntiles > 1) flush_hist(hist, kDigit1, ws.hist1 + int64_t(s) * kDigit1);
+            // a one-tile or a light segment leaves the LDS histogram zero
+            if (inf.ntiles > 1 && bracket != kBracketLight)
+                flush_hist(hist, kDigit1, ws.hist1 + int64_t(s) * kDigit1);
             s = segment_after(ws.tile_prefix, nseg, s, t);
             next = ws.tile_prefix[s + 1];
             inf = ws.info[s];
@@ -1039,6 +1083,7 @@ __device__ void pass1_slice(const float *__restrict__ g, float *__restrict__ e, 
             }
         }
         uint32_t emit_mask = 0, cand_mask = 0;
+        const bool digits = bracket != kBracketLight;
 #pragma unroll
         for (int j = 0; j < kVecPerThread; ++j) {
             if (!__any(((valid >> (4 * j)) & 0xfu) != 0u)) continue;  // none in this wave
@@ -1047,7 +1092,7 @@ __device__ void pass1_slice(const float *__restrict__ g, float *__restrict__ e, 
                 const uint32_t bit = 1u << (4 * j + c);
                 if (!(valid & bit)) continue;
                 const uint32_t key = magnitude_key(p[j][c]);
-                atomicAdd(&hist[key >> kShift1], 1u);
+                if (digits) atomicAdd(&hist[key >> kShift1], 1u);
                 if (key > hi) emit_mask |= bit;
                 else if (key >= lo) cand_mask |= bit;
             }
@@ -1063,7 +1108,8 @@ __device__ void pass1_slice(const float *__restrict__ g, float *__restrict__ e, 
         flush_emit(sg, efill, st, inf, idx, val);
         flush_cand(sg, cfill, st, inf, ws.cand, fine);
     }
-    if (inf.ntiles > 1) flush_hist(hist, kDigit1, ws.hist1 + int64_t(s) * kDigit1);
+    if (inf.ntiles > 1 && bracket != kBracketLight)
+        flush_hist(hist, kDigit1, ws.hist1 + int64_t(s) * kDigit1);
     __syncthreads();  // the next slice starts with another segment's state
 }
 
@@ -1123,7 +1169,60 @@ __device__ void choose_digit1(const SegWs &ws, int32_t s, const SegInfo &inf, Se
     if (sweep) mark_sweep(ws, inf);
 }
 
-__device__ void select1_segment(const SegWs &ws, int32_t s, uint32_t *s_wave, uint32_t *s_out) {
+// The digit-1 histogram of a light segment whose bracket missed (pass1 kept
+// none for it), formed from its elements: e holds p everywhere in the
+// segment, since pass1 clears e only once the bracket is confirmed.  The
+// counts are at most kLightTiles * kTile, so two 16-bit counts share an LDS
+// word (16 KiB); the 8192 bins are then stored whole into the segment's
+// global histogram, which choose_digit1 reads.  One sweep of e in 16-byte
+// vectors (the few elements before the first 16-byte boundary and after the
+// last one at a time).  Called by every thread of the workgroup.
+__device__ void light_digit1(const SegWs &ws, const float *__restrict__ e, const SegInfo &inf,
+                             int32_t s, uint32_t *pack) {
+    const uint32_t tid = threadIdx.x;
+    for (uint32_t b = tid; b < uint32_t(kDigit1 / 2); b += kBlock) pack[b] = 0u;
+    __syncthreads();
+    const float *seg = e + inf.off;
+    const uint32_t n = uint32_t(inf.size);
+    // seg + h is the first 16-byte boundary at or after seg (e is 4-byte aligned)
+    const uint32_t h = min(n, uint32_t(((16u - (reinterpret_cast<uintptr_t>(seg) & 15u)) & 15u) / 4u));
+    const uint32_t nv = (n - h) / 4u;
+    const uint32_t t0 = h + 4u * nv;
+    for (uint32_t i = tid; i < h + (n - t0); i += kBlock) {
+        const uint32_t d1 = magnitude_key(seg[i < h ? i : t0 + (i - h)]) >> kShift1;
+        atomicAdd(&pack[d1 >> 1], 1u << (16u * (d1 & 1u)));
+    }
+    const f32x4 *v4 = reinterpret_cast<const f32x4 *>(seg + h);
+    constexpr uint32_t kV = 4;  // 16-byte loads per thread in flight
+    for (uint32_t base = 0; base < nv; base += kV * kBlock) {
+        f32x4 x[kV];
+#pragma unroll
+        for (uint32_t u = 0; u < kV; ++u) {
+            const uint32_t q = base + u * kBlock + tid;
+            if (q < nv) x[u] = v4[q];
+        }
+#pragma unroll
+        for (uint32_t u = 0; u < kV; ++u) {
+            if (base + u * kBlock + tid < nv) {
+#pragma unroll
+                for (int c = 0; c < 4; ++c) {
+                    const uint32_t d1 = magnitude_key(x[u][c]) >> kShift1;
+                    atomicAdd(&pack[d1 >> 1], 1u << (16u * (d1 & 1u)));
+                }
+            }
+        }
+    }
+    __syncthreads();
+    uint2 *h1 = reinterpret_cast<uint2 *>(ws.hist1 + int64_t(s) * kDigit1);
+    for (uint32_t b = tid; b < uint32_t(kDigit1 / 2); b += kBlock) {
+        const uint32_t v = pack[b];
+        h1[b] = make_uint2(v & 0xffffu, v >> 16);
+    }
+    __syncthreads();  // the workgroup reads the histogram back
+}
+
+__device__ void select1_segment(const SegWs &ws, const float *__restrict__ e, int32_t s,
+                                uint32_t *s_wave, uint32_t *s_out, uint32_t *s_pack) {
     const SegInfo inf = ws.info[s];
     SegState *st = ws.st + s;
     if (inf.ntiles <= 1) {  // selected in pass1 (or empty)
@@ -1195,16 +1294,18 @@ __device__ void select1_segment(const SegWs &ws, int32_t s, uint32_t *s_wave, ui
             st->miss = int64_t(cur.emit) > inf.k ? 2u
                        : (int64_t(cur.emit) + cur.ccur < inf.k ? 1u : 3u);
     }
+    if (cur.bracket == kBracketLight) light_digit1(ws, e, inf, s, s_pack);
     choose_digit1(ws, s, inf, st, s_wave, s_out);
 }
 
 // One workgroup per segment (a loop over segments per workgroup serialises
 // their latencies: measured slower with thousands of segments).
-__global__ __launch_bounds__(kBlock) void seg_select1_kernel(SegWs ws) {
+__global__ __launch_bounds__(kBlock) void seg_select1_kernel(SegWs ws, const float *__restrict__ e) {
     __shared__ uint32_t s_wave[kWaves];
     __shared__ uint32_t s_out[3];
+    __shared__ uint32_t s_pack[kDigit1 / 2];
     if (ws.ctl->status != 0u) return;
-    select1_segment(ws, int32_t(blockIdx.x), s_wave, s_out);
+    select1_segment(ws, e, int32_t(blockIdx.x), s_wave, s_out, s_pack);
 }
 
 // ---------------------------------------------------------------------------
@@ -1300,31 +1401,35 @@ __device__ void pass2_tiles(float *__restrict__ e, int32_t *__restrict__ idx,
     if (dirty) flush_hist(hist, kDigit2, ws.hist2 + int64_t(s) * kDigit2);
 }
 
-// One work item of a segment on the bracket path (select1 lists them):
+// One work item of a segment on the bracket path (select1 lists them), run
+// by one wave (the four waves of a workgroup take four items at once, so a
+// workgroup's items cost a quarter of the dependent round trips in turn):
 //   kind 0: payload slots [first, first + kChunk) of the pairs above the
 //           bracket: their e is cleared (pass1 left it for a fallback);
 //   kind 1: candidates [first, first + kChunk): bins above da to the payload
-//           (e cleared), bin da appended to the list after the candidates.
+//           (e cleared), bin da appended to the list after the candidates,
+//           kWorkPerLane per lane behind one pair of atomics.
+
 __device__ void bracket_work(uint2 item, float *__restrict__ e, int32_t *__restrict__ idx,
-                             float *__restrict__ val, const SegWs &ws, Stage &sg) {
+                             float *__restrict__ val, const SegWs &ws) {
     const int32_t s = int32_t(item.x & 0x7fffffffu);
     const uint32_t first = item.y;
+    const uint32_t lane = threadIdx.x & (kWave - 1);
     const SegInfo inf = ws.info[s];
     SegState *st = ws.st + s;
     if (!(item.x >> 31)) {
         const uint32_t end = min(first + kChunk, st->ecut);
-        for (uint32_t q = first + threadIdx.x; q < end; q += kBlock) e[idx[inf.kout + q]] = 0.0f;
+        for (uint32_t q = first + lane; q < end; q += kWave) e[idx[inf.kout + q]] = 0.0f;
         return;
     }
-    constexpr int kPer = kChunk / kBlock;
     const uint32_t lo = st->lo, shift = st->shift, da = st->da, ccur = st->ccur;
     const uint32_t end = min(first + kChunk, ccur);
     const uint2 *cand = ws.cand + inf.coff;
-    uint2 v[kPer];
+    uint2 v[kWorkPerLane];
     uint32_t keep = 0u, tie = 0u;
 #pragma unroll
-    for (int u = 0; u < kPer; ++u) {
-        const uint32_t q = first + uint32_t(u * kBlock) + threadIdx.x;
+    for (int u = 0; u < kWorkPerLane; ++u) {
+        const uint32_t q = first + uint32_t(u * kWave) + lane;
         v[u] = make_uint2(0u, 0u);
         if (q < end) {
             v[u] = cand[q];
@@ -1334,18 +1439,17 @@ __device__ void bracket_work(uint2 item, float *__restrict__ e, int32_t *__restr
         }
     }
     uint32_t tk, tt;
-    uint32_t pk = block_prefix_small(uint32_t(__popc(keep)), sg.wave, tk);
-    uint32_t pt = block_prefix_small(uint32_t(__popc(tie)), sg.wave, tt);
-    if (threadIdx.x == 0) {
-        sg.wave[0] = tk ? atomicAdd(&st->emit, tk) : 0u;
-        sg.wave[1] = tt ? atomicAdd(&st->tcur, tt) : 0u;
+    uint32_t pk = wave_prefix_small(uint32_t(__popc(keep)), tk);
+    uint32_t pt = wave_prefix_small(uint32_t(__popc(tie)), tt);
+    uint32_t bk = 0u, bt = 0u;
+    if (lane == 0u) {
+        bk = tk ? atomicAdd(&st->emit, tk) : 0u;
+        bt = tt ? atomicAdd(&st->tcur, tt) : 0u;
     }
-    __syncthreads();
-    pk += sg.wave[0];
-    pt += sg.wave[1];
-    __syncthreads();  // sg.wave is reused by the next item
+    pk += uint32_t(__shfl(int(bk), 0));
+    pt += uint32_t(__shfl(int(bt), 0));
 #pragma unroll
-    for (int u = 0; u < kPer; ++u) {
+    for (int u = 0; u < kWorkPerLane; ++u) {
         if ((keep >> u) & 1u) {
             if (int64_t(pk) < inf.k) {
                 idx[inf.kout + pk] = int32_t(v[u].y);
@@ -1398,7 +1502,8 @@ __global__ __launch_bounds__(kBlock) void seg_pass2_kernel(float *__restrict__ e
         const uint32_t pos = block_prefix_small(use ? 1u : 0u, sg.wave, n_use);
         if (use) list[pos] = item;
         __syncthreads();
-        for (uint32_t q = 0; q < n_use; ++q) bracket_work(list[q], e, idx, val, ws, sg);
+        for (uint32_t q = threadIdx.x / kWave; q < n_use; q += kWaves)
+            bracket_work(list[q], e, idx, val, ws);
         __syncthreads();  // the list is rewritten by the next round
     }
 }
@@ -1712,7 +1817,7 @@ hipError_t launch_topk_segmented(const float *g, float *e, int64_t d, float lr, 
         seg_pass1_kernel<true><<<grid, kBlock, 0, stream>>>(g, e, lr, idx, val, nseg, ws, uint32_t(slice));
     else
         seg_pass1_kernel<false><<<grid, kBlock, 0, stream>>>(g, e, lr, idx, val, nseg, ws, uint32_t(slice));
-    seg_select1_kernel<<<uint32_t(nseg), kBlock, 0, stream>>>(ws);
+    seg_select1_kernel<<<uint32_t(nseg), kBlock, 0, stream>>>(ws, e);
     if (aligned)
         seg_pass2_kernel<true><<<grid, kBlock, 0, stream>>>(e, idx, val, nseg, ws, uint32_t(slice));
     else

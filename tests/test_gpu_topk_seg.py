@@ -423,6 +423,46 @@ def test_segmented_bracket_from_another_scale_falls_back():
     assert hits[2] == ks.size
 
 
+def test_segmented_light_layers_miss_their_brackets():
+    # layers of two to four tiles starting anywhere in a block (the sizes
+    # whose bracket path keeps no digit-1 histogram), error feedback carried:
+    # the thresholds grow over the first steps and leave the brackets, settle
+    # on one scale, then a 30x jump puts every threshold above its bracket,
+    # a 100x drop follows and a quantised step ties many keys; a missed
+    # layer's digit-1 histogram then comes from its elements.  Every step
+    # against the oracle
+    rng = np.random.default_rng(4242)
+    sizes = rng.integers(4097, 3 * 4096 + 4000, size=60)
+    sizes[::7] = rng.integers(1, 4000, size=sizes[::7].size)   # one-tile layers among them
+    off = np.concatenate([[0], np.cumsum(sizes)]).astype(np.int64)
+    d = int(off[-1])
+    ks = synth.layerwise_k(off, 0.01)
+    k_total = int(ks.sum())
+    ws = efs.new_topk_segmented_workspace(ks.size, k_total, DEV)
+    e = np.zeros(d, np.float32)
+    scales = [1.0] * 8 + [30.0] * 3 + [0.01, 1.0]
+    hits = []
+    say("segmented light layers d=%d nseg=%d" % (d, ks.size))
+    for t, sc in enumerate(scales):
+        g = (synth.small_gradient(4300 + t, d) * np.float32(sc)).astype(np.float32)
+        if t == len(scales) - 1:
+            g = (np.round(g / np.float32(4e-4)) * np.float32(4e-4)).astype(np.float32)
+        gi, gv, ge, _ = run_gpu(g, e, off, ks, k_total=k_total, ws=ws)
+        assert efs.topk_segmented_status(ws) == 0
+        ri, rv, re = oracle.topk_segmented(g, e, LR, off, ks)
+        order = np.lexsort((gi, np.repeat(np.arange(ks.size), np.minimum(ks, sizes))))
+        np.testing.assert_array_equal(gi[order], ri, "t=%d indices" % t)
+        assert_bits_equal(gv[order], rv, "t=%d values" % t)
+        assert_bits_equal(ge, re, "t=%d e'" % t)
+        e = re
+        hits.append(efs.topk_segmented_bracket_segments(ws))
+        say("  step %d scale %g ok (bracket in %d layers)" % (t, sc, hits[-1]))
+    multi = int(np.sum(sizes > 4096))
+    assert min(hits[1:4]) < multi // 4   # growing thresholds: most brackets missed
+    assert hits[7] > multi // 2          # settled on one scale: brackets hold
+    assert hits[8] < multi // 4          # the jump: most brackets missed
+
+
 @pytest.mark.parametrize("levels", [4, 1000])
 def test_segmented_many_small_layers(levels):
     # hundreds of layers that fit in one 4096-element tile (selected inside
