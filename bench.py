@@ -111,6 +111,12 @@ def parse():
                          "hard-threshold launches")
     ap.add_argument("--parse-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
                     help="summarise two rocprofv3 --pmc output folders and exit")
+    ap.add_argument("--layerwise-only", action="store_true",
+                    help="time only the 20,000-layer layer-wise Top-k and print its figures "
+                         "(not the contract line)")
+    ap.add_argument("--trace-last", type=int, metavar="N",
+                    help="with --parse-trace: per-kernel statistics over each kernel's last N "
+                         "dispatches only (the timed calls of a run that times N)")
     return ap.parse_args()
 
 
@@ -205,6 +211,26 @@ def parse_trace(folder, steps):
     return "\n".join(lines) + "\n"
 
 
+def parse_trace_last(folder, n):
+    """Per-kernel duration statistics of a rocprofv3 kernel trace over the
+    last `n` dispatches of each kernel (every kernel of a run that ends with
+    n timed calls)."""
+    trace = list(csv.DictReader(open(os.path.join(folder, "run_kernel_trace.csv"))))
+    trace.sort(key=lambda r: int(r["Start_Timestamp"]))
+    by = {}
+    for r in trace:
+        us = (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3
+        by.setdefault(_short_kernel_name(r["Kernel_Name"]), []).append(us)
+    lines = ["%-36s %6s %9s %9s %9s" % ("kernel", "calls", "avg_us", "min_us", "max_us")]
+    rows = []
+    for name, xs in by.items():
+        x = xs[-n:]
+        rows.append((sum(x) / len(x), name, len(x), min(x), max(x)))
+    for avg, name, cnt, lo, hi in sorted(rows, reverse=True):
+        lines.append("%-36s %6d %9.2f %9.2f %9.2f" % (name, cnt, avg, lo, hi))
+    return "\n".join(lines) + "\n"
+
+
 def format_traffic(res, workload, args):
     lines = ["# HBM traffic of %s per launch from rocprofv3 counters, %s" % (HT_PLAIN, workload),
              "# (KiB per dispatch, averaged over the kernel's first %d dispatches, the"
@@ -291,7 +317,10 @@ def main():
         sys.stdout.write(format_traffic(res, wl.name, args))
         return
     if args.parse_trace:
-        sys.stdout.write(parse_trace(args.parse_trace, args.steps))
+        if args.trace_last:
+            sys.stdout.write(parse_trace_last(args.parse_trace, args.trace_last))
+        else:
+            sys.stdout.write(parse_trace(args.parse_trace, args.steps))
         return
 
     import torch
@@ -302,6 +331,9 @@ def main():
     torch.cuda.set_device(dev)
     efs.load_library()
     cur = torch.cuda.current_stream()
+    if args.layerwise_only:
+        print(json.dumps(bench_many_layers(efs, torch, synth, cur)), flush=True)
+        return
     lr = synth.LR
     if args.pool is None:
         args.pool = 2 if d >= 100_000_000 else 4
@@ -446,6 +478,7 @@ def main():
     }
     if not args.no_extra:
         line["extra"] = {"segments_25.6m": bench_segments(efs, torch, synth, cur, threads),
+                         "layerwise_20000_layers": bench_many_layers(efs, torch, synth, cur),
                          "sparse_apply_8_workers": average.pop("_apply", None)}
     average.pop("_apply", None)
     if not args.no_cpu:
@@ -592,6 +625,45 @@ def bench_segments(efs, torch, synth, cur, threads):
         **rate(12.0 * d + 8.0 * kt, us)}
     say("25.6e6 workload: %s" % res)
     del pool, e, idx, val, ws, sws
+    torch.cuda.empty_cache()
+    return res
+
+
+def bench_many_layers(efs, torch, synth, cur):
+    """Layer-wise Top-k over a model with 20,000 tensors: d = 25,600,000 split
+    into 20,000 layers of log-uniform sizes (1 to 10^4 before scaling to d),
+    k_s = ceil(0.1 % of each layer), Gaussian gradients; K = 20 back-to-back
+    error-feedback steps on four gradients in turn after 30 untimed steps."""
+    import numpy as np
+    d, nseg = 25_600_000, 20_000
+    sizes = synth.segment_sizes(7, nseg, d, lo=1.0, hi=1e4)
+    off = np.concatenate([[0], np.cumsum(sizes)]).astype(np.int64)
+    ks = synth.layerwise_k(off, 0.001)
+    kt = int(ks.sum())
+    pool = [torch.from_numpy(synth.small_gradient(3000 + t, d)).to("cuda") for t in range(4)]
+    lr = synth.LR
+    reps, pre = 20, 30
+    e = torch.zeros(d, dtype=torch.float32, device="cuda")
+    sidx = torch.empty(kt, dtype=torch.int32, device="cuda")
+    sval = torch.empty(kt, dtype=torch.float32, device="cuda")
+    sws = efs.new_topk_segmented_workspace(nseg, kt, "cuda")
+    offd = torch.from_numpy(off).to("cuda")
+    kd = torch.from_numpy(ks).to("cuda")
+    for s in range(pre):
+        efs.topk_segmented_compress(pool[s % 4], e, lr, offd, kd, sidx, sval, sws)
+    with Timer(torch, cur) as t:
+        for s in range(reps):
+            efs.topk_segmented_compress(pool[s % 4], e, lr, offd, kd, sidx, sval, sws)
+    us = t.us / reps
+    # layers touching more than one 4096-element block of the vector
+    first, last = off[:-1] // 4096, (off[1:] - 1) // 4096
+    multi = int(np.sum((sizes > 0) & (last > first)))
+    res = {"d": d, "segments": nseg, "multi_tile_segments": multi,
+           "k_total": kt, "us": round(us, 2),
+           "bracket_segments_last_call": efs.topk_segmented_bracket_segments(sws),
+           **rate(12.0 * d + 8.0 * kt, us)}
+    say("20,000-layer layer-wise Top-k: %s" % res)
+    del pool, e, sidx, sval, sws
     torch.cuda.empty_cache()
     return res
 

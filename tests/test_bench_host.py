@@ -107,3 +107,19 @@ def test_more_than_one_gpu_is_refused():
     assert r.returncode == 2
     assert "one GPU" in r.stderr
     assert r.stdout == ""
+
+
+def test_parse_trace_last_takes_each_kernels_last_dispatches(tmp_path):
+    # warm-up calls slower than the timed ones: only each kernel's last n
+    # dispatches count, and kernels are ordered by their average
+    P1 = "void efs::(anonymous namespace)::seg_pass1_kernel<true>(float const*, float*)"
+    FIN = "void efs::(anonymous namespace)::seg_final_kernel<3840>(float*, int*)"
+    seq = []
+    for _ in range(5):
+        seq += [(P1, 900_000), (FIN, 400_000)]
+    for d in (100_000, 120_000, 110_000):
+        seq += [(P1, d), (FIN, 40_000)]
+    _trace(str(tmp_path), seq)
+    out = bench.parse_trace_last(str(tmp_path), 3).splitlines()
+    assert out[1].split() == ["seg_pass1_kernel<true>", "3", "110.00", "100.00", "120.00"]
+    assert out[2].split() == ["seg_final_kernel<3840>", "3", "40.00", "40.00", "40.00"]
