@@ -200,6 +200,28 @@ def small_gradient(seed: int, d: int, scale: float = 1e-3) -> np.ndarray:
     return (rng.standard_normal(d, dtype=np.float32) * np.float32(scale))
 
 
+def long_gradient(seed: int, d: int, scale: float = 1e-3, threads: int = 1) -> np.ndarray:
+    """A Gaussian vector of any length (tests up to 2^31 - 1 elements),
+    N(0, scale^2) in float32, drawn per BLOCK elements each from its own
+    seed, `threads` blocks at a time."""
+    out = np.empty(d, dtype=np.float32)
+
+    def one(b):
+        lo, hi = b * BLOCK, min(d, (b + 1) * BLOCK)
+        _rng(10, seed, b).standard_normal(out=out[lo:hi], dtype=np.float32)
+        out[lo:hi] *= np.float32(scale)
+
+    blocks = range((d + BLOCK - 1) // BLOCK)
+    if threads > 1:
+        from concurrent.futures import ThreadPoolExecutor
+        with ThreadPoolExecutor(threads) as ex:
+            list(ex.map(one, blocks))
+    else:
+        for b in blocks:
+            one(b)
+    return out
+
+
 LAMBDA_FILE = "workload_lambdas.json"
 
 
