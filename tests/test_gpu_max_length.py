@@ -1,8 +1,9 @@
 """GPU parity at the largest vector length the ABI takes, d = 2^31 - 1
 (int32 indices; 8.6 GB per fp32 vector): the hard threshold over two
 error-feedback steps, the flat Top-k on its radix path and then from its
-bracket, and the average of their two payloads, each against the oracle
-chunk by chunk.  Large magnitudes are planted at the last elements of the
+bracket, the layer-wise Top-k over five layers (first call and a later one
+from the brackets), and the average of the first two payloads, each against
+the oracle chunk by chunk.  Large magnitudes are planted at the last elements of the
 vector (the ragged last tile) and around the last 4096-element boundary, so
 that pairs with the largest indices are kept."""
 import os
@@ -112,7 +113,47 @@ def test_vector_of_two_to_the_31_minus_one_elements():
                                         cap=0, mt=True)[2],
         e_next_fn=lambda lo, hi: et[lo:hi].cpu().numpy(), chunk=CHUNK)
     say(t0, "Top-k bracket path ok (call %d)" % t)
-    del et, e_before, ws, g_dev
+    del et, ws
+    torch.cuda.empty_cache()
+
+    # layer-wise Top-k: a one-element layer, a light two-tile layer, a
+    # one-tile layer and two layers of about 10^9 elements; the first call
+    # ranks every layer by its radix path, a later call (e carried) selects
+    # the large layers from their brackets; each layer checked chunk by chunk
+    off = np.array([0, 1, 1 + 4097, 1 + 4097 + 1000, 1_000_000_000, D], dtype=np.int64)
+    ks = np.array([1, 10, 5, 700, 1500], dtype=np.int64)
+    kt = int(ks.sum())
+    es = torch.zeros(D, dtype=torch.float32, device=DEV)
+    sidx = torch.empty(kt, dtype=torch.int32, device=DEV)
+    sval = torch.empty(kt, dtype=torch.float32, device=DEV)
+    sws = efs.new_topk_segmented_workspace(ks.size, kt, DEV)
+    sws.zero_()
+    offd, kd = torch.from_numpy(off).to(DEV), torch.from_numpy(ks).to(DEV)
+
+    def check_layers(prev, what):
+        gi, gv = sidx.cpu().numpy(), sval.cpu().numpy()
+        pos = 0
+        for s_ in range(ks.size):
+            lo_s, hi_s, k_s = int(off[s_]), int(off[s_ + 1]), int(ks[s_])
+            check_topk_chunked(
+                hi_s - lo_s, k_s, gi[pos:pos + k_s] - lo_s, gv[pos:pos + k_s],
+                acc_fn=lambda lo, hi: oracle.ht(g[lo_s + lo:lo_s + hi], prev(lo_s + lo, lo_s + hi), LR,
+                                                np.inf, cap=0, mt=True)[2],
+                e_next_fn=lambda lo, hi: es[lo_s + lo:lo_s + hi].cpu().numpy(), chunk=CHUNK)
+            pos += k_s
+        say(t0, "layer-wise %s ok (bracket in %d layers)" % (what, efs.topk_segmented_bracket_segments(sws)))
+
+    efs.topk_segmented_compress(g_dev, es, LR, offd, kd, sidx, sval, sws)
+    assert efs.topk_segmented_status(sws) == 0
+    check_layers(lambda lo, hi: zeros[:hi - lo], "first call")
+    for t in range(1, 9):
+        e_before.copy_(es)
+        efs.topk_segmented_compress(g_dev, es, LR, offd, kd, sidx, sval, sws)
+        if efs.topk_segmented_bracket_segments(sws) >= 2:
+            break
+    assert efs.topk_segmented_bracket_segments(sws) >= 2, "the large layers never used their brackets"
+    check_layers(lambda lo, hi: e_before[lo:hi].cpu().numpy(), "call %d" % t)
+    del es, e_before, sws, g_dev
     torch.cuda.empty_cache()
 
     # the average of the two payloads over d = 2^31 - 1 coordinates
