@@ -423,7 +423,8 @@ def test_segmented_bracket_from_another_scale_falls_back():
     assert hits[2] == ks.size
 
 
-def test_segmented_light_layers_miss_their_brackets():
+@pytest.mark.parametrize("unaligned", [False, True])
+def test_segmented_light_layers_miss_their_brackets(unaligned):
     # layers of two to four tiles starting anywhere in a block (the sizes
     # whose bracket path keeps no digit-1 histogram), error feedback carried:
     # the thresholds grow over the first steps and leave the brackets, settle
@@ -442,12 +443,12 @@ def test_segmented_light_layers_miss_their_brackets():
     e = np.zeros(d, np.float32)
     scales = [1.0] * 8 + [30.0] * 3 + [0.01, 1.0]
     hits = []
-    say("segmented light layers d=%d nseg=%d" % (d, ks.size))
+    say("segmented light layers d=%d nseg=%d unaligned=%s" % (d, ks.size, unaligned))
     for t, sc in enumerate(scales):
         g = (synth.small_gradient(4300 + t, d) * np.float32(sc)).astype(np.float32)
         if t == len(scales) - 1:
             g = (np.round(g / np.float32(4e-4)) * np.float32(4e-4)).astype(np.float32)
-        gi, gv, ge, _ = run_gpu(g, e, off, ks, k_total=k_total, ws=ws)
+        gi, gv, ge, _ = run_gpu(g, e, off, ks, k_total=k_total, ws=ws, unaligned=unaligned)
         assert efs.topk_segmented_status(ws) == 0
         ri, rv, re = oracle.topk_segmented(g, e, LR, off, ks)
         order = np.lexsort((gi, np.repeat(np.arange(ks.size), np.minimum(ks, sizes))))
