@@ -562,7 +562,7 @@ __global__ __launch_bounds__(kBlock) void apply_range_kernel(RangeArgs a) {
             if (len == kRange) {
                 f32x4 *x4 = reinterpret_cast<f32x4 *>(a.x + r0);
 #pragma unroll
-                for (int q = 0; q < kVec; ++q) x4[q * kBlock + tid] = z;
+                for (int q = 0; q < kVec; ++q) __builtin_nontemporal_store(z, x4 + q * kBlock + tid);
             } else {
                 for (int64_t q = tid; q < len; q += kBlock) a.x[r0 + q] = 0.0f;
             }
@@ -611,7 +611,7 @@ __global__ __launch_bounds__(kBlock) void apply_range_kernel(RangeArgs a) {
                 f32x4 v = sh.acc4[q * kBlock + tid];
 #pragma unroll
                 for (int c = 0; c < 4; ++c) v[c] = average_of(v[c], n, fn);
-                x4[q * kBlock + tid] = v;
+                __builtin_nontemporal_store(v, x4 + q * kBlock + tid);
             }
         } else {
             for (int64_t q = tid; q < len; q += kBlock) a.x[r0 + q] = average_of(acc[q], n, fn);
