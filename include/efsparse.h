@@ -153,7 +153,7 @@ size_t topk_path_flag_offset(void);
  *               16-byte aligned: per-segment tables and histograms (36 KiB per
  *               segment), a candidate region of 16*k_total + 4096*nseg
  *               (key, index) pairs, a work list of one 8-byte entry per
- *               2048 of those pairs or payload slots, and 32 KiB of flags
+ *               512 of those pairs or payload slots, and 32 KiB of flags
  *               over groups of tiles.  Results never depend on its contents.
  *               Not shareable between concurrent calls.
  * Host-visible arguments are checked before anything is launched (EFS_EINVAL,
