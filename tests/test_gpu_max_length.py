@@ -1,8 +1,9 @@
 """GPU parity at the largest vector length the ABI takes, d = 2^31 - 1
 (int32 indices; 8.6 GB per fp32 vector): the hard threshold over two
-error-feedback steps, the flat Top-k on its radix path and then from its
-bracket, the layer-wise Top-k over five layers (first call and a later one
-from the brackets), and the average of the first two payloads, each against
+error-feedback steps with its telemetry, the flat Top-k on its radix path
+and then from its bracket, the layer-wise Top-k over five layers (first
+call and a later one from the brackets), the average of the first two
+payloads and the same average fused with the momentum update, each against
 the oracle chunk by chunk.  Large magnitudes are planted at the last elements of the
 vector (the ragged last tile) and around the last 4096-element boundary, so
 that pairs with the largest indices are kept."""
@@ -59,8 +60,10 @@ def test_vector_of_two_to_the_31_minus_one_elements():
     ctr = efs.new_counter(DEV)
     e_ref = np.zeros(D, np.float32)
     payload0 = None
+    tel = efs.new_telemetry(DEV)
+    err2, sent, maxbits = 0.0, 0, 0
     for t in range(2):
-        efs.ht_compress(g_dev, e, LR, lam, idx, val, ctr)
+        efs.ht_compress_telemetry(g_dev, e, LR, lam, idx, val, ctr, tel)
         n = efs.counter_value(ctr)
         assert n <= cap
         gi, gv = canonical(idx[:n].cpu().numpy(), val[:n].cpu().numpy())
@@ -76,8 +79,16 @@ def test_vector_of_two_to_the_31_minus_one_elements():
             assert_payload_equal(gi[a:b] - lo, gv[a:b], ri, rv, "ht t=%d chunk %d" % (t, lo))
             assert_bits_equal(e[lo:hi].cpu().numpy(), e_chunk, "ht e' t=%d chunk %d" % (t, lo))
             total += rk
+            err2 += float(np.sum(e_chunk.astype(np.float64) ** 2))
+            maxbits = max(maxbits, int(np.max(e_chunk.view(np.uint32) & np.uint32(0x7FFFFFFF))))
         assert n == total
+        sent += n
         say(t0, "hard threshold t=%d: k_t=%d, last index %d" % (t, n, gi[-1]))
+    got = efs.read_telemetry(tel)
+    assert got["calls"] == 2 and got["sent_total"] == sent
+    assert got["max_abs_bits"] == maxbits
+    assert abs(got["err2_total"] - err2) <= 1e-9 * err2
+    say(t0, "telemetry ok: sum ||e'||^2 %.6g, max |e'| %.6g" % (err2, got["max_abs"]))
     del e, e_ref, idx, val
     torch.cuda.empty_cache()
 
@@ -166,3 +177,16 @@ def test_vector_of_two_to_the_31_minus_one_elements():
     for lo in range(0, D, CHUNK):
         assert_bits_equal(out[lo:lo + CHUNK].cpu().numpy(), ref[lo:lo + CHUNK], "average chunk %d" % lo)
     say(t0, "average of the two payloads ok")
+    del out, ref
+    torch.cuda.empty_cache()
+
+    # the same average fused with the momentum update of Algorithm 2
+    m_host = synth.long_gradient(32, D, threads=THREADS)
+    x_dev, m_dev = to_dev(g), to_dev(m_host)
+    efs.sparse_apply(ps, D, efs.APPLY_MOMENTUM, x_dev, aws, m=m_dev, beta=0.9, gamma=0.05)
+    assert efs.sparse_status(aws) == 0
+    rx, rm = oracle.update([payload0, payload1], g, 2, m=m_host, beta=0.9, gamma=0.05)
+    for lo in range(0, D, CHUNK):
+        assert_bits_equal(m_dev[lo:lo + CHUNK].cpu().numpy(), rm[lo:lo + CHUNK], "m chunk %d" % lo)
+        assert_bits_equal(x_dev[lo:lo + CHUNK].cpu().numpy(), rx[lo:lo + CHUNK], "x chunk %d" % lo)
+    say(t0, "momentum update ok")
