@@ -428,6 +428,9 @@ def main():
         for s in range(3):
             efs.copy_probe(pool[s % len(pool)], pool[(s + 1) % len(pool)])
     copy_us = tc.us / 3
+    ceiling = stream_ceiling(efs, torch, cur, pool, d)
+    ceiling["ht_frac_over_best_2r1w"] = round(
+        ht_bytes / (ht_us * 1e-6) / 1e9 / HBM_PEAK_GBPS / ceiling["best_2r1w_frac"], 3)
     del pool
     torch.cuda.empty_cache()
 
@@ -475,6 +478,7 @@ def main():
             bytes_model="12 d + 8 k: what the step must move (frac is against this)"),
         "average": average,
         "copy_probe": {"us": round(copy_us, 2), "bytes": 8.0 * d, **rate(8.0 * d, copy_us)},
+        "stream_ceiling": ceiling,
     }
     if not args.no_extra:
         line["extra"] = {"segments_25.6m": bench_segments(efs, torch, synth, cur, threads),
@@ -484,6 +488,38 @@ def main():
     if not args.no_cpu:
         line["cpu_baseline"], line["cpu_baseline_1core"] = cpu_baselines(pool_host, wl, lam)
     print(json.dumps(line), flush=True)
+
+
+def stream_ceiling(efs, torch, cur, pool, d, calls=6):
+    """Plain streaming kernels over the workload's d elements, per traffic
+    mix, in the hard threshold's persistent grid and with one workgroup per
+    4096-element tile: what a kernel with the hard threshold's traffic
+    (2r1w: read g, read e, write e in place) reaches on this GPU.  The calls
+    rotate over pairs of the pool's buffers, so that the data comes from HBM
+    (the pool spans more than the 256 MB Infinity Cache)."""
+    pairs = [(pool[i], pool[(i + 1) % len(pool)]) for i in range(0, max(len(pool), 2), 2)]
+    if len(pool) < 2:
+        pairs = [(pool[0], torch.empty_like(pool[0]))]
+    whole = d // 4096 * 4096
+    out = {"note": "us per call, back to back; bytes per call: copy 8d, read 4d, write 4d, "
+                   "2r1w 12d (whole 4096-element tiles)"}
+    best = 0.0
+    for name, mode, nbytes in (("copy", 0, 8.0 * d), ("read", 1, 4.0 * whole),
+                               ("write", 2, 4.0 * whole), ("2r1w", 3, 12.0 * whole)):
+        for shape, bit in (("persistent", 0), ("tile_per_workgroup", 4)):
+            for x, y in pairs:
+                efs.stream_probe(x, y, mode + bit)
+            with Timer(torch, cur) as t:
+                for c in range(calls):
+                    x, y = pairs[c % len(pairs)]
+                    efs.stream_probe(x, y, mode + bit)
+            us = t.us / calls
+            r = rate(nbytes, us)
+            out["%s_%s" % (name, shape)] = dict(us=round(us, 2), **r)
+            if name == "2r1w":
+                best = max(best, r["frac"])
+    out["best_2r1w_frac"] = best
+    return out
 
 
 def describe(wl):

@@ -304,19 +304,23 @@ efs_status sparse_apply(const int32_t *const *idx, const float *const *val,
                         void *workspace, size_t workspace_bytes, void *stream);
 
 /* Streaming copy dst[0..n) = src[0..n) with the same 16-byte access pattern
- * as the compression kernels: a bandwidth ceiling for measurements, not part
- * of the method.  src and dst 16-byte aligned, n >= 0. */
+ * and grid as the hard-threshold kernel: the reference transfer for
+ * measurements, not part of the method.  src and dst 16-byte aligned,
+ * 0 <= n <= INT32_MAX * 4096. */
 efs_status efs_copy_probe(const float *src, float *dst, int64_t n, void *stream);
 
-/* Streaming bandwidth probes over n floats with the same tile shape and grid
- * as the compression kernels (measurement aids, not part of the method):
+/* Streaming bandwidth probes over n floats with the same tile shape as the
+ * compression kernels (measurement aids, not part of the method):
  *   mode 0  copy       y = x                (4n bytes read, 4n written)
  *   mode 1  read       sum of x, discarded  (4n read; y[0..255] reserved)
  *   mode 2  write      y = constant         (4n written)
  *   mode 3  2R1W       y = y + 0.5 x        (8n read, 4n written; the
  *                                            access pattern of ht_compress)
- * Modes 1-3 cover whole 4096-element tiles only.  x and y 16-byte aligned,
- * n >= 0; for mode 1, y must hold at least 256 floats. */
+ * plus 4: the same traffic with one workgroup per 4096-element tile instead
+ * of the hard threshold's persistent grid.  Modes 1-3 (5-7) cover whole
+ * 4096-element tiles only.  x and y 16-byte aligned, 0 <= n <=
+ * INT32_MAX * 4096; for mode 1 (5), y must hold at least 256 floats.  Other
+ * modes: EFS_EINVAL. */
 efs_status efs_stream_probe(const float *x, float *y, int64_t n, int mode, void *stream);
 
 /* Static text for a status code. */

@@ -438,11 +438,12 @@ def copy_probe(src, dst, stream=None) -> None:
 
 
 def stream_probe(x, y, mode: int, stream=None) -> None:
-    """Bandwidth probe: 0 copy, 1 read, 2 write, 3 two reads + one write."""
+    """Bandwidth probe: 0 copy, 1 read, 2 write, 3 two reads + one write;
+    plus 4, one workgroup per 4096-element tile instead of the persistent grid."""
     import torch
     lib = load_library()
     _require(x, torch.float32, "x")
     _require(y, torch.float32, "y")
-    if mode != 1 and x.numel() != y.numel():
+    if int(mode) & 3 != 1 and x.numel() != y.numel():
         raise ValueError("x and y differ in length")
     _check(lib, lib.efs_stream_probe(_ptr(x), _ptr(y), x.numel(), int(mode), _stream_handle(stream)))

@@ -331,24 +331,35 @@ efs_status sparse_apply(const int32_t *const *idx, const float *const *val,
                         "sparse_apply");
 }
 
+// The probes address at most INT32_MAX tiles (one workgroup each in the
+// one-tile-per-workgroup shape).
+constexpr int64_t kProbeMaxElements = int64_t(INT32_MAX) * efs::kTile;
+
 efs_status efs_copy_probe(const float *src, float *dst, int64_t n, void *stream) {
-    if (n < 0) return fail(EFS_EINVAL, "efs_copy_probe: n < 0");
+    if (n < 0 || n > kProbeMaxElements)
+        return fail(EFS_EINVAL, "efs_copy_probe: n = %lld outside [0, %lld]", (long long)n,
+                    (long long)kProbeMaxElements);
     if (n > 0 && (src == nullptr || dst == nullptr || !aligned(src, 16) || !aligned(dst, 16)))
         return fail(EFS_EINVAL, "efs_copy_probe: src and dst must be non-NULL and 16-byte aligned");
-    return check_launch(efs::launch_copy(src, dst, n, static_cast<hipStream_t>(stream)),
+    return check_launch(efs::launch_copy(src, dst, n, false, static_cast<hipStream_t>(stream)),
                         "efs_copy_probe");
 }
 
 efs_status efs_stream_probe(const float *x, float *y, int64_t n, int mode, void *stream) {
-    if (n < 0) return fail(EFS_EINVAL, "efs_stream_probe: n < 0");
-    if (mode < 0 || mode > 3) return fail(EFS_EINVAL, "efs_stream_probe: mode %d outside 0..3", mode);
+    if (n < 0 || n > kProbeMaxElements)
+        return fail(EFS_EINVAL, "efs_stream_probe: n = %lld outside [0, %lld]", (long long)n,
+                    (long long)kProbeMaxElements);
+    if (mode < 0 || mode > 7) return fail(EFS_EINVAL, "efs_stream_probe: mode %d outside 0..7", mode);
+    const bool per_tile = (mode & 4) != 0;
+    mode &= 3;
     if (n > 0 && (x == nullptr || y == nullptr || !aligned(x, 16) || !aligned(y, 16)))
         return fail(EFS_EINVAL, "efs_stream_probe: x and y must be non-NULL and 16-byte aligned");
     if (mode == 0)
-        return check_launch(efs::launch_copy(x, y, n, static_cast<hipStream_t>(stream)),
+        return check_launch(efs::launch_copy(x, y, n, per_tile, static_cast<hipStream_t>(stream)),
                             "efs_stream_probe");
-    return check_launch(efs::launch_stream_probe(x, y, n, mode, static_cast<hipStream_t>(stream)),
-                        "efs_stream_probe");
+    return check_launch(
+        efs::launch_stream_probe(x, y, n, mode, per_tile, static_cast<hipStream_t>(stream)),
+        "efs_stream_probe");
 }
 
 }  // extern "C"

@@ -47,8 +47,9 @@ hipError_t launch_apply(const int32_t *const *idx, const float *const *val,
 constexpr size_t kStaticScratchBytes = size_t(64) << 20;
 hipError_t static_scratch(void **ptr);
 
-hipError_t launch_copy(const float *src, float *dst, int64_t n, hipStream_t stream);
-hipError_t launch_stream_probe(const float *x, float *y, int64_t n, int mode, hipStream_t stream);
+hipError_t launch_copy(const float *src, float *dst, int64_t n, bool per_tile, hipStream_t stream);
+hipError_t launch_stream_probe(const float *x, float *y, int64_t n, int mode, bool per_tile,
+                               hipStream_t stream);
 
 // Workgroups for a grid-stride pass over `work_tiles` tiles: enough to fill
 // every compute unit several times over, never more than there is work.

@@ -1,7 +1,12 @@
 // Streaming bandwidth probes (measurement aids, not part of the method):
-// the same tile shape, grid sizing and cache hints as the hard-threshold
-// kernel, so that their rates are the ceilings the compression passes are
-// compared with.
+// the same tile shape and cache hints as the hard-threshold kernel, so that
+// their rates are the ceilings the compression passes are compared with.
+// Each launches either the hard threshold's persistent grid (two
+// workgroups per CU striding over the tiles, XCD by XCD for long sweeps) or
+// one workgroup per 4096-element tile, dispatched in tile order; a plain
+// stream runs faster in the second shape, which the compression passes
+// cannot take (their one payload atomic per workgroup would then serialise
+// on a single address).
 #include "device_common.hpp"
 #include "launch.hpp"
 
@@ -14,9 +19,10 @@ namespace {
 // non-temporal stores.
 __global__ __launch_bounds__(kBlock) void copy_kernel(const float *__restrict__ src,
                                                       float *__restrict__ dst, int64_t n,
-                                                      uint32_t ntiles) {
+                                                      uint32_t ntiles, bool by_xcd) {
     const int tid = threadIdx.x;
-    for (uint32_t tile = blockIdx.x; tile < ntiles; tile += gridDim.x) {
+    const TileWalk walk = tile_walk(ntiles, by_xcd);
+    for (uint32_t tile = walk.first; tile < walk.end; tile += walk.stride) {
         const int64_t tile0 = int64_t(tile) * kTile;
         if (tile0 + kTile <= n) {
             const f32x4 *s4 = reinterpret_cast<const f32x4 *>(src + tile0);
@@ -40,10 +46,11 @@ __global__ __launch_bounds__(kBlock) void copy_kernel(const float *__restrict__ 
 template <int kMode>
 __global__ __launch_bounds__(kBlock) void stream_probe_kernel(const float *__restrict__ x,
                                                               float *__restrict__ y, int64_t n,
-                                                              uint32_t ntiles) {
+                                                              uint32_t ntiles, bool by_xcd) {
     const int tid = threadIdx.x;
     f32x4 acc = {0.0f, 0.0f, 0.0f, 0.0f};
-    for (uint32_t tile = blockIdx.x; tile < ntiles; tile += gridDim.x) {
+    const TileWalk walk = tile_walk(ntiles, by_xcd);
+    for (uint32_t tile = walk.first; tile < walk.end; tile += walk.stride) {
         const int64_t tile0 = int64_t(tile) * kTile;
         if (tile0 + kTile > n) continue;  // the probe covers whole tiles only
         const f32x4 *x4 = reinterpret_cast<const f32x4 *>(x + tile0);
@@ -72,23 +79,38 @@ __global__ __launch_bounds__(kBlock) void stream_probe_kernel(const float *__res
 
 }  // namespace
 
-hipError_t launch_stream_probe(const float *x, float *y, int64_t n, int mode,
+// The persistent grid of the hard threshold (with its XCD-by-XCD walk of
+// long sweeps), or one workgroup per tile.
+struct ProbeGrid {
+    uint32_t grid;
+    bool by_xcd;
+};
+
+ProbeGrid probe_grid(int64_t tiles, bool per_tile) {
+    if (per_tile) return ProbeGrid{uint32_t(tiles), false};
+    const uint32_t grid = balanced_grid(tiles, kHtWorkgroupsPerCU);
+    return ProbeGrid{grid, tiles >= int64_t(kXcdWalkMinTiles) * grid};
+}
+
+hipError_t launch_stream_probe(const float *x, float *y, int64_t n, int mode, bool per_tile,
                                hipStream_t stream) {
     const int64_t tiles = n > 0 ? (n + kTile - 1) / kTile : 1;
-    const uint32_t grid = balanced_grid(tiles, kHtWorkgroupsPerCU);
+    const ProbeGrid pg = probe_grid(tiles, per_tile);
+    const uint32_t nt = uint32_t(tiles);
     if (mode == 1)
-        stream_probe_kernel<1><<<grid, kBlock, 0, stream>>>(x, y, n, uint32_t(tiles));
+        stream_probe_kernel<1><<<pg.grid, kBlock, 0, stream>>>(x, y, n, nt, pg.by_xcd);
     else if (mode == 2)
-        stream_probe_kernel<2><<<grid, kBlock, 0, stream>>>(x, y, n, uint32_t(tiles));
+        stream_probe_kernel<2><<<pg.grid, kBlock, 0, stream>>>(x, y, n, nt, pg.by_xcd);
     else
-        stream_probe_kernel<3><<<grid, kBlock, 0, stream>>>(x, y, n, uint32_t(tiles));
+        stream_probe_kernel<3><<<pg.grid, kBlock, 0, stream>>>(x, y, n, nt, pg.by_xcd);
     return hipGetLastError();
 }
 
-hipError_t launch_copy(const float *src, float *dst, int64_t n, hipStream_t stream) {
+hipError_t launch_copy(const float *src, float *dst, int64_t n, bool per_tile,
+                       hipStream_t stream) {
     const int64_t tiles = n > 0 ? (n + kTile - 1) / kTile : 1;
-    copy_kernel<<<balanced_grid(tiles, kHtWorkgroupsPerCU), kBlock, 0, stream>>>(src, dst, n,
-                                                                               uint32_t(tiles));
+    const ProbeGrid pg = probe_grid(tiles, per_tile);
+    copy_kernel<<<pg.grid, kBlock, 0, stream>>>(src, dst, n, uint32_t(tiles), pg.by_xcd);
     return hipGetLastError();
 }
 

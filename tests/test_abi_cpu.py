@@ -131,6 +131,12 @@ def test_accumulate_rejects_bad_arguments(lib):
     assert lib.sparse_accumulate_workspace_bytes(binding.MAX_WORKERS + 1, 10, 10) == 0
     assert lib.sparse_status_offset() < 256
     assert lib.efs_copy_probe(fake + 4, fake, 8, None) == binding.EFS_EINVAL
+    big = 2 ** 31 * 4096   # one tile past the probes' INT32_MAX tiles
+    assert lib.efs_copy_probe(fake, fake, big, None) == binding.EFS_EINVAL
+    for mode in (-1, 8):
+        assert lib.efs_stream_probe(fake, fake, 8, mode, None) == binding.EFS_EINVAL
+    assert lib.efs_stream_probe(fake, fake, big, 7, None) == binding.EFS_EINVAL
+    assert lib.efs_stream_probe(fake + 4, fake, 8, 4, None) == binding.EFS_EINVAL
 
 
 def test_workspace_size_grows_with_tiles(lib):

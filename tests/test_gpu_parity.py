@@ -690,20 +690,22 @@ def test_copy_probe_copies():
         assert torch.equal(src, dst)
 
 
-def test_stream_probes():
+@pytest.mark.parametrize("shape", [0, 4], ids=["persistent", "tile_per_workgroup"])
+def test_stream_probes(shape):
     n = 4096 * 7 + 5
     x = torch.arange(n, dtype=torch.float32, device=DEV)
     y = torch.full((n,), 2.0, dtype=torch.float32, device=DEV)
-    efs.stream_probe(x, y, 0)
+    efs.stream_probe(x, y, 0 + shape)
     assert torch.equal(x, y)
     y.fill_(2.0)
-    efs.stream_probe(x, y, 3)
+    efs.stream_probe(x, y, 3 + shape)
     whole = 4096 * 7
     assert torch.equal(y[:whole], 2.0 + 0.5 * x[:whole])
     assert torch.all(y[whole:] == 2.0)
-    efs.stream_probe(x, y, 2)
-    assert torch.equal(y[:8], torch.tensor([1, 2, 3, 4, 1, 2, 3, 4], dtype=torch.float32, device=DEV))
-    efs.stream_probe(x, y, 1)
+    efs.stream_probe(x, y, 2 + shape)
+    assert torch.equal(y[:whole].view(-1, 4), torch.tensor([1.0, 2.0, 3.0, 4.0], device=DEV).expand(whole // 4, 4))
+    efs.stream_probe(x, y, 1 + shape)
+    torch.cuda.synchronize()
 
 
 def test_sticky_last_error():
