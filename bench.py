@@ -353,7 +353,7 @@ def main():
 
     # ---- hard threshold: K timed steps --------------------------------------
     e_ht = torch.zeros(d, dtype=torch.float32, device=dev)
-    cap = min(d, max(1 << 20, d // 8))   # k_t grows under error feedback with a fixed lambda
+    cap = d   # k_t grows under error feedback with a fixed lambda (past d/8 on heavy tails)
     idx = torch.empty(cap, dtype=torch.int32, device=dev)
     val = torch.empty(cap, dtype=torch.float32, device=dev)
     ctr = efs.new_counter(dev)
