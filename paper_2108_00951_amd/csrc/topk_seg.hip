@@ -373,6 +373,58 @@ __device__ __forceinline__ int32_t segment_after(const uint32_t *tp, int32_t nse
     return tp[s + 2] > t ? s + 1 : segment_of_tile(tp, nseg, t);
 }
 
+// Word i of a table held one dword a lane (lane i), as a wave-uniform value.
+__device__ __forceinline__ uint32_t tab_word(uint32_t v, int i) {
+    return __builtin_amdgcn_readlane(v, i);
+}
+
+__device__ __forceinline__ int64_t tab_i64(uint32_t v, int i) {
+    return int64_t(uint64_t(tab_word(v, i)) | (uint64_t(tab_word(v, i + 1)) << 32));
+}
+static_assert(offsetof(SegInfo, size) == 8 && offsetof(SegInfo, kout) == 16 &&
+                  offsetof(SegInfo, k) == 24 && offsetof(SegInfo, coff) == 32 &&
+                  offsetof(SegInfo, ccap) == 40 && offsetof(SegInfo, tile0) == 48 &&
+                  offsetof(SegInfo, ntiles) == 52 && offsetof(SegInfo, wmax) == 60,
+              "SegInfo words read from a lane-spread table");
+
+// The tables of segment s spread over the lanes of a wave, so that a sweep
+// loads the next segment's while it works on the current one (one register,
+// no LDS): lanes 0..15 its SegInfo, lane 16 tile_prefix[s + 1] (where it
+// ends), lanes 17..20 the bracket, lo, hi and shift of its state (which
+// pass1 does not change).  Nothing is loaded for s >= nseg; every wave loads
+// its own copy.
+constexpr int kTabNext = 16, kTabState = 17, kTabLanes = 21;
+static_assert(offsetof(SegState, lo) == offsetof(SegState, bracket) + 4 &&
+                  offsetof(SegState, hi) == offsetof(SegState, bracket) + 8 &&
+                  offsetof(SegState, shift) == offsetof(SegState, bracket) + 12,
+              "bracket, lo, hi, shift are consecutive words");
+
+__device__ __forceinline__ uint32_t load_seg_table(const SegWs &ws, int32_t nseg, int32_t s) {
+    const int lane = threadIdx.x & (kWave - 1);
+    if (s >= nseg || lane >= kTabLanes) return 0u;
+    const uint32_t *src =
+        lane < kTabNext ? reinterpret_cast<const uint32_t *>(ws.info + s) + lane
+        : lane == kTabNext ? ws.tile_prefix + s + 1
+                           : reinterpret_cast<const uint32_t *>(ws.st + s) +
+                                 offsetof(SegState, bracket) / 4 + (lane - kTabState);
+    return *src;
+}
+
+__device__ __forceinline__ SegInfo tab_info(uint32_t v, int b) {
+    SegInfo r;
+    r.off = tab_i64(v, b + 0);
+    r.size = tab_i64(v, b + 2);
+    r.kout = tab_i64(v, b + 4);
+    r.k = tab_i64(v, b + 6);
+    r.coff = tab_i64(v, b + 8);
+    r.ccap = tab_i64(v, b + 10);
+    r.tile0 = tab_word(v, b + 12);
+    r.ntiles = tab_word(v, b + 13);
+    r.wbase = tab_word(v, b + 14);
+    r.wmax = tab_word(v, b + 15);
+    return r;
+}
+
 // Element (j, c) of this thread in the 4096-element block starting at
 // `block0` (index block0 + (j * kBlock + tid) * 4 + c, the hard threshold's
 // map).
@@ -786,6 +838,36 @@ __device__ __forceinline__ void flush_cand(Stage &sg, uint32_t &fill, SegState *
     __syncthreads();
 }
 
+// Both stages flushed at once, as at the end of a segment: the two slot
+// reservations (one atomic each, from two waves) are in flight together, one
+// round trip instead of two.
+__device__ __forceinline__ void flush_both(Stage &sg, uint32_t &efill, uint32_t &cfill,
+                                           SegState *st, const SegInfo &inf, int32_t *idx,
+                                           float *val, uint2 *cand, const Fine &fine) {
+    __syncthreads();
+    if (efill == 0u && cfill == 0u) return;
+    if (threadIdx.x == 0 && efill != 0u) sg.wave[0] = atomicAdd(&st->emit, efill);
+    if (threadIdx.x == kWave && cfill != 0u) sg.wave[1] = atomicAdd(&st->ccur, cfill);
+    __syncthreads();
+    const uint32_t ebase = sg.wave[0], cbase = sg.wave[1];
+    for (uint32_t q = threadIdx.x; q < efill; q += kBlock) {
+        const int64_t slot = int64_t(ebase) + q;
+        if (slot < inf.k) {
+            idx[inf.kout + slot] = int32_t(sg.e_idx[q]);
+            val[inf.kout + slot] = __uint_as_float(sg.e_val[q]);
+        }
+    }
+    for (uint32_t q = threadIdx.x; q < cfill; q += kBlock) {
+        const int64_t slot = int64_t(cbase) + q;
+        const uint2 v = sg.cand[q];
+        if (slot < inf.ccap) cand[inf.coff + slot] = v;
+        count_fine(fine, v.x);
+    }
+    efill = 0u;
+    cfill = 0u;
+    __syncthreads();
+}
+
 // Stages this tile's selections (called by every thread of the workgroup):
 // elements of `emit_mask` for the payload (e cleared there when zero_e), of
 // `cand_mask` for the candidates (counted in `fine` when it has a
@@ -996,6 +1078,136 @@ __device__ void select_in_tile(const float (&p)[kVecPerThread][4], uint32_t vali
             }
 }
 
+// Small one-tile segments (at most kWaveLayerMax elements, k <= kSmallK or
+// every element kept) are selected by one wave each, so that a workgroup
+// takes up to kWaves of them at once with no barrier: models with thousands
+// of tensors have mostly such layers, and one at a time each cost the
+// workgroup a memory round trip and a few barriers.
+constexpr int kWaveLayerMax = 16 * kWave;  // 16 elements a lane
+
+__device__ __forceinline__ bool wave_layer(int64_t size, int64_t k) {
+    return size <= kWaveLayerMax && (k <= kSmallK || k >= size);
+}
+
+// One wave: the error-feedback step and the selection of segment `inf`
+// (one tile, 1 <= size <= kWaveLayerMax): element q * 64 + lane of the
+// segment in slot q of the lane, k rounds of a wave-wide maximum of (key,
+// lower index first) as in select_in_tile, the kept pairs written to the
+// segment's payload region in index order, e' = p elsewhere and +0 at them.
+__device__ __forceinline__ void select_in_wave(const float *__restrict__ g, float *__restrict__ e,
+                                               float lr, int32_t *__restrict__ idx,
+                                               float *__restrict__ val, const SegInfo &inf) {
+    constexpr int kSlots = kWaveLayerMax / kWave;
+    const uint32_t lane = threadIdx.x & (kWave - 1);
+    const uint32_t size = uint32_t(inf.size);
+    const float *gs = g + inf.off;
+    float *es = e + inf.off;
+    float p[kSlots];
+    uint32_t valid = 0;
+    // loads first (a slot past the end reads the last element, which the
+    // segment owns), then p
+    float gv[kSlots], ev[kSlots];
+#pragma unroll
+    for (int q = 0; q < kSlots; ++q) {
+        if (uint32_t(q) * kWave >= size) break;  // the same for the whole wave
+        const uint32_t o = min(uint32_t(q) * kWave + lane, size - 1u);
+        gv[q] = gs[o];
+        ev[q] = es[o];
+    }
+#pragma unroll
+    for (int q = 0; q < kSlots; ++q) {
+        p[q] = 0.0f;
+        if (uint32_t(q) * kWave >= size) break;
+        p[q] = ef_accumulate(ev[q], lr, gv[q]);
+        if (uint32_t(q) * kWave + lane < size) valid |= 1u << q;
+    }
+    uint32_t keep = 0;
+    if (inf.k >= inf.size) {
+        keep = valid;
+    } else {
+#pragma unroll 1
+        for (int r = 0; r < int(inf.k); ++r) {
+            // slots in q order are in index order: the first strictly larger
+            // key is this lane's best
+            const uint32_t open = valid & ~keep;
+            uint32_t bk = 0, bq = 32;
+#pragma unroll
+            for (int q = 0; q < kSlots; ++q)
+                if (((open >> q) & 1u) && (bq == 32 || magnitude_key(p[q]) > bk)) {
+                    bk = magnitude_key(p[q]);
+                    bq = uint32_t(q);
+                }
+            uint64_t best = 0;  // every valid element scores above 0
+            if (bq != 32) best = (uint64_t(bk) << 32) | (0xffffffffu - (bq * kWave + lane));
+            const uint32_t o = 0xffffffffu - uint32_t(wave_max_u64(best));
+            if ((o & (kWave - 1)) == lane) keep |= 1u << (o / kWave);
+        }
+    }
+    // e' and the kept pairs, ranked in index order (slot, then lane)
+    uint32_t rank = 0;
+#pragma unroll
+    for (int q = 0; q < kSlots; ++q) {
+        if (uint32_t(q) * kWave >= size) break;
+        const bool kq = (keep >> q) & 1u;
+        const uint64_t m = __ballot(kq);
+        const uint32_t o = uint32_t(q) * kWave + lane;
+        if (kq) {
+            const int64_t slot = inf.kout + rank + lanes_below(m);
+            idx[slot] = int32_t(inf.off + o);
+            val[slot] = p[q];
+        }
+        if ((valid >> q) & 1u) es[o] = kq ? 0.0f : p[q];
+        rank += uint32_t(__popcll(m));
+    }
+}
+
+// Segment s (holding tile t, one tile, small) and the segments after it
+// that hold tiles t + 1, t + 2, ... (below t1) and are small one-tile
+// segments as well, up to kWaves of them: wave w selects segment s + w.
+// Returns how many were taken (at least 1; the same in every thread).  No
+// barrier: each wave reads the tables of s + 1 .. s + 3 itself, one dword a
+// lane (lanes 16 (w - 1) .. 16 w - 1 hold segment s + w's SegInfo).
+__device__ __forceinline__ uint32_t wave_layers(const float *__restrict__ g,
+                                                float *__restrict__ e, float lr,
+                                                int32_t *__restrict__ idx,
+                                                float *__restrict__ val, int32_t nseg,
+                                                const SegWs &ws, int32_t s, const SegInfo &inf,
+                                                uint32_t t, uint32_t t1) {
+    constexpr int kInfoWords = sizeof(SegInfo) / 4;
+    const int lane = threadIdx.x & (kWave - 1);
+    const int wave = __builtin_amdgcn_readfirstlane(int(threadIdx.x) / kWave);
+    uint32_t tab = 0u;  // a segment not loaded reads as 0 tiles
+    {
+        const int w = 1 + lane / kInfoWords;
+        if (w < kWaves && s + w < nseg && t + uint32_t(w) < t1)
+            tab = reinterpret_cast<const uint32_t *>(ws.info + s + w)[lane % kInfoWords];
+    }
+    uint32_t run = 1;
+#pragma unroll
+    for (int w = 1; w < kWaves; ++w) {
+        const int b = kInfoWords * (w - 1);
+        // segments s .. s + w - 1 hold one tile each, so s + w (when it
+        // holds any tile) holds tile t + w
+        if (run == uint32_t(w) && tab_word(tab, b + 13) == 1u &&
+            wave_layer(tab_i64(tab, b + 2), tab_i64(tab, b + 6)))
+            run = uint32_t(w + 1);
+    }
+    if (uint32_t(wave) < run) {
+        if (wave == 0) {
+            select_in_wave(g, e, lr, idx, val, inf);
+        } else {
+            const int b = kInfoWords * (wave - 1);
+            SegInfo mi;
+            mi.off = tab_i64(tab, b + 0);
+            mi.size = tab_i64(tab, b + 2);
+            mi.kout = tab_i64(tab, b + 4);
+            mi.k = tab_i64(tab, b + 6);
+            select_in_wave(g, e, lr, idx, val, mi);
+        }
+    }
+    return run;
+}
+
 // Tiles [t0, t1) of pass1; every selection, count and histogram is flushed
 // before it returns (the LDS histogram is left zero).
 template <bool kAligned>
@@ -1009,25 +1221,52 @@ __device__ void pass1_slice(const float *__restrict__ g, float *__restrict__ e, 
     SegState *st = ws.st + s;
     uint32_t bracket = st->bracket, lo = st->lo, hi = st->hi;
     Fine fine = {ws.hist2 + int64_t(s) * kDigit2, lo, st->shift};
+    // the following segment's tables, in flight while this one is swept
+    uint32_t tab = load_seg_table(ws, nseg, s + 1);
     uint32_t efill = 0, cfill = 0;
     __syncthreads();
     for (uint32_t t = t0; t < t1; ++t) {
         if (t >= next) {
             if (bracket) {
-                flush_emit(sg, efill, st, inf, idx, val);
-                flush_cand(sg, cfill, st, inf, ws.cand, fine);
+                flush_both(sg, efill, cfill, st, inf, idx, val, ws.cand, fine);
             }
             // a one-tile or a light segment leaves the LDS histogram zero
             if (inf.ntiles > 1 && bracket != kBracketLight)
                 flush_hist(hist, kDigit1, ws.hist1 + int64_t(s) * kDigit1);
-            s = segment_after(ws.tile_prefix, nseg, s, t);
-            next = ws.tile_prefix[s + 1];
-            inf = ws.info[s];
+            if (s + 1 < nseg && tab_word(tab, kTabNext) > t) {
+                // tile t (== tile_prefix[s + 1]) opens segment s + 1: the
+                // prefetched tables
+                ++s;
+                inf = tab_info(tab, 0);
+                next = tab_word(tab, kTabNext);
+                bracket = tab_word(tab, kTabState);
+                lo = tab_word(tab, kTabState + 1);
+                hi = tab_word(tab, kTabState + 2);
+                fine = Fine{ws.hist2 + int64_t(s) * kDigit2, lo, tab_word(tab, kTabState + 3)};
+            } else {
+                // past empty segments
+                s = segment_of_tile(ws.tile_prefix, nseg, t);
+                next = ws.tile_prefix[s + 1];
+                inf = ws.info[s];
+                bracket = ws.st[s].bracket;
+                lo = ws.st[s].lo;
+                hi = ws.st[s].hi;
+                fine = Fine{ws.hist2 + int64_t(s) * kDigit2, lo, ws.st[s].shift};
+            }
             st = ws.st + s;
-            bracket = st->bracket;
-            lo = st->lo;
-            hi = st->hi;
-            fine = Fine{ws.hist2 + int64_t(s) * kDigit2, lo, st->shift};
+            tab = load_seg_table(ws, nseg, s + 1);
+        }
+        if (inf.ntiles == 1 && wave_layer(inf.size, inf.k)) {
+            // this and the following small one-tile segments, a wave each;
+            // the last of them becomes the current segment (no bracket, no
+            // histogram: nothing to flush when the next tile leaves it)
+            const uint32_t run = wave_layers(g, e, lr, idx, val, nseg, ws, s, inf, t, t1);
+            s += int32_t(run) - 1;
+            t += run - 1;
+            next = t + 1;
+            st = ws.st + s;
+            if (run > 1) tab = load_seg_table(ws, nseg, s + 1);
+            continue;
         }
         const TileRange r = tile_range(inf, t);
         float p[kVecPerThread][4];
@@ -1105,8 +1344,7 @@ __device__ void pass1_slice(const float *__restrict__ g, float *__restrict__ e, 
                        val, e, false, fine);
     }
     if (bracket) {
-        flush_emit(sg, efill, st, inf, idx, val);
-        flush_cand(sg, cfill, st, inf, ws.cand, fine);
+        flush_both(sg, efill, cfill, st, inf, idx, val, ws.cand, fine);
     }
     if (inf.ntiles > 1 && bracket != kBracketLight)
         flush_hist(hist, kDigit1, ws.hist1 + int64_t(s) * kDigit1);
@@ -1330,8 +1568,7 @@ __device__ void pass2_tiles(float *__restrict__ e, int32_t *__restrict__ idx,
     __syncthreads();
     for (uint32_t t = t0; t < t1; ++t) {
         if (t >= next) {
-            flush_emit(sg, efill, st, inf, idx, val);
-            flush_cand(sg, cfill, st, inf, ws.cand, nofine);
+            flush_both(sg, efill, cfill, st, inf, idx, val, ws.cand, nofine);
             if (dirty) flush_hist(hist, kDigit2, ws.hist2 + int64_t(s) * kDigit2);
             dirty = false;
             s = segment_after(ws.tile_prefix, nseg, s, t);
@@ -1396,8 +1633,7 @@ __device__ void pass2_tiles(float *__restrict__ e, int32_t *__restrict__ idx,
             stage_tile(sg, efill, cfill, p, r.block0, emit_mask, cand_mask, inf, st, ws.cand, idx,
                        val, e, true, nofine);
     }
-    flush_emit(sg, efill, st, inf, idx, val);
-    flush_cand(sg, cfill, st, inf, ws.cand, nofine);
+    flush_both(sg, efill, cfill, st, inf, idx, val, ws.cand, nofine);
     if (dirty) flush_hist(hist, kDigit2, ws.hist2 + int64_t(s) * kDigit2);
 }
 

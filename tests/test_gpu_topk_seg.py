@@ -423,6 +423,42 @@ def test_segmented_bracket_from_another_scale_falls_back():
     assert hits[2] == ks.size
 
 
+def small_layer_layout(rng, nseg):
+    """Mostly small layers (1 to 1100 elements, so that runs of them fit one
+    4096-element block each and others straddle two), with empty layers and
+    exact sizes 1, 64, 65, 1023, 1024, 1025 mixed in."""
+    sizes = np.exp(rng.uniform(0.0, np.log(1100.0), size=nseg)).astype(np.int64)
+    special = np.array([0, 1, 64, 65, 1023, 1024, 1025, 0], dtype=np.int64)
+    pick = rng.random(nseg) < 0.15
+    sizes[pick] = special[rng.integers(0, special.size, size=int(pick.sum()))]
+    return np.concatenate([[0], np.cumsum(sizes)]).astype(np.int64)
+
+
+@pytest.mark.parametrize("nseg,unaligned", [(700, False), (700, True), (5000, False)])
+def test_segmented_small_layers_by_wave(nseg, unaligned):
+    # one-tile layers of at most 1,024 elements with k <= 8 or k >= size are
+    # selected a wave each, up to four at once; every k from 0 to 9 and k at
+    # or past the size, ties among quantised values, two error-feedback calls
+    # (above 4,096 layers the sweeps take longer slices)
+    rng = np.random.default_rng(4600 + nseg + int(unaligned))
+    off = small_layer_layout(rng, nseg)
+    sizes = np.diff(off)
+    d = int(off[-1])
+    ks = rng.integers(0, 10, size=nseg).astype(np.int64)
+    full = rng.random(nseg) < 0.08
+    ks[full] = sizes[full] + rng.integers(0, 3, size=int(full.sum()))
+    g = synth.small_gradient(4610 + nseg, d)
+    g = (np.round(g / np.float32(2e-4)) * np.float32(2e-4)).astype(np.float32)  # ties
+    e = np.zeros(d, np.float32)
+    one_tile = np.array([(sz > 0) and (o // 4096 == (o + sz - 1) // 4096) for o, sz in zip(off[:-1], sizes)])
+    wave = one_tile & (sizes <= 1024) & ((ks <= 8) | (ks >= sizes))
+    say("segmented small layers nseg=%d unaligned=%s d=%d, %d by wave" % (nseg, unaligned, d, int(wave.sum())))
+    assert wave.sum() > nseg // 2
+    for step in range(2):
+        _, _, e = check(g, e, off, ks, unaligned=unaligned, what="small layers step %d" % step)
+        e = e.copy()
+
+
 @pytest.mark.parametrize("unaligned", [False, True])
 def test_segmented_light_layers_miss_their_brackets(unaligned):
     # layers of two to four tiles starting anywhere in a block (the sizes
