@@ -1901,17 +1901,11 @@ __device__ void final_fast(Sh &sh, const SegInfo &inf, const SegState &st,
                             uint32_t(inf.k) - st.needa, hint, width);
 }
 
-template <typename Sh>
-__device__ void final_segment(float *__restrict__ e, int32_t *__restrict__ idx,
-                              float *__restrict__ val, const SegWs &ws, int32_t s, Sh &sh) {
-    const SegState st = ws.st[s];
-    if (st.mode != kModeCand && st.mode != kModeScan && st.mode != kModeFast) return;
-    const SegInfo inf = ws.info[s];
-    SegHint *hint = ws.hint + s;
-    // next bracket widths: the lower side narrower after a bracket that held
-    // many more keys below the threshold than the segment keeps, or more than
-    // it can hold; both sides wider after the threshold fell outside it
-    const SegHint oh = *hint;
+// The next bracket widths: the lower side narrower after a bracket that
+// held many more keys below the threshold than the segment keeps, or more
+// than it can hold; both sides wider after the threshold fell outside it.
+__device__ __forceinline__ uint32_t next_width(const SegHint &oh, const SegState &st,
+                                               const SegInfo &inf) {
     const uint32_t w0 = oh.magic == kHintMagic && widths_ok(oh.width)
                             ? oh.width : make_widths(kWidthStart, kWidthStart);
     uint32_t wl = width_lo(w0), wh = width_hi(w0);
@@ -1923,7 +1917,60 @@ __device__ void final_segment(float *__restrict__ e, int32_t *__restrict__ idx,
         wl = min(wl + 1u, kWidthMax);
         wh = min(wh + 1u, kWidthMax);
     }
-    const uint32_t width = make_widths(wl, wh);
+    return make_widths(wl, wh);
+}
+
+// The bracket path's final step for a segment whose bin da lists at most
+// kWave keys, by one wave and without barriers: each lane ranks one listed
+// key against the others (larger key first, then the lower index), the
+// `needa` best are emitted into the segment's last slots with e cleared at
+// them, and the key ranked needa-th is the threshold T kept as the next
+// hint: the same result as final_fast.
+__device__ __forceinline__ void final_fast_wave(float *__restrict__ e, int32_t *__restrict__ idx,
+                                                float *__restrict__ val, const SegWs &ws,
+                                                int32_t s) {
+    const uint32_t lane = threadIdx.x & (kWave - 1);
+    const SegState st = ws.st[s];
+    const SegInfo inf = ws.info[s];
+    SegHint *hint = ws.hint + s;
+    const SegHint oh = *hint;
+    const uint32_t width = next_width(oh, st, inf);
+    if (st.needa == 0u) {  // the pairs above the bracket were exactly k
+        if (lane == 0u) *hint = next_hint(oh, min(st.hi, 0x7ffffffeu) + 1u, width);
+        return;
+    }
+    const uint32_t n = min(st.ca, st.tcur);  // at most kWave, at least needa
+    const uint2 *list = ws.cand + inf.coff + st.ccur;
+    const bool mine = lane < n;
+    uint2 it = make_uint2(0u, 0u);
+    if (mine) it = list[lane];
+    const uint32_t key = it.x & 0x7fffffffu;
+    uint32_t rank = 0;
+#pragma unroll 1
+    for (uint32_t j = 0; j < n; ++j) {
+        const uint32_t kj = __builtin_amdgcn_readlane(key, j);
+        const uint32_t ij = __builtin_amdgcn_readlane(it.y, j);
+        rank += (kj > key || (kj == key && ij < it.y)) ? 1u : 0u;
+    }
+    const uint64_t at = __ballot(mine && rank == st.needa - 1u);
+    const uint32_t T = __builtin_amdgcn_readlane(key, at != 0ull ? __builtin_ctzll(at) : 0);
+    if (mine && rank < st.needa) {
+        const int64_t slot = inf.k - int64_t(st.needa) + rank;
+        idx[inf.kout + slot] = int32_t(it.y);
+        val[inf.kout + slot] = __uint_as_float(it.x);
+        e[it.y] = 0.0f;
+    }
+    if (lane == 0u) *hint = next_hint(oh, T, width);
+}
+
+template <typename Sh>
+__device__ void final_segment(float *__restrict__ e, int32_t *__restrict__ idx,
+                              float *__restrict__ val, const SegWs &ws, int32_t s, Sh &sh) {
+    const SegState st = ws.st[s];
+    if (st.mode != kModeCand && st.mode != kModeScan && st.mode != kModeFast) return;
+    const SegInfo inf = ws.info[s];
+    SegHint *hint = ws.hint + s;
+    const uint32_t width = next_width(*hint, st, inf);
     const uint32_t *h2 = ws.hist2 + int64_t(s) * kDigit2;
     if (st.mode == kModeScan) {
         final_select<kModeScan, false>(sh, inf, st, nullptr, inf.size, e, idx, val, h2, hint, width);
@@ -1978,16 +2025,29 @@ __global__ __launch_bounds__(kBlock) void seg_final_kernel(float *__restrict__ e
     if (ws.ctl->status != 0u) return;
     uint32_t fast = 0;  // segments resolved from the bracket, counted per thread
     const int32_t per = (nseg - int32_t(blockIdx.x) + int32_t(gridDim.x) - 1) / int32_t(gridDim.x);
+    const uint32_t wave = threadIdx.x / kWave;
     for (int32_t g0 = 0; g0 < per; g0 += kBlock) {
         const int32_t q = g0 + int32_t(threadIdx.x);
         const int32_t s = int32_t(blockIdx.x) + q * int32_t(gridDim.x);
-        const uint32_t mode = q < per ? ws.st[s].mode : uint32_t(kModeNone);
+        uint32_t mode = kModeNone, listed = 0u;
+        if (q < per) {
+            const SegState *p = ws.st + s;
+            mode = p->mode;
+            if (mode == kModeFast) listed = p->needa != 0u ? min(p->ca, p->tcur) : 0u;
+        }
         fast += mode == kModeFast ? 1u : 0u;
-        const bool work = mode == kModeCand || mode == kModeScan || mode == kModeFast;
-        uint32_t n_work;
+        // bracket-path segments with at most kWave keys to rank go to the
+        // waves (listed from the end of s_list), the rest to the workgroup
+        const bool small = mode == kModeFast && listed <= uint32_t(kWave);
+        const bool work = !small && (mode == kModeCand || mode == kModeScan || mode == kModeFast);
+        uint32_t n_work, n_small;
         const uint32_t pos = block_prefix_small(work ? 1u : 0u, s_wave, n_work);
+        const uint32_t spos = block_prefix_small(small ? 1u : 0u, s_wave, n_small);
         if (work) s_list[pos] = s;
+        if (small) s_list[kBlock - 1 - int(spos)] = s;
         __syncthreads();
+        for (uint32_t i = wave; i < n_small; i += kWaves)
+            final_fast_wave(e, idx, val, ws, s_list[kBlock - 1 - int(i)]);
         for (uint32_t i = 0; i < n_work; ++i) {
             final_segment(e, idx, val, ws, s_list[i], sh);
             __syncthreads();  // the LDS of this segment is free

@@ -459,6 +459,53 @@ def test_segmented_small_layers_by_wave(nseg, unaligned):
         e = e.copy()
 
 
+def test_segmented_bracket_small_bins_with_ties():
+    # two- to four-tile layers on the bracket path whose bin of the k-th key
+    # holds a few tied keys (ranked a wave per layer in the final pass,
+    # ties to the lower index): g on a power-of-two grid and lr = 1 keep
+    # p = e + g exact, so equal magnitudes stay equal from step to step
+    rng = np.random.default_rng(4700)
+    sizes = rng.integers(4500, 16000, size=400).astype(np.int64)
+    off = np.concatenate([[0], np.cumsum(sizes)]).astype(np.int64)
+    d = int(off[-1])
+    ks = np.ceil(sizes * 0.002).astype(np.int64)
+    e = np.zeros(d, np.float32)
+    ws = efs.new_topk_segmented_workspace(ks.size, int(ks.sum()), DEV)
+    hits, split_ties = [], 0
+    say("segmented bracket small bins with ties d=%d" % d)
+    for t in range(5):
+        g = (np.round(rng.standard_normal(d) * 8.0) * 2.0 ** -13).astype(np.float32)
+        gi, gv, ge, _ = run_gpu(g, e, off, ks, lr=1.0, ws=ws)
+        ri, rv, re = oracle.topk_segmented(g, e, 1.0, off, ks)
+        pos = 0
+        for s_ in range(ks.size):
+            n = int(ks[s_])
+            o = np.argsort(gi[pos:pos + n], kind="stable")
+            np.testing.assert_array_equal(gi[pos:pos + n][o], ri[pos:pos + n], "step %d segment %d" % (t, s_))
+            assert_bits_equal(gv[pos:pos + n][o], rv[pos:pos + n], "step %d segment %d values" % (t, s_))
+            pos += n
+        assert_bits_equal(ge, re, "step %d e'" % t)
+        hits.append(efs.topk_segmented_bracket_segments(ws))
+        if t > 0:
+            # layers whose k-th magnitude is shared by kept and dropped
+            # coordinates, at most 64 of them (a bracket bin here spans one
+            # grid level, so the bin ranked in the final pass is the tie)
+            p = (e + g).astype(np.float32)
+            pos = 0
+            for s_ in range(ks.size):
+                n = int(ks[s_])
+                mag = np.abs(p[off[s_]:off[s_ + 1]])
+                kth = np.abs(rv[pos:pos + n]).min()
+                tied = int(np.sum(mag == kth))
+                kept = int(np.sum(np.abs(rv[pos:pos + n]) == kth))
+                split_ties += int(kept < tied <= 64)
+                pos += n
+        e = re
+    say("  bracket layers per step: %s, split ties %d" % (hits, split_ties))
+    assert hits[0] == 0 and sum(hits[1:]) > 0
+    assert split_ties > 0
+
+
 @pytest.mark.parametrize("unaligned", [False, True])
 def test_segmented_light_layers_miss_their_brackets(unaligned):
     # layers of two to four tiles starting anywhere in a block (the sizes
