@@ -30,17 +30,18 @@
 //          top digit from the pass-1 histogram, then histogram bits 19..0 of
 //          the keys under it (a 4 B/element read of p) into 1024 coarse and
 //          2^20 fine bins.
-//   step4  radix path: coarse then fine selection, so T is exact.  When
-//          ties at T must be split (0 < m < #(key == T)): on the bracket
-//          path with at most kTieList ties, a list of the tied candidates
-//          (every key equal to T is a candidate); otherwise per-tile counts
-//          of key == T.
-//   emit   radix path: keep key > T and the ties of index rank < m (a read
-//          of p); bracket path: only the ties of rank < m, when some are
-//          dropped (from the list: one workgroup selects the m lowest
-//          indices).  Tie ranks over the vector: exclusive sums of the
-//          per-tile counts (each workgroup sums the tiles before its own),
-//          then a block scan in index order inside the tile.
+//   step4  radix path: coarse then fine selection, so T is exact, then
+//          one read of p that sends every key > T (and every key == T when
+//          no tie is dropped).  When ties at T must be split
+//          (0 < m < #(key == T)) and at most kTieList of them exist, they
+//          are listed (radix path: in that read; bracket path: from the
+//          candidates, which hold every key equal to T); with more, per-tile
+//          counts of key == T.
+//   emit   only the ties of index rank < m, when some are dropped: from the
+//          list, one workgroup selects the m lowest indices; from per-tile
+//          counts, a read of p ranks them over the vector (exclusive sums
+//          of the counts, each workgroup summing the tiles before its own,
+//          then a block scan in index order inside the tile).
 //
 // Selections made by every workgroup read the same histograms, so they agree;
 // workgroup 0 records them in the control block.  Workgroups exchange data
@@ -669,16 +670,25 @@ __global__ __launch_bounds__(kBlock) void topk_step3_kernel(float *__restrict__ 
     }
 }
 
-// Step 4: radix path, coarse then fine selection of bits 19..0 (T exact);
-// then, on either path, the per-tile tie counts when ties at T must be split.
+// Step 4.  Radix path: coarse then fine selection of bits 19..0 (T exact),
+// then one sweep of p that appends every key > T to the payload (and the
+// keys equal to T when all of them are kept) and, when ties at T must be
+// split, lists the tied indices (at most kTieList of them) or counts them
+// per tile (more).  Bracket path, ties to split: the tied candidates listed
+// (at most kTieList), else per-tile tie counts.
 template <bool kVector>
-__global__ __launch_bounds__(kBlock) void topk_step4_kernel(const float *__restrict__ e, int64_t d,
-                                                            uint32_t ntiles, Workspace ws) {
+__global__ __launch_bounds__(kBlock) void topk_step4_kernel(float *__restrict__ e, int64_t d,
+                                                            uint32_t ntiles,
+                                                            int32_t *__restrict__ idx,
+                                                            float *__restrict__ val, uint64_t cap,
+                                                            Workspace ws) {
+    __shared__ PairStage st;
     __shared__ SelectShared ss;
-    __shared__ uint32_t s_wave[kWaves];
     TopkCtl *c = ws.ctl;
-    uint32_t T, tie_mode;
-    if (c->fast == 0u) {
+    const uint32_t lane = threadIdx.x & (kWave - 1);
+    uint32_t T, tie_mode, ties;
+    const bool radix = c->fast == 0u;
+    if (radix) {
         const uint32_t need = c->n1;
         select_bin<kCoarse>(ws.rcoarse, need, ss.scan, ss.sel);
         const uint32_t cb = ss.sel[0], above_c = ss.sel[1];
@@ -687,45 +697,85 @@ __global__ __launch_bounds__(kBlock) void topk_step4_kernel(const float *__restr
                                    ss.scan, ss.sel);
         T = (c->p1 << 20) | (cb << 10) | ss.sel[0];
         const uint32_t m = need - above_c - ss.sel[1];
-        tie_mode = m < ss.sel[2] ? 1u : 0u;
-        if (blockIdx.x == 0 && threadIdx.x == 0) set_threshold(c, T, m, ss.sel[2]);
+        ties = ss.sel[2];
+        tie_mode = m < ties ? 1u : 0u;
+        if (blockIdx.x == 0 && threadIdx.x == 0) set_threshold(c, T, m, ties);
     } else {
         T = c->T;
         tie_mode = c->tie_mode;
+        ties = c->ties;
     }
-    if (tie_mode == 0u) return;
-    if (c->fast != 0u && c->ties <= kTieList) {
-        // bracket path: every key equal to T is a candidate; list them
-        const uint32_t n = c->ncand;
-        const uint32_t stride = gridDim.x * kBlock;
-        const uint32_t lane = threadIdx.x & (kWave - 1);
-        for (uint32_t base = blockIdx.x * kBlock; base < n; base += stride) {
-            const uint32_t j = base + threadIdx.x;
-            const bool tie = j < n && magnitude_key(ws.cand_val[j]) == T;
-            const uint64_t mask = __ballot(tie);
-            if (mask == 0) continue;
-            uint32_t slot = 0;
-            if (lane == 0) slot = atomicAdd(&c->tie_list, uint32_t(__popcll(mask)));
-            slot = __shfl(slot, 0) + lanes_below(mask);
-            if (tie && slot < kTieList) ws.ties[slot] = ws.cand_idx[j];
+    const bool list = tie_mode != 0u && ties <= kTieList;
+    if (!radix) {
+        if (tie_mode == 0u) return;
+        if (list) {
+            // every key equal to T is a candidate; list them
+            const uint32_t n = c->ncand;
+            const uint32_t stride = gridDim.x * kBlock;
+            for (uint32_t base = blockIdx.x * kBlock; base < n; base += stride) {
+                const uint32_t j = base + threadIdx.x;
+                const bool tie = j < n && magnitude_key(ws.cand_val[j]) == T;
+                const uint64_t mask = __ballot(tie);
+                if (mask == 0) continue;
+                uint32_t slot = 0;
+                if (lane == 0) slot = atomicAdd(&c->tie_list, uint32_t(__popcll(mask)));
+                slot = __shfl(slot, 0) + lanes_below(mask);
+                if (tie && slot < kTieList) ws.ties[slot] = ws.cand_idx[j];
+            }
+            return;
         }
-        return;
     }
+    // A sweep of p: radix path, the payload's keys > T (all of it when no
+    // tie is dropped) from slot 0; either path with many ties to split, the
+    // per-tile tie counts.  With per-tile counts e is left as p here (the
+    // emission ranks ties by scanning e for T, which may be the key of
+    // zero) and the emission clears it; otherwise e is cleared at once.
+    const bool counts = tie_mode != 0u && !list;
+    uint32_t fill = 0;
     for (uint32_t tile = blockIdx.x; tile < ntiles; tile += gridDim.x) {
         const int64_t tile0 = int64_t(tile) * kTile;
         float v[kVecPerThread][4];
         uint32_t valid;
         load_tile<kVector>(e, tile0, d, v, valid);
-        uint32_t cnt = 0;
+        uint32_t keep = 0, tie = 0;
 #pragma unroll
         for (int j = 0; j < kVecPerThread; ++j)
 #pragma unroll
-            for (int cc = 0; cc < 4; ++cc)
-                cnt += (((valid >> (4 * j + cc)) & 1u) && magnitude_key(v[j][cc]) == T) ? 1u : 0u;
-        uint32_t total;
-        block_prefix_small(cnt, s_wave, total);
-        if (threadIdx.x == 0) ws.tile_ties[tile] = total;
+            for (int cc = 0; cc < 4; ++cc) {
+                const int b = 4 * j + cc;
+                const uint32_t key = magnitude_key(v[j][cc]);
+                const bool ok = (valid >> b) & 1u;
+                keep |= uint32_t(ok && (key > T || (tie_mode == 0u && key == T))) << b;
+                tie |= uint32_t(ok && key == T) << b;
+            }
+        if (counts) {
+            uint32_t total;
+            block_prefix_small(uint32_t(__popc(tie)), st.wave, total);
+            if (threadIdx.x == 0) ws.tile_ties[tile] = total;
+        } else if (tie_mode != 0u && __ballot(tie != 0u) != 0ull) {
+            // list the tied indices of this wave, slot by slot
+#pragma unroll
+            for (int b = 0; b < 16; ++b) {
+                const bool t = (tie >> b) & 1u;
+                const uint64_t mask = __ballot(t);
+                if (mask == 0) continue;
+                uint32_t slot = 0;
+                if (lane == 0) slot = atomicAdd(&c->tie_list, uint32_t(__popcll(mask)));
+                slot = __shfl(slot, 0) + lanes_below(mask);
+                if (t && slot < kTieList) ws.ties[slot] = int32_t(elem_index(tile0, b / 4, b % 4));
+            }
+        }
+        if (!radix) continue;
+        stage_mask(st, fill, keep, v, tile0, &c->emit2, cap, idx, val);
+        if (!counts) {
+#pragma unroll
+            for (int j = 0; j < kVecPerThread; ++j)
+#pragma unroll
+                for (int cc = 0; cc < 4; ++cc)
+                    if ((keep >> (4 * j + cc)) & 1u) e[elem_index(tile0, j, cc)] = 0.0f;
+        }
     }
+    if (radix) stage_flush(st, fill, false, &c->emit2, nullptr, cap, idx, val);
 }
 
 // Sum of tile_ties[lo, hi) over the workgroup.
@@ -777,10 +827,12 @@ __device__ void emit_listed_ties(const Workspace &ws, uint32_t m, float *e, int3
     }
 }
 
-// Final emission over the whole vector.  Radix path: every key > T plus the
-// ties of rank < m (all ties when none is dropped).  Bracket path: only the
-// ties of rank < m when some are dropped (everything else is already sent);
-// returns at once otherwise.
+// Final emission: the ties of rank < m when some are dropped (every other
+// kept pair is already sent, by step 3 on the bracket path and by step 4 on
+// the radix path); returns at once otherwise.  Listed ties: one workgroup
+// keeps the m lowest indices.  Counted ties: a sweep ranks them in index
+// order, and on the radix path also clears e at the keys > T, which step 4
+// left as p.
 template <bool kVector>
 __global__ __launch_bounds__(kBlock) void topk_emit_kernel(float *__restrict__ e, int64_t d,
                                                            int32_t *__restrict__ idx,
@@ -791,7 +843,7 @@ __global__ __launch_bounds__(kBlock) void topk_emit_kernel(float *__restrict__ e
     __shared__ SelectShared ss;
     const bool fast = ws.ctl->fast != 0u;
     const bool tie_mode = ws.ctl->tie_mode != 0u;
-    if (fast && !tie_mode) return;
+    if (!tie_mode) return;
     const uint32_t T = ws.ctl->T;
     const uint32_t m = ws.ctl->m;
     // Radix path: the whole payload from slot 0.  Bracket path: after the
@@ -800,7 +852,7 @@ __global__ __launch_bounds__(kBlock) void topk_emit_kernel(float *__restrict__ e
     idx += base;
     val += base;
     cap -= base;
-    if (fast && ws.ctl->ties <= kTieList) {
+    if (ws.ctl->ties <= kTieList) {
         // the ties step 4 listed: workgroup 0 keeps the m lowest indices
         if (blockIdx.x == 0) emit_listed_ties(ws, m, e, idx, val, cap, st, ss);
         return;
@@ -814,7 +866,7 @@ __global__ __launch_bounds__(kBlock) void topk_emit_kernel(float *__restrict__ e
         float v[kVecPerThread][4];
         uint32_t valid;
         load_tile<kVector>(e, tile0, d, v, valid);
-        uint32_t keep = 0, tie = 0;
+        uint32_t keep = 0, tie = 0, above = 0;
 #pragma unroll
         for (int j = 0; j < kVecPerThread; ++j) {
 #pragma unroll
@@ -822,40 +874,37 @@ __global__ __launch_bounds__(kBlock) void topk_emit_kernel(float *__restrict__ e
                 const int b = 4 * j + c;
                 const uint32_t key = magnitude_key(v[j][c]);
                 const bool ok = (valid >> b) & 1u;
-                keep |= uint32_t(ok && !fast && key > T) << b;
+                above |= uint32_t(ok && !fast && key > T) << b;
                 tie |= uint32_t(ok && key == T) << b;
             }
         }
-        if (!tie_mode) {
-            keep |= tie;
-        } else {
-            // Rank of each tied element in index order: earlier tiles, then
-            // earlier vector slots j (all lower indices), then lower threads
-            // in slot j, then lower c within the thread.
-            ties_before += tie_count_range(ws.tile_ties, counted_to, tile, st.wave);
-            counted_to = tile;
-            uint32_t rank = ties_before;
+        // Rank of each tied element in index order: earlier tiles, then
+        // earlier vector slots j (all lower indices), then lower threads in
+        // slot j, then lower c within the thread.
+        ties_before += tie_count_range(ws.tile_ties, counted_to, tile, st.wave);
+        counted_to = tile;
+        uint32_t rank = ties_before;
 #pragma unroll
-            for (int j = 0; j < kVecPerThread; ++j) {
-                const uint32_t tj = (tie >> (4 * j)) & 0xfu;
-                uint32_t slot_total;
-                uint32_t r = rank + block_prefix_small(__popc(tj), st.wave, slot_total);
+        for (int j = 0; j < kVecPerThread; ++j) {
+            const uint32_t tj = (tie >> (4 * j)) & 0xfu;
+            uint32_t slot_total;
+            uint32_t r = rank + block_prefix_small(__popc(tj), st.wave, slot_total);
 #pragma unroll
-                for (int c = 0; c < 4; ++c) {
-                    if ((tj >> c) & 1u) {
-                        keep |= uint32_t(r < m) << (4 * j + c);
-                        ++r;
-                    }
+            for (int c = 0; c < 4; ++c) {
+                if ((tj >> c) & 1u) {
+                    keep |= uint32_t(r < m) << (4 * j + c);
+                    ++r;
                 }
-                rank += slot_total;
             }
+            rank += slot_total;
         }
         stage_mask(st, fill, keep, v, tile0, &ws.ctl->emit2, cap, idx, val);
+        const uint32_t clear = keep | above;
 #pragma unroll
         for (int j = 0; j < kVecPerThread; ++j)
 #pragma unroll
             for (int c = 0; c < 4; ++c)
-                if ((keep >> (4 * j + c)) & 1u) e[elem_index(tile0, j, c)] = 0.0f;
+                if ((clear >> (4 * j + c)) & 1u) e[elem_index(tile0, j, c)] = 0.0f;
     }
     stage_flush(st, fill, false, &ws.ctl->emit2, nullptr, cap, idx, val);
 }
@@ -893,11 +942,11 @@ hipError_t launch_topk(const float *g, float *e, int64_t d, float lr, int64_t k,
     if (k == 0) return hipGetLastError();
     if (vec) {
         topk_step3_kernel<true><<<grid, kBlock, 0, stream>>>(e, d, ntiles, kk, idx, val, ws);
-        topk_step4_kernel<true><<<grid, kBlock, 0, stream>>>(e, d, ntiles, ws);
+        topk_step4_kernel<true><<<sgrid, kBlock, 0, stream>>>(e, d, ntiles, idx, val, uint64_t(k), ws);
         topk_emit_kernel<true><<<sgrid, kBlock, 0, stream>>>(e, d, idx, val, uint64_t(k), ntiles, ws);
     } else {
         topk_step3_kernel<false><<<grid, kBlock, 0, stream>>>(e, d, ntiles, kk, idx, val, ws);
-        topk_step4_kernel<false><<<grid, kBlock, 0, stream>>>(e, d, ntiles, ws);
+        topk_step4_kernel<false><<<sgrid, kBlock, 0, stream>>>(e, d, ntiles, idx, val, uint64_t(k), ws);
         topk_emit_kernel<false><<<sgrid, kBlock, 0, stream>>>(e, d, idx, val, uint64_t(k), ntiles, ws);
     }
     return hipGetLastError();

@@ -318,6 +318,37 @@ def test_topk_all_equal_and_zero_vectors():
             assert_bits_equal(ge, re)
 
 
+@pytest.mark.parametrize("unaligned", [False, True])
+@pytest.mark.parametrize("case", ["many_ties", "many_zero_ties", "listed_zero_ties"])
+def test_topk_radix_path_ties_below_larger_keys(case, unaligned):
+    # Fresh workspace (radix path): larger keys elsewhere in the vector and
+    # ties at the k-th magnitude split by index.  many_ties: ~40k ties at
+    # 0.5 under ~10k larger keys (more ties than a list holds, so they are
+    # counted per tile and ranked by a second read); many_zero_ties: ~60k
+    # zeros tie at a zero threshold (the coordinates cleared for the larger
+    # keys must not read as ties); listed_zero_ties: ~10k zeros, few enough
+    # to be listed in the same read that sends the larger keys.
+    d = 100_003
+    rng = np.random.default_rng({"many_ties": 71, "many_zero_ties": 72, "listed_zero_ties": 73}[case])
+    u = rng.random(d)
+    small = (rng.standard_normal(d) * 1e-3).astype(np.float32)
+    if case == "many_ties":
+        g = np.where(u < 0.4, np.float32(0.5), np.where(u < 0.5, np.float32(1.0) + small, small))
+        k = 30_000
+    elif case == "many_zero_ties":
+        g = np.where(u < 0.6, np.float32(0.0), np.float32(1.0) + small)
+        k = 50_000
+    else:
+        g = np.where(u < 0.1, np.float32(0.0), np.float32(1.0) + small)
+        k = 95_000
+    g = g.astype(np.float32)
+    e = np.zeros(d, dtype=np.float32)
+    gi, gv, ge = topk_gpu(g, e, k, unaligned=unaligned)
+    ri, rv, re = oracle.topk(g, e, LR, k)
+    assert_payload_equal(gi, gv, ri, rv, case)
+    assert_bits_equal(ge, re, case)
+
+
 def test_topk_special_values():
     d = 9000
     g = synth.small_gradient(63, d)
