@@ -727,10 +727,12 @@ __global__ __launch_bounds__(kBlock) void topk_step4_kernel(float *__restrict__ 
     }
     // A sweep of p: radix path, the payload's keys > T (all of it when no
     // tie is dropped) from slot 0; either path with many ties to split, the
-    // per-tile tie counts.  With per-tile counts e is left as p here (the
-    // emission ranks ties by scanning e for T, which may be the key of
-    // zero) and the emission clears it; otherwise e is cleared at once.
+    // per-tile tie counts.  e is cleared at the sent keys at once, except
+    // with per-tile counts at T = 0: the emission ranks ties by scanning e
+    // for T, where cleared coordinates would read as ties, so it clears
+    // them itself.
     const bool counts = tie_mode != 0u && !list;
+    const bool clear_now = !counts || T != 0u;
     uint32_t fill = 0;
     for (uint32_t tile = blockIdx.x; tile < ntiles; tile += gridDim.x) {
         const int64_t tile0 = int64_t(tile) * kTile;
@@ -767,7 +769,7 @@ __global__ __launch_bounds__(kBlock) void topk_step4_kernel(float *__restrict__ 
         }
         if (!radix) continue;
         stage_mask(st, fill, keep, v, tile0, &c->emit2, cap, idx, val);
-        if (!counts) {
+        if (clear_now) {
 #pragma unroll
             for (int j = 0; j < kVecPerThread; ++j)
 #pragma unroll
@@ -831,8 +833,9 @@ __device__ void emit_listed_ties(const Workspace &ws, uint32_t m, float *e, int3
 // kept pair is already sent, by step 3 on the bracket path and by step 4 on
 // the radix path); returns at once otherwise.  Listed ties: one workgroup
 // keeps the m lowest indices.  Counted ties: a sweep ranks them in index
-// order, and on the radix path also clears e at the keys > T, which step 4
-// left as p.
+// order, reading only the tiles that hold ties, except at T = 0 on the
+// radix path, where it also clears e at the keys > T (step 4 left them as p)
+// and so reads every tile.
 template <bool kVector>
 __global__ __launch_bounds__(kBlock) void topk_emit_kernel(float *__restrict__ e, int64_t d,
                                                            int32_t *__restrict__ idx,
@@ -861,7 +864,9 @@ __global__ __launch_bounds__(kBlock) void topk_emit_kernel(float *__restrict__ e
     // ties in the tiles before this workgroup's current tile
     uint32_t ties_before = 0, counted_to = 0;
 
+    const bool every_tile = !fast && T == 0u;
     for (uint32_t tile = blockIdx.x; tile < ntiles; tile += gridDim.x) {
+        if (!every_tile && ws.tile_ties[tile] == 0u) continue;  // the same in every thread
         const int64_t tile0 = int64_t(tile) * kTile;
         float v[kVecPerThread][4];
         uint32_t valid;
@@ -874,7 +879,7 @@ __global__ __launch_bounds__(kBlock) void topk_emit_kernel(float *__restrict__ e
                 const int b = 4 * j + c;
                 const uint32_t key = magnitude_key(v[j][c]);
                 const bool ok = (valid >> b) & 1u;
-                above |= uint32_t(ok && !fast && key > T) << b;
+                above |= uint32_t(ok && every_tile && key > T) << b;
                 tie |= uint32_t(ok && key == T) << b;
             }
         }
