@@ -39,9 +39,11 @@
 //          counts of key == T.
 //   emit   only the ties of index rank < m, when some are dropped: from the
 //          list, one workgroup selects the m lowest indices; from per-tile
-//          counts, a read of p ranks them over the vector (exclusive sums
-//          of the counts, each workgroup summing the tiles before its own,
-//          then a block scan in index order inside the tile).
+//          counts, a read of the tiles holding ties ranks them over the
+//          vector (exclusive sums of the counts, each workgroup summing the
+//          tiles before its own, then a block scan in index order inside
+//          the tile); at T = 0 on the radix path that read covers every
+//          tile and also clears e at the keys > T, which step 4 left as p.
 //
 // Selections made by every workgroup read the same histograms, so they agree;
 // workgroup 0 records them in the control block.  Workgroups exchange data
