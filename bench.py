@@ -578,10 +578,14 @@ def bench_average(efs, torch, synth, cur, steps, warmup, threads):
            "bytes_model": "4 d + 8 per pair (dense output write, payload read)"}
     say("average of %d payloads (%d pairs): %.1f us" % (w.n_workers, pairs, us))
     # the fused model updates on the same payloads, (x, m) rotating over four sets
-    touched = int(torch.unique(torch.cat(
-        [p[0][:efs.counter_value(p[2])] for p in payloads])).numel())
+    touched_idx = torch.unique(torch.cat(
+        [p[0][:efs.counter_value(p[2])] for p in payloads]))
+    touched = int(touched_idx.numel())
+    # the SGD update reads and writes x only where a payload touches it:
+    # scattered 4-byte updates, each moving its 128-byte cache line
+    lines = int(torch.unique(touched_idx // 32).numel())
     ms = [torch.zeros(d, dtype=torch.float32, device="cuda") for _ in range(4)]
-    upd = {"touched": touched}
+    upd = {"touched": touched, "lines_128b": lines}
     for mode, name, nb in ((efs.APPLY_SGD, "sgd", 8.0 * pairs + 8.0 * touched),
                            (efs.APPLY_MOMENTUM, "momentum", 8.0 * pairs + 16.0 * d)):
         fns = [efs.prepare_sparse_apply(payloads, d, mode, outs[r], ws, m=ms[r], beta=0.9,
@@ -592,6 +596,11 @@ def bench_average(efs, torch, synth, cur, steps, warmup, threads):
             for s in range(steps):
                 fns[s % 4]()
         upd[name] = {"us": round(t.us / steps, 2), "bytes": nb, **rate(nb, t.us / steps)}
+        if mode == efs.APPLY_SGD:
+            lb = 8.0 * pairs + 2 * 128.0 * lines
+            upd[name]["line_traffic"] = {
+                "bytes": lb, **rate(lb, t.us / steps),
+                "model": "8 per pair read + each touched 128-byte line of x read and written"}
     res["_apply"] = upd
     del ws, outs, ms, payloads
     torch.cuda.empty_cache()
