@@ -114,6 +114,11 @@ def parse():
     ap.add_argument("--layerwise-only", action="store_true",
                     help="time only the 20,000-layer layer-wise Top-k and print its figures "
                          "(not the contract line)")
+    ap.add_argument("--radix-only", action="store_true",
+                    help="time only Top-k from a fresh workspace (the radix path) on the "
+                         "workload's first gradient, as drawn and quantised to 2^-16 and 2^-10 "
+                         "(ties at the threshold to split), and print its figures (not the "
+                         "contract line)")
     ap.add_argument("--trace-last", type=int, metavar="N",
                     help="with --parse-trace: per-kernel statistics over each kernel's last N "
                          "dispatches only (the timed calls of a run that times N)")
@@ -333,6 +338,9 @@ def main():
     cur = torch.cuda.current_stream()
     if args.layerwise_only:
         print(json.dumps(bench_many_layers(efs, torch, synth, cur)), flush=True)
+        return
+    if args.radix_only:
+        print(json.dumps(bench_radix(efs, torch, synth, cur, wl, dev)), flush=True)
         return
     lr = synth.LR
     if args.pool is None:
@@ -709,6 +717,41 @@ def bench_many_layers(efs, torch, synth, cur):
            **rate(12.0 * d + 8.0 * kt, us)}
     say("20,000-layer layer-wise Top-k: %s" % res)
     del pool, e, sidx, sval, sws
+    torch.cuda.empty_cache()
+    return res
+
+
+def bench_radix(efs, torch, synth, cur, wl, dev, calls=4):
+    """Top-k from a fresh workspace (no threshold recorded, so the radix path)
+    with e = 0 on the workload's first gradient: as drawn, and rounded to
+    multiples of 2^-16 and 2^-10, which put ties at the threshold that must
+    be split by index (a few hundred, listed; tens of thousands, counted per
+    tile).  Each call timed alone with events on the stream it runs on."""
+    import numpy as np
+    d, k = wl.d, wl.topk_k[0]
+    host = synth.Stream(wl.ident).gradient(0, threads=min(16, os.cpu_count() or 1))
+    g = to_device(torch, host, dev)
+    del host
+    e = torch.zeros(d, dtype=torch.float32, device=dev)
+    idx = torch.empty(k, dtype=torch.int32, device=dev)
+    val = torch.empty(k, dtype=torch.float32, device=dev)
+    ws = efs.new_topk_workspace(d, k, dev)
+    res = {"workload": wl.name, "d": d, "k": k}
+    for q in (0, 16, 10):
+        if q:
+            g.mul_(2.0 ** q).round_().div_(2.0 ** q)   # multiples of 2^-q, exact in fp32
+        each = []
+        for _ in range(calls):
+            e.zero_()
+            ws.zero_()
+            with Timer(torch, cur) as t:
+                efs.topk_compress(g, e, synth.LR, k, idx, val, ws)
+            assert not efs.topk_took_bracket_path(ws)
+            each.append(t.us)
+        key = "as_drawn" if q == 0 else "multiples_of_2^-%d" % q
+        res[key] = dict(stats_us(each), **rate(12.0 * d + 8.0 * k, float(np.median(each))))
+        say("Top-k radix path, %s: %s" % (key, res[key]))
+    del g, e, idx, val, ws
     torch.cuda.empty_cache()
     return res
 
